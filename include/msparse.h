@@ -1,0 +1,219 @@
+/*
+ * msparse -- vertical-slash dynamic sparse attention for long-context training
+ * on one AMD Instinct MI355X (gfx950).  C ABI of libmsparse.so.
+ *
+ * The library implements the single-GPU hot path of MTraining (arXiv
+ * 2510.18830): per-head pattern estimation from the last queries (Algorithm 1,
+ * Section 4.1), conversion of the selected vertical and slash lines into a
+ * 64 x 64 block index plus a token-level column index (Section 4.1 (ii),
+ * convert_index of Algorithms 1 and 2), and a sparse FlashAttention forward
+ * (out + LSE) and backward (dQ, dK, dV) over only the selected blocks and
+ * columns (block_bar_sparse_attention_forward of Algorithm 2; gradients by
+ * Eq. softmax_gradient and Eq. attention_backward).  A ring worker's share
+ * (Section 4.2, Algorithm 2) is one call per ring step with a msparse_ring
+ * descriptor, and partial results are combined by msparse_merge_out_lse
+ * (merge_out_and_lse of Algorithm 2).
+ *
+ * Conventions shared by every entry point
+ *   - Tensors are device pointers to contiguous row-major arrays, 16-byte
+ *     aligned: Q, O, dO bf16 [B, Hq, Nq, d]; K, V bf16 [B, Hkv, Nk, d];
+ *     lse fp32 [B, Hq, Nq] (natural log); dQ fp32 [B, Hq, Nq, d];
+ *     dK, dV fp32 [B, Hkv, Nk, d].
+ *   - GQA: query head h reads KV head h / (Hq / Hkv) (contiguous groups).
+ *   - Causal attention with 64-token blocks only.  scale <= 0 selects
+ *     1 / sqrt(head_dim).
+ *   - The caller owns every buffer, including the workspace; the library
+ *     allocates no device memory and keeps no state besides its loaded code.
+ *     Calls are re-entrant.
+ *   - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream) and
+ *     returns before it finishes.  Only msparse_index_count waits for the GPU.
+ *     Setting MSPARSE_SYNC_CHECK=1 in the environment makes every call wait
+ *     for its kernels and report asynchronous faults as MSPARSE_ERR_HIP.
+ *   - Arguments are validated on the host before anything is launched, so a
+ *     call that returns an error has enqueued no work.
+ */
+#ifndef MSPARSE_H
+#define MSPARSE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#ifndef MSPARSE_API
+#define MSPARSE_API __attribute__((visibility("default")))
+#endif
+
+typedef enum {
+    MSPARSE_OK = 0,
+    MSPARSE_ERR_INVALID = -1,     /* null pointer, k or last_q outside [1, N], Hq % Hkv != 0, bad ring */
+    MSPARSE_ERR_UNSUPPORTED = -2, /* head_dim not 64/128, N % 64 != 0, non-causal, block != 64, last_q > 64 */
+    MSPARSE_ERR_CAPACITY = -3,    /* index capacities below what the call must write */
+    MSPARSE_ERR_WORKSPACE = -4,   /* workspace missing or smaller than the *_workspace query */
+    MSPARSE_ERR_HIP = -5          /* a HIP launch or runtime call failed */
+} msparse_status;
+
+/* Problem shape.  seq_q and seq_k are the local lengths (equal for a whole
+ * sequence; in ring mode the worker's query shard and one KV shard, both
+ * N_global / world). */
+typedef struct {
+    int32_t batch;
+    int32_t seq_q;
+    int32_t seq_k;
+    int32_t heads_q;
+    int32_t heads_kv;
+    int32_t head_dim; /* 64 or 128 */
+    int32_t block;    /* must be 64 */
+    int32_t causal;   /* must be 1 */
+    float scale;      /* <= 0: 1 / sqrt(head_dim) */
+} msparse_dims;
+
+enum { MSPARSE_LAYOUT_STRIPED = 0, MSPARSE_LAYOUT_ZIGZAG = 1 };
+
+/* One step of a ring (Section 4.2).  The global sequence of world * seq_q
+ * tokens is split into 64-token blocks; block g belongs to
+ *   STRIPED: worker g mod world;
+ *   ZIGZAG:  worker c if c < world else 2 world - 1 - c, c = g / (nb / (2 world)).
+ * A worker keeps its blocks in ascending global order.  At step t worker
+ * `rank` holds the KV shard of worker (rank - t) mod world.  Passing NULL
+ * instead of a descriptor means the whole sequence (world = 1). */
+typedef struct {
+    int32_t world;
+    int32_t rank;
+    int32_t step;
+    int32_t layout;
+} msparse_ring;
+
+/* The sparse index of one call (whole sequence or one ring step).  All arrays
+ * are device memory owned by the caller; bh = b * Hq + h.
+ *   blk_ptr  int64 [B*Hq*nqb + 1]  blk_idx[blk_ptr[bh*nqb+i] .. blk_ptr[bh*nqb+i+1])
+ *                                  are the ascending local key blocks of local
+ *                                  query block i (nqb = seq_q / 64)
+ *   col_ptr  int64 [B*Hq*nqb + 1]  col_idx: ascending local key token offsets of
+ *                                  the vertical columns of query block i that no
+ *                                  selected block already covers
+ *   kblk_ptr int64 [B*Hq*nkb + 1]  kblk_idx: the transpose of the block lists
+ *                                  (ascending local query blocks per local key
+ *                                  block, nkb = seq_k / 64); same length as blk_idx
+ *   vcol_ptr int64 [B*Hq + 1]      vcol_idx: ascending local key offsets of the
+ *                                  head's verticals that lie in this KV shard
+ *   diag_bits uint32 [B*Hq*ceil(nb/32)]  bit x set when block-diagonal x (query
+ *                                  block - key block, global) is selected;
+ *                                  nb = global blocks
+ *   q_blk_global int32 [nqb], k_blk_global int32 [nkb]: global block numbers
+ *   overflow int32 [1] (may be NULL): set to 1 by msparse_build_index when a
+ *                                  capacity was too small (what does not fit
+ *                                  is dropped, nothing is written out of bounds)
+ * blk_cap, col_cap, vcol_cap are host-side element capacities of blk_idx (and
+ * kblk_idx), col_idx and vcol_idx. */
+typedef struct {
+    int64_t* blk_ptr;
+    int32_t* blk_idx;
+    int64_t blk_cap;
+    int64_t* col_ptr;
+    int32_t* col_idx;
+    int64_t col_cap;
+    int64_t* kblk_ptr;
+    int32_t* kblk_idx;
+    int64_t* vcol_ptr;
+    int32_t* vcol_idx;
+    int64_t vcol_cap;
+    uint32_t* diag_bits;
+    int32_t* q_blk_global;
+    int32_t* k_blk_global;
+    int32_t* overflow;
+} msparse_index;
+
+/* Human-readable name of a status code (static storage). */
+MSPARSE_API const char* msparse_strerror(msparse_status status);
+
+/* Detail of the last error returned on the calling host thread. */
+MSPARSE_API const char* msparse_last_error(void);
+
+/* ------------------------------------------------------------------------ */
+/* Pattern estimation (Algorithm 1 on one GPU).  For every (b, h): the last
+ * last_q query rows n attend causally to all keys m <= n with logits
+ * scale * q_n . k_m; P is their row-wise softmax over the whole sequence;
+ * v_score[m] = sum_n P[n, m] (vertical scores, sum_v) and
+ * s_score[delta] = sum_n P[n, n - delta] (slash scores along n - m = delta,
+ * sum_s).  v_idx receives the k_v largest vertical scores and s_idx the k_s
+ * largest slash scores (argtopk with a fixed budget; equal scores go to the
+ * lower index), each list ascending.
+ *   q, k      bf16 [B, Hq, N, d] and [B, Hkv, N, d], N = seq_q = seq_k
+ *   v_idx     int32 [B, Hq, k_v];  s_idx int32 [B, Hq, k_s]
+ *   v_score, s_score  fp32 [B, Hq, N], or NULL to keep them in the workspace
+ * Requires 1 <= last_q <= min(64, N), 1 <= k_v, k_s <= N. */
+MSPARSE_API size_t msparse_estimate_workspace(const msparse_dims* dims, int32_t last_q, int32_t k_v, int32_t k_s);
+MSPARSE_API msparse_status msparse_estimate(const msparse_dims* dims, const void* q, const void* k, int32_t last_q,
+                                int32_t k_v, int32_t k_s, int32_t* v_idx, int32_t* s_idx, float* v_score,
+                                float* s_score, void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Index construction (Section 4.1 (ii); convert_index of Algorithms 1, 2).
+ * v_idx [B, Hq, k_v] and s_idx [B, Hq, k_s] are in global token coordinates:
+ * vertical positions and slash offsets delta = n - m.  Each slash offset is
+ * executed as the 64 x 64 block-diagonals floor(delta/64) and ceil(delta/64)
+ * (D); query block i gets the key blocks i - x for x in D, x <= i, and the
+ * verticals v <= 64 i + 63 whose block-diagonal i - v/64 is not in D.  With a
+ * ring descriptor, the lists are restricted to the step's KV shard and written
+ * in local coordinates.  Duplicate entries in v_idx or s_idx count once.
+ *
+ * msparse_index_count returns the exact element counts the build will write
+ * (it waits for the GPU).  msparse_build_index writes them asynchronously,
+ * never past blk_cap / col_cap / vcol_cap; when a capacity is too small it sets
+ * *overflow and the host-visible caps check returns MSPARSE_ERR_CAPACITY only
+ * when a cap is below the trivial lower bound (use msparse_index_count). */
+MSPARSE_API size_t msparse_index_workspace(const msparse_dims* dims, int32_t k_v, int32_t k_s, const msparse_ring* ring);
+MSPARSE_API msparse_status msparse_index_count(const msparse_dims* dims, const int32_t* v_idx, int32_t k_v,
+                                   const int32_t* s_idx, int32_t k_s, const msparse_ring* ring,
+                                   int64_t* blk_nnz, int64_t* col_nnz, int64_t* vcol_nnz, void* workspace,
+                                   size_t workspace_bytes, void* stream);
+MSPARSE_API msparse_status msparse_build_index(const msparse_dims* dims, const int32_t* v_idx, int32_t k_v,
+                                   const int32_t* s_idx, int32_t k_s, const msparse_ring* ring,
+                                   const msparse_index* index, void* workspace, size_t workspace_bytes,
+                                   void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Sparse attention forward (block_bar_sparse_attention_forward, Algorithm 2).
+ * For each query row n of local query block i, softmax attention over the
+ * keys of the selected blocks and columns of i that are causally visible
+ * (global key position <= global query position):
+ *   out_n = sum_m P[n, m] v_m,  lse_n = log sum_m exp(scale q_n . k_m).
+ * A row that sees no key gets out = 0 and lse = -inf.  out is bf16 (round to
+ * nearest even), lse fp32.  Needs no workspace (pass NULL, 0). */
+MSPARSE_API msparse_status msparse_attn_fwd(const msparse_dims* dims, const void* q, const void* k, const void* v,
+                                const msparse_index* index, void* out, float* lse, void* workspace,
+                                size_t workspace_bytes, void* stream);
+
+/* Log-sum-exp merge of one ring step's partial result into a running one
+ * (merge_out_and_lse, Algorithm 2): lse = logaddexp(lse_acc, lse_part),
+ * o_acc = exp(lse_acc - lse) o_acc + exp(lse_part - lse) o_part.
+ *   o_part bf16 [B, Hq, Nq, d], lse_part fp32 [B, Hq, Nq] (from msparse_attn_fwd)
+ *   o_acc fp32 [B, Hq, Nq, d], lse_acc fp32 [B, Hq, Nq] (read unless `first`,
+ *   which copies the partial instead)
+ *   out_bf16 bf16 [B, Hq, Nq, d] or NULL: also stores the merged O as bf16. */
+MSPARSE_API msparse_status msparse_merge_out_lse(const msparse_dims* dims, const void* o_part, const float* lse_part,
+                                     float* o_acc, float* lse_acc, void* out_bf16, int32_t first, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Sparse attention backward over the same index (Eq. softmax_gradient,
+ * Eq. attention_backward; the index is a constant).  With
+ * P = exp(scale q k^T - lse) on the executed entries and Delta_n = dO_n . O_n:
+ *   dV = P^T dO,  dZ = P o (dO V^T - Delta),  dQ = scale dZ K,  dK = scale dZ^T Q,
+ * dK and dV summed over the query heads of each KV head.  out and lse are the
+ * forward's final (merged) results.  dq, dk, dv are fp32 and overwritten,
+ * except that dq_accumulate = 1 adds into dq (ring steps after the first).
+ * Workspace: msparse_attn_bwd_workspace(dims, vcol_cap) bytes. */
+MSPARSE_API size_t msparse_attn_bwd_workspace(const msparse_dims* dims, int64_t vcol_cap);
+MSPARSE_API msparse_status msparse_attn_bwd(const msparse_dims* dims, const void* q, const void* k, const void* v,
+                                const void* out, const void* dout, const float* lse,
+                                const msparse_index* index, float* dq, float* dk, float* dv,
+                                int32_t dq_accumulate, void* workspace, size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MSPARSE_H */

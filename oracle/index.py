@@ -57,7 +57,7 @@ def head_lists(v_idx, s_idx, N: int):
     D = diag_set(s_idx, nb)
     in_d = np.zeros(nb, dtype=bool)
     in_d[D] = True
-    V = np.sort(np.asarray(v_idx, dtype=np.int64))
+    V = np.unique(np.asarray(v_idx, dtype=np.int64))   # ascending, duplicates count once
     blocks, cols = [], []
     for i in range(nb):
         blocks.append(np.sort(i - D[D <= i]))
@@ -114,7 +114,7 @@ class Index:
                                     for c in cols[g] if int(c) // BLOCK in kloc], dtype=np.int64))
             self.blocks.append(hb)
             self.cols.append(hc)
-            V = np.sort(v2[bh].astype(np.int64))
+            V = np.unique(v2[bh].astype(np.int64))
             self.vcols.append(np.array([kloc[int(c) // BLOCK] * BLOCK + int(c) % BLOCK
                                         for c in V if int(c) // BLOCK in kloc], dtype=np.int64))
 

@@ -1,0 +1,451 @@
+// C ABI of libmsparse: argument validation, workspace carve-up and launches.
+// Every check runs on the host before the first launch, so an error return
+// leaves the stream untouched.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <string>
+
+#include "common.h"
+#include "kernels.h"
+
+using namespace msparse;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+msparse_status fail(msparse_status st, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return st;
+}
+
+bool sync_check_enabled() {
+    static int v = [] {
+        const char* e = getenv("MSPARSE_SYNC_CHECK");
+        return (e && e[0] && e[0] != '0') ? 1 : 0;
+    }();
+    return v != 0;
+}
+
+msparse_status check_hip(hipError_t e, hipStream_t s, const char* what) {
+    if (e != hipSuccess) return fail(MSPARSE_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+    if (sync_check_enabled()) {
+        e = hipStreamSynchronize(s);
+        if (e == hipSuccess) e = hipGetLastError();
+        if (e != hipSuccess) return fail(MSPARSE_ERR_HIP, "%s (sync check): %s", what, hipGetErrorString(e));
+    }
+    return MSPARSE_OK;
+}
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+// Bump allocator over the caller's workspace.
+struct Carve {
+    char* base;
+    size_t off = 0;
+    template <class T>
+    T* take(size_t count) {
+        T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+        off = align_up(off + count * sizeof(T));
+        return p;
+    }
+};
+
+float resolve_scale(const msparse_dims* d) { return d->scale > 0.f ? d->scale : 1.0f / std::sqrt(float(d->head_dim)); }
+
+msparse_status check_dims(const msparse_dims* d, bool same_len) {
+    if (!d) return fail(MSPARSE_ERR_INVALID, "dims is NULL");
+    if (d->batch < 1 || d->heads_q < 1 || d->heads_kv < 1 || d->seq_q < 0 || d->seq_k < 0)
+        return fail(MSPARSE_ERR_INVALID, "batch, heads must be >= 1 and lengths >= 0");
+    if (d->heads_q % d->heads_kv != 0)
+        return fail(MSPARSE_ERR_INVALID, "heads_q (%d) is not a multiple of heads_kv (%d)", d->heads_q, d->heads_kv);
+    if (d->head_dim != 64 && d->head_dim != 128)
+        return fail(MSPARSE_ERR_UNSUPPORTED, "head_dim %d (supported: 64, 128)", d->head_dim);
+    if (d->block != kBlock) return fail(MSPARSE_ERR_UNSUPPORTED, "block %d (supported: 64)", d->block);
+    if (d->causal != 1) return fail(MSPARSE_ERR_UNSUPPORTED, "only causal attention is supported");
+    if (d->seq_q % kBlock || d->seq_k % kBlock)
+        return fail(MSPARSE_ERR_UNSUPPORTED, "sequence lengths (%d, %d) must be multiples of 64", d->seq_q, d->seq_k);
+    if (same_len && d->seq_q != d->seq_k) return fail(MSPARSE_ERR_INVALID, "seq_q != seq_k");
+    if (!std::isfinite(d->scale)) return fail(MSPARSE_ERR_INVALID, "scale is not finite");
+    const int64_t big = int64_t(d->batch) * d->heads_q * int64_t(std::max(d->seq_q, d->seq_k));
+    if (big > (int64_t(1) << 31) - 1) return fail(MSPARSE_ERR_UNSUPPORTED, "batch * heads * seq exceeds 2^31 rows");
+    return MSPARSE_OK;
+}
+
+struct RingInfo {
+    int32_t world = 1, rank = 0, step = 0, layout = MSPARSE_LAYOUT_STRIPED, shard = 0;
+};
+
+msparse_status check_ring(const msparse_dims* d, const msparse_ring* r, RingInfo* out) {
+    RingInfo ri;
+    if (r) {
+        if (r->world < 1 || r->rank < 0 || r->rank >= r->world || r->step < 0 || r->step >= r->world)
+            return fail(MSPARSE_ERR_INVALID, "ring world %d rank %d step %d", r->world, r->rank, r->step);
+        if (r->layout != MSPARSE_LAYOUT_STRIPED && r->layout != MSPARSE_LAYOUT_ZIGZAG)
+            return fail(MSPARSE_ERR_INVALID, "ring layout %d", r->layout);
+        ri.world = r->world;
+        ri.rank = r->rank;
+        ri.step = r->step;
+        ri.layout = r->layout;
+        ri.shard = ((r->rank - r->step) % r->world + r->world) % r->world;
+        if (r->layout == MSPARSE_LAYOUT_ZIGZAG && (d->seq_q / kBlock) % 2 != 0)
+            return fail(MSPARSE_ERR_UNSUPPORTED, "zigzag shards need an even number of 64-token blocks");
+    }
+    if (d->seq_q != d->seq_k) return fail(MSPARSE_ERR_INVALID, "query and KV shards must have equal length");
+    const int64_t ng = int64_t(d->seq_q) * ri.world;
+    if (ng > (int64_t(1) << 30)) return fail(MSPARSE_ERR_UNSUPPORTED, "global sequence too long");
+    *out = ri;
+    return MSPARSE_OK;
+}
+
+// ------------------------------------------------------------------ index
+struct IndexPlan {
+    IndexArgs a{};
+    size_t bytes = 0;
+};
+
+IndexPlan plan_index(const msparse_dims* d, int32_t k_v, int32_t k_s, const RingInfo& ri, void* ws,
+                     bool own_ptrs) {
+    IndexPlan p;
+    IndexArgs& a = p.a;
+    a.BH = d->batch * d->heads_q;
+    a.k_v = k_v;
+    a.k_s = k_s;
+    a.nqb = d->seq_q / kBlock;
+    a.nkb = d->seq_k / kBlock;
+    a.nb = a.nqb * ri.world;
+    a.world = ri.world;
+    a.rank = ri.rank;
+    a.shard = ri.shard;
+    a.layout = ri.layout;
+    const int64_t ng = int64_t(a.nb) * kBlock;
+    a.vwords = int32_t((ng + 31) / 32);
+    a.dwords = (a.nb + 31) / 32;
+    Carve c{static_cast<char*>(ws)};
+    a.vbits = c.take<uint32_t>(size_t(a.BH) * a.vwords);
+    a.vlist = c.take<int32_t>(size_t(a.BH) * k_v);
+    a.vcnt = c.take<int32_t>(a.BH);
+    a.dlist = c.take<int32_t>(size_t(a.BH) * a.nb);
+    a.dcnt = c.take<int32_t>(a.BH);
+    a.dbits = c.take<uint32_t>(size_t(a.BH) * a.dwords);
+    a.cnt_blk = c.take<int64_t>(size_t(a.BH) * a.nqb);
+    a.cnt_col = c.take<int64_t>(size_t(a.BH) * a.nqb);
+    a.cnt_kblk = c.take<int64_t>(size_t(a.BH) * a.nkb);
+    a.cnt_vcol = c.take<int64_t>(a.BH);
+    if (own_ptrs) {
+        a.blk_ptr = c.take<int64_t>(size_t(a.BH) * a.nqb + 1);
+        a.col_ptr = c.take<int64_t>(size_t(a.BH) * a.nqb + 1);
+        a.kblk_ptr = c.take<int64_t>(size_t(a.BH) * a.nkb + 1);
+        a.vcol_ptr = c.take<int64_t>(size_t(a.BH) + 1);
+    } else {
+        // room for the pointer arrays is reserved either way so the size query
+        // does not depend on the mode
+        c.take<int64_t>(size_t(a.BH) * a.nqb + 1);
+        c.take<int64_t>(size_t(a.BH) * a.nqb + 1);
+        c.take<int64_t>(size_t(a.BH) * a.nkb + 1);
+        c.take<int64_t>(size_t(a.BH) + 1);
+    }
+    p.bytes = c.off;
+    return p;
+}
+
+msparse_status check_index_inputs(const msparse_dims* d, const int32_t* v_idx, int32_t k_v, const int32_t* s_idx,
+                                  int32_t k_s, const msparse_ring* ring, RingInfo* ri) {
+    msparse_status st = check_dims(d, false);
+    if (st) return st;
+    if ((st = check_ring(d, ring, ri))) return st;
+    if (!v_idx || !s_idx) return fail(MSPARSE_ERR_INVALID, "v_idx / s_idx is NULL");
+    const int64_t ng = int64_t(d->seq_q) * ri->world;
+    if (k_v < 1 || k_v > ng || k_s < 1 || k_s > ng)
+        return fail(MSPARSE_ERR_INVALID, "budgets k_v=%d k_s=%d outside [1, %lld]", k_v, k_s, (long long)ng);
+    if (d->seq_q == 0) return fail(MSPARSE_ERR_INVALID, "empty sequence");
+    return MSPARSE_OK;
+}
+
+msparse_status check_index_struct(const msparse_dims* d, const msparse_index* x, bool need_transpose) {
+    if (!x) return fail(MSPARSE_ERR_INVALID, "index is NULL");
+    if (!x->blk_ptr || !x->col_ptr || !x->q_blk_global || !x->k_blk_global || !x->diag_bits)
+        return fail(MSPARSE_ERR_INVALID, "index arrays are NULL");
+    if ((x->blk_cap > 0 && !x->blk_idx) || (x->col_cap > 0 && !x->col_idx))
+        return fail(MSPARSE_ERR_INVALID, "index entry arrays are NULL");
+    if (need_transpose && (!x->kblk_ptr || !x->vcol_ptr || (x->blk_cap > 0 && !x->kblk_idx) ||
+                           (x->vcol_cap > 0 && !x->vcol_idx)))
+        return fail(MSPARSE_ERR_INVALID, "transposed index arrays are NULL");
+    if (x->blk_cap < 0 || x->col_cap < 0 || x->vcol_cap < 0) return fail(MSPARSE_ERR_INVALID, "negative capacity");
+    (void)d;
+    return MSPARSE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* msparse_strerror(msparse_status s) {
+    switch (s) {
+        case MSPARSE_OK: return "ok";
+        case MSPARSE_ERR_INVALID: return "invalid argument";
+        case MSPARSE_ERR_UNSUPPORTED: return "unsupported configuration";
+        case MSPARSE_ERR_CAPACITY: return "index capacity too small";
+        case MSPARSE_ERR_WORKSPACE: return "workspace too small";
+        case MSPARSE_ERR_HIP: return "HIP runtime error";
+    }
+    return "unknown status";
+}
+
+const char* msparse_last_error(void) { return g_last_error.c_str(); }
+
+// ------------------------------------------------------------------ index
+size_t msparse_index_workspace(const msparse_dims* dims, int32_t k_v, int32_t k_s, const msparse_ring* ring) {
+    RingInfo ri;
+    if (check_dims(dims, false) || check_ring(dims, ring, &ri) || k_v < 1 || k_s < 1) return 0;
+    return plan_index(dims, k_v, k_s, ri, nullptr, true).bytes;
+}
+
+msparse_status msparse_index_count(const msparse_dims* dims, const int32_t* v_idx, int32_t k_v, const int32_t* s_idx,
+                                   int32_t k_s, const msparse_ring* ring, int64_t* blk_nnz, int64_t* col_nnz,
+                                   int64_t* vcol_nnz, void* ws, size_t ws_bytes, void* stream) {
+    RingInfo ri;
+    msparse_status st = check_index_inputs(dims, v_idx, k_v, s_idx, k_s, ring, &ri);
+    if (st) return st;
+    if (!blk_nnz || !col_nnz || !vcol_nnz) return fail(MSPARSE_ERR_INVALID, "count outputs are NULL");
+    IndexPlan p = plan_index(dims, k_v, k_s, ri, ws, true);
+    if (!ws || ws_bytes < p.bytes)
+        return fail(MSPARSE_ERR_WORKSPACE, "index workspace %zu < %zu bytes", ws_bytes, p.bytes);
+    p.a.v_idx = v_idx;
+    p.a.s_idx = s_idx;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if ((st = check_hip(launch_index_prep(p.a, s), s, "index prep"))) return st;
+    if ((st = check_hip(launch_index_count(p.a, s), s, "index count"))) return st;
+    if ((st = check_hip(launch_index_scan(p.a, s), s, "index scan"))) return st;
+    int64_t tot[3];
+    const int64_t nq = int64_t(p.a.BH) * p.a.nqb;
+    hipError_t e = hipMemcpyAsync(&tot[0], p.a.blk_ptr + nq, 8, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(&tot[1], p.a.col_ptr + nq, 8, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(&tot[2], p.a.vcol_ptr + p.a.BH, 8, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return fail(MSPARSE_ERR_HIP, "index count readback: %s", hipGetErrorString(e));
+    *blk_nnz = tot[0];
+    *col_nnz = tot[1];
+    *vcol_nnz = tot[2];
+    return MSPARSE_OK;
+}
+
+msparse_status msparse_build_index(const msparse_dims* dims, const int32_t* v_idx, int32_t k_v, const int32_t* s_idx,
+                                   int32_t k_s, const msparse_ring* ring, const msparse_index* index, void* ws,
+                                   size_t ws_bytes, void* stream) {
+    RingInfo ri;
+    msparse_status st = check_index_inputs(dims, v_idx, k_v, s_idx, k_s, ring, &ri);
+    if (st) return st;
+    if ((st = check_index_struct(dims, index, true))) return st;
+    IndexPlan p = plan_index(dims, k_v, k_s, ri, ws, false);
+    if (!ws || ws_bytes < p.bytes)
+        return fail(MSPARSE_ERR_WORKSPACE, "index workspace %zu < %zu bytes", ws_bytes, p.bytes);
+    // Without an overflow flag the capacities must cover the worst case.
+    const int64_t BH = p.a.BH, nqb = p.a.nqb, nkb = p.a.nkb;
+    const int64_t dmax = std::min<int64_t>(p.a.nb, 2 * int64_t(k_s));
+    const int64_t blk_bound = BH * nqb * std::min<int64_t>(nkb, dmax);
+    const int64_t col_bound = BH * nqb * std::min<int64_t>(k_v, nkb * kBlock);
+    const int64_t vcol_bound = BH * std::min<int64_t>(k_v, nkb * kBlock);
+    if (!index->overflow && (index->blk_cap < blk_bound || index->col_cap < col_bound || index->vcol_cap < vcol_bound))
+        return fail(MSPARSE_ERR_CAPACITY,
+                    "capacities (%lld, %lld, %lld) below the worst case (%lld, %lld, %lld) and no overflow flag",
+                    (long long)index->blk_cap, (long long)index->col_cap, (long long)index->vcol_cap,
+                    (long long)blk_bound, (long long)col_bound, (long long)vcol_bound);
+    IndexArgs& a = p.a;
+    a.v_idx = v_idx;
+    a.s_idx = s_idx;
+    a.blk_ptr = index->blk_ptr;
+    a.col_ptr = index->col_ptr;
+    a.kblk_ptr = index->kblk_ptr;
+    a.vcol_ptr = index->vcol_ptr;
+    a.blk_idx = index->blk_idx;
+    a.blk_cap = index->blk_cap;
+    a.col_idx = index->col_idx;
+    a.col_cap = index->col_cap;
+    a.kblk_idx = index->kblk_idx;
+    a.vcol_idx = index->vcol_idx;
+    a.vcol_cap = index->vcol_cap;
+    a.diag_bits_out = index->diag_bits;
+    a.q_blk_global = index->q_blk_global;
+    a.k_blk_global = index->k_blk_global;
+    a.overflow = index->overflow;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (a.overflow) {
+        hipError_t e = hipMemsetAsync(a.overflow, 0, sizeof(int32_t), s);
+        if (e != hipSuccess) return fail(MSPARSE_ERR_HIP, "overflow reset: %s", hipGetErrorString(e));
+    }
+    if ((st = check_hip(launch_index_prep(a, s), s, "index prep"))) return st;
+    if ((st = check_hip(launch_index_count(a, s), s, "index count"))) return st;
+    if ((st = check_hip(launch_index_scan(a, s), s, "index scan"))) return st;
+    return check_hip(launch_index_fill(a, s), s, "index fill");
+}
+
+// ------------------------------------------------------------------ attention
+static msparse_status fill_attn(const msparse_dims* d, const msparse_index* x, AttnArgs* a) {
+    a->B = d->batch;
+    a->Hq = d->heads_q;
+    a->Hkv = d->heads_kv;
+    a->Nq = d->seq_q;
+    a->Nk = d->seq_k;
+    a->d = d->head_dim;
+    a->nqb = d->seq_q / kBlock;
+    a->nkb = d->seq_k / kBlock;
+    a->scale = resolve_scale(d);
+    a->blk_ptr = x->blk_ptr;
+    a->blk_idx = x->blk_idx;
+    a->col_ptr = x->col_ptr;
+    a->col_idx = x->col_idx;
+    a->kblk_ptr = x->kblk_ptr;
+    a->kblk_idx = x->kblk_idx;
+    a->vcol_ptr = x->vcol_ptr;
+    a->vcol_idx = x->vcol_idx;
+    a->diag_bits = x->diag_bits;
+    a->q_blk_global = x->q_blk_global;
+    a->k_blk_global = x->k_blk_global;
+    return MSPARSE_OK;
+}
+
+msparse_status msparse_attn_fwd(const msparse_dims* dims, const void* q, const void* k, const void* v,
+                                const msparse_index* index, void* out, float* lse, void* ws, size_t ws_bytes,
+                                void* stream) {
+    (void)ws;
+    (void)ws_bytes;
+    msparse_status st = check_dims(dims, false);
+    if (st) return st;
+    if (!q || !k || !v || !out || !lse) return fail(MSPARSE_ERR_INVALID, "tensor pointer is NULL");
+    if ((st = check_index_struct(dims, index, false))) return st;
+    if (dims->seq_q == 0) return MSPARSE_OK;
+    AttnArgs a{};
+    fill_attn(dims, index, &a);
+    a.q = static_cast<const uint16_t*>(q);
+    a.k = static_cast<const uint16_t*>(k);
+    a.v = static_cast<const uint16_t*>(v);
+    a.out = static_cast<uint16_t*>(out);
+    a.lse = lse;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    return check_hip(launch_attn_fwd(a, s), s, "attn fwd");
+}
+
+msparse_status msparse_merge_out_lse(const msparse_dims* dims, const void* o_part, const float* lse_part, float* o_acc,
+                                     float* lse_acc, void* out_bf16, int32_t first, void* stream) {
+    msparse_status st = check_dims(dims, false);
+    if (st) return st;
+    if (!o_part || !lse_part || !o_acc || !lse_acc) return fail(MSPARSE_ERR_INVALID, "tensor pointer is NULL");
+    if (dims->seq_q == 0) return MSPARSE_OK;
+    MergeArgs m{};
+    m.o_part = static_cast<const uint16_t*>(o_part);
+    m.lse_part = lse_part;
+    m.o_acc = o_acc;
+    m.lse_acc = lse_acc;
+    m.out = static_cast<uint16_t*>(out_bf16);
+    m.first = first;
+    m.rows = int64_t(dims->batch) * dims->heads_q * dims->seq_q;
+    m.d = dims->head_dim;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    return check_hip(launch_merge(m, s), s, "merge out/lse");
+}
+
+size_t msparse_attn_bwd_workspace(const msparse_dims* dims, int64_t vcol_cap) {
+    if (check_dims(dims, false) || vcol_cap < 0) return 0;
+    Carve c{nullptr};
+    c.take<float>(size_t(dims->batch) * dims->heads_q * dims->seq_q);
+    c.take<float>(size_t(vcol_cap) * dims->head_dim);
+    c.take<float>(size_t(vcol_cap) * dims->head_dim);
+    return c.off;
+}
+
+msparse_status msparse_attn_bwd(const msparse_dims* dims, const void* q, const void* k, const void* v,
+                                const void* out, const void* dout, const float* lse, const msparse_index* index,
+                                float* dq, float* dk, float* dv, int32_t dq_accumulate, void* ws, size_t ws_bytes,
+                                void* stream) {
+    msparse_status st = check_dims(dims, false);
+    if (st) return st;
+    if (!q || !k || !v || !out || !dout || !lse || !dq || !dk || !dv)
+        return fail(MSPARSE_ERR_INVALID, "tensor pointer is NULL");
+    if ((st = check_index_struct(dims, index, true))) return st;
+    const size_t need = msparse_attn_bwd_workspace(dims, index->vcol_cap);
+    if (!ws || ws_bytes < need) return fail(MSPARSE_ERR_WORKSPACE, "bwd workspace %zu < %zu bytes", ws_bytes, need);
+    if (dims->seq_q == 0 && dims->seq_k == 0) return MSPARSE_OK;
+    AttnArgs a{};
+    fill_attn(dims, index, &a);
+    Carve c{static_cast<char*>(ws)};
+    a.delta = c.take<float>(size_t(dims->batch) * dims->heads_q * dims->seq_q);
+    a.dk_col = c.take<float>(size_t(index->vcol_cap) * dims->head_dim);
+    a.dv_col = c.take<float>(size_t(index->vcol_cap) * dims->head_dim);
+    a.q = static_cast<const uint16_t*>(q);
+    a.k = static_cast<const uint16_t*>(k);
+    a.v = static_cast<const uint16_t*>(v);
+    a.o = static_cast<const uint16_t*>(out);
+    a.dout = static_cast<const uint16_t*>(dout);
+    a.lse = const_cast<float*>(lse);
+    a.dq = dq;
+    a.dk = dk;
+    a.dv = dv;
+    a.dq_accumulate = dq_accumulate;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    return check_hip(launch_attn_bwd(a, s), s, "attn bwd");
+}
+
+// ------------------------------------------------------------------ estimation
+size_t msparse_estimate_workspace(const msparse_dims* dims, int32_t last_q, int32_t k_v, int32_t k_s) {
+    (void)k_v;
+    (void)k_s;
+    if (check_dims(dims, true) || last_q < 1) return 0;
+    const size_t scores = align_up(size_t(dims->batch) * dims->heads_q * dims->seq_q * sizeof(float));
+    return 2 * scores + est_workspace_bytes(dims->batch, dims->heads_q, dims->seq_q, last_q);
+}
+
+msparse_status msparse_estimate(const msparse_dims* dims, const void* q, const void* k, int32_t last_q, int32_t k_v,
+                                int32_t k_s, int32_t* v_idx, int32_t* s_idx, float* v_score, float* s_score, void* ws,
+                                size_t ws_bytes, void* stream) {
+    msparse_status st = check_dims(dims, true);
+    if (st) return st;
+    const int32_t N = dims->seq_q;
+    if (!q || !k || !v_idx || !s_idx) return fail(MSPARSE_ERR_INVALID, "tensor pointer is NULL");
+    if (N < 1) return fail(MSPARSE_ERR_INVALID, "empty sequence");
+    if (last_q < 1 || last_q > N) return fail(MSPARSE_ERR_INVALID, "last_q %d outside [1, %d]", last_q, N);
+    if (last_q > kBlock) return fail(MSPARSE_ERR_UNSUPPORTED, "last_q %d > 64", last_q);
+    if (k_v < 1 || k_v > N || k_s < 1 || k_s > N)
+        return fail(MSPARSE_ERR_INVALID, "budgets k_v=%d k_s=%d outside [1, %d]", k_v, k_s, N);
+    const size_t need = msparse_estimate_workspace(dims, last_q, k_v, k_s);
+    if (!ws || ws_bytes < need) return fail(MSPARSE_ERR_WORKSPACE, "estimate workspace %zu < %zu", ws_bytes, need);
+    EstArgs a{};
+    a.q = static_cast<const uint16_t*>(q);
+    a.k = static_cast<const uint16_t*>(k);
+    a.B = dims->batch;
+    a.Hq = dims->heads_q;
+    a.Hkv = dims->heads_kv;
+    a.N = N;
+    a.d = dims->head_dim;
+    a.L = last_q;
+    a.k_v = k_v;
+    a.k_s = k_s;
+    a.scale = resolve_scale(dims);
+    a.v_idx = v_idx;
+    a.s_idx = s_idx;
+    char* base = static_cast<char*>(ws);
+    const size_t scores = align_up(size_t(dims->batch) * dims->heads_q * N * sizeof(float));
+    a.v_score = v_score ? v_score : reinterpret_cast<float*>(base);
+    a.s_score = s_score ? s_score : reinterpret_cast<float*>(base + scores);
+    Carve c{base + 2 * scores};
+    const int64_t BH = int64_t(a.B) * a.Hq;
+    a.nchunk = (N + 1023) / 1024;
+    a.part_max = c.take<float>(size_t(BH) * a.nchunk * kBlock);
+    a.part_sum = c.take<float>(size_t(BH) * a.nchunk * kBlock);
+    a.row_lse = c.take<float>(size_t(BH) * kBlock);
+    a.diag_part = c.take<float>(size_t(BH) * (N / kBlock) * 2 * kBlock);
+    a.topk_state = c.take<uint32_t>(size_t(2 * BH) * 8);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    return check_hip(launch_estimate(a, s), s, "estimate");
+}
+
+}  // extern "C"

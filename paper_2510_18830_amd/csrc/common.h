@@ -1,0 +1,88 @@
+// Shared device helpers for the gfx950 kernels: bf16 packing, MFMA wrappers,
+// wavefront reductions, ring-layout block maps and the launch-error plumbing.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/msparse.h"
+
+namespace msparse {
+
+constexpr int kBlock = 64;   // token block edge (Section 4.1 (ii))
+constexpr int kWave = 64;    // CDNA wavefront width
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(16))) float f32x16;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
+typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
+
+// ---------------------------------------------------------------- bf16 <-> fp32
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float(uint32_t(h) << 16); }
+
+// fp32 -> bf16 bits, round to nearest even (inputs here are finite or +-inf).
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+    uint32_t u = __float_as_uint(f);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return u >> 16;
+}
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
+}
+
+// ---------------------------------------------------------------- MFMA
+// D(32x32) += A(32x16) * B(16x32), bf16 inputs, fp32 accumulate.
+// Lane l supplies A[l%32][8*(l/32) .. +8] and B[8*(l/32) .. +8][l%32];
+// accumulator element r of lane l is D[8*(r/4) + 4*(l/32) + r%4][l%32].
+__device__ __forceinline__ f32x16 mfma32(const u32x4& a, const u32x4& b, const f32x16& c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
+                                                  0, 0, 0);
+}
+
+// ---------------------------------------------------------------- math
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+    return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+    return v;
+}
+
+// ---------------------------------------------------------------- ring layout
+// Global 64-token blocks are dealt to `world` workers (Section 4.2).
+struct Layout {
+    int32_t world, nb, layout;  // nb = global block count
+
+    __host__ __device__ int32_t owner(int32_t g) const {
+        if (world == 1) return 0;
+        if (layout == MSPARSE_LAYOUT_STRIPED) return g % world;
+        int32_t c = g / (nb / (2 * world));
+        return c < world ? c : 2 * world - 1 - c;
+    }
+    // local block number of global block g inside its owner
+    __host__ __device__ int32_t local(int32_t g) const {
+        if (world == 1) return g;
+        if (layout == MSPARSE_LAYOUT_STRIPED) return g / world;
+        int32_t chunk = nb / (2 * world);
+        int32_t c = g / chunk;
+        return c < world ? g - c * chunk : chunk + (g - c * chunk);
+    }
+    // global block number of local block l of worker w
+    __host__ __device__ int32_t global(int32_t w, int32_t l) const {
+        if (world == 1) return l;
+        if (layout == MSPARSE_LAYOUT_STRIPED) return l * world + w;
+        int32_t chunk = nb / (2 * world);
+        return l < chunk ? w * chunk + l : (2 * world - 1 - w) * chunk + (l - chunk);
+    }
+};
+
+}  // namespace msparse

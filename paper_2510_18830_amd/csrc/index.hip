@@ -1,0 +1,339 @@
+// Sparse index construction on the GPU (Section 4.1 (ii); convert_index of
+// Algorithms 1 and 2).
+//
+// Each selected slash offset delta is executed as the 64 x 64 block-diagonals
+// floor(delta/64) and ceil(delta/64) (the set D); query block i gets the key
+// blocks i - x (x in D, x <= i) and the verticals v <= 64 i + 63 that lie in a
+// block-diagonal outside D.  A ring step keeps only the keys of its KV shard,
+// in that shard's local numbering.
+//
+// Four launches, all deterministic (no atomics decide an output position):
+//   prep  one workgroup per head: vertical bitmap -> unique ascending list,
+//         slash offsets -> D bitset -> ascending list, shard vertical counts;
+//   count one wavefront per (head, query block) and per (head, key block);
+//   scan  exclusive prefix sums of the counts (one workgroup per array);
+//   fill  the count pass again, writing entries in order via wave ballots.
+#include "common.h"
+#include "kernels.h"
+
+namespace msparse {
+
+namespace {
+
+constexpr int kPrepThreads = 1024;
+constexpr int kItemWaves = 4;  // wavefronts per workgroup in count / fill
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
+
+__device__ __forceinline__ uint64_t lanes_below() { return (1ull << lane_id()) - 1ull; }
+
+// Exclusive prefix sum over a 1024-thread workgroup.  `tmp` holds 16 ints.
+__device__ int block_exclusive_scan(int v, int* tmp, int* total) {
+    const int lane = lane_id(), wid = threadIdx.x >> 6;
+    int x = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        int y = __shfl_up(x, o);
+        if (lane >= o) x += y;
+    }
+    if (lane == 63) tmp[wid] = x;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int run = 0;
+        for (int w = 0; w < kPrepThreads / 64; ++w) {
+            int t = tmp[w];
+            tmp[w] = run;
+            run += t;
+        }
+        tmp[16] = run;
+    }
+    __syncthreads();
+    int res = tmp[wid] + x - v;
+    *total = tmp[16];
+    __syncthreads();
+    return res;
+}
+
+__global__ void __launch_bounds__(kPrepThreads) index_prep_kernel(IndexArgs a) {
+    __shared__ int tmp[17];
+    extern __shared__ uint32_t dsh[];  // D bitset, dwords words
+    const int bh = blockIdx.x;
+    const int tid = threadIdx.x;
+    const Layout L{a.world, a.nb, a.layout};
+    const int64_t Ng = int64_t(a.nb) * kBlock;
+
+    // ---- verticals: bitmap (dedupes and sorts), then ordered compaction
+    uint32_t* vb = a.vbits + int64_t(bh) * a.vwords;
+    for (int w = tid; w < a.vwords; w += kPrepThreads) vb[w] = 0u;
+    for (int w = tid; w < a.dwords; w += kPrepThreads) dsh[w] = 0u;
+    __threadfence();
+    __syncthreads();
+    const int32_t* vi = a.v_idx + int64_t(bh) * a.k_v;
+    for (int j = tid; j < a.k_v; j += kPrepThreads) {
+        int32_t v = vi[j];
+        if (v >= 0 && v < Ng) atomicOr(&vb[v >> 5], 1u << (v & 31));
+    }
+    const int32_t* si = a.s_idx + int64_t(bh) * a.k_s;
+    for (int j = tid; j < a.k_s; j += kPrepThreads) {
+        int32_t dl = si[j];
+        if (dl < 0 || dl >= Ng) continue;
+        int32_t lo = dl / kBlock, hi = (dl + kBlock - 1) / kBlock;
+        atomicOr(&dsh[lo >> 5], 1u << (lo & 31));
+        if (hi < a.nb) atomicOr(&dsh[hi >> 5], 1u << (hi & 31));
+    }
+    __threadfence();
+    __syncthreads();
+
+    // each thread owns a contiguous run of bitmap words
+    {
+        const int per = (a.vwords + kPrepThreads - 1) / kPrepThreads;
+        const int w0 = tid * per, w1 = min(a.vwords, w0 + per);
+        int cnt = 0, own = 0;
+        for (int w = w0; w < w1; ++w) {
+            uint32_t bits = __atomic_load_n(&vb[w], __ATOMIC_RELAXED);
+            cnt += __popc(bits);
+            for (uint32_t b = bits; b; b &= b - 1) {
+                int32_t v = (w << 5) + __ffs(b) - 1;
+                own += (L.owner(v / kBlock) == a.shard);
+            }
+        }
+        int total = 0;
+        int pos = block_exclusive_scan(cnt, tmp, &total);
+        int32_t* out = a.vlist + int64_t(bh) * a.k_v;
+        for (int w = w0; w < w1; ++w) {
+            uint32_t bits = __atomic_load_n(&vb[w], __ATOMIC_RELAXED);
+            for (uint32_t b = bits; b; b &= b - 1) out[pos++] = (w << 5) + __ffs(b) - 1;
+        }
+        int owned = 0;
+        block_exclusive_scan(own, tmp, &owned);
+        if (tid == 0) {
+            a.vcnt[bh] = total;
+            a.cnt_vcol[bh] = owned;
+        }
+    }
+    // ---- block-diagonals: bitset copy and ascending list
+    {
+        uint32_t* db = a.dbits + int64_t(bh) * a.dwords;
+        for (int w = tid; w < a.dwords; w += kPrepThreads) {
+            db[w] = dsh[w];
+            if (a.diag_bits_out) a.diag_bits_out[int64_t(bh) * a.dwords + w] = dsh[w];
+        }
+        const int per = (a.dwords + kPrepThreads - 1) / kPrepThreads;
+        const int w0 = tid * per, w1 = min(a.dwords, w0 + per);
+        int cnt = 0;
+        for (int w = w0; w < w1; ++w) cnt += __popc(dsh[w]);
+        int total = 0;
+        int pos = block_exclusive_scan(cnt, tmp, &total);
+        int32_t* out = a.dlist + int64_t(bh) * a.nb;
+        for (int w = w0; w < w1; ++w)
+            for (uint32_t b = dsh[w]; b; b &= b - 1) out[pos++] = (w << 5) + __ffs(b) - 1;
+        if (tid == 0) a.dcnt[bh] = total;
+    }
+    if (bh == 0) {
+        if (a.q_blk_global)
+            for (int l = tid; l < a.nqb; l += kPrepThreads) a.q_blk_global[l] = L.global(a.rank, l);
+        if (a.k_blk_global)
+            for (int l = tid; l < a.nkb; l += kPrepThreads) a.k_blk_global[l] = L.global(a.shard, l);
+    }
+}
+
+__device__ __forceinline__ bool dbit(const uint32_t* db, int32_t x) { return (db[x >> 5] >> (x & 31)) & 1u; }
+
+// One wavefront walks the lists of one item.  FILL = false counts, FILL = true
+// writes the entries at the scanned offsets.
+template <bool FILL>
+__global__ void __launch_bounds__(64 * kItemWaves) index_items_kernel(IndexArgs a) {
+    const int64_t item = int64_t(blockIdx.x) * kItemWaves + (threadIdx.x >> 6);
+    const int lane = lane_id();
+    const Layout L{a.world, a.nb, a.layout};
+    const int64_t nq_items = int64_t(a.BH) * a.nqb;
+    const int64_t nk_items = int64_t(a.BH) * a.nkb;
+
+    if (item < nq_items) {
+        const int bh = int(item / a.nqb);
+        const int lq = int(item % a.nqb);
+        const int32_t qg = L.global(a.rank, lq);
+        const int32_t* dl = a.dlist + int64_t(bh) * a.nb;
+        const int dc = a.dcnt[bh];
+        const uint32_t* db = a.dbits + int64_t(bh) * a.dwords;
+        // ---- key blocks qg - x, x in D, ascending key block = descending x
+        int64_t base = FILL ? a.blk_ptr[item] : 0;
+        bool ok = true;
+        if (FILL) {
+            if (a.blk_ptr[item + 1] > a.blk_cap) {
+                ok = false;
+                if (lane == 0 && a.overflow) atomicOr(a.overflow, 1);
+            }
+        }
+        int64_t n = 0;
+        for (int c0 = 0; c0 < dc; c0 += 64) {
+            const int j = dc - 1 - (c0 + lane);
+            bool pred = false;
+            int32_t kg = 0;
+            if (j >= 0) {
+                const int32_t x = dl[j];
+                kg = qg - x;
+                pred = (x <= qg) && (L.owner(kg) == a.shard);
+            }
+            const uint64_t m = __ballot(pred);
+            if (FILL && ok && pred) a.blk_idx[base + n + __popcll(m & lanes_below())] = L.local(kg);
+            n += __popcll(m);
+        }
+        if (!FILL && lane == 0) a.cnt_blk[item] = n;
+        // ---- columns: verticals v <= 64 qg + 63 outside the selected diagonals
+        const int32_t* vl = a.vlist + int64_t(bh) * a.k_v;
+        const int vc = a.vcnt[bh];
+        const int32_t limit = qg * kBlock + kBlock - 1;
+        base = FILL ? a.col_ptr[item] : 0;
+        ok = true;
+        if (FILL) {
+            if (a.col_ptr[item + 1] > a.col_cap) {
+                ok = false;
+                if (lane == 0 && a.overflow) atomicOr(a.overflow, 1);
+            }
+        }
+        n = 0;
+        for (int c0 = 0; c0 < vc; c0 += 64) {
+            if (vl[c0] > limit) break;  // list is ascending
+            const int j = c0 + lane;
+            bool pred = false;
+            int32_t v = 0;
+            if (j < vc) {
+                v = vl[j];
+                const int32_t vb = v / kBlock;
+                pred = (v <= limit) && !dbit(db, qg - vb) && (L.owner(vb) == a.shard);
+            }
+            const uint64_t m = __ballot(pred);
+            if (FILL && ok && pred)
+                a.col_idx[base + n + __popcll(m & lanes_below())] = L.local(v / kBlock) * kBlock + v % kBlock;
+            n += __popcll(m);
+        }
+        if (!FILL && lane == 0) a.cnt_col[item] = n;
+        return;
+    }
+    if (item < nq_items + nk_items) {
+        // ---- transposed block lists: query blocks kg + x, x in D, ascending
+        const int64_t it = item - nq_items;
+        const int bh = int(it / a.nkb);
+        const int lk = int(it % a.nkb);
+        const int32_t kg = L.global(a.shard, lk);
+        const int32_t* dl = a.dlist + int64_t(bh) * a.nb;
+        const int dc = a.dcnt[bh];
+        int64_t base = FILL ? a.kblk_ptr[it] : 0;
+        bool ok = true;
+        if (FILL && a.kblk_ptr[it + 1] > a.blk_cap) {
+            ok = false;
+            if (lane == 0 && a.overflow) atomicOr(a.overflow, 1);
+        }
+        int64_t n = 0;
+        for (int c0 = 0; c0 < dc; c0 += 64) {
+            const int j = c0 + lane;
+            bool pred = false;
+            int32_t qg = 0;
+            if (j < dc) {
+                qg = kg + dl[j];
+                pred = (qg < a.nb) && (L.owner(qg) == a.rank);
+            }
+            const uint64_t m = __ballot(pred);
+            if (FILL && ok && pred) a.kblk_idx[base + n + __popcll(m & lanes_below())] = L.local(qg);
+            n += __popcll(m);
+        }
+        if (!FILL && lane == 0) a.cnt_kblk[it] = n;
+        return;
+    }
+    if (FILL && item < nq_items + nk_items + a.BH) {
+        // ---- this shard's verticals in local coordinates
+        const int bh = int(item - nq_items - nk_items);
+        const int32_t* vl = a.vlist + int64_t(bh) * a.k_v;
+        const int vc = a.vcnt[bh];
+        const int64_t base = a.vcol_ptr[bh];
+        if (a.vcol_ptr[bh + 1] > a.vcol_cap) {
+            if (lane == 0 && a.overflow) atomicOr(a.overflow, 1);
+            return;
+        }
+        int64_t n = 0;
+        for (int c0 = 0; c0 < vc; c0 += 64) {
+            const int j = c0 + lane;
+            bool pred = false;
+            int32_t v = 0;
+            if (j < vc) {
+                v = vl[j];
+                pred = L.owner(v / kBlock) == a.shard;
+            }
+            const uint64_t m = __ballot(pred);
+            if (pred) a.vcol_idx[base + n + __popcll(m & lanes_below())] = L.local(v / kBlock) * kBlock + v % kBlock;
+            n += __popcll(m);
+        }
+    }
+}
+
+// dst[0] = 0, dst[i + 1] = cnt[0] + ... + cnt[i]; one workgroup per array.
+__global__ void __launch_bounds__(1024) index_scan_kernel(IndexArgs a) {
+    __shared__ int64_t tmp[17];
+    const int64_t* cnt;
+    int64_t* dst;
+    int64_t n;
+    switch (blockIdx.x) {
+        case 0: cnt = a.cnt_blk; dst = a.blk_ptr; n = int64_t(a.BH) * a.nqb; break;
+        case 1: cnt = a.cnt_col; dst = a.col_ptr; n = int64_t(a.BH) * a.nqb; break;
+        case 2: cnt = a.cnt_kblk; dst = a.kblk_ptr; n = int64_t(a.BH) * a.nkb; break;
+        default: cnt = a.cnt_vcol; dst = a.vcol_ptr; n = a.BH; break;
+    }
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    const int64_t per = (n + 1023) / 1024;
+    const int64_t i0 = tid * per, i1 = min(n, i0 + per);
+    int64_t s = 0;
+    for (int64_t i = i0; i < i1; ++i) s += cnt[i];
+    int64_t x = s;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        int64_t y = __shfl_up(x, o);
+        if (lane >= o) x += y;
+    }
+    if (lane == 63) tmp[wid] = x;
+    __syncthreads();
+    if (tid == 0) {
+        int64_t run = 0;
+        for (int w = 0; w < 16; ++w) {
+            int64_t t = tmp[w];
+            tmp[w] = run;
+            run += t;
+        }
+    }
+    __syncthreads();
+    int64_t run = tmp[wid] + x - s;
+    if (tid == 0) dst[0] = 0;
+    for (int64_t i = i0; i < i1; ++i) {
+        run += cnt[i];
+        dst[i + 1] = run;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_index_prep(const IndexArgs& a, hipStream_t s) {
+    const size_t shmem = size_t(a.dwords) * sizeof(uint32_t);
+    hipLaunchKernelGGL(index_prep_kernel, dim3(a.BH), dim3(kPrepThreads), shmem, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_index_count(const IndexArgs& a, hipStream_t s) {
+    const int64_t items = int64_t(a.BH) * (a.nqb + a.nkb);
+    const int64_t grid = (items + kItemWaves - 1) / kItemWaves;
+    hipLaunchKernelGGL(index_items_kernel<false>, dim3(unsigned(grid)), dim3(64 * kItemWaves), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_index_scan(const IndexArgs& a, hipStream_t s) {
+    hipLaunchKernelGGL(index_scan_kernel, dim3(4), dim3(1024), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_index_fill(const IndexArgs& a, hipStream_t s) {
+    const int64_t items = int64_t(a.BH) * (a.nqb + a.nkb) + a.BH;
+    const int64_t grid = (items + kItemWaves - 1) / kItemWaves;
+    hipLaunchKernelGGL(index_items_kernel<true>, dim3(unsigned(grid)), dim3(64 * kItemWaves), 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace msparse

@@ -1,0 +1,123 @@
+// Host-side launchers of the gfx950 kernels (internal to libmsparse).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/msparse.h"
+
+namespace msparse {
+
+// ---------------------------------------------------------------- index build
+struct IndexArgs {
+    const int32_t* v_idx;  // [BH, k_v] global token positions
+    const int32_t* s_idx;  // [BH, k_s] global slash offsets
+    int32_t BH, k_v, k_s;
+    int32_t nqb, nkb;      // local query / key blocks
+    int32_t nb;            // global blocks
+    int32_t world, rank, shard, layout;
+    // workspace carve-up
+    uint32_t* vbits;       // [BH, vwords]
+    int32_t vwords;
+    int32_t* vlist;        // [BH, k_v] unique ascending verticals
+    int32_t* vcnt;         // [BH]
+    int32_t* dlist;        // [BH, nb] ascending block-diagonals
+    int32_t* dcnt;         // [BH]
+    uint32_t* dbits;       // [BH, dwords]
+    int32_t dwords;
+    int64_t* cnt_blk;      // [BH*nqb]
+    int64_t* cnt_col;      // [BH*nqb]
+    int64_t* cnt_kblk;     // [BH*nkb]
+    int64_t* cnt_vcol;     // [BH]
+    // scanned offsets (n + 1 entries each)
+    int64_t* blk_ptr;
+    int64_t* col_ptr;
+    int64_t* kblk_ptr;
+    int64_t* vcol_ptr;
+    // outputs (fill only)
+    int32_t* blk_idx;
+    int64_t blk_cap;
+    int32_t* col_idx;
+    int64_t col_cap;
+    int32_t* kblk_idx;
+    int32_t* vcol_idx;
+    int64_t vcol_cap;
+    uint32_t* diag_bits_out;
+    int32_t* q_blk_global;
+    int32_t* k_blk_global;
+    int32_t* overflow;
+};
+hipError_t launch_index_prep(const IndexArgs& a, hipStream_t s);
+hipError_t launch_index_count(const IndexArgs& a, hipStream_t s);
+hipError_t launch_index_scan(const IndexArgs& a, hipStream_t s);
+hipError_t launch_index_fill(const IndexArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------- attention
+struct AttnArgs {
+    const uint16_t* q;     // bf16 [B,Hq,Nq,d]
+    const uint16_t* k;     // bf16 [B,Hkv,Nk,d]
+    const uint16_t* v;
+    const uint16_t* o;     // forward output (bwd)
+    const uint16_t* dout;  // bf16 [B,Hq,Nq,d] (bwd)
+    uint16_t* out;         // bf16 [B,Hq,Nq,d] (fwd)
+    float* lse;            // fwd output / bwd input
+    float* delta;          // bwd workspace [B,Hq,Nq]
+    float* dq;
+    float* dk;
+    float* dv;
+    float* dk_col;         // bwd workspace [vcol_cap, d]
+    float* dv_col;
+    int32_t dq_accumulate;
+    int32_t B, Hq, Hkv, Nq, Nk, d;
+    int32_t nqb, nkb;
+    float scale;
+    const int64_t* blk_ptr;
+    const int32_t* blk_idx;
+    const int64_t* col_ptr;
+    const int32_t* col_idx;
+    const int64_t* kblk_ptr;
+    const int32_t* kblk_idx;
+    const int64_t* vcol_ptr;
+    const int32_t* vcol_idx;
+    const uint32_t* diag_bits;
+    int32_t dwords;
+    const int32_t* q_blk_global;
+    const int32_t* k_blk_global;
+};
+hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t s);
+hipError_t launch_attn_bwd(const AttnArgs& a, hipStream_t s);
+
+struct MergeArgs {
+    const uint16_t* o_part;
+    const float* lse_part;
+    float* o_acc;
+    float* lse_acc;
+    uint16_t* out;
+    int32_t first;
+    int64_t rows;  // B*Hq*Nq
+    int32_t d;
+};
+hipError_t launch_merge(const MergeArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------- estimation
+struct EstArgs {
+    const uint16_t* q;  // bf16 [B,Hq,N,d]
+    const uint16_t* k;  // bf16 [B,Hkv,N,d]
+    int32_t B, Hq, Hkv, N, d, L, k_v, k_s;
+    float scale;
+    float* v_score;     // [B*Hq, N]
+    float* s_score;     // [B*Hq, N]
+    int32_t* v_idx;
+    int32_t* s_idx;
+    // workspace
+    float* part_max;    // [B*Hq, nchunk, L]
+    float* part_sum;    // [B*Hq, nchunk, L]
+    float* row_lse;     // [B*Hq, L] (log2 domain)
+    float* diag_part;   // [B*Hq, nkb, 128]
+    int32_t nchunk;
+    uint32_t* topk_state;  // [2*B*Hq, 4]
+};
+size_t est_workspace_bytes(int32_t B, int32_t Hq, int32_t N, int32_t L);
+hipError_t launch_estimate(const EstArgs& a, hipStream_t s);
+
+}  // namespace msparse

@@ -1,0 +1,95 @@
+"""Shared test plumbing: seeded inputs, oracle runs and GPU index extraction.
+
+Inputs come only from synth/ (seeded generator); expected values only from
+oracle/.  Tolerances follow the parity rules for this path: out / dQ / dK / dV
+max-abs <= 2e-2 and mean-abs <= 2e-3 (bf16 inputs, fp32 accumulation); lse
+max-abs <= 1e-3; index arrays bit-exact; estimated index sets equal except for
+entries whose fp64 score lies within 1e-4 relative of the k-th score.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+import torch
+
+from oracle import bf16 as OB
+from oracle import estimate as OE
+from oracle import index as OI
+from synth import make_inputs, bf16_bits
+
+MAX_ABS = 2e-2
+MEAN_ABS = 2e-3
+LSE_ABS = 1e-3
+TOPK_REL = 1e-4
+
+
+def to_f64(t: torch.Tensor) -> np.ndarray:
+    return OB.to_f64(bf16_bits(t))
+
+
+def inputs_f64(x: dict, names=("q", "k", "v", "do")) -> dict:
+    return {n: to_f64(x[n]) for n in names if x.get(n) is not None}
+
+
+def oracle_indices(f64: dict, wl, heads=None):
+    """Reference (v_idx, s_idx, v_score, s_score) for every head (or the given heads)."""
+    q, k = f64["q"], f64["k"]
+    if heads is not None:
+        G = q.shape[1] // k.shape[1]
+        out = [OE.estimate(q[:, [h]], k[:, [h // G]], wl.last_q, wl.k_v, wl.k_s, 1 / math.sqrt(wl.head_dim))
+               for h in heads]
+        return tuple(np.concatenate([o[i] for o in out], axis=1) for i in range(4))
+    return OE.estimate(q, k, wl.last_q, wl.k_v, wl.k_s, 1 / math.sqrt(wl.head_dim))
+
+
+def gpu_csr(idx) -> dict:
+    """Copy a GPU SparseIndex to host arrays trimmed to their used lengths."""
+    t = {k: v.cpu().numpy() for k, v in idx.tensors.items()}
+    nb = int(t["blk_ptr"][-1])
+    nc = int(t["col_ptr"][-1])
+    nv = int(t["vcol_ptr"][-1])
+    return dict(blk_ptr=t["blk_ptr"], blk_idx=t["blk_idx"][:nb], col_ptr=t["col_ptr"], col_idx=t["col_idx"][:nc],
+                kblk_ptr=t["kblk_ptr"], kblk_idx=t["kblk_idx"][:nb], vcol_ptr=t["vcol_ptr"],
+                vcol_idx=t["vcol_idx"][:nv], diag_bits=t["diag_bits"].view(np.uint32),
+                q_blk_global=t["q_blk_global"], k_blk_global=t["k_blk_global"])
+
+
+def head_csr(c: dict, bh: int, nqb: int, nkb: int) -> dict:
+    """Per-head slices of a CSR dict (offsets rebased to 0)."""
+    def seg(ptr, idx, n):
+        p = ptr[bh * n: bh * n + n + 1]
+        return p - p[0], idx[p[0]:p[-1]]
+    bp, bi = seg(c["blk_ptr"], c["blk_idx"], nqb)
+    cp, ci = seg(c["col_ptr"], c["col_idx"], nqb)
+    kp, ki = seg(c["kblk_ptr"], c["kblk_idx"], nkb)
+    vp, vi = seg(c["vcol_ptr"], c["vcol_idx"], 1)
+    return dict(blk_ptr=bp, blk_idx=bi, col_ptr=cp, col_idx=ci, kblk_ptr=kp, kblk_idx=ki, vcol_ptr=vp, vcol_idx=vi)
+
+
+def assert_close(name, got, ref, max_abs=MAX_ABS, mean_abs=MEAN_ABS):
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    assert got.shape == ref.shape, (name, got.shape, ref.shape)
+    err = np.abs(got - ref)
+    assert np.isfinite(err).all(), f"{name}: non-finite difference"
+    assert err.max() <= max_abs and err.mean() <= mean_abs, \
+        f"{name}: max-abs {err.max():.3e} mean-abs {err.mean():.3e}"
+
+
+def assert_lse_close(got, ref, tol=LSE_ABS):
+    got = np.asarray(got, dtype=np.float64)
+    inf_r = np.isneginf(ref)
+    assert (np.isneginf(got) == inf_r).all(), "lse -inf pattern differs"
+    err = np.abs(got[~inf_r] - ref[~inf_r])
+    assert err.size == 0 or err.max() <= tol, f"lse max-abs {err.max():.3e}"
+
+
+def assert_topk_match(got, ref, score, k, rel=TOPK_REL):
+    """Sets equal except entries within `rel` of the oracle's k-th score."""
+    order = np.sort(score)[::-1]
+    t_k = order[k - 1]
+    diff = np.setxor1d(np.asarray(got), np.asarray(ref))
+    bad = diff[np.abs(score[diff] - t_k) > rel * abs(t_k)]
+    assert bad.size == 0, f"{bad.size} index differences outside the tie band (t_k={t_k:.6e})"
+    assert len(np.unique(got)) == k and np.all(np.diff(got) > 0)

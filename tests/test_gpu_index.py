@@ -1,0 +1,82 @@
+"""GPU index build vs the oracle's index: bit-exact, whole sequence and ring steps."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2510_18830_amd as ms
+from oracle import index as OI
+from tests.helpers import gpu_csr
+
+pytestmark = pytest.mark.gpu
+
+
+def _indices(rng, B, Hq, Ng, k_v, k_s, contiguous=True):
+    v = rng.integers(0, Ng, (B, Hq, k_v))
+    v[..., :3] = v[..., 3:6]                      # duplicates count once
+    s = rng.integers(0, Ng, (B, Hq, k_s))
+    if contiguous:                                # a band from the diagonal plus scattered slashes
+        n = k_s // 2
+        s[..., :n] = np.arange(n)
+    return v.astype(np.int32), s.astype(np.int32)
+
+
+def _compare(got, ref):
+    for key, r in ref.items():
+        g = got[key]
+        assert g.shape == r.shape and np.array_equal(g.astype(np.int64), r.astype(np.int64)), key
+
+
+CASES = [
+    # B, Hq, Hkv, N_global, k_v, k_s, world, rank, step, layout
+    (1, 1, 1, 4096, 128, 256, 1, 0, 0, "striped"),
+    (2, 4, 2, 8192, 300, 700, 1, 0, 0, "striped"),
+    (1, 3, 1, 8192, 97, 1000, 4, 0, 0, "striped"),
+    (1, 3, 1, 8192, 97, 1000, 4, 2, 1, "striped"),
+    (1, 2, 2, 16384, 200, 1500, 8, 0, 5, "striped"),
+    (1, 3, 1, 8192, 97, 1000, 4, 0, 2, "zigzag"),
+    (1, 2, 1, 16384, 200, 1500, 8, 3, 6, "zigzag"),
+]
+
+
+@pytest.mark.parametrize("case", CASES)
+def test_index_bit_exact(gpu, case):
+    B, Hq, Hkv, Ng, k_v, k_s, W, r, t, layout = case
+    rng = np.random.default_rng(Ng + 31 * W + 7 * r + t)
+    v, s = _indices(rng, B, Hq, Ng, k_v, k_s)
+    print(f"case {case}", flush=True)
+    ref = OI.Index(v, s, Ng, world=W, rank=r, step=t, layout=layout).csr()
+    dims = ms.make_dims(B, Ng // W, Hq, Hkv, 128)
+    ring = ms.make_ring(W, r, t, layout)
+    idx = ms.make_index(dims, torch.from_numpy(v).to(gpu), torch.from_numpy(s).to(gpu), ring)
+    torch.cuda.synchronize()
+    _compare(gpu_csr(idx), ref)
+    assert int(idx["overflow"].item()) == 0
+
+
+def test_index_deterministic_and_count(gpu):
+    rng = np.random.default_rng(5)
+    v, s = _indices(rng, 1, 4, 32768, 1000, 6096)
+    dims = ms.make_dims(1, 32768, 4, 2, 128)
+    tv, ts = torch.from_numpy(v).to(gpu), torch.from_numpy(s).to(gpu)
+    a = gpu_csr(ms.make_index(dims, tv, ts))
+    b = gpu_csr(ms.make_index(dims, tv, ts))
+    for key in a:
+        assert np.array_equal(a[key], b[key]), key
+    blk, col, vcol = ms.index_count(dims, tv, ts)
+    assert blk == a["blk_idx"].size and col == a["col_idx"].size and vcol == a["vcol_idx"].size
+
+
+def test_index_overflow_flag(gpu):
+    rng = np.random.default_rng(6)
+    v, s = _indices(rng, 1, 2, 4096, 128, 256)
+    dims = ms.make_dims(1, 4096, 2, 1, 64)
+    tv, ts = torch.from_numpy(v).to(gpu), torch.from_numpy(s).to(gpu)
+    blk, col, vcol = ms.index_count(dims, tv, ts)
+    small = ms.alloc_index(dims, blk // 2, col // 2, vcol, gpu)
+    ms.build_index(dims, tv, ts, small)
+    torch.cuda.synchronize()
+    assert int(small["overflow"].item()) == 1
+    ok = ms.alloc_index(dims, blk, col, vcol, gpu)
+    ms.build_index(dims, tv, ts, ok)
+    torch.cuda.synchronize()
+    assert int(ok["overflow"].item()) == 0

@@ -1,0 +1,86 @@
+"""Host-side checks of the C ABI: the library loads, exports every declared
+symbol, and rejects bad arguments before touching the GPU."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2510_18830_amd as ms
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "msparse.h")
+
+
+def declared():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(msparse_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol():
+    so = ms.lib()
+    names = declared()
+    assert len(names) >= 11
+    for n in names:
+        assert hasattr(so, n), n
+
+
+def test_strerror():
+    L = ms.lib()
+    assert L.msparse_strerror(0) == b"ok"
+    assert L.msparse_strerror(-3) == b"index capacity too small"
+
+
+def _bad(status_expected, fn, *args):
+    st = fn(*args)
+    assert st == status_expected, (st, ms.lib().msparse_last_error())
+
+
+def test_validation_before_launch():
+    L = ms.lib()
+    d = ms.make_dims(1, 4096, 4, 2, 128)
+    fake = ctypes.c_void_p(16)   # never dereferenced: validation fails first
+    iv = ctypes.c_void_p(32)
+    # bad head_dim / block / causal / N % 64 / GQA
+    for field, val, st in (("head_dim", 96, -2), ("block", 128, -2), ("causal", 0, -2), ("seq_q", 4000, -2),
+                           ("heads_kv", 3, -1)):
+        dd = ms.make_dims(1, 4096, 4, 2, 128)
+        setattr(dd, field, val)
+        if field == "seq_q":
+            dd.seq_k = val
+        _bad(st, L.msparse_estimate, ctypes.byref(dd), fake, fake, 64, 10, 10, iv, iv, None, None, fake, 1 << 30,
+             None)
+    # budgets and last_q
+    _bad(-1, L.msparse_estimate, ctypes.byref(d), fake, fake, 0, 10, 10, iv, iv, None, None, fake, 1 << 30, None)
+    _bad(-1, L.msparse_estimate, ctypes.byref(d), fake, fake, 64, 0, 10, iv, iv, None, None, fake, 1 << 30, None)
+    _bad(-1, L.msparse_estimate, ctypes.byref(d), fake, fake, 64, 10, 4097, iv, iv, None, None, fake, 1 << 30, None)
+    _bad(-2, L.msparse_estimate, ctypes.byref(d), fake, fake, 65, 10, 10, iv, iv, None, None, fake, 1 << 30, None)
+    _bad(-1, L.msparse_estimate, ctypes.byref(d), None, fake, 64, 10, 10, iv, iv, None, None, fake, 1 << 30, None)
+    # workspace too small
+    _bad(-4, L.msparse_estimate, ctypes.byref(d), fake, fake, 64, 10, 10, iv, iv, None, None, fake, 8, None)
+    # ring descriptors
+    r = ms.Ring(4, 4, 0, 0)
+    _bad(-1, L.msparse_index_count, ctypes.byref(d), iv, 10, iv, 10, ctypes.byref(r), ctypes.byref(ctypes.c_int64()),
+         ctypes.byref(ctypes.c_int64()), ctypes.byref(ctypes.c_int64()), fake, 1 << 30, None)
+    r = ms.Ring(4, 1, 0, 7)
+    _bad(-1, L.msparse_index_count, ctypes.byref(d), iv, 10, iv, 10, ctypes.byref(r), ctypes.byref(ctypes.c_int64()),
+         ctypes.byref(ctypes.c_int64()), ctypes.byref(ctypes.c_int64()), fake, 1 << 30, None)
+    # a null index
+    _bad(-1, L.msparse_attn_fwd, ctypes.byref(d), fake, fake, fake, None, fake, fake, None, 0, None)
+
+
+def test_index_capacity_needs_overflow_flag_or_bound():
+    L = ms.lib()
+    d = ms.make_dims(1, 4096, 1, 1, 64)
+    fake = ctypes.c_void_p(16)
+    x = ms.IndexStruct(fake, fake, 10, fake, fake, 10, fake, fake, fake, fake, 10, fake, fake, fake, None)
+    ws = L.msparse_index_workspace(ctypes.byref(d), 8, 8, None)
+    assert ws > 0
+    _bad(-3, L.msparse_build_index, ctypes.byref(d), fake, 8, fake, 8, None, ctypes.byref(x), fake, ws, None)
+
+
+def test_workspace_queries_are_positive():
+    L = ms.lib()
+    d = ms.make_dims(1, 131072, 32, 8, 128)
+    assert L.msparse_estimate_workspace(ctypes.byref(d), 64, 2048, 8192) >= 2 * 32 * 131072 * 4
+    assert L.msparse_attn_bwd_workspace(ctypes.byref(d), 32 * 2048) >= 32 * 131072 * 4
+    assert L.msparse_index_workspace(ctypes.byref(d), 2048, 8192, ctypes.byref(ms.Ring(8, 0, 3, 1))) > 0
