@@ -1,5 +1,484 @@
+// Sparse attention backward over the forward's index (Eq. softmax_gradient and
+// Eq. attention_backward; the index is a constant).  With z = scale q k^T,
+// P = exp(z - lse) on the executed entries and Delta_n = dO_n . O_n:
+//   dV = P^T dO,  dZ = P o (dO V^T - Delta),  dQ = scale dZ K,  dK = scale dZ^T Q.
+//
+// Five launches on the caller's stream, all deterministic (no atomics):
+//   delta   Delta_n = dO_n . O_n                     one thread group per 16 rows
+//   dq      query-major, the forward's block + column lists; per tile
+//           S^T = K Q^T, dP^T = V dO^T, dQ^T += K^T dZ^T          (3 MFMA GEMMs)
+//   dkdv    key-major over 64-key blocks: for every query head of the KV group
+//           and every query block that selected this key block (the transposed
+//           lists), S = Q K^T, dP = dO V^T, dV^T += dO^T P, dK^T += Q^T dZ
+//           (4 MFMA GEMMs); dK / dV of the block are written once
+//   dkdv-col the same tile body for the gathered vertical columns of one query
+//           head (64 per workgroup) against every query block that sees them
+//           outside its selected block-diagonals; per-head partials go to the
+//           workspace
+//   merge   adds the per-head column partials into dK / dV, heads in order.
 #include "common.h"
 #include "kernels.h"
+#include "tiles.h"
+
 namespace msparse {
-hipError_t launch_attn_bwd(const AttnArgs&, hipStream_t) { return hipErrorNotSupported; }
+
+namespace {
+
+constexpr int kThreads = 128;
+constexpr float kLog2e = 1.4426950408889634f;
+
+// ------------------------------------------------------------------ Delta
+__global__ void __launch_bounds__(256) bwd_delta_kernel(AttnArgs a) {
+    // 16 lanes per row, 8 elements per lane (d = 128) or 4 (d = 64)
+    const int64_t rows = int64_t(a.B) * a.Hq * a.Nq;
+    const int64_t row = int64_t(blockIdx.x) * 16 + (threadIdx.x >> 4);
+    const int sub = threadIdx.x & 15;
+    float acc = 0.f;
+    if (row < rows) {
+        const int per = a.d / 16;
+        const uint16_t* o = a.o + row * a.d + sub * per;
+        const uint16_t* g = a.dout + row * a.d + sub * per;
+        for (int j = 0; j < per; ++j) acc += bf16_to_f32(o[j]) * bf16_to_f32(g[j]);
+    }
+#pragma unroll
+    for (int off = 8; off >= 1; off >>= 1) acc += __shfl_xor(acc, off);
+    if (row < rows && sub == 0) a.delta[row] = acc;
+}
+
+// ------------------------------------------------------------------ dQ (query-major)
+template <int D>
+struct DqLds {
+    uint16_t k[TileLds<D>::kRowElems];
+    uint16_t v[TileLds<D>::kRowElems];
+    uint16_t kt[TileLds<D>::kTElems];
+    int32_t kidx[64];
+    int32_t lim[64];
+};
+
+template <int D>
+__global__ void __launch_bounds__(kThreads) bwd_dq_kernel(AttnArgs a) {
+    constexpr int KD = D / 16, ND = D / 32;
+    __shared__ DqLds<D> sm;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, l32 = lane & 31;
+    const int BH = a.B * a.Hq;
+    const int64_t t = blockIdx.x;
+    const int bh = int(t % BH);
+    const int qb = a.nqb - 1 - int(t / BH);
+    const int b = bh / a.Hq, hq = bh % a.Hq, hk = hq / (a.Hq / a.Hkv);
+    const int qrow = 32 * w + l32;
+    const int64_t grow = int64_t(bh) * a.Nq + int64_t(qb) * 64 + qrow;
+
+    const uint16_t* __restrict__ kp = a.k + (int64_t(b) * a.Hkv + hk) * int64_t(a.Nk) * D;
+    const uint16_t* __restrict__ vp = a.v + (int64_t(b) * a.Hkv + hk) * int64_t(a.Nk) * D;
+    u32x4 qreg[KD], dreg[KD];
+#pragma unroll
+    for (int s = 0; s < KD; ++s) {
+        qreg[s] = *reinterpret_cast<const u32x4*>(a.q + grow * D + 16 * s + 8 * h);
+        dreg[s] = *reinterpret_cast<const u32x4*>(a.dout + grow * D + 16 * s + 8 * h);
+    }
+    const float c2 = a.scale * kLog2e;
+    const float lse_n = a.lse[grow];
+    const float lse2 = lse_n == -INFINITY ? INFINITY : lse_n * kLog2e;   // empty row: P = 0
+    const float dlt = a.delta[grow];
+
+    f32x16 acc[ND];
+#pragma unroll
+    for (int i = 0; i < ND; ++i) acc[i] = f32x16{};
+
+    const int64_t item = int64_t(bh) * a.nqb + qb;
+    const int64_t b0 = a.blk_ptr[item], b1 = a.blk_ptr[item + 1];
+    const int64_t c0 = a.col_ptr[item], c1 = a.col_ptr[item + 1];
+    const int nblk = int(b1 - b0);
+    const int ncolt = int((c1 - c0 + 63) / 64);
+    const int32_t qg = a.q_blk_global[qb];
+
+    for (int tt = 0; tt < nblk + ncolt; ++tt) {
+        bool masked;
+        if (tt < nblk) {
+            const int kb = a.blk_idx[b0 + tt];
+            masked = a.k_blk_global[kb] == qg;
+            if (tid < 64) {
+                sm.kidx[tid] = kb * 64 + tid;
+                sm.lim[tid] = tid;
+            }
+        } else {
+            masked = true;
+            const int64_t cbase = c0 + int64_t(tt - nblk) * 64;
+            const int cnt = int(min<int64_t>(64, c1 - cbase));
+            if (tid < 64) {
+                const int j = tid < cnt ? tid : 0;
+                const int32_t col = a.col_idx[cbase + j];
+                sm.kidx[tid] = col;
+                sm.lim[tid] = tid < cnt ? (a.k_blk_global[col >> 6] == qg ? (col & 63) : 0) : 64;
+            }
+        }
+        __syncthreads();
+        stage_rows<D, kThreads>(sm.k, kp, sm.kidx, tid);
+        stage_rows<D, kThreads>(sm.v, vp, sm.kidx, tid);
+        stage_transposed<D, kThreads>(sm.kt, kp, sm.kidx, tid);
+        __syncthreads();
+
+        f32x16 sacc[2], pacc[2];
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+            sacc[c] = f32x16{};
+            pacc[c] = f32x16{};
+            const uint16_t* krow = sm.k + (32 * c + l32) * TileLds<D>::kRowStride + 8 * h;
+            const uint16_t* vrow = sm.v + (32 * c + l32) * TileLds<D>::kRowStride + 8 * h;
+#pragma unroll
+            for (int s = 0; s < KD; ++s) {
+                sacc[c] = mfma32(lds_read16(krow + 16 * s), qreg[s], sacc[c]);
+                pacc[c] = mfma32(lds_read16(vrow + 16 * s), dreg[s], pacc[c]);
+            }
+        }
+        // dZ^T = P o (dP^T - Delta), P = exp2(c2 s - lse2) on visible entries
+#pragma unroll
+        for (int c = 0; c < 2; ++c)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                float p = fast_exp2(sacc[c][r] * c2 - lse2);
+                if (masked) {
+                    const int key = 32 * c + 8 * (r >> 2) + 4 * h + (r & 3);
+                    if (qrow < sm.lim[key]) p = 0.f;
+                }
+                sacc[c][r] = p * (pacc[c][r] - dlt);
+            }
+        u32x4 zb[4];
+        zb[0] = pack8(sacc[0], 0);
+        zb[1] = pack8(sacc[0], 8);
+        zb[2] = pack8(sacc[1], 0);
+        zb[3] = pack8(sacc[1], 8);
+#pragma unroll
+        for (int i = 0; i < ND; ++i) {
+            const uint16_t* trow = sm.kt + (32 * i + l32) * TileLds<D>::kTStride + 8 * h;
+#pragma unroll
+            for (int g = 0; g < 4; ++g) acc[i] = mfma32(lds_read16(trow + 16 * g), zb[g], acc[i]);
+        }
+        __syncthreads();
+    }
+    float* dq = a.dq + grow * D;
+#pragma unroll
+    for (int i = 0; i < ND; ++i)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            f32x4 val;
+            val.x = acc[i][4 * g + 0] * a.scale;
+            val.y = acc[i][4 * g + 1] * a.scale;
+            val.z = acc[i][4 * g + 2] * a.scale;
+            val.w = acc[i][4 * g + 3] * a.scale;
+            f32x4* dst = reinterpret_cast<f32x4*>(dq + 32 * i + 8 * g + 4 * h);
+            if (a.dq_accumulate) val += *dst;
+            *dst = val;
+        }
+}
+
+// ------------------------------------------------------------------ dK / dV (key-major)
+template <int D>
+struct KvLds {
+    uint16_t q[TileLds<D>::kRowElems];
+    uint16_t qt[TileLds<D>::kTElems];
+    uint16_t g[TileLds<D>::kRowElems];    // dO
+    uint16_t gt[TileLds<D>::kTElems];
+    float lse2[64];
+    float dlt[64];
+};
+
+// Contiguous row range staged through the shared helpers.
+struct RowsFrom {
+    int32_t base;
+};
+
+template <int D, int NT>
+__device__ __forceinline__ void stage_rows_contig(uint16_t* lds, const uint16_t* __restrict__ src, int tid) {
+    constexpr int kChunks = D / 8;
+    constexpr int kRowsPerPass = NT / kChunks;
+#pragma unroll
+    for (int p = 0; p < 64 / kRowsPerPass; ++p) {
+        const int r = p * kRowsPerPass + tid / kChunks;
+        const int c = tid % kChunks;
+        *reinterpret_cast<u32x4*>(lds + r * TileLds<D>::kRowStride + c * 8) =
+            *reinterpret_cast<const u32x4*>(src + int64_t(r) * D + c * 8);
+    }
+}
+
+template <int D, int NT>
+__device__ __forceinline__ void stage_transposed_contig(uint16_t* lds, const uint16_t* __restrict__ src, int tid) {
+    constexpr int kItems = 16 * (D / 8);
+#pragma unroll
+    for (int p = 0; p < (kItems + NT - 1) / NT; ++p) {
+        const int item = p * NT + tid;
+        if (kItems % NT != 0 && item >= kItems) break;
+        const int q4 = item & 15, dc = item >> 4;
+        u32x4 r[4];
+#pragma unroll
+        for (int bb = 0; bb < 4; ++bb) r[bb] = *reinterpret_cast<const u32x4*>(src + int64_t(4 * q4 + bb) * D + dc * 8);
+        const int pos = tpos(4 * q4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const uint32_t w0 = r[0][e], w1 = r[1][e], w2 = r[2][e], w3 = r[3][e];
+            u32x2 even, odd;
+            even.x = (w0 & 0xffffu) | (w1 << 16);
+            even.y = (w2 & 0xffffu) | (w3 << 16);
+            odd.x = (w0 >> 16) | (w1 & 0xffff0000u);
+            odd.y = (w2 >> 16) | (w3 & 0xffff0000u);
+            const int d0 = dc * 8 + 2 * e;
+            *reinterpret_cast<u32x2*>(lds + d0 * TileLds<D>::kTStride + pos) = even;
+            *reinterpret_cast<u32x2*>(lds + (d0 + 1) * TileLds<D>::kTStride + pos) = odd;
+        }
+    }
+}
+
+// One 64-row query tile against this wave's 32 keys.  `active` / `lim` give
+// the per-key visibility: key visible to in-block query row r iff active and
+// r >= lim.
+template <int D>
+__device__ __forceinline__ void kv_tile(const KvLds<D>& sm, const u32x4* kreg, const u32x4* vreg, bool masked,
+                                        bool active, int lim, float c2, int h, int l32, f32x16* dv, f32x16* dk) {
+    constexpr int KD = D / 16, ND = D / 32;
+    f32x16 sacc[2], pacc[2];
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb) {
+        sacc[rb] = f32x16{};
+        pacc[rb] = f32x16{};
+        const uint16_t* qrow = sm.q + (32 * rb + l32) * TileLds<D>::kRowStride + 8 * h;
+        const uint16_t* grow = sm.g + (32 * rb + l32) * TileLds<D>::kRowStride + 8 * h;
+#pragma unroll
+        for (int s = 0; s < KD; ++s) {
+            sacc[rb] = mfma32(lds_read16(qrow + 16 * s), kreg[s], sacc[rb]);
+            pacc[rb] = mfma32(lds_read16(grow + 16 * s), vreg[s], pacc[rb]);
+        }
+    }
+    // rows of acc element r: 32 rb + 8 (r/4) + 4 h + r%4; column = this lane's key
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int row = 32 * rb + 8 * (r >> 2) + 4 * h + (r & 3);
+            float p = fast_exp2(sacc[rb][r] * c2 - sm.lse2[row]);
+            if (masked && (!active || row < lim)) p = 0.f;
+            sacc[rb][r] = p;
+            pacc[rb][r] = p * (pacc[rb][r] - sm.dlt[row]);
+        }
+    u32x4 pb[4], zb[4];
+    pb[0] = pack8(sacc[0], 0);
+    pb[1] = pack8(sacc[0], 8);
+    pb[2] = pack8(sacc[1], 0);
+    pb[3] = pack8(sacc[1], 8);
+    zb[0] = pack8(pacc[0], 0);
+    zb[1] = pack8(pacc[0], 8);
+    zb[2] = pack8(pacc[1], 0);
+    zb[3] = pack8(pacc[1], 8);
+#pragma unroll
+    for (int i = 0; i < ND; ++i) {
+        const uint16_t* gt = sm.gt + (32 * i + l32) * TileLds<D>::kTStride + 8 * h;
+        const uint16_t* qt = sm.qt + (32 * i + l32) * TileLds<D>::kTStride + 8 * h;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            dv[i] = mfma32(lds_read16(gt + 16 * g), pb[g], dv[i]);
+            dk[i] = mfma32(lds_read16(qt + 16 * g), zb[g], dk[i]);
+        }
+    }
+}
+
+template <int D>
+__device__ __forceinline__ void kv_stage_query_tile(KvLds<D>& sm, const AttnArgs& a, int bh, int qb, int tid) {
+    const int64_t row0 = int64_t(bh) * a.Nq + int64_t(qb) * 64;
+    stage_rows_contig<D, kThreads>(sm.q, a.q + row0 * D, tid);
+    stage_transposed_contig<D, kThreads>(sm.qt, a.q + row0 * D, tid);
+    stage_rows_contig<D, kThreads>(sm.g, a.dout + row0 * D, tid);
+    stage_transposed_contig<D, kThreads>(sm.gt, a.dout + row0 * D, tid);
+    if (tid < 64) {
+        const float l = a.lse[row0 + tid];
+        sm.lse2[tid] = l == -INFINITY ? INFINITY : l * kLog2e;
+        sm.dlt[tid] = a.delta[row0 + tid];
+    }
+}
+
+// Key-major pass over 64-key blocks: grid = B * Hkv * nkb.
+template <int D>
+__global__ void __launch_bounds__(kThreads) bwd_dkdv_kernel(AttnArgs a) {
+    constexpr int KD = D / 16, ND = D / 32;
+    __shared__ KvLds<D> sm;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, l32 = lane & 31;
+    const int BK = a.B * a.Hkv;
+    const int64_t t = blockIdx.x;
+    const int bk = int(t % BK);
+    const int kb = int(t / BK);
+    const int b = bk / a.Hkv, hk = bk % a.Hkv;
+    const int G = a.Hq / a.Hkv;
+    const int key = 32 * w + l32;  // this lane's key inside the block
+    const int64_t krow = int64_t(bk) * a.Nk + int64_t(kb) * 64 + key;
+
+    u32x4 kreg[KD], vreg[KD];
+#pragma unroll
+    for (int s = 0; s < KD; ++s) {
+        kreg[s] = *reinterpret_cast<const u32x4*>(a.k + krow * D + 16 * s + 8 * h);
+        vreg[s] = *reinterpret_cast<const u32x4*>(a.v + krow * D + 16 * s + 8 * h);
+    }
+    f32x16 dv[ND], dk[ND];
+#pragma unroll
+    for (int i = 0; i < ND; ++i) {
+        dv[i] = f32x16{};
+        dk[i] = f32x16{};
+    }
+    const float c2 = a.scale * kLog2e;
+    const int32_t kg = a.k_blk_global[kb];
+    for (int g = 0; g < G; ++g) {
+        const int bh = b * a.Hq + hk * G + g;
+        const int64_t item = int64_t(bh) * a.nkb + kb;
+        const int64_t p0 = a.kblk_ptr[item], p1 = a.kblk_ptr[item + 1];
+        for (int64_t p = p0; p < p1; ++p) {
+            const int qb = a.kblk_idx[p];
+            const bool masked = a.q_blk_global[qb] == kg;   // diagonal tile
+            kv_stage_query_tile<D>(sm, a, bh, qb, tid);
+            __syncthreads();
+            kv_tile<D>(sm, kreg, vreg, masked, true, key, c2, h, l32, dv, dk);
+            __syncthreads();
+        }
+    }
+    float* dkp = a.dk + krow * D;
+    float* dvp = a.dv + krow * D;
+#pragma unroll
+    for (int i = 0; i < ND; ++i)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            f32x4 x, y;
+            x.x = dk[i][4 * g + 0] * a.scale;
+            x.y = dk[i][4 * g + 1] * a.scale;
+            x.z = dk[i][4 * g + 2] * a.scale;
+            x.w = dk[i][4 * g + 3] * a.scale;
+            y.x = dv[i][4 * g + 0];
+            y.y = dv[i][4 * g + 1];
+            y.z = dv[i][4 * g + 2];
+            y.w = dv[i][4 * g + 3];
+            *reinterpret_cast<f32x4*>(dkp + 32 * i + 8 * g + 4 * h) = x;
+            *reinterpret_cast<f32x4*>(dvp + 32 * i + 8 * g + 4 * h) = y;
+        }
+}
+
+__device__ __forceinline__ bool dbit(const uint32_t* db, int32_t x) { return (db[x >> 5] >> (x & 31)) & 1u; }
+
+// Column pass: one workgroup per (head, 64 consecutive entries of the head's
+// vertical list).  Grid = B * Hq * ceil(max verticals per head / 64); surplus
+// workgroups exit.
+template <int D>
+__global__ void __launch_bounds__(kThreads) bwd_dkdv_col_kernel(AttnArgs a, int32_t chunks_per_head) {
+    constexpr int KD = D / 16, ND = D / 32;
+    __shared__ KvLds<D> sm;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, l32 = lane & 31;
+    const int bh = int(blockIdx.x / chunks_per_head);
+    const int chunk = int(blockIdx.x % chunks_per_head);
+    const int64_t v0 = a.vcol_ptr[bh], v1 = a.vcol_ptr[bh + 1];
+    const int64_t e0 = v0 + int64_t(chunk) * 64;
+    if (e0 >= v1) return;
+    const int cnt = int(min<int64_t>(64, v1 - e0));
+    const int b = bh / a.Hq, hq = bh % a.Hq, hk = hq / (a.Hq / a.Hkv);
+    const int key = 32 * w + l32;
+    const bool valid = key < cnt;
+    const int32_t col = a.vcol_idx[e0 + (valid ? key : 0)];
+    const int32_t cg = a.k_blk_global[col >> 6];
+    const int32_t cin = col & 63;
+    const int64_t krow = (int64_t(b) * a.Hkv + hk) * a.Nk + col;
+    u32x4 kreg[KD], vreg[KD];
+#pragma unroll
+    for (int s = 0; s < KD; ++s) {
+        kreg[s] = *reinterpret_cast<const u32x4*>(a.k + krow * D + 16 * s + 8 * h);
+        vreg[s] = *reinterpret_cast<const u32x4*>(a.v + krow * D + 16 * s + 8 * h);
+    }
+    f32x16 dv[ND], dk[ND];
+#pragma unroll
+    for (int i = 0; i < ND; ++i) {
+        dv[i] = f32x16{};
+        dk[i] = f32x16{};
+    }
+    const float c2 = a.scale * kLog2e;
+    const uint32_t* db = a.diag_bits + int64_t(bh) * a.dwords;
+    // the first column of the chunk has the smallest global block
+    const int32_t cg_min = a.k_blk_global[a.vcol_idx[e0] >> 6];
+    for (int qb = 0; qb < a.nqb; ++qb) {
+        const int32_t qg = a.q_blk_global[qb];
+        if (qg < cg_min) continue;   // uniform across the workgroup
+        const bool active = valid && qg >= cg && !dbit(db, qg - cg);
+        const int lim = qg == cg ? cin : 0;
+        kv_stage_query_tile<D>(sm, a, bh, qb, tid);
+        __syncthreads();
+        kv_tile<D>(sm, kreg, vreg, true, active, lim, c2, h, l32, dv, dk);
+        __syncthreads();
+    }
+    if (!valid) return;
+    float* dkp = a.dk_col + (e0 + key) * D;
+    float* dvp = a.dv_col + (e0 + key) * D;
+#pragma unroll
+    for (int i = 0; i < ND; ++i)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            f32x4 x, y;
+            x.x = dk[i][4 * g + 0] * a.scale;
+            x.y = dk[i][4 * g + 1] * a.scale;
+            x.z = dk[i][4 * g + 2] * a.scale;
+            x.w = dk[i][4 * g + 3] * a.scale;
+            y.x = dv[i][4 * g + 0];
+            y.y = dv[i][4 * g + 1];
+            y.z = dv[i][4 * g + 2];
+            y.w = dv[i][4 * g + 3];
+            *reinterpret_cast<f32x4*>(dkp + 32 * i + 8 * g + 4 * h) = x;
+            *reinterpret_cast<f32x4*>(dvp + 32 * i + 8 * g + 4 * h) = y;
+        }
+}
+
+// Adds the per-head column partials of key block kb into dK / dV: one
+// workgroup per (b, KV head, key block), query heads in order.
+__global__ void __launch_bounds__(128) bwd_colmerge_kernel(AttnArgs a) {
+    const int BK = a.B * a.Hkv;
+    const int bk = int(blockIdx.x % BK);
+    const int kb = int(blockIdx.x / BK);
+    const int b = bk / a.Hkv, hk = bk % a.Hkv;
+    const int G = a.Hq / a.Hkv;
+    const int lo = kb * 64, hi = lo + 64;
+    for (int g = 0; g < G; ++g) {
+        const int bh = b * a.Hq + hk * G + g;
+        const int64_t v0 = a.vcol_ptr[bh], v1 = a.vcol_ptr[bh + 1];
+        // first entry >= lo
+        int64_t L = v0, R = v1;
+        while (L < R) {
+            const int64_t m = (L + R) >> 1;
+            if (a.vcol_idx[m] < lo) L = m + 1; else R = m;
+        }
+        for (int64_t e = L; e < v1 && a.vcol_idx[e] < hi; ++e) {
+            const int64_t row = int64_t(bk) * a.Nk + a.vcol_idx[e];
+            for (int j = threadIdx.x; j < a.d; j += blockDim.x) {
+                a.dk[row * a.d + j] += a.dk_col[e * a.d + j];
+                a.dv[row * a.d + j] += a.dv_col[e * a.d + j];
+            }
+        }
+    }
+}
+
+template <int D>
+hipError_t launch_bwd_d(const AttnArgs& a, hipStream_t s) {
+    const int64_t rows = int64_t(a.B) * a.Hq * a.Nq;
+    if (rows > 0) hipLaunchKernelGGL(bwd_delta_kernel, dim3(unsigned((rows + 15) / 16)), dim3(256), 0, s, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int64_t qgrid = int64_t(a.B) * a.Hq * a.nqb;
+    if (qgrid > 0) hipLaunchKernelGGL(bwd_dq_kernel<D>, dim3(unsigned(qgrid)), dim3(kThreads), 0, s, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    const int64_t kgrid = int64_t(a.B) * a.Hkv * a.nkb;
+    if (kgrid > 0) hipLaunchKernelGGL(bwd_dkdv_kernel<D>, dim3(unsigned(kgrid)), dim3(kThreads), 0, s, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    // column chunks: at most ceil(Nk / 64) per head (a head has <= Nk verticals in a shard)
+    const int32_t chunks = a.nkb;
+    const int64_t cgrid = int64_t(a.B) * a.Hq * chunks;
+    if (cgrid > 0) hipLaunchKernelGGL(bwd_dkdv_col_kernel<D>, dim3(unsigned(cgrid)), dim3(kThreads), 0, s, a, chunks);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (kgrid > 0) hipLaunchKernelGGL(bwd_colmerge_kernel, dim3(unsigned(kgrid)), dim3(128), 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_attn_bwd(const AttnArgs& a, hipStream_t s) {
+    return a.d == 128 ? launch_bwd_d<128>(a, s) : launch_bwd_d<64>(a, s);
+}
+
 }  // namespace msparse
