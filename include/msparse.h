@@ -106,6 +106,8 @@ typedef struct {
  *   overflow int32 [1] (may be NULL): set to 1 by msparse_build_index when a
  *                                  capacity was too small (what does not fit
  *                                  is dropped, nothing is written out of bounds)
+ *   world    host-side: ring workers the index was built for (1 for a whole
+ *            sequence), so nb = world * seq_q / 64
  * blk_cap, col_cap, vcol_cap are host-side element capacities of blk_idx (and
  * kblk_idx), col_idx and vcol_idx. */
 typedef struct {
@@ -124,6 +126,7 @@ typedef struct {
     int32_t* q_blk_global;
     int32_t* k_blk_global;
     int32_t* overflow;
+    int32_t world;
 } msparse_index;
 
 /* Human-readable name of a status code (static storage). */
@@ -182,19 +185,22 @@ MSPARSE_API msparse_status msparse_build_index(const msparse_dims* dims, const i
  * (global key position <= global query position):
  *   out_n = sum_m P[n, m] v_m,  lse_n = log sum_m exp(scale q_n . k_m).
  * A row that sees no key gets out = 0 and lse = -inf.  out is bf16 (round to
- * nearest even), lse fp32.  Needs no workspace (pass NULL, 0). */
+ * nearest even), lse fp32.  out_f32 (fp32 [B, Hq, Nq, d], may be NULL) also
+ * receives the unrounded output; msparse_attn_bwd computes
+ * Delta = dO . O more accurately from it, and ring steps merge it.  out may be
+ * NULL when out_f32 is given. */
 MSPARSE_API msparse_status msparse_attn_fwd(const msparse_dims* dims, const void* q, const void* k, const void* v,
-                                const msparse_index* index, void* out, float* lse, void* workspace,
-                                size_t workspace_bytes, void* stream);
+                                const msparse_index* index, void* out, float* lse, float* out_f32, void* stream);
 
 /* Log-sum-exp merge of one ring step's partial result into a running one
  * (merge_out_and_lse, Algorithm 2): lse = logaddexp(lse_acc, lse_part),
  * o_acc = exp(lse_acc - lse) o_acc + exp(lse_part - lse) o_part.
- *   o_part bf16 [B, Hq, Nq, d], lse_part fp32 [B, Hq, Nq] (from msparse_attn_fwd)
- *   o_acc fp32 [B, Hq, Nq, d], lse_acc fp32 [B, Hq, Nq] (read unless `first`,
- *   which copies the partial instead)
+ *   o_part fp32 [B, Hq, Nq, d], lse_part fp32 [B, Hq, Nq]: the step's out_f32
+ *   and lse from msparse_attn_fwd
+ *   o_acc fp32 [B, Hq, Nq, d], lse_acc fp32 [B, Hq, Nq]: read unless `first`,
+ *   which copies the partial instead
  *   out_bf16 bf16 [B, Hq, Nq, d] or NULL: also stores the merged O as bf16. */
-MSPARSE_API msparse_status msparse_merge_out_lse(const msparse_dims* dims, const void* o_part, const float* lse_part,
+MSPARSE_API msparse_status msparse_merge_out_lse(const msparse_dims* dims, const float* o_part, const float* lse_part,
                                      float* o_acc, float* lse_acc, void* out_bf16, int32_t first, void* stream);
 
 /* ------------------------------------------------------------------------ */
@@ -202,13 +208,16 @@ MSPARSE_API msparse_status msparse_merge_out_lse(const msparse_dims* dims, const
  * Eq. attention_backward; the index is a constant).  With
  * P = exp(scale q k^T - lse) on the executed entries and Delta_n = dO_n . O_n:
  *   dV = P^T dO,  dZ = P o (dO V^T - Delta),  dQ = scale dZ K,  dK = scale dZ^T Q,
- * dK and dV summed over the query heads of each KV head.  out and lse are the
- * forward's final (merged) results.  dq, dk, dv are fp32 and overwritten,
- * except that dq_accumulate = 1 adds into dq (ring steps after the first).
+ * dK and dV summed over the query heads of each KV head.  out (bf16) and lse
+ * are the forward's final (merged) results; out_f32 (may be NULL) is the same
+ * output unrounded and is used for Delta when given (recommended: Delta from
+ * a bf16-rounded O moves large gradients by about 2^-9 of their size).
+ * dq, dk, dv are fp32 and overwritten, except that dq_accumulate = 1 adds into
+ * dq (ring steps after the first).
  * Workspace: msparse_attn_bwd_workspace(dims, vcol_cap) bytes. */
 MSPARSE_API size_t msparse_attn_bwd_workspace(const msparse_dims* dims, int64_t vcol_cap);
 MSPARSE_API msparse_status msparse_attn_bwd(const msparse_dims* dims, const void* q, const void* k, const void* v,
-                                const void* out, const void* dout, const float* lse,
+                                const void* out, const float* out_f32, const void* dout, const float* lse,
                                 const msparse_index* index, float* dq, float* dk, float* dv,
                                 int32_t dq_accumulate, void* workspace, size_t workspace_bytes, void* stream);
 

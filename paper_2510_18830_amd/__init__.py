@@ -39,7 +39,8 @@ class IndexStruct(ctypes.Structure):
                 ("col_ptr", c_vp), ("col_idx", c_vp), ("col_cap", c_i64),
                 ("kblk_ptr", c_vp), ("kblk_idx", c_vp),
                 ("vcol_ptr", c_vp), ("vcol_idx", c_vp), ("vcol_cap", c_i64),
-                ("diag_bits", c_vp), ("q_blk_global", c_vp), ("k_blk_global", c_vp), ("overflow", c_vp)]
+                ("diag_bits", c_vp), ("q_blk_global", c_vp), ("k_blk_global", c_vp), ("overflow", c_vp),
+                ("world", c_i32)]
 
 
 _P = ctypes.POINTER
@@ -52,11 +53,11 @@ _SIGS = {
     "msparse_index_count": (c_i32, [_P(Dims), c_vp, c_i32, c_vp, c_i32, _P(Ring), _P(c_i64), _P(c_i64), _P(c_i64),
                                     c_vp, c_sz, c_vp]),
     "msparse_build_index": (c_i32, [_P(Dims), c_vp, c_i32, c_vp, c_i32, _P(Ring), _P(IndexStruct), c_vp, c_sz, c_vp]),
-    "msparse_attn_fwd": (c_i32, [_P(Dims), c_vp, c_vp, c_vp, _P(IndexStruct), c_vp, c_vp, c_vp, c_sz, c_vp]),
+    "msparse_attn_fwd": (c_i32, [_P(Dims), c_vp, c_vp, c_vp, _P(IndexStruct), c_vp, c_vp, c_vp, c_vp]),
     "msparse_merge_out_lse": (c_i32, [_P(Dims), c_vp, c_vp, c_vp, c_vp, c_vp, c_i32, c_vp]),
     "msparse_attn_bwd_workspace": (c_sz, [_P(Dims), c_i64]),
-    "msparse_attn_bwd": (c_i32, [_P(Dims), c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, _P(IndexStruct), c_vp, c_vp, c_vp,
-                                 c_i32, c_vp, c_sz, c_vp]),
+    "msparse_attn_bwd": (c_i32, [_P(Dims), c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, _P(IndexStruct), c_vp, c_vp,
+                                 c_vp, c_i32, c_vp, c_sz, c_vp]),
 }
 
 _lib = None
@@ -180,7 +181,7 @@ def alloc_index(dims, blk_cap, col_cap, vcol_cap, device, world=1) -> SparseInde
     }
     s = IndexStruct(_p(t["blk_ptr"]), _p(t["blk_idx"]), blk_cap, _p(t["col_ptr"]), _p(t["col_idx"]), col_cap,
                     _p(t["kblk_ptr"]), _p(t["kblk_idx"]), _p(t["vcol_ptr"]), _p(t["vcol_idx"]), vcol_cap,
-                    _p(t["diag_bits"]), _p(t["q_blk_global"]), _p(t["k_blk_global"]), _p(t["overflow"]))
+                    _p(t["diag_bits"]), _p(t["q_blk_global"]), _p(t["k_blk_global"]), _p(t["overflow"]), world)
     return SparseIndex(t, s, nqb, nkb)
 
 
@@ -204,13 +205,14 @@ def make_index(dims, v_idx, s_idx, ring=None, stream=None) -> SparseIndex:
 
 
 # ------------------------------------------------------------------ attention
-def attn_fwd(dims, q, k, v, index: SparseIndex, out=None, lse=None, stream=None):
-    """msparse_attn_fwd: returns (out bf16 [B,Hq,Nq,d], lse fp32 [B,Hq,Nq])."""
-    out = torch.empty_like(q) if out is None else out
+def attn_fwd(dims, q, k, v, index: SparseIndex, out=None, lse=None, out_f32=None, stream=None, bf16_out=True):
+    """msparse_attn_fwd: returns (out bf16 [B,Hq,Nq,d] or None, lse fp32 [B,Hq,Nq]); out_f32 is optional."""
+    if out is None and bf16_out:
+        out = torch.empty_like(q)
     if lse is None:
         lse = torch.empty(q.shape[:-1], dtype=torch.float32, device=q.device)
     _check(lib().msparse_attn_fwd(ctypes.byref(dims), _p(q), _p(k), _p(v), ctypes.byref(index.struct), _p(out),
-                                  _p(lse), None, 0, _stream(stream)))
+                                  _p(lse), _p(out_f32), _stream(stream)))
     return out, lse
 
 
@@ -224,7 +226,7 @@ def attn_bwd_workspace_bytes(dims, vcol_cap):
 
 
 def attn_bwd(dims, q, k, v, out, dout, lse, index: SparseIndex, dq=None, dk=None, dv=None, dq_accumulate=False,
-             workspace=None, stream=None):
+             out_f32=None, workspace=None, stream=None):
     """msparse_attn_bwd: returns (dq, dk, dv) fp32."""
     f32 = torch.float32
     dq = torch.empty(q.shape, dtype=f32, device=q.device) if dq is None else dq
@@ -232,7 +234,7 @@ def attn_bwd(dims, q, k, v, out, dout, lse, index: SparseIndex, dq=None, dk=None
     dv = torch.empty(v.shape, dtype=f32, device=q.device) if dv is None else dv
     if workspace is None:
         workspace = _workspace(attn_bwd_workspace_bytes(dims, index.struct.vcol_cap), q.device)
-    _check(lib().msparse_attn_bwd(ctypes.byref(dims), _p(q), _p(k), _p(v), _p(out), _p(dout), _p(lse),
+    _check(lib().msparse_attn_bwd(ctypes.byref(dims), _p(q), _p(k), _p(v), _p(out), _p(out_f32), _p(dout), _p(lse),
                                   ctypes.byref(index.struct), _p(dq), _p(dk), _p(dv), int(bool(dq_accumulate)),
                                   _p(workspace), workspace.numel(), _stream(stream)))
     return dq, dk, dv

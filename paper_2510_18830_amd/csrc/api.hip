@@ -181,6 +181,7 @@ msparse_status check_index_struct(const msparse_dims* d, const msparse_index* x,
                            (x->vcol_cap > 0 && !x->vcol_idx)))
         return fail(MSPARSE_ERR_INVALID, "transposed index arrays are NULL");
     if (x->blk_cap < 0 || x->col_cap < 0 || x->vcol_cap < 0) return fail(MSPARSE_ERR_INVALID, "negative capacity");
+    if (x->world < 1) return fail(MSPARSE_ERR_INVALID, "index world %d < 1", x->world);
     (void)d;
     return MSPARSE_OK;
 }
@@ -246,6 +247,8 @@ msparse_status msparse_build_index(const msparse_dims* dims, const int32_t* v_id
     msparse_status st = check_index_inputs(dims, v_idx, k_v, s_idx, k_s, ring, &ri);
     if (st) return st;
     if ((st = check_index_struct(dims, index, true))) return st;
+    if (index->world != ri.world)
+        return fail(MSPARSE_ERR_INVALID, "index world %d differs from the ring world %d", index->world, ri.world);
     IndexPlan p = plan_index(dims, k_v, k_s, ri, ws, false);
     if (!ws || ws_bytes < p.bytes)
         return fail(MSPARSE_ERR_WORKSPACE, "index workspace %zu < %zu bytes", ws_bytes, p.bytes);
@@ -309,19 +312,17 @@ static msparse_status fill_attn(const msparse_dims* d, const msparse_index* x, A
     a->vcol_ptr = x->vcol_ptr;
     a->vcol_idx = x->vcol_idx;
     a->diag_bits = x->diag_bits;
+    a->dwords = (d->seq_q / kBlock * x->world + 31) / 32;
     a->q_blk_global = x->q_blk_global;
     a->k_blk_global = x->k_blk_global;
     return MSPARSE_OK;
 }
 
 msparse_status msparse_attn_fwd(const msparse_dims* dims, const void* q, const void* k, const void* v,
-                                const msparse_index* index, void* out, float* lse, void* ws, size_t ws_bytes,
-                                void* stream) {
-    (void)ws;
-    (void)ws_bytes;
+                                const msparse_index* index, void* out, float* lse, float* out_f32, void* stream) {
     msparse_status st = check_dims(dims, false);
     if (st) return st;
-    if (!q || !k || !v || !out || !lse) return fail(MSPARSE_ERR_INVALID, "tensor pointer is NULL");
+    if (!q || !k || !v || (!out && !out_f32) || !lse) return fail(MSPARSE_ERR_INVALID, "tensor pointer is NULL");
     if ((st = check_index_struct(dims, index, false))) return st;
     if (dims->seq_q == 0) return MSPARSE_OK;
     AttnArgs a{};
@@ -330,19 +331,20 @@ msparse_status msparse_attn_fwd(const msparse_dims* dims, const void* q, const v
     a.k = static_cast<const uint16_t*>(k);
     a.v = static_cast<const uint16_t*>(v);
     a.out = static_cast<uint16_t*>(out);
+    a.out_f32 = out_f32;
     a.lse = lse;
     hipStream_t s = static_cast<hipStream_t>(stream);
     return check_hip(launch_attn_fwd(a, s), s, "attn fwd");
 }
 
-msparse_status msparse_merge_out_lse(const msparse_dims* dims, const void* o_part, const float* lse_part, float* o_acc,
+msparse_status msparse_merge_out_lse(const msparse_dims* dims, const float* o_part, const float* lse_part, float* o_acc,
                                      float* lse_acc, void* out_bf16, int32_t first, void* stream) {
     msparse_status st = check_dims(dims, false);
     if (st) return st;
     if (!o_part || !lse_part || !o_acc || !lse_acc) return fail(MSPARSE_ERR_INVALID, "tensor pointer is NULL");
     if (dims->seq_q == 0) return MSPARSE_OK;
     MergeArgs m{};
-    m.o_part = static_cast<const uint16_t*>(o_part);
+    m.o_part = o_part;
     m.lse_part = lse_part;
     m.o_acc = o_acc;
     m.lse_acc = lse_acc;
@@ -360,13 +362,14 @@ size_t msparse_attn_bwd_workspace(const msparse_dims* dims, int64_t vcol_cap) {
     c.take<float>(size_t(dims->batch) * dims->heads_q * dims->seq_q);
     c.take<float>(size_t(vcol_cap) * dims->head_dim);
     c.take<float>(size_t(vcol_cap) * dims->head_dim);
+    c.take<uint32_t>(1);
     return c.off;
 }
 
 msparse_status msparse_attn_bwd(const msparse_dims* dims, const void* q, const void* k, const void* v,
-                                const void* out, const void* dout, const float* lse, const msparse_index* index,
-                                float* dq, float* dk, float* dv, int32_t dq_accumulate, void* ws, size_t ws_bytes,
-                                void* stream) {
+                                const void* out, const float* out_f32, const void* dout, const float* lse,
+                                const msparse_index* index, float* dq, float* dk, float* dv, int32_t dq_accumulate,
+                                void* ws, size_t ws_bytes, void* stream) {
     msparse_status st = check_dims(dims, false);
     if (st) return st;
     if (!q || !k || !v || !out || !dout || !lse || !dq || !dk || !dv)
@@ -381,6 +384,8 @@ msparse_status msparse_attn_bwd(const msparse_dims* dims, const void* q, const v
     a.delta = c.take<float>(size_t(dims->batch) * dims->heads_q * dims->seq_q);
     a.dk_col = c.take<float>(size_t(index->vcol_cap) * dims->head_dim);
     a.dv_col = c.take<float>(size_t(index->vcol_cap) * dims->head_dim);
+    a.dmax = c.take<uint32_t>(1);
+    a.o_f32 = out_f32;
     a.q = static_cast<const uint16_t*>(q);
     a.k = static_cast<const uint16_t*>(k);
     a.v = static_cast<const uint16_t*>(v);

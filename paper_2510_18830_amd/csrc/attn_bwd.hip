@@ -3,19 +3,26 @@
 // P = exp(z - lse) on the executed entries and Delta_n = dO_n . O_n:
 //   dV = P^T dO,  dZ = P o (dO V^T - Delta),  dQ = scale dZ K,  dK = scale dZ^T Q.
 //
-// Five launches on the caller's stream, all deterministic (no atomics):
-//   delta   Delta_n = dO_n . O_n                     one thread group per 16 rows
-//   dq      query-major, the forward's block + column lists; per tile
-//           S^T = K Q^T, dP^T = V dO^T, dQ^T += K^T dZ^T          (3 MFMA GEMMs)
-//   dkdv    key-major over 64-key blocks: for every query head of the KV group
-//           and every query block that selected this key block (the transposed
-//           lists), S = Q K^T, dP = dO V^T, dV^T += dO^T P, dK^T += Q^T dZ
-//           (4 MFMA GEMMs); dK / dV of the block are written once
-//   dkdv-col the same tile body for the gathered vertical columns of one query
-//           head (64 per workgroup) against every query block that sees them
-//           outside its selected block-diagonals; per-head partials go to the
-//           workspace
-//   merge   adds the per-head column partials into dK / dV, heads in order.
+// Launches on the caller's stream, all deterministic (no atomics decide a
+// value; the only atomic is an order-free max):
+//   init/delta  Delta_n = dO_n . O_n (from the fp32 forward output when given)
+//               and max |dO| over the tensor
+//   dq          query-major over the forward's block + column lists; per tile
+//               S^T = K Q^T, dP^T = V dO^T, dQ^T += K^T dZ^T        (3 GEMMs)
+//   dkdv        key-major over 64-key blocks: for every query head of the KV
+//               group and every query block that selected this key block (the
+//               transposed lists), S = Q K^T, dP = dO V^T, dV^T += dO^T P,
+//               dK^T += Q^T dZ (4 GEMMs); dK / dV of the block written once
+//   dkdv-col    the same tile body for the gathered vertical columns of one
+//               query head (64 per workgroup) against every query block that
+//               sees them outside its selected block-diagonals; per-head
+//               partials go to the workspace
+//   merge       adds the per-head column partials into dK / dV, heads in order.
+// The second GEMM of each pair takes fp16 operands (P or dZ, and Q^T, K^T or
+// dO^T converted while staging): 3 more significand bits than bf16 at the same
+// MFMA rate.  dO is multiplied by a power of two s so that max |s dO| = 16,
+// which keeps s dP, s Delta and s dZ inside the fp16 range whatever the scale
+// of the incoming gradient; results are divided by s.
 #include "common.h"
 #include "kernels.h"
 #include "tiles.h"
@@ -28,21 +35,49 @@ constexpr int kThreads = 128;
 constexpr float kLog2e = 1.4426950408889634f;
 
 // ------------------------------------------------------------------ Delta
+__global__ void bwd_init_kernel(AttnArgs a) {
+    if (threadIdx.x == 0) *a.dmax = 0u;
+}
+
 __global__ void __launch_bounds__(256) bwd_delta_kernel(AttnArgs a) {
-    // 16 lanes per row, 8 elements per lane (d = 128) or 4 (d = 64)
+    // 16 lanes per row, d / 16 elements per lane
     const int64_t rows = int64_t(a.B) * a.Hq * a.Nq;
     const int64_t row = int64_t(blockIdx.x) * 16 + (threadIdx.x >> 4);
     const int sub = threadIdx.x & 15;
-    float acc = 0.f;
+    float acc = 0.f, mx = 0.f;
     if (row < rows) {
         const int per = a.d / 16;
-        const uint16_t* o = a.o + row * a.d + sub * per;
         const uint16_t* g = a.dout + row * a.d + sub * per;
-        for (int j = 0; j < per; ++j) acc += bf16_to_f32(o[j]) * bf16_to_f32(g[j]);
+        if (a.o_f32) {
+            const float* o = a.o_f32 + row * a.d + sub * per;
+            for (int j = 0; j < per; ++j) {
+                const float x = bf16_to_f32(g[j]);
+                acc += o[j] * x;
+                mx = fmaxf(mx, fabsf(x));
+            }
+        } else {
+            const uint16_t* o = a.o + row * a.d + sub * per;
+            for (int j = 0; j < per; ++j) {
+                const float x = bf16_to_f32(g[j]);
+                acc += bf16_to_f32(o[j]) * x;
+                mx = fmaxf(mx, fabsf(x));
+            }
+        }
     }
 #pragma unroll
     for (int off = 8; off >= 1; off >>= 1) acc += __shfl_xor(acc, off);
     if (row < rows && sub == 0) a.delta[row] = acc;
+    mx = wave_max(mx);
+    if ((threadIdx.x & 63) == 0) atomicMax(a.dmax, __float_as_uint(mx));   // mx >= 0: bits order like values
+}
+
+// Power-of-two factor s with max |s dO| in [8, 16); 1 for an all-zero dO.
+__device__ __forceinline__ float dout_scale(const uint32_t* dmax) {
+    const float mx = __uint_as_float(*dmax);
+    if (!(mx > 0.f) || !isfinite(mx)) return 1.f;
+    int e;
+    frexpf(mx, &e);           // mx = f 2^e, f in [0.5, 1)
+    return ldexpf(1.f, max(-100, min(100, 4 - e)));
 }
 
 // ------------------------------------------------------------------ dQ (query-major)
@@ -79,7 +114,8 @@ __global__ void __launch_bounds__(kThreads) bwd_dq_kernel(AttnArgs a) {
     const float c2 = a.scale * kLog2e;
     const float lse_n = a.lse[grow];
     const float lse2 = lse_n == -INFINITY ? INFINITY : lse_n * kLog2e;   // empty row: P = 0
-    const float dlt = a.delta[grow];
+    const float sc = dout_scale(a.dmax);
+    const float dlt = a.delta[grow] * sc;
 
     f32x16 acc[ND];
 #pragma unroll
@@ -113,9 +149,9 @@ __global__ void __launch_bounds__(kThreads) bwd_dq_kernel(AttnArgs a) {
             }
         }
         __syncthreads();
-        stage_rows<D, kThreads>(sm.k, kp, sm.kidx, tid);
-        stage_rows<D, kThreads>(sm.v, vp, sm.kidx, tid);
-        stage_transposed<D, kThreads>(sm.kt, kp, sm.kidx, tid);
+        stage_rows<D, kThreads>(sm.k, kp, IndexedRows{sm.kidx}, tid);
+        stage_rows<D, kThreads>(sm.v, vp, IndexedRows{sm.kidx}, tid);
+        stage_transposed_f16<D, kThreads>(sm.kt, kp, IndexedRows{sm.kidx}, 1.0f, tid);
         __syncthreads();
 
         f32x16 sacc[2], pacc[2];
@@ -131,7 +167,7 @@ __global__ void __launch_bounds__(kThreads) bwd_dq_kernel(AttnArgs a) {
                 pacc[c] = mfma32(lds_read16(vrow + 16 * s), dreg[s], pacc[c]);
             }
         }
-        // dZ^T = P o (dP^T - Delta), P = exp2(c2 s - lse2) on visible entries
+        // s dZ^T = P o (s dP^T - s Delta), P = exp2(c2 z - lse2) on visible entries
 #pragma unroll
         for (int c = 0; c < 2; ++c)
 #pragma unroll
@@ -141,31 +177,32 @@ __global__ void __launch_bounds__(kThreads) bwd_dq_kernel(AttnArgs a) {
                     const int key = 32 * c + 8 * (r >> 2) + 4 * h + (r & 3);
                     if (qrow < sm.lim[key]) p = 0.f;
                 }
-                sacc[c][r] = p * (pacc[c][r] - dlt);
+                sacc[c][r] = p * (pacc[c][r] * sc - dlt);
             }
         u32x4 zb[4];
-        zb[0] = pack8(sacc[0], 0);
-        zb[1] = pack8(sacc[0], 8);
-        zb[2] = pack8(sacc[1], 0);
-        zb[3] = pack8(sacc[1], 8);
+        zb[0] = pack8_f16<0>(sacc[0]);
+        zb[1] = pack8_f16<8>(sacc[0]);
+        zb[2] = pack8_f16<0>(sacc[1]);
+        zb[3] = pack8_f16<8>(sacc[1]);
 #pragma unroll
         for (int i = 0; i < ND; ++i) {
             const uint16_t* trow = sm.kt + (32 * i + l32) * TileLds<D>::kTStride + 8 * h;
 #pragma unroll
-            for (int g = 0; g < 4; ++g) acc[i] = mfma32(lds_read16(trow + 16 * g), zb[g], acc[i]);
+            for (int g = 0; g < 4; ++g) acc[i] = mfma32h(lds_read16(trow + 16 * g), zb[g], acc[i]);
         }
         __syncthreads();
     }
     float* dq = a.dq + grow * D;
+    const float fin = a.scale / sc;
 #pragma unroll
     for (int i = 0; i < ND; ++i)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
             f32x4 val;
-            val.x = acc[i][4 * g + 0] * a.scale;
-            val.y = acc[i][4 * g + 1] * a.scale;
-            val.z = acc[i][4 * g + 2] * a.scale;
-            val.w = acc[i][4 * g + 3] * a.scale;
+            val.x = acc[i][4 * g + 0] * fin;
+            val.y = acc[i][4 * g + 1] * fin;
+            val.z = acc[i][4 * g + 2] * fin;
+            val.w = acc[i][4 * g + 3] * fin;
             f32x4* dst = reinterpret_cast<f32x4*>(dq + 32 * i + 8 * g + 4 * h);
             if (a.dq_accumulate) val += *dst;
             *dst = val;
@@ -183,57 +220,13 @@ struct KvLds {
     float dlt[64];
 };
 
-// Contiguous row range staged through the shared helpers.
-struct RowsFrom {
-    int32_t base;
-};
-
-template <int D, int NT>
-__device__ __forceinline__ void stage_rows_contig(uint16_t* lds, const uint16_t* __restrict__ src, int tid) {
-    constexpr int kChunks = D / 8;
-    constexpr int kRowsPerPass = NT / kChunks;
-#pragma unroll
-    for (int p = 0; p < 64 / kRowsPerPass; ++p) {
-        const int r = p * kRowsPerPass + tid / kChunks;
-        const int c = tid % kChunks;
-        *reinterpret_cast<u32x4*>(lds + r * TileLds<D>::kRowStride + c * 8) =
-            *reinterpret_cast<const u32x4*>(src + int64_t(r) * D + c * 8);
-    }
-}
-
-template <int D, int NT>
-__device__ __forceinline__ void stage_transposed_contig(uint16_t* lds, const uint16_t* __restrict__ src, int tid) {
-    constexpr int kItems = 16 * (D / 8);
-#pragma unroll
-    for (int p = 0; p < (kItems + NT - 1) / NT; ++p) {
-        const int item = p * NT + tid;
-        if (kItems % NT != 0 && item >= kItems) break;
-        const int q4 = item & 15, dc = item >> 4;
-        u32x4 r[4];
-#pragma unroll
-        for (int bb = 0; bb < 4; ++bb) r[bb] = *reinterpret_cast<const u32x4*>(src + int64_t(4 * q4 + bb) * D + dc * 8);
-        const int pos = tpos(4 * q4);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const uint32_t w0 = r[0][e], w1 = r[1][e], w2 = r[2][e], w3 = r[3][e];
-            u32x2 even, odd;
-            even.x = (w0 & 0xffffu) | (w1 << 16);
-            even.y = (w2 & 0xffffu) | (w3 << 16);
-            odd.x = (w0 >> 16) | (w1 & 0xffff0000u);
-            odd.y = (w2 >> 16) | (w3 & 0xffff0000u);
-            const int d0 = dc * 8 + 2 * e;
-            *reinterpret_cast<u32x2*>(lds + d0 * TileLds<D>::kTStride + pos) = even;
-            *reinterpret_cast<u32x2*>(lds + (d0 + 1) * TileLds<D>::kTStride + pos) = odd;
-        }
-    }
-}
-
 // One 64-row query tile against this wave's 32 keys.  `active` / `lim` give
 // the per-key visibility: key visible to in-block query row r iff active and
 // r >= lim.
 template <int D>
 __device__ __forceinline__ void kv_tile(const KvLds<D>& sm, const u32x4* kreg, const u32x4* vreg, bool masked,
-                                        bool active, int lim, float c2, int h, int l32, f32x16* dv, f32x16* dk) {
+                                        bool active, int lim, float c2, float sc, int h, int l32, f32x16* dv,
+                                        f32x16* dk) {
     constexpr int KD = D / 16, ND = D / 32;
     f32x16 sacc[2], pacc[2];
 #pragma unroll
@@ -257,40 +250,42 @@ __device__ __forceinline__ void kv_tile(const KvLds<D>& sm, const u32x4* kreg, c
             float p = fast_exp2(sacc[rb][r] * c2 - sm.lse2[row]);
             if (masked && (!active || row < lim)) p = 0.f;
             sacc[rb][r] = p;
-            pacc[rb][r] = p * (pacc[rb][r] - sm.dlt[row]);
+            pacc[rb][r] = p * (pacc[rb][r] * sc - sm.dlt[row]);
         }
     u32x4 pb[4], zb[4];
-    pb[0] = pack8(sacc[0], 0);
-    pb[1] = pack8(sacc[0], 8);
-    pb[2] = pack8(sacc[1], 0);
-    pb[3] = pack8(sacc[1], 8);
-    zb[0] = pack8(pacc[0], 0);
-    zb[1] = pack8(pacc[0], 8);
-    zb[2] = pack8(pacc[1], 0);
-    zb[3] = pack8(pacc[1], 8);
+    pb[0] = pack8_f16<0>(sacc[0]);
+    pb[1] = pack8_f16<8>(sacc[0]);
+    pb[2] = pack8_f16<0>(sacc[1]);
+    pb[3] = pack8_f16<8>(sacc[1]);
+    zb[0] = pack8_f16<0>(pacc[0]);
+    zb[1] = pack8_f16<8>(pacc[0]);
+    zb[2] = pack8_f16<0>(pacc[1]);
+    zb[3] = pack8_f16<8>(pacc[1]);
 #pragma unroll
     for (int i = 0; i < ND; ++i) {
         const uint16_t* gt = sm.gt + (32 * i + l32) * TileLds<D>::kTStride + 8 * h;
         const uint16_t* qt = sm.qt + (32 * i + l32) * TileLds<D>::kTStride + 8 * h;
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-            dv[i] = mfma32(lds_read16(gt + 16 * g), pb[g], dv[i]);
-            dk[i] = mfma32(lds_read16(qt + 16 * g), zb[g], dk[i]);
+            dv[i] = mfma32h(lds_read16(gt + 16 * g), pb[g], dv[i]);
+            dk[i] = mfma32h(lds_read16(qt + 16 * g), zb[g], dk[i]);
         }
     }
 }
 
 template <int D>
-__device__ __forceinline__ void kv_stage_query_tile(KvLds<D>& sm, const AttnArgs& a, int bh, int qb, int tid) {
+__device__ __forceinline__ void kv_stage_query_tile(KvLds<D>& sm, const AttnArgs& a, int bh, int qb, float sc,
+                                                    int tid) {
     const int64_t row0 = int64_t(bh) * a.Nq + int64_t(qb) * 64;
-    stage_rows_contig<D, kThreads>(sm.q, a.q + row0 * D, tid);
-    stage_transposed_contig<D, kThreads>(sm.qt, a.q + row0 * D, tid);
-    stage_rows_contig<D, kThreads>(sm.g, a.dout + row0 * D, tid);
-    stage_transposed_contig<D, kThreads>(sm.gt, a.dout + row0 * D, tid);
+    const ContiguousRows rows{row0};
+    stage_rows<D, kThreads>(sm.q, a.q, rows, tid);
+    stage_transposed_f16<D, kThreads>(sm.qt, a.q, rows, 1.0f, tid);
+    stage_rows<D, kThreads>(sm.g, a.dout, rows, tid);
+    stage_transposed_f16<D, kThreads>(sm.gt, a.dout, rows, sc, tid);
     if (tid < 64) {
         const float l = a.lse[row0 + tid];
         sm.lse2[tid] = l == -INFINITY ? INFINITY : l * kLog2e;
-        sm.dlt[tid] = a.delta[row0 + tid];
+        sm.dlt[tid] = a.delta[row0 + tid] * sc;
     }
 }
 
@@ -322,6 +317,7 @@ __global__ void __launch_bounds__(kThreads) bwd_dkdv_kernel(AttnArgs a) {
         dk[i] = f32x16{};
     }
     const float c2 = a.scale * kLog2e;
+    const float sc = dout_scale(a.dmax);
     const int32_t kg = a.k_blk_global[kb];
     for (int g = 0; g < G; ++g) {
         const int bh = b * a.Hq + hk * G + g;
@@ -330,27 +326,28 @@ __global__ void __launch_bounds__(kThreads) bwd_dkdv_kernel(AttnArgs a) {
         for (int64_t p = p0; p < p1; ++p) {
             const int qb = a.kblk_idx[p];
             const bool masked = a.q_blk_global[qb] == kg;   // diagonal tile
-            kv_stage_query_tile<D>(sm, a, bh, qb, tid);
+            kv_stage_query_tile<D>(sm, a, bh, qb, sc, tid);
             __syncthreads();
-            kv_tile<D>(sm, kreg, vreg, masked, true, key, c2, h, l32, dv, dk);
+            kv_tile<D>(sm, kreg, vreg, masked, true, key, c2, sc, h, l32, dv, dk);
             __syncthreads();
         }
     }
     float* dkp = a.dk + krow * D;
     float* dvp = a.dv + krow * D;
+    const float fk = a.scale / sc, fv = 1.f / sc;
 #pragma unroll
     for (int i = 0; i < ND; ++i)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
             f32x4 x, y;
-            x.x = dk[i][4 * g + 0] * a.scale;
-            x.y = dk[i][4 * g + 1] * a.scale;
-            x.z = dk[i][4 * g + 2] * a.scale;
-            x.w = dk[i][4 * g + 3] * a.scale;
-            y.x = dv[i][4 * g + 0];
-            y.y = dv[i][4 * g + 1];
-            y.z = dv[i][4 * g + 2];
-            y.w = dv[i][4 * g + 3];
+            x.x = dk[i][4 * g + 0] * fk;
+            x.y = dk[i][4 * g + 1] * fk;
+            x.z = dk[i][4 * g + 2] * fk;
+            x.w = dk[i][4 * g + 3] * fk;
+            y.x = dv[i][4 * g + 0] * fv;
+            y.y = dv[i][4 * g + 1] * fv;
+            y.z = dv[i][4 * g + 2] * fv;
+            y.w = dv[i][4 * g + 3] * fv;
             *reinterpret_cast<f32x4*>(dkp + 32 * i + 8 * g + 4 * h) = x;
             *reinterpret_cast<f32x4*>(dvp + 32 * i + 8 * g + 4 * h) = y;
         }
@@ -392,6 +389,7 @@ __global__ void __launch_bounds__(kThreads) bwd_dkdv_col_kernel(AttnArgs a, int3
         dk[i] = f32x16{};
     }
     const float c2 = a.scale * kLog2e;
+    const float sc = dout_scale(a.dmax);
     const uint32_t* db = a.diag_bits + int64_t(bh) * a.dwords;
     // the first column of the chunk has the smallest global block
     const int32_t cg_min = a.k_blk_global[a.vcol_idx[e0] >> 6];
@@ -400,27 +398,28 @@ __global__ void __launch_bounds__(kThreads) bwd_dkdv_col_kernel(AttnArgs a, int3
         if (qg < cg_min) continue;   // uniform across the workgroup
         const bool active = valid && qg >= cg && !dbit(db, qg - cg);
         const int lim = qg == cg ? cin : 0;
-        kv_stage_query_tile<D>(sm, a, bh, qb, tid);
+        kv_stage_query_tile<D>(sm, a, bh, qb, sc, tid);
         __syncthreads();
-        kv_tile<D>(sm, kreg, vreg, true, active, lim, c2, h, l32, dv, dk);
+        kv_tile<D>(sm, kreg, vreg, true, active, lim, c2, sc, h, l32, dv, dk);
         __syncthreads();
     }
     if (!valid) return;
     float* dkp = a.dk_col + (e0 + key) * D;
     float* dvp = a.dv_col + (e0 + key) * D;
+    const float fk = a.scale / sc, fv = 1.f / sc;
 #pragma unroll
     for (int i = 0; i < ND; ++i)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
             f32x4 x, y;
-            x.x = dk[i][4 * g + 0] * a.scale;
-            x.y = dk[i][4 * g + 1] * a.scale;
-            x.z = dk[i][4 * g + 2] * a.scale;
-            x.w = dk[i][4 * g + 3] * a.scale;
-            y.x = dv[i][4 * g + 0];
-            y.y = dv[i][4 * g + 1];
-            y.z = dv[i][4 * g + 2];
-            y.w = dv[i][4 * g + 3];
+            x.x = dk[i][4 * g + 0] * fk;
+            x.y = dk[i][4 * g + 1] * fk;
+            x.z = dk[i][4 * g + 2] * fk;
+            x.w = dk[i][4 * g + 3] * fk;
+            y.x = dv[i][4 * g + 0] * fv;
+            y.y = dv[i][4 * g + 1] * fv;
+            y.z = dv[i][4 * g + 2] * fv;
+            y.w = dv[i][4 * g + 3] * fv;
             *reinterpret_cast<f32x4*>(dkp + 32 * i + 8 * g + 4 * h) = x;
             *reinterpret_cast<f32x4*>(dvp + 32 * i + 8 * g + 4 * h) = y;
         }
@@ -457,6 +456,7 @@ __global__ void __launch_bounds__(128) bwd_colmerge_kernel(AttnArgs a) {
 template <int D>
 hipError_t launch_bwd_d(const AttnArgs& a, hipStream_t s) {
     const int64_t rows = int64_t(a.B) * a.Hq * a.Nq;
+    hipLaunchKernelGGL(bwd_init_kernel, dim3(1), dim3(64), 0, s, a);
     if (rows > 0) hipLaunchKernelGGL(bwd_delta_kernel, dim3(unsigned((rows + 15) / 16)), dim3(256), 0, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

@@ -8,7 +8,9 @@
 //   online softmax    (each lane owns one query row, the partner lane l^32
 //                      holds the other half of its keys),
 //   O^T += V^T P^T    (A = V^T from the transposed LDS copy, B = P straight
-//                      from the S^T accumulator).
+//                      from the S^T accumulator; this product runs in fp16,
+//                      whose 3 extra significand bits keep the rounding of P
+//                      well below the output tolerance at the same MFMA rate).
 // Block tiles come first, then the column list in chunks of 64 gathered keys.
 // Scores use exp2 with scale * log2(e) folded in; lse is stored as a natural log.
 #include "common.h"
@@ -95,8 +97,8 @@ __global__ void __launch_bounds__(kFwdThreads) attn_fwd_kernel(AttnArgs a) {
             }
         }
         __syncthreads();
-        stage_rows<D, kFwdThreads>(sm.k, kp, sm.kidx, tid);
-        stage_transposed<D, kFwdThreads>(sm.vt, vp, sm.kidx, tid);
+        stage_rows<D, kFwdThreads>(sm.k, kp, IndexedRows{sm.kidx}, tid);
+        stage_transposed_f16<D, kFwdThreads>(sm.vt, vp, IndexedRows{sm.kidx}, 1.0f, tid);
         __syncthreads();
 
         // ---- S^T for keys 0-31 (c = 0) and 32-63 (c = 1)
@@ -143,15 +145,15 @@ __global__ void __launch_bounds__(kFwdThreads) attn_fwd_kernel(AttnArgs a) {
 
         // ---- O^T += V^T P^T
         u32x4 pb[4];
-        pb[0] = pack8(sacc[0], 0);
-        pb[1] = pack8(sacc[0], 8);
-        pb[2] = pack8(sacc[1], 0);
-        pb[3] = pack8(sacc[1], 8);
+        pb[0] = pack8_f16<0>(sacc[0]);
+        pb[1] = pack8_f16<8>(sacc[0]);
+        pb[2] = pack8_f16<0>(sacc[1]);
+        pb[3] = pack8_f16<8>(sacc[1]);
 #pragma unroll
         for (int i = 0; i < ND; ++i) {
             const uint16_t* vrow = sm.vt + (32 * i + l32) * TileLds<D>::kTStride + 8 * h;
 #pragma unroll
-            for (int g = 0; g < 4; ++g) oacc[i] = mfma32(lds_read16(vrow + 16 * g), pb[g], oacc[i]);
+            for (int g = 0; g < 4; ++g) oacc[i] = mfma32h(lds_read16(vrow + 16 * g), pb[g], oacc[i]);
         }
         __syncthreads();
     }
@@ -159,15 +161,23 @@ __global__ void __launch_bounds__(kFwdThreads) attn_fwd_kernel(AttnArgs a) {
     // ---- epilogue: normalise, store bf16 out and natural-log lse
     const bool empty = !(l_run > 0.f);
     const float inv = empty ? 0.f : 1.f / l_run;
-    uint16_t* op = a.out + (int64_t(bh) * a.Nq + int64_t(qb) * 64 + qrow) * D;
+    const int64_t orow = (int64_t(bh) * a.Nq + int64_t(qb) * 64 + qrow) * D;
 #pragma unroll
     for (int i = 0; i < ND; ++i)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-            u32x2 pk;
-            pk.x = pack_bf16x2(oacc[i][4 * g + 0] * inv, oacc[i][4 * g + 1] * inv);
-            pk.y = pack_bf16x2(oacc[i][4 * g + 2] * inv, oacc[i][4 * g + 3] * inv);
-            *reinterpret_cast<u32x2*>(op + 32 * i + 8 * g + 4 * h) = pk;
+            f32x4 o4;
+            o4.x = oacc[i][4 * g + 0] * inv;
+            o4.y = oacc[i][4 * g + 1] * inv;
+            o4.z = oacc[i][4 * g + 2] * inv;
+            o4.w = oacc[i][4 * g + 3] * inv;
+            if (a.out) {
+                u32x2 pk;
+                pk.x = pack_bf16x2(o4.x, o4.y);
+                pk.y = pack_bf16x2(o4.z, o4.w);
+                *reinterpret_cast<u32x2*>(a.out + orow + 32 * i + 8 * g + 4 * h) = pk;
+            }
+            if (a.out_f32) *reinterpret_cast<f32x4*>(a.out_f32 + orow + 32 * i + 8 * g + 4 * h) = o4;
         }
     if (h == 0) {
         float* lp = a.lse + int64_t(bh) * a.Nq + int64_t(qb) * 64 + qrow;
@@ -183,8 +193,8 @@ __global__ void merge_kernel(MergeArgs m) {
     const int64_t row = i / per_row;
     const int64_t col = (i % per_row) * 4;
     const float lp = m.lse_part[row];
-    const u32x2 pk = *reinterpret_cast<const u32x2*>(m.o_part + row * m.d + col);
-    float po[4] = {bf16_lo(pk.x), bf16_hi(pk.x), bf16_lo(pk.y), bf16_hi(pk.y)};
+    const f32x4 pk = *reinterpret_cast<const f32x4*>(m.o_part + row * m.d + col);
+    float po[4] = {pk.x, pk.y, pk.z, pk.w};
     float res[4];
     float lnew;
     if (m.first) {

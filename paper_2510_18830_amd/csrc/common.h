@@ -33,6 +33,19 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
 }
 
+// bf16 bits -> fp16 bits.  Exact for |x| in [2^-14, 65504] (fp16 carries more
+// significand bits than bf16); smaller magnitudes lose precision as fp16
+// subnormals.  `mul` is a power of two applied first (exact).
+__device__ __forceinline__ uint32_t bf16_to_f16_bits(uint32_t b, float mul) {
+    const _Float16 h = (_Float16)(__uint_as_float(b << 16) * mul);
+    return uint32_t(__builtin_bit_cast(uint16_t, h));
+}
+__device__ __forceinline__ uint32_t pack_f16x2(float lo, float hi) {
+    const uint32_t a = __builtin_bit_cast(uint16_t, (_Float16)lo);
+    const uint32_t b = __builtin_bit_cast(uint16_t, (_Float16)hi);
+    return a | (b << 16);
+}
+
 // ---------------------------------------------------------------- MFMA
 // D(32x32) += A(32x16) * B(16x32), bf16 inputs, fp32 accumulate.
 // Lane l supplies A[l%32][8*(l/32) .. +8] and B[8*(l/32) .. +8][l%32];
@@ -40,6 +53,13 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 __device__ __forceinline__ f32x16 mfma32(const u32x4& a, const u32x4& b, const f32x16& c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
                                                   0, 0, 0);
+}
+
+typedef __attribute__((ext_vector_type(8))) _Float16 f16x8;
+// Same layout as mfma32, fp16 inputs.
+__device__ __forceinline__ f32x16 mfma32h(const u32x4& a, const u32x4& b, const f32x16& c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c, 0,
+                                                 0, 0);
 }
 
 // ---------------------------------------------------------------- math

@@ -60,6 +60,9 @@ struct AttnArgs {
     const uint16_t* o;     // forward output (bwd)
     const uint16_t* dout;  // bf16 [B,Hq,Nq,d] (bwd)
     uint16_t* out;         // bf16 [B,Hq,Nq,d] (fwd)
+    float* out_f32;        // optional fp32 copy of out (fwd)
+    const float* o_f32;    // optional fp32 forward output for Delta (bwd)
+    uint32_t* dmax;        // bwd workspace: max |dO| as fp32 bits
     float* lse;            // fwd output / bwd input
     float* delta;          // bwd workspace [B,Hq,Nq]
     float* dq;
@@ -88,7 +91,7 @@ hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t s);
 hipError_t launch_attn_bwd(const AttnArgs& a, hipStream_t s);
 
 struct MergeArgs {
-    const uint16_t* o_part;
+    const float* o_part;
     const float* lse_part;
     float* o_acc;
     float* lse_acc;

@@ -1,16 +1,21 @@
-// LDS staging of 64-key tiles shared by the attention kernels.
+// LDS staging of 64-row tiles shared by the attention kernels.
 //
-// A "key tile" is 64 key rows of one KV head: either a 64 x 64 block of the
-// grid (rows kb*64 .. kb*64 + 63) or up to 64 gathered vertical columns.  It
-// is staged two ways:
-//   row-major  X[key][d]        (operand whose contraction runs over d)
-//   transposed Xt[d][pos(key)]  (operand whose contraction runs over keys)
-// The transposed copy stores each 16-key group in the order
-//   keys 0-3, 8-11, 4-7, 12-15
+// A tile is 64 rows of one head: a 64 x 64 block of the grid, or up to 64
+// gathered vertical columns (key rows named by an index list).  It is staged
+// two ways:
+//   row-major  X[row][d]        (operand whose contraction runs over d)
+//   transposed Xt[d][pos(row)]  (operand whose contraction runs over rows)
+// The transposed copy stores each 16-row group in the order
+//   rows 0-3, 8-11, 4-7, 12-15
 // because a 32x32 MFMA accumulator gives lane half h the rows
 // 8*(r/4) + 4*h + r%4; reading 8 consecutive positions at offset 8*h of a
-// 16-group then yields exactly the keys that the same lane holds in its
-// accumulator, so P (or dS) feeds the next MFMA straight from registers.
+// 16-group then yields exactly the rows that the same lane holds in its
+// accumulator, so P (or dZ) feeds the next MFMA straight from registers.
+//
+// The transposed copy is converted to fp16 (times a power-of-two factor) for
+// the second GEMM of each pair (P V, P^T dO, dZ K, dZ^T Q): fp16 holds 3 more
+// significand bits than bf16, which keeps the rounding of P and dZ far below
+// the gradient tolerance at the same MFMA rate.
 #pragma once
 
 #include "common.h"
@@ -19,39 +24,49 @@ namespace msparse {
 
 template <int D>
 struct TileLds {
-    static constexpr int kRowStride = D + 8;    // bf16 elements, row-major rows
-    static constexpr int kTStride = 64 + 8;     // bf16 elements, transposed rows
+    static constexpr int kRowStride = D + 8;    // 16-bit elements per row-major row
+    static constexpr int kTStride = 64 + 8;     // 16-bit elements per transposed row
     static constexpr int kRowElems = 64 * kRowStride;
     static constexpr int kTElems = D * kTStride;
 };
 
-// position of key k (0..63) inside a transposed row
+// position of row k (0..63) inside a transposed row
 __device__ __forceinline__ int tpos(int k) {
     const int a = (k >> 2) & 3;
     const int sw = ((a & 1) << 1) | (a >> 1);
     return (k & ~15) | (sw << 2) | (k & 3);
 }
 
-// Row-major staging: 64 rows x D bf16 from `src` rows kidx[r] (row length D).
-template <int D, int NT>
-__device__ __forceinline__ void stage_rows(uint16_t* lds, const uint16_t* __restrict__ src, const int32_t* kidx,
-                                           int tid) {
+// Row sources: rows named by an LDS index list, or a contiguous run.
+struct IndexedRows {
+    const int32_t* idx;
+    __device__ __forceinline__ int64_t operator()(int r) const { return idx[r]; }
+};
+struct ContiguousRows {
+    int64_t base;
+    __device__ __forceinline__ int64_t operator()(int r) const { return base + r; }
+};
+
+// Row-major staging of 64 rows x D bf16 (row length D in `src`).
+template <int D, int NT, class Rows>
+__device__ __forceinline__ void stage_rows(uint16_t* lds, const uint16_t* __restrict__ src, Rows rows, int tid) {
     constexpr int kChunks = D / 8;              // 16-byte chunks per row
     constexpr int kRowsPerPass = NT / kChunks;
 #pragma unroll
     for (int p = 0; p < 64 / kRowsPerPass; ++p) {
         const int r = p * kRowsPerPass + tid / kChunks;
         const int c = tid % kChunks;
-        const u32x4 v = *reinterpret_cast<const u32x4*>(src + int64_t(kidx[r]) * D + c * 8);
+        const u32x4 v = *reinterpret_cast<const u32x4*>(src + rows(r) * D + c * 8);
         *reinterpret_cast<u32x4*>(lds + r * TileLds<D>::kRowStride + c * 8) = v;
     }
 }
 
-// Transposed staging: Xt[d][tpos(key)] for 64 rows kidx[r] of `src`.
-template <int D, int NT>
-__device__ __forceinline__ void stage_transposed(uint16_t* lds, const uint16_t* __restrict__ src,
-                                                 const int32_t* kidx, int tid) {
-    constexpr int kItems = 16 * (D / 8);  // (4-key quad) x (8-wide d chunk)
+// Transposed staging Xt[d][tpos(row)], converted to fp16 after multiplying by
+// `mul` (a power of two).
+template <int D, int NT, class Rows>
+__device__ __forceinline__ void stage_transposed_f16(uint16_t* lds, const uint16_t* __restrict__ src, Rows rows,
+                                                     float mul, int tid) {
+    constexpr int kItems = 16 * (D / 8);  // (4-row quad) x (8-wide d chunk)
 #pragma unroll
     for (int p = 0; p < (kItems + NT - 1) / NT; ++p) {
         const int item = p * NT + tid;
@@ -60,17 +75,15 @@ __device__ __forceinline__ void stage_transposed(uint16_t* lds, const uint16_t* 
         const int dc = item >> 4;
         u32x4 r[4];
 #pragma unroll
-        for (int b = 0; b < 4; ++b)
-            r[b] = *reinterpret_cast<const u32x4*>(src + int64_t(kidx[4 * q4 + b]) * D + dc * 8);
+        for (int b = 0; b < 4; ++b) r[b] = *reinterpret_cast<const u32x4*>(src + rows(4 * q4 + b) * D + dc * 8);
         const int pos = tpos(4 * q4);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            const uint32_t w0 = r[0][e], w1 = r[1][e], w2 = r[2][e], w3 = r[3][e];
             u32x2 even, odd;
-            even.x = (w0 & 0xffffu) | (w1 << 16);
-            even.y = (w2 & 0xffffu) | (w3 << 16);
-            odd.x = (w0 >> 16) | (w1 & 0xffff0000u);
-            odd.y = (w2 >> 16) | (w3 & 0xffff0000u);
+            even.x = bf16_to_f16_bits(r[0][e] & 0xffffu, mul) | (bf16_to_f16_bits(r[1][e] & 0xffffu, mul) << 16);
+            even.y = bf16_to_f16_bits(r[2][e] & 0xffffu, mul) | (bf16_to_f16_bits(r[3][e] & 0xffffu, mul) << 16);
+            odd.x = bf16_to_f16_bits(r[0][e] >> 16, mul) | (bf16_to_f16_bits(r[1][e] >> 16, mul) << 16);
+            odd.y = bf16_to_f16_bits(r[2][e] >> 16, mul) | (bf16_to_f16_bits(r[3][e] >> 16, mul) << 16);
             const int d0 = dc * 8 + 2 * e;
             *reinterpret_cast<u32x2*>(lds + d0 * TileLds<D>::kTStride + pos) = even;
             *reinterpret_cast<u32x2*>(lds + (d0 + 1) * TileLds<D>::kTStride + pos) = odd;
@@ -81,13 +94,14 @@ __device__ __forceinline__ void stage_transposed(uint16_t* lds, const uint16_t* 
 // 16-byte LDS read
 __device__ __forceinline__ u32x4 lds_read16(const uint16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
 
-// pack 8 consecutive accumulator values (regs base .. base+7) to bf16 x 8
-__device__ __forceinline__ u32x4 pack8(const f32x16& acc, int base) {
+// pack 8 consecutive accumulator values (regs base .. base+7) to fp16 x 8
+template <int BASE>
+__device__ __forceinline__ u32x4 pack8_f16(const f32x16& acc) {
     u32x4 r;
-    r.x = pack_bf16x2(acc[base + 0], acc[base + 1]);
-    r.y = pack_bf16x2(acc[base + 2], acc[base + 3]);
-    r.z = pack_bf16x2(acc[base + 4], acc[base + 5]);
-    r.w = pack_bf16x2(acc[base + 6], acc[base + 7]);
+    r.x = pack_f16x2(acc[BASE + 0], acc[BASE + 1]);
+    r.y = pack_f16x2(acc[BASE + 2], acc[BASE + 3]);
+    r.z = pack_f16x2(acc[BASE + 4], acc[BASE + 5]);
+    r.w = pack_f16x2(acc[BASE + 6], acc[BASE + 7]);
     return r;
 }
 

@@ -98,7 +98,8 @@ def test_fwd_ring_steps_merge(gpu, layout, W):
         k_loc = x["k"][:, :, krows].contiguous().to(gpu)
         v_loc = x["v"][:, :, krows].contiguous().to(gpu)
         idx = ms.make_index(dims, tv, ts, ring)
-        po, pl = ms.attn_fwd(dims, q_loc, k_loc, v_loc, idx)
+        po = torch.empty(q_loc.shape, dtype=torch.float32, device=q_loc.device)
+        _, pl = ms.attn_fwd(dims, q_loc, k_loc, v_loc, idx, out_f32=po, bf16_out=False)
         ms.merge_out_lse(dims, po, pl, o_acc, l_acc, out if t == W - 1 else None, first=(t == 0))
     torch.cuda.synchronize()
     assert_close("ring out", out.float().cpu().numpy(), ref_o)

@@ -65,14 +65,14 @@ def test_validation_before_launch():
     _bad(-1, L.msparse_index_count, ctypes.byref(d), iv, 10, iv, 10, ctypes.byref(r), ctypes.byref(ctypes.c_int64()),
          ctypes.byref(ctypes.c_int64()), ctypes.byref(ctypes.c_int64()), fake, 1 << 30, None)
     # a null index
-    _bad(-1, L.msparse_attn_fwd, ctypes.byref(d), fake, fake, fake, None, fake, fake, None, 0, None)
+    _bad(-1, L.msparse_attn_fwd, ctypes.byref(d), fake, fake, fake, None, fake, fake, None, None)
 
 
 def test_index_capacity_needs_overflow_flag_or_bound():
     L = ms.lib()
     d = ms.make_dims(1, 4096, 1, 1, 64)
     fake = ctypes.c_void_p(16)
-    x = ms.IndexStruct(fake, fake, 10, fake, fake, 10, fake, fake, fake, fake, 10, fake, fake, fake, None)
+    x = ms.IndexStruct(fake, fake, 10, fake, fake, 10, fake, fake, fake, fake, 10, fake, fake, fake, None, 1)
     ws = L.msparse_index_workspace(ctypes.byref(d), 8, 8, None)
     assert ws > 0
     _bad(-3, L.msparse_build_index, ctypes.byref(d), fake, 8, fake, 8, None, ctypes.byref(x), fake, ws, None)
