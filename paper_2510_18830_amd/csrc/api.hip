@@ -441,14 +441,7 @@ msparse_status msparse_estimate(const msparse_dims* dims, const void* q, const v
     const size_t scores = align_up(size_t(dims->batch) * dims->heads_q * N * sizeof(float));
     a.v_score = v_score ? v_score : reinterpret_cast<float*>(base);
     a.s_score = s_score ? s_score : reinterpret_cast<float*>(base + scores);
-    Carve c{base + 2 * scores};
-    const int64_t BH = int64_t(a.B) * a.Hq;
-    a.nchunk = (N + 1023) / 1024;
-    a.part_max = c.take<float>(size_t(BH) * a.nchunk * kBlock);
-    a.part_sum = c.take<float>(size_t(BH) * a.nchunk * kBlock);
-    a.row_lse = c.take<float>(size_t(BH) * kBlock);
-    a.diag_part = c.take<float>(size_t(BH) * (N / kBlock) * 2 * kBlock);
-    a.topk_state = c.take<uint32_t>(size_t(2 * BH) * 8);
+    est_carve(a, base + 2 * scores);
     hipStream_t s = static_cast<hipStream_t>(stream);
     return check_hip(launch_estimate(a, s), s, "estimate");
 }

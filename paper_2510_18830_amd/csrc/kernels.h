@@ -112,15 +112,15 @@ struct EstArgs {
     float* s_score;     // [B*Hq, N]
     int32_t* v_idx;
     int32_t* s_idx;
-    // workspace
-    float* part_max;    // [B*Hq, nchunk, L]
-    float* part_sum;    // [B*Hq, nchunk, L]
-    float* row_lse;     // [B*Hq, L] (log2 domain)
-    float* diag_part;   // [B*Hq, nkb, 128]
+    // workspace (est_carve)
+    float* part_max;    // [B*Hq, nchunk, 64]
+    float* part_sum;    // [B*Hq, nchunk, 64]
+    float* row_lse;     // [B*Hq, 64] (log2 domain)
+    float* diag_part;   // [B*Hq, N/64, 128]
     int32_t nchunk;
-    uint32_t* topk_state;  // [2*B*Hq, 4]
 };
 size_t est_workspace_bytes(int32_t B, int32_t Hq, int32_t N, int32_t L);
+void est_carve(EstArgs& a, char* base);
 hipError_t launch_estimate(const EstArgs& a, hipStream_t s);
 
 }  // namespace msparse
