@@ -221,6 +221,22 @@ MSPARSE_API msparse_status msparse_attn_bwd(const msparse_dims* dims, const void
                                 const msparse_index* index, float* dq, float* dk, float* dv,
                                 int32_t dq_accumulate, void* workspace, size_t workspace_bytes, void* stream);
 
+/* ------------------------------------------------------------------------ */
+/* Kernel-level tracing for measurement.  While enabled, every kernel the
+ * library launches is bracketed by two HIP events on its stream.
+ * msparse_trace_read waits for the recorded events, writes up to `cap`
+ * per-kernel totals (launch count and summed milliseconds) into `out`, clears
+ * the record and returns the number of distinct kernels.  Host-side state,
+ * shared by all threads; do not enable it around graph capture. */
+typedef struct {
+    char name[32];
+    int32_t launches;
+    double total_ms;
+} msparse_trace_entry;
+
+MSPARSE_API void msparse_trace_enable(int32_t on);
+MSPARSE_API int32_t msparse_trace_read(msparse_trace_entry* out, int32_t cap);
+
 #ifdef __cplusplus
 }
 #endif

@@ -109,12 +109,19 @@ class Index:
             hb, hc = [], []
             for qi in range(nqb):
                 g = int(qg[qi])
+                if W == 1:     # whole sequence: local numbering is the global one
+                    hb.append(blocks[g])
+                    hc.append(cols[g])
+                    continue
                 hb.append(np.array([kloc[int(j)] for j in blocks[g] if int(j) in kloc], dtype=np.int64))
                 hc.append(np.array([kloc[int(c) // BLOCK] * BLOCK + int(c) % BLOCK
                                     for c in cols[g] if int(c) // BLOCK in kloc], dtype=np.int64))
             self.blocks.append(hb)
             self.cols.append(hc)
             V = np.unique(v2[bh].astype(np.int64))
+            if W == 1:
+                self.vcols.append(V)
+                continue
             self.vcols.append(np.array([kloc[int(c) // BLOCK] * BLOCK + int(c) % BLOCK
                                         for c in V if int(c) // BLOCK in kloc], dtype=np.int64))
 

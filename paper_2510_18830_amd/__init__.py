@@ -43,8 +43,14 @@ class IndexStruct(ctypes.Structure):
                 ("world", c_i32)]
 
 
+class TraceEntry(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 32), ("launches", c_i32), ("total_ms", ctypes.c_double)]
+
+
 _P = ctypes.POINTER
 _SIGS = {
+    "msparse_trace_enable": (None, [c_i32]),
+    "msparse_trace_read": (c_i32, [_P(TraceEntry), c_i32]),
     "msparse_strerror": (ctypes.c_char_p, [c_i32]),
     "msparse_last_error": (ctypes.c_char_p, []),
     "msparse_estimate_workspace": (c_sz, [_P(Dims), c_i32, c_i32, c_i32]),
@@ -242,3 +248,17 @@ def attn_bwd(dims, q, k, v, out, dout, lse, index: SparseIndex, dq=None, dk=None
 
 def default_scale(head_dim: int) -> float:
     return 1.0 / math.sqrt(head_dim)
+
+
+# ------------------------------------------------------------------ tracing
+def trace_enable(on: bool = True):
+    """Bracket every library kernel launch with HIP events (for measurement)."""
+    lib().msparse_trace_enable(int(bool(on)))
+
+
+def trace_read() -> dict:
+    """{kernel name: (launches, total ms)} since the last read (waits for the events)."""
+    cap = 64
+    buf = (TraceEntry * cap)()
+    n = lib().msparse_trace_read(buf, cap)
+    return {buf[i].name.decode(): (int(buf[i].launches), float(buf[i].total_ms)) for i in range(min(n, cap))}

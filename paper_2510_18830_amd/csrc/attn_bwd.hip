@@ -25,6 +25,7 @@
 // of the incoming gradient; results are divided by s.
 #include "common.h"
 #include "kernels.h"
+#include "trace.h"
 #include "tiles.h"
 
 namespace msparse {
@@ -40,27 +41,29 @@ __global__ void bwd_init_kernel(AttnArgs a) {
 }
 
 __global__ void __launch_bounds__(256) bwd_delta_kernel(AttnArgs a) {
-    // 16 lanes per row, d / 16 elements per lane
+    // 16 lanes per row, d / 16 consecutive elements per lane (8 for d = 128)
     const int64_t rows = int64_t(a.B) * a.Hq * a.Nq;
     const int64_t row = int64_t(blockIdx.x) * 16 + (threadIdx.x >> 4);
     const int sub = threadIdx.x & 15;
     float acc = 0.f, mx = 0.f;
     if (row < rows) {
-        const int per = a.d / 16;
-        const uint16_t* g = a.dout + row * a.d + sub * per;
-        if (a.o_f32) {
-            const float* o = a.o_f32 + row * a.d + sub * per;
-            for (int j = 0; j < per; ++j) {
-                const float x = bf16_to_f32(g[j]);
-                acc += o[j] * x;
-                mx = fmaxf(mx, fabsf(x));
+        const int per = a.d / 16;                 // 8 or 4
+        const int64_t base = row * a.d + sub * per;
+        for (int j0 = 0; j0 < per; j0 += 4) {
+            const u32x2 g = *reinterpret_cast<const u32x2*>(a.dout + base + j0);
+            const float gv[4] = {bf16_lo(g.x), bf16_hi(g.x), bf16_lo(g.y), bf16_hi(g.y)};
+            float ov[4];
+            if (a.o_f32) {
+                const f32x4 o = *reinterpret_cast<const f32x4*>(a.o_f32 + base + j0);
+                ov[0] = o.x; ov[1] = o.y; ov[2] = o.z; ov[3] = o.w;
+            } else {
+                const u32x2 o = *reinterpret_cast<const u32x2*>(a.o + base + j0);
+                ov[0] = bf16_lo(o.x); ov[1] = bf16_hi(o.x); ov[2] = bf16_lo(o.y); ov[3] = bf16_hi(o.y);
             }
-        } else {
-            const uint16_t* o = a.o + row * a.d + sub * per;
-            for (int j = 0; j < per; ++j) {
-                const float x = bf16_to_f32(g[j]);
-                acc += bf16_to_f32(o[j]) * x;
-                mx = fmaxf(mx, fabsf(x));
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                acc += ov[j] * gv[j];
+                mx = fmaxf(mx, fabsf(gv[j]));
             }
         }
     }
@@ -398,6 +401,8 @@ __global__ void __launch_bounds__(kThreads) bwd_dkdv_col_kernel(AttnArgs a, int3
         if (qg < cg_min) continue;   // uniform across the workgroup
         const bool active = valid && qg >= cg && !dbit(db, qg - cg);
         const int lim = qg == cg ? cin : 0;
+        // every column covered by a selected block-diagonal: nothing to do here
+        if (!__syncthreads_or(active)) continue;
         kv_stage_query_tile<D>(sm, a, bh, qb, sc, tid);
         __syncthreads();
         kv_tile<D>(sm, kreg, vreg, true, active, lim, c2, sc, h, l32, dv, dk);
@@ -456,22 +461,22 @@ __global__ void __launch_bounds__(128) bwd_colmerge_kernel(AttnArgs a) {
 template <int D>
 hipError_t launch_bwd_d(const AttnArgs& a, hipStream_t s) {
     const int64_t rows = int64_t(a.B) * a.Hq * a.Nq;
-    hipLaunchKernelGGL(bwd_init_kernel, dim3(1), dim3(64), 0, s, a);
-    if (rows > 0) hipLaunchKernelGGL(bwd_delta_kernel, dim3(unsigned((rows + 15) / 16)), dim3(256), 0, s, a);
+    { TraceScope _t("bwd_init", s); hipLaunchKernelGGL(bwd_init_kernel, dim3(1), dim3(64), 0, s, a); }
+    if (rows > 0) { TraceScope _t("bwd_delta", s); hipLaunchKernelGGL(bwd_delta_kernel, dim3(unsigned((rows + 15) / 16)), dim3(256), 0, s, a); }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int64_t qgrid = int64_t(a.B) * a.Hq * a.nqb;
-    if (qgrid > 0) hipLaunchKernelGGL(bwd_dq_kernel<D>, dim3(unsigned(qgrid)), dim3(kThreads), 0, s, a);
+    if (qgrid > 0) { TraceScope _t("bwd_dq", s); hipLaunchKernelGGL(bwd_dq_kernel<D>, dim3(unsigned(qgrid)), dim3(kThreads), 0, s, a); }
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const int64_t kgrid = int64_t(a.B) * a.Hkv * a.nkb;
-    if (kgrid > 0) hipLaunchKernelGGL(bwd_dkdv_kernel<D>, dim3(unsigned(kgrid)), dim3(kThreads), 0, s, a);
+    if (kgrid > 0) { TraceScope _t("bwd_dkdv", s); hipLaunchKernelGGL(bwd_dkdv_kernel<D>, dim3(unsigned(kgrid)), dim3(kThreads), 0, s, a); }
     if ((e = hipGetLastError()) != hipSuccess) return e;
     // column chunks: at most ceil(Nk / 64) per head (a head has <= Nk verticals in a shard)
     const int32_t chunks = a.nkb;
     const int64_t cgrid = int64_t(a.B) * a.Hq * chunks;
-    if (cgrid > 0) hipLaunchKernelGGL(bwd_dkdv_col_kernel<D>, dim3(unsigned(cgrid)), dim3(kThreads), 0, s, a, chunks);
+    if (cgrid > 0) { TraceScope _t("bwd_dkdv_col", s); hipLaunchKernelGGL(bwd_dkdv_col_kernel<D>, dim3(unsigned(cgrid)), dim3(kThreads), 0, s, a, chunks); }
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    if (kgrid > 0) hipLaunchKernelGGL(bwd_colmerge_kernel, dim3(unsigned(kgrid)), dim3(128), 0, s, a);
+    if (kgrid > 0) { TraceScope _t("bwd_colmerge", s); hipLaunchKernelGGL(bwd_colmerge_kernel, dim3(unsigned(kgrid)), dim3(128), 0, s, a); }
     return hipGetLastError();
 }
 

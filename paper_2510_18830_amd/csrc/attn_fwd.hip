@@ -15,6 +15,7 @@
 // Scores use exp2 with scale * log2(e) folded in; lse is stored as a natural log.
 #include "common.h"
 #include "kernels.h"
+#include "trace.h"
 #include "tiles.h"
 
 namespace msparse {
@@ -230,16 +231,16 @@ __global__ void merge_kernel(MergeArgs m) {
 hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t s) {
     const int64_t grid = int64_t(a.B) * a.Hq * a.nqb;
     if (a.d == 128)
-        hipLaunchKernelGGL(attn_fwd_kernel<128>, dim3(unsigned(grid)), dim3(kFwdThreads), 0, s, a);
+        { TraceScope _t("attn_fwd", s); hipLaunchKernelGGL(attn_fwd_kernel<128>, dim3(unsigned(grid)), dim3(kFwdThreads), 0, s, a); }
     else
-        hipLaunchKernelGGL(attn_fwd_kernel<64>, dim3(unsigned(grid)), dim3(kFwdThreads), 0, s, a);
+        { TraceScope _t("attn_fwd", s); hipLaunchKernelGGL(attn_fwd_kernel<64>, dim3(unsigned(grid)), dim3(kFwdThreads), 0, s, a); }
     return hipGetLastError();
 }
 
 hipError_t launch_merge(const MergeArgs& m, hipStream_t s) {
     const int64_t n = m.rows * (m.d / 4);
     const int threads = 256;
-    hipLaunchKernelGGL(merge_kernel, dim3(unsigned((n + threads - 1) / threads)), dim3(threads), 0, s, m);
+    { TraceScope _t("merge_out_lse", s); hipLaunchKernelGGL(merge_kernel, dim3(unsigned((n + threads - 1) / threads)), dim3(threads), 0, s, m); }
     return hipGetLastError();
 }
 

@@ -23,6 +23,7 @@
 // for in-block row r and key c.
 #include "common.h"
 #include "kernels.h"
+#include "trace.h"
 #include "tiles.h"
 
 namespace msparse {
@@ -318,12 +319,12 @@ __global__ void __launch_bounds__(kTopkThreads) est_topk_kernel(EstArgs a) {
 template <int D>
 hipError_t launch_d(const EstArgs& a, hipStream_t s) {
     const int BH = a.B * a.Hq;
-    hipLaunchKernelGGL(est_pass1_kernel<D>, dim3(BH * a.nchunk), dim3(kThreads), 0, s, a);
-    hipLaunchKernelGGL(est_combine_kernel, dim3(BH), dim3(64), 0, s, a);
-    hipLaunchKernelGGL(est_pass2_kernel<D>, dim3(BH * a.nchunk), dim3(kThreads), 0, s, a);
+    { TraceScope _t("est_pass1", s); hipLaunchKernelGGL(est_pass1_kernel<D>, dim3(BH * a.nchunk), dim3(kThreads), 0, s, a); }
+    { TraceScope _t("est_combine", s); hipLaunchKernelGGL(est_combine_kernel, dim3(BH), dim3(64), 0, s, a); }
+    { TraceScope _t("est_pass2", s); hipLaunchKernelGGL(est_pass2_kernel<D>, dim3(BH * a.nchunk), dim3(kThreads), 0, s, a); }
     const int64_t n = int64_t(BH) * a.N;
-    hipLaunchKernelGGL(est_diag_kernel, dim3(unsigned((n + 255) / 256)), dim3(256), 0, s, a);
-    hipLaunchKernelGGL(est_topk_kernel, dim3(2 * BH), dim3(kTopkThreads), 0, s, a);
+    { TraceScope _t("est_diag", s); hipLaunchKernelGGL(est_diag_kernel, dim3(unsigned((n + 255) / 256)), dim3(256), 0, s, a); }
+    { TraceScope _t("est_topk", s); hipLaunchKernelGGL(est_topk_kernel, dim3(2 * BH), dim3(kTopkThreads), 0, s, a); }
     return hipGetLastError();
 }
 

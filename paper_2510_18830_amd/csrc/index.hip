@@ -15,6 +15,7 @@
 //   fill  the count pass again, writing entries in order via wave ballots.
 #include "common.h"
 #include "kernels.h"
+#include "trace.h"
 
 namespace msparse {
 
@@ -313,26 +314,26 @@ __global__ void __launch_bounds__(1024) index_scan_kernel(IndexArgs a) {
 
 hipError_t launch_index_prep(const IndexArgs& a, hipStream_t s) {
     const size_t shmem = size_t(a.dwords) * sizeof(uint32_t);
-    hipLaunchKernelGGL(index_prep_kernel, dim3(a.BH), dim3(kPrepThreads), shmem, s, a);
+    { TraceScope _t("index_prep", s); hipLaunchKernelGGL(index_prep_kernel, dim3(a.BH), dim3(kPrepThreads), shmem, s, a); }
     return hipGetLastError();
 }
 
 hipError_t launch_index_count(const IndexArgs& a, hipStream_t s) {
     const int64_t items = int64_t(a.BH) * (a.nqb + a.nkb);
     const int64_t grid = (items + kItemWaves - 1) / kItemWaves;
-    hipLaunchKernelGGL(index_items_kernel<false>, dim3(unsigned(grid)), dim3(64 * kItemWaves), 0, s, a);
+    { TraceScope _t("index_count", s); hipLaunchKernelGGL(index_items_kernel<false>, dim3(unsigned(grid)), dim3(64 * kItemWaves), 0, s, a); }
     return hipGetLastError();
 }
 
 hipError_t launch_index_scan(const IndexArgs& a, hipStream_t s) {
-    hipLaunchKernelGGL(index_scan_kernel, dim3(4), dim3(1024), 0, s, a);
+    { TraceScope _t("index_scan", s); hipLaunchKernelGGL(index_scan_kernel, dim3(4), dim3(1024), 0, s, a); }
     return hipGetLastError();
 }
 
 hipError_t launch_index_fill(const IndexArgs& a, hipStream_t s) {
     const int64_t items = int64_t(a.BH) * (a.nqb + a.nkb) + a.BH;
     const int64_t grid = (items + kItemWaves - 1) / kItemWaves;
-    hipLaunchKernelGGL(index_items_kernel<true>, dim3(unsigned(grid)), dim3(64 * kItemWaves), 0, s, a);
+    { TraceScope _t("index_fill", s); hipLaunchKernelGGL(index_items_kernel<true>, dim3(unsigned(grid)), dim3(64 * kItemWaves), 0, s, a); }
     return hipGetLastError();
 }
 
