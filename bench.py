@@ -95,7 +95,19 @@ def main():
     ap.add_argument("--also", default="layer_128k", help="second workload timed the same way ('' to skip)")
     ap.add_argument("--cpu-rows", type=int, default=64)
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB (HBM counter calibration) and exit")
     args = ap.parse_args()
+    if args.copy_calibration:
+        import torch
+        n = args.copy_calibration * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_each_way": n * 4, "launches": 3}))
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU: the sparse path here runs on a single MI355X "
@@ -120,6 +132,7 @@ def main():
                                dev)
         idx_ws = ms._workspace(ms.index_workspace_bytes(dims, wl.k_v, wl.k_s), dev)
         bwd_ws = ms._workspace(ms.attn_bwd_workspace_bytes(dims, B * Hq * wl.k_v), dev)
+        fwd_ws = ms._workspace(ms.attn_fwd_workspace_bytes(dims), dev)
         v_idx = torch.empty((B, Hq, wl.k_v), dtype=torch.int32, device=dev)
         s_idx = torch.empty((B, Hq, wl.k_s), dtype=torch.int32, device=dev)
         out = torch.empty_like(q)
@@ -149,7 +162,7 @@ def main():
             ms.build_index(dims, v_idx, s_idx, idx, workspace=idx_ws)
             mark("index", 1)
             mark("fwd", 0)
-            ms.attn_fwd(dims, q, k, v, idx, out=out, lse=lse, out_f32=out32)
+            ms.attn_fwd(dims, q, k, v, idx, out=out, lse=lse, out_f32=out32, workspace=fwd_ws)
             mark("fwd", 1)
             mark("bwd", 0)
             ms.attn_bwd(dims, q, k, v, out, do, lse, idx, dq, dk, dv, out_f32=out32, workspace=bwd_ws)

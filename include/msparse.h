@@ -188,9 +188,12 @@ MSPARSE_API msparse_status msparse_build_index(const msparse_dims* dims, const i
  * nearest even), lse fp32.  out_f32 (fp32 [B, Hq, Nq, d], may be NULL) also
  * receives the unrounded output; msparse_attn_bwd computes
  * Delta = dO . O more accurately from it, and ring steps merge it.  out may be
- * NULL when out_f32 is given. */
+ * NULL when out_f32 is given.  Workspace: msparse_attn_fwd_workspace(dims)
+ * bytes (currently 0; NULL is accepted then). */
+MSPARSE_API size_t msparse_attn_fwd_workspace(const msparse_dims* dims);
 MSPARSE_API msparse_status msparse_attn_fwd(const msparse_dims* dims, const void* q, const void* k, const void* v,
-                                const msparse_index* index, void* out, float* lse, float* out_f32, void* stream);
+                                const msparse_index* index, void* out, float* lse, float* out_f32,
+                                void* workspace, size_t workspace_bytes, void* stream);
 
 /* Log-sum-exp merge of one ring step's partial result into a running one
  * (merge_out_and_lse, Algorithm 2): lse = logaddexp(lse_acc, lse_part),

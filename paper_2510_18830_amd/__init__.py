@@ -59,7 +59,8 @@ _SIGS = {
     "msparse_index_count": (c_i32, [_P(Dims), c_vp, c_i32, c_vp, c_i32, _P(Ring), _P(c_i64), _P(c_i64), _P(c_i64),
                                     c_vp, c_sz, c_vp]),
     "msparse_build_index": (c_i32, [_P(Dims), c_vp, c_i32, c_vp, c_i32, _P(Ring), _P(IndexStruct), c_vp, c_sz, c_vp]),
-    "msparse_attn_fwd": (c_i32, [_P(Dims), c_vp, c_vp, c_vp, _P(IndexStruct), c_vp, c_vp, c_vp, c_vp]),
+    "msparse_attn_fwd_workspace": (c_sz, [_P(Dims)]),
+    "msparse_attn_fwd": (c_i32, [_P(Dims), c_vp, c_vp, c_vp, _P(IndexStruct), c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]),
     "msparse_merge_out_lse": (c_i32, [_P(Dims), c_vp, c_vp, c_vp, c_vp, c_vp, c_i32, c_vp]),
     "msparse_attn_bwd_workspace": (c_sz, [_P(Dims), c_i64]),
     "msparse_attn_bwd": (c_i32, [_P(Dims), c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, _P(IndexStruct), c_vp, c_vp,
@@ -211,14 +212,21 @@ def make_index(dims, v_idx, s_idx, ring=None, stream=None) -> SparseIndex:
 
 
 # ------------------------------------------------------------------ attention
-def attn_fwd(dims, q, k, v, index: SparseIndex, out=None, lse=None, out_f32=None, stream=None, bf16_out=True):
+def attn_fwd_workspace_bytes(dims):
+    return int(lib().msparse_attn_fwd_workspace(ctypes.byref(dims)))
+
+
+def attn_fwd(dims, q, k, v, index: SparseIndex, out=None, lse=None, out_f32=None, stream=None, bf16_out=True,
+             workspace=None):
     """msparse_attn_fwd: returns (out bf16 [B,Hq,Nq,d] or None, lse fp32 [B,Hq,Nq]); out_f32 is optional."""
     if out is None and bf16_out:
         out = torch.empty_like(q)
     if lse is None:
         lse = torch.empty(q.shape[:-1], dtype=torch.float32, device=q.device)
+    if workspace is None:
+        workspace = _workspace(attn_fwd_workspace_bytes(dims), q.device)
     _check(lib().msparse_attn_fwd(ctypes.byref(dims), _p(q), _p(k), _p(v), ctypes.byref(index.struct), _p(out),
-                                  _p(lse), _p(out_f32), _stream(stream)))
+                                  _p(lse), _p(out_f32), _p(workspace), workspace.numel(), _stream(stream)))
     return out, lse
 
 

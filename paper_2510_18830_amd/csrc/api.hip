@@ -318,12 +318,21 @@ static msparse_status fill_attn(const msparse_dims* d, const msparse_index* x, A
     return MSPARSE_OK;
 }
 
+size_t msparse_attn_fwd_workspace(const msparse_dims* dims) {
+    (void)dims;
+    return 0;
+}
+
 msparse_status msparse_attn_fwd(const msparse_dims* dims, const void* q, const void* k, const void* v,
-                                const msparse_index* index, void* out, float* lse, float* out_f32, void* stream) {
+                                const msparse_index* index, void* out, float* lse, float* out_f32, void* ws,
+                                size_t ws_bytes, void* stream) {
     msparse_status st = check_dims(dims, false);
     if (st) return st;
     if (!q || !k || !v || (!out && !out_f32) || !lse) return fail(MSPARSE_ERR_INVALID, "tensor pointer is NULL");
     if ((st = check_index_struct(dims, index, false))) return st;
+    const size_t need = msparse_attn_fwd_workspace(dims);
+    if (need && (!ws || ws_bytes < need))
+        return fail(MSPARSE_ERR_WORKSPACE, "fwd workspace %zu < %zu bytes", ws_bytes, need);
     if (dims->seq_q == 0) return MSPARSE_OK;
     AttnArgs a{};
     fill_attn(dims, index, &a);
@@ -358,10 +367,11 @@ msparse_status msparse_merge_out_lse(const msparse_dims* dims, const float* o_pa
 
 size_t msparse_attn_bwd_workspace(const msparse_dims* dims, int64_t vcol_cap) {
     if (check_dims(dims, false) || vcol_cap < 0) return 0;
+    const size_t segs = (size_t(dims->seq_q / kBlock) + kColSeg - 1) / kColSeg;
     Carve c{nullptr};
     c.take<float>(size_t(dims->batch) * dims->heads_q * dims->seq_q);
-    c.take<float>(size_t(vcol_cap) * dims->head_dim);
-    c.take<float>(size_t(vcol_cap) * dims->head_dim);
+    c.take<float>(segs * size_t(vcol_cap) * dims->head_dim);
+    c.take<float>(segs * size_t(vcol_cap) * dims->head_dim);
     c.take<uint32_t>(1);
     return c.off;
 }
@@ -382,8 +392,10 @@ msparse_status msparse_attn_bwd(const msparse_dims* dims, const void* q, const v
     fill_attn(dims, index, &a);
     Carve c{static_cast<char*>(ws)};
     a.delta = c.take<float>(size_t(dims->batch) * dims->heads_q * dims->seq_q);
-    a.dk_col = c.take<float>(size_t(index->vcol_cap) * dims->head_dim);
-    a.dv_col = c.take<float>(size_t(index->vcol_cap) * dims->head_dim);
+    const size_t segs = (size_t(dims->seq_q / kBlock) + kColSeg - 1) / kColSeg;
+    a.dk_col = c.take<float>(segs * size_t(index->vcol_cap) * dims->head_dim);
+    a.dv_col = c.take<float>(segs * size_t(index->vcol_cap) * dims->head_dim);
+    a.vcol_cap = index->vcol_cap;
     a.dmax = c.take<uint32_t>(1);
     a.o_f32 = out_f32;
     a.q = static_cast<const uint16_t*>(q);

@@ -40,48 +40,53 @@ __global__ void bwd_init_kernel(AttnArgs a) {
     if (threadIdx.x == 0) *a.dmax = 0u;
 }
 
+constexpr int kDeltaBlocks = 2048;
+
 __global__ void __launch_bounds__(256) bwd_delta_kernel(AttnArgs a) {
-    // 16 lanes per row, d / 16 consecutive elements per lane (8 for d = 128)
+    // 16 lanes per row, d / 16 consecutive elements per lane; grid-stride over
+    // groups of 16 rows, one max-atomic per workgroup
+    __shared__ float wmax[4];
     const int64_t rows = int64_t(a.B) * a.Hq * a.Nq;
-    const int64_t row = int64_t(blockIdx.x) * 16 + (threadIdx.x >> 4);
     const int sub = threadIdx.x & 15;
-    float acc = 0.f, mx = 0.f;
-    if (row < rows) {
-        const int per = a.d / 16;                 // 8 or 4
-        const int64_t base = row * a.d + sub * per;
-        for (int j0 = 0; j0 < per; j0 += 4) {
-            const u32x2 g = *reinterpret_cast<const u32x2*>(a.dout + base + j0);
-            const float gv[4] = {bf16_lo(g.x), bf16_hi(g.x), bf16_lo(g.y), bf16_hi(g.y)};
-            float ov[4];
-            if (a.o_f32) {
-                const f32x4 o = *reinterpret_cast<const f32x4*>(a.o_f32 + base + j0);
-                ov[0] = o.x; ov[1] = o.y; ov[2] = o.z; ov[3] = o.w;
-            } else {
-                const u32x2 o = *reinterpret_cast<const u32x2*>(a.o + base + j0);
-                ov[0] = bf16_lo(o.x); ov[1] = bf16_hi(o.x); ov[2] = bf16_lo(o.y); ov[3] = bf16_hi(o.y);
-            }
+    const int per = a.d / 16;                 // 8 or 4
+    float mx = 0.f;
+    for (int64_t row0 = int64_t(blockIdx.x) * 16; row0 < rows; row0 += int64_t(gridDim.x) * 16) {
+        const int64_t row = row0 + (threadIdx.x >> 4);
+        float acc = 0.f;
+        if (row < rows) {
+            const int64_t base = row * a.d + sub * per;
+            for (int j0 = 0; j0 < per; j0 += 4) {
+                const u32x2 g = *reinterpret_cast<const u32x2*>(a.dout + base + j0);
+                const float gv[4] = {bf16_lo(g.x), bf16_hi(g.x), bf16_lo(g.y), bf16_hi(g.y)};
+                float ov[4];
+                if (a.o_f32) {
+                    const f32x4 o = *reinterpret_cast<const f32x4*>(a.o_f32 + base + j0);
+                    ov[0] = o.x; ov[1] = o.y; ov[2] = o.z; ov[3] = o.w;
+                } else {
+                    const u32x2 o = *reinterpret_cast<const u32x2*>(a.o + base + j0);
+                    ov[0] = bf16_lo(o.x); ov[1] = bf16_hi(o.x); ov[2] = bf16_lo(o.y); ov[3] = bf16_hi(o.y);
+                }
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                acc += ov[j] * gv[j];
-                mx = fmaxf(mx, fabsf(gv[j]));
+                for (int j = 0; j < 4; ++j) {
+                    acc += ov[j] * gv[j];
+                    mx = fmaxf(mx, fabsf(gv[j]));
+                }
             }
         }
-    }
 #pragma unroll
-    for (int off = 8; off >= 1; off >>= 1) acc += __shfl_xor(acc, off);
-    if (row < rows && sub == 0) a.delta[row] = acc;
+        for (int off = 8; off >= 1; off >>= 1) acc += __shfl_xor(acc, off);
+        if (row < rows && sub == 0) a.delta[row] = acc;
+    }
     mx = wave_max(mx);
-    if ((threadIdx.x & 63) == 0) atomicMax(a.dmax, __float_as_uint(mx));   // mx >= 0: bits order like values
+    if ((threadIdx.x & 63) == 0) wmax[threadIdx.x >> 6] = mx;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const float m = fmaxf(fmaxf(wmax[0], wmax[1]), fmaxf(wmax[2], wmax[3]));
+        atomicMax(a.dmax, __float_as_uint(m));   // m >= 0: bit patterns order like values
+    }
 }
 
-// Power-of-two factor s with max |s dO| in [8, 16); 1 for an all-zero dO.
-__device__ __forceinline__ float dout_scale(const uint32_t* dmax) {
-    const float mx = __uint_as_float(*dmax);
-    if (!(mx > 0.f) || !isfinite(mx)) return 1.f;
-    int e;
-    frexpf(mx, &e);           // mx = f 2^e, f in [0.5, 1)
-    return ldexpf(1.f, max(-100, min(100, 4 - e)));
-}
+__device__ __forceinline__ float dout_scale(const uint32_t* dmax) { return pow2_scale(dmax); }
 
 // ------------------------------------------------------------------ dQ (query-major)
 template <int D>
@@ -133,13 +138,11 @@ __global__ void __launch_bounds__(kThreads) bwd_dq_kernel(AttnArgs a) {
 
     for (int tt = 0; tt < nblk + ncolt; ++tt) {
         bool masked;
+        int kb = -1;
         if (tt < nblk) {
-            const int kb = a.blk_idx[b0 + tt];
+            kb = a.blk_idx[b0 + tt];
             masked = a.k_blk_global[kb] == qg;
-            if (tid < 64) {
-                sm.kidx[tid] = kb * 64 + tid;
-                sm.lim[tid] = tid;
-            }
+            if (masked && tid < 64) sm.lim[tid] = tid;
         } else {
             masked = true;
             const int64_t cbase = c0 + int64_t(tt - nblk) * 64;
@@ -150,11 +153,18 @@ __global__ void __launch_bounds__(kThreads) bwd_dq_kernel(AttnArgs a) {
                 sm.kidx[tid] = col;
                 sm.lim[tid] = tid < cnt ? (a.k_blk_global[col >> 6] == qg ? (col & 63) : 0) : 64;
             }
+            __syncthreads();
         }
-        __syncthreads();
-        stage_rows<D, kThreads>(sm.k, kp, IndexedRows{sm.kidx}, tid);
-        stage_rows<D, kThreads>(sm.v, vp, IndexedRows{sm.kidx}, tid);
-        stage_transposed_f16<D, kThreads>(sm.kt, kp, IndexedRows{sm.kidx}, 1.0f, tid);
+        if (kb >= 0) {
+            const ContiguousRows rows{int64_t(kb) * 64};
+            stage_rows<D, kThreads>(sm.k, kp, rows, tid);
+            stage_rows<D, kThreads>(sm.v, vp, rows, tid);
+            stage_transposed_f16<D, kThreads>(sm.kt, kp, rows, 1.0f, tid);
+        } else {
+            stage_rows<D, kThreads>(sm.k, kp, IndexedRows{sm.kidx}, tid);
+            stage_rows<D, kThreads>(sm.v, vp, IndexedRows{sm.kidx}, tid);
+            stage_transposed_f16<D, kThreads>(sm.kt, kp, IndexedRows{sm.kidx}, 1.0f, tid);
+        }
         __syncthreads();
 
         f32x16 sacc[2], pacc[2];
@@ -175,12 +185,12 @@ __global__ void __launch_bounds__(kThreads) bwd_dq_kernel(AttnArgs a) {
         for (int c = 0; c < 2; ++c)
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                float p = fast_exp2(sacc[c][r] * c2 - lse2);
+                float p = fast_exp2(__builtin_fmaf(sacc[c][r], c2, -lse2));
                 if (masked) {
                     const int key = 32 * c + 8 * (r >> 2) + 4 * h + (r & 3);
                     if (qrow < sm.lim[key]) p = 0.f;
                 }
-                sacc[c][r] = p * (pacc[c][r] * sc - dlt);
+                sacc[c][r] = p * __builtin_fmaf(pacc[c][r], sc, -dlt);
             }
         u32x4 zb[4];
         zb[0] = pack8_f16<0>(sacc[0]);
@@ -250,10 +260,10 @@ __device__ __forceinline__ void kv_tile(const KvLds<D>& sm, const u32x4* kreg, c
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             const int row = 32 * rb + 8 * (r >> 2) + 4 * h + (r & 3);
-            float p = fast_exp2(sacc[rb][r] * c2 - sm.lse2[row]);
+            float p = fast_exp2(__builtin_fmaf(sacc[rb][r], c2, -sm.lse2[row]));
             if (masked && (!active || row < lim)) p = 0.f;
             sacc[rb][r] = p;
-            pacc[rb][r] = p * (pacc[rb][r] * sc - sm.dlt[row]);
+            pacc[rb][r] = p * __builtin_fmaf(pacc[rb][r], sc, -sm.dlt[row]);
         }
     u32x4 pb[4], zb[4];
     pb[0] = pack8_f16<0>(sacc[0]);
@@ -359,8 +369,10 @@ __global__ void __launch_bounds__(kThreads) bwd_dkdv_kernel(AttnArgs a) {
 __device__ __forceinline__ bool dbit(const uint32_t* db, int32_t x) { return (db[x >> 5] >> (x & 31)) & 1u; }
 
 // Column pass: one workgroup per (head, 64 consecutive entries of the head's
-// vertical list).  Grid = B * Hq * ceil(max verticals per head / 64); surplus
-// workgroups exit.
+// vertical list, segment of kColSeg query blocks); grid.x covers
+// B * Hq * ceil(max verticals per head / 64) (surplus workgroups exit), grid.y
+// the segments.  Each writes the segment's partial dK / dV of its columns;
+// the merge kernel sums the segments in order.
 template <int D>
 __global__ void __launch_bounds__(kThreads) bwd_dkdv_col_kernel(AttnArgs a, int32_t chunks_per_head) {
     constexpr int KD = D / 16, ND = D / 32;
@@ -368,6 +380,7 @@ __global__ void __launch_bounds__(kThreads) bwd_dkdv_col_kernel(AttnArgs a, int3
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, l32 = lane & 31;
     const int bh = int(blockIdx.x / chunks_per_head);
     const int chunk = int(blockIdx.x % chunks_per_head);
+    const int seg = blockIdx.y;
     const int64_t v0 = a.vcol_ptr[bh], v1 = a.vcol_ptr[bh + 1];
     const int64_t e0 = v0 + int64_t(chunk) * 64;
     if (e0 >= v1) return;
@@ -396,7 +409,8 @@ __global__ void __launch_bounds__(kThreads) bwd_dkdv_col_kernel(AttnArgs a, int3
     const uint32_t* db = a.diag_bits + int64_t(bh) * a.dwords;
     // the first column of the chunk has the smallest global block
     const int32_t cg_min = a.k_blk_global[a.vcol_idx[e0] >> 6];
-    for (int qb = 0; qb < a.nqb; ++qb) {
+    const int qb1 = min(a.nqb, (seg + 1) * kColSeg);
+    for (int qb = seg * kColSeg; qb < qb1; ++qb) {
         const int32_t qg = a.q_blk_global[qb];
         if (qg < cg_min) continue;   // uniform across the workgroup
         const bool active = valid && qg >= cg && !dbit(db, qg - cg);
@@ -409,8 +423,9 @@ __global__ void __launch_bounds__(kThreads) bwd_dkdv_col_kernel(AttnArgs a, int3
         __syncthreads();
     }
     if (!valid) return;
-    float* dkp = a.dk_col + (e0 + key) * D;
-    float* dvp = a.dv_col + (e0 + key) * D;
+    const int64_t slot = int64_t(seg) * a.vcol_cap + e0 + key;
+    float* dkp = a.dk_col + slot * D;
+    float* dvp = a.dv_col + slot * D;
     const float fk = a.scale / sc, fv = 1.f / sc;
 #pragma unroll
     for (int i = 0; i < ND; ++i)
@@ -448,11 +463,17 @@ __global__ void __launch_bounds__(128) bwd_colmerge_kernel(AttnArgs a) {
             const int64_t m = (L + R) >> 1;
             if (a.vcol_idx[m] < lo) L = m + 1; else R = m;
         }
+        const int segs = (a.nqb + kColSeg - 1) / kColSeg;
         for (int64_t e = L; e < v1 && a.vcol_idx[e] < hi; ++e) {
             const int64_t row = int64_t(bk) * a.Nk + a.vcol_idx[e];
             for (int j = threadIdx.x; j < a.d; j += blockDim.x) {
-                a.dk[row * a.d + j] += a.dk_col[e * a.d + j];
-                a.dv[row * a.d + j] += a.dv_col[e * a.d + j];
+                float sk = 0.f, sv = 0.f;
+                for (int sg = 0; sg < segs; ++sg) {
+                    sk += a.dk_col[(int64_t(sg) * a.vcol_cap + e) * a.d + j];
+                    sv += a.dv_col[(int64_t(sg) * a.vcol_cap + e) * a.d + j];
+                }
+                a.dk[row * a.d + j] += sk;
+                a.dv[row * a.d + j] += sv;
             }
         }
     }
@@ -462,7 +483,12 @@ template <int D>
 hipError_t launch_bwd_d(const AttnArgs& a, hipStream_t s) {
     const int64_t rows = int64_t(a.B) * a.Hq * a.Nq;
     { TraceScope _t("bwd_init", s); hipLaunchKernelGGL(bwd_init_kernel, dim3(1), dim3(64), 0, s, a); }
-    if (rows > 0) { TraceScope _t("bwd_delta", s); hipLaunchKernelGGL(bwd_delta_kernel, dim3(unsigned((rows + 15) / 16)), dim3(256), 0, s, a); }
+    if (rows > 0) {
+        TraceScope _t("bwd_delta", s);
+        const int64_t groups = (rows + 15) / 16;
+        hipLaunchKernelGGL(bwd_delta_kernel, dim3(unsigned(groups < kDeltaBlocks ? groups : int64_t(kDeltaBlocks))),
+                           dim3(256), 0, s, a);
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int64_t qgrid = int64_t(a.B) * a.Hq * a.nqb;
@@ -471,10 +497,16 @@ hipError_t launch_bwd_d(const AttnArgs& a, hipStream_t s) {
     const int64_t kgrid = int64_t(a.B) * a.Hkv * a.nkb;
     if (kgrid > 0) { TraceScope _t("bwd_dkdv", s); hipLaunchKernelGGL(bwd_dkdv_kernel<D>, dim3(unsigned(kgrid)), dim3(kThreads), 0, s, a); }
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    // column chunks: at most ceil(Nk / 64) per head (a head has <= Nk verticals in a shard)
-    const int32_t chunks = a.nkb;
+    // column chunks: a head has at most min(vcol_cap, Nk) verticals in a shard
+    const int64_t vmax = a.vcol_cap < int64_t(a.Nk) ? a.vcol_cap : int64_t(a.Nk);
+    const int32_t chunks = int32_t((vmax + 63) / 64);
     const int64_t cgrid = int64_t(a.B) * a.Hq * chunks;
-    if (cgrid > 0) { TraceScope _t("bwd_dkdv_col", s); hipLaunchKernelGGL(bwd_dkdv_col_kernel<D>, dim3(unsigned(cgrid)), dim3(kThreads), 0, s, a, chunks); }
+    const int segs = (a.nqb + kColSeg - 1) / kColSeg;
+    if (cgrid > 0 && segs > 0) {
+        TraceScope _t("bwd_dkdv_col", s);
+        hipLaunchKernelGGL(bwd_dkdv_col_kernel<D>, dim3(unsigned(cgrid), unsigned(segs)), dim3(kThreads), 0, s, a,
+                           chunks);
+    }
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (kgrid > 0) { TraceScope _t("bwd_colmerge", s); hipLaunchKernelGGL(bwd_colmerge_kernel, dim3(unsigned(kgrid)), dim3(128), 0, s, a); }
     return hipGetLastError();

@@ -25,6 +25,7 @@ namespace {
 constexpr int kFwdThreads = 128;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
+constexpr float kSlack = 8.f;   // log2 units
 
 template <int D>
 struct FwdLds {
@@ -34,8 +35,11 @@ struct FwdLds {
     int32_t lim[64];   // key visible to in-block query row r iff r >= lim
 };
 
+// Two waves per SIMD (at most 256 registers per lane): the staging of one
+// workgroup overlaps the MFMA work of the other.
 template <int D>
-__global__ void __launch_bounds__(kFwdThreads) attn_fwd_kernel(AttnArgs a) {
+__global__ void __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+attn_fwd_kernel(AttnArgs a) {
     constexpr int KD = D / 16;   // k-steps over head_dim
     constexpr int ND = D / 32;   // 32-wide output column blocks
     __shared__ FwdLds<D> sm;
@@ -79,13 +83,11 @@ __global__ void __launch_bounds__(kFwdThreads) attn_fwd_kernel(AttnArgs a) {
     for (int tt = 0; tt < nblk + ncolt; ++tt) {
         // ---- tile metadata: key rows and per-key visibility limit
         bool masked;
+        int kb = -1;
         if (tt < nblk) {
-            const int kb = a.blk_idx[b0 + tt];
+            kb = a.blk_idx[b0 + tt];
             masked = a.k_blk_global[kb] == qg;    // diagonal tile: causal inside
-            if (tid < 64) {
-                sm.kidx[tid] = kb * 64 + tid;
-                sm.lim[tid] = tid;
-            }
+            if (masked && tid < 64) sm.lim[tid] = tid;
         } else {
             masked = true;
             const int64_t cbase = c0 + int64_t(tt - nblk) * 64;
@@ -96,10 +98,16 @@ __global__ void __launch_bounds__(kFwdThreads) attn_fwd_kernel(AttnArgs a) {
                 sm.kidx[tid] = col;
                 sm.lim[tid] = tid < cnt ? (a.k_blk_global[col >> 6] == qg ? (col & 63) : 0) : 64;
             }
+            __syncthreads();
         }
-        __syncthreads();
-        stage_rows<D, kFwdThreads>(sm.k, kp, IndexedRows{sm.kidx}, tid);
-        stage_transposed_f16<D, kFwdThreads>(sm.vt, vp, IndexedRows{sm.kidx}, 1.0f, tid);
+        if (kb >= 0) {
+            const ContiguousRows rows{int64_t(kb) * 64};
+            stage_rows<D, kFwdThreads>(sm.k, kp, rows, tid);
+            stage_transposed_f16<D, kFwdThreads>(sm.vt, vp, rows, 1.0f, tid);
+        } else {
+            stage_rows<D, kFwdThreads>(sm.k, kp, IndexedRows{sm.kidx}, tid);
+            stage_transposed_f16<D, kFwdThreads>(sm.vt, vp, IndexedRows{sm.kidx}, 1.0f, tid);
+        }
         __syncthreads();
 
         // ---- S^T for keys 0-31 (c = 0) and 32-63 (c = 1)
@@ -111,38 +119,46 @@ __global__ void __launch_bounds__(kFwdThreads) attn_fwd_kernel(AttnArgs a) {
 #pragma unroll
             for (int s = 0; s < KD; ++s) sacc[c] = mfma32(lds_read16(krow + 16 * s), qreg[s], sacc[c]);
         }
-        // ---- scale, mask, running max
+        // ---- mask, tile max (raw logits; scale > 0 commutes with max)
+        if (masked) {
+#pragma unroll
+            for (int c = 0; c < 2; ++c)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int key = 32 * c + 8 * (r >> 2) + 4 * h + (r & 3);
+                    if (qrow < sm.lim[key]) sacc[c][r] = -INFINITY;
+                }
+        }
         float mx = -INFINITY;
 #pragma unroll
         for (int c = 0; c < 2; ++c)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                float x = sacc[c][r] * c2;
-                if (masked) {
-                    const int key = 32 * c + 8 * (r >> 2) + 4 * h + (r & 3);
-                    if (qrow < sm.lim[key]) x = -INFINITY;
-                }
-                sacc[c][r] = x;
-                mx = fmaxf(mx, x);
-            }
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float m_new = fmaxf(m_run, mx);
-        const float m_use = m_new == -INFINITY ? 0.f : m_new;
-        const float alpha = fast_exp2(m_run - m_use);   // m_run = -inf -> 0
+            for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[c][r]);
+        mx = fmaxf(mx, __shfl_xor(mx, 32)) * c2;
+        // Lazy rescaling: keep the running maximum unless the tile exceeds it
+        // by more than kSlack (P then stays below 2^kSlack, well inside fp16),
+        // so the O accumulator is rescaled only on the rare tiles that raise
+        // the row maximum substantially.
+        const bool raise = mx > m_run + kSlack;
+        if (__any(raise)) {
+            const float m_new = raise ? mx : m_run;
+            const float alpha = m_run == -INFINITY ? 0.f : fast_exp2(m_run - m_new);
+            l_run *= alpha;
+#pragma unroll
+            for (int i = 0; i < ND; ++i) oacc[i] *= alpha;
+            m_run = m_new;
+        }
+        const float m_use = m_run == -INFINITY ? 0.f : m_run;
         float rs = 0.f;
 #pragma unroll
         for (int c = 0; c < 2; ++c)
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                const float p = fast_exp2(sacc[c][r] - m_use);
+                const float p = fast_exp2(__builtin_fmaf(sacc[c][r], c2, -m_use));
                 sacc[c][r] = p;
                 rs += p;
             }
-        rs += __shfl_xor(rs, 32);
-        l_run = l_run * alpha + rs;
-        m_run = m_new;
-#pragma unroll
-        for (int i = 0; i < ND; ++i) oacc[i] *= alpha;
+        l_run += rs + __shfl_xor(rs, 32);
 
         // ---- O^T += V^T P^T
         u32x4 pb[4];

@@ -23,14 +23,15 @@ __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w 
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float(uint32_t(h) << 16); }
 
-// fp32 -> bf16 bits, round to nearest even (inputs here are finite or +-inf).
-__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
-    uint32_t u = __float_as_uint(f);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return u >> 16;
-}
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+typedef __attribute__((ext_vector_type(2))) _Float16 f16x2;
+
+// fp32 pair -> packed bf16 / fp16, round to nearest even (one v_cvt_pk_* each)
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-    return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
+    bf16x2 v;
+    v.x = (__bf16)lo;
+    v.y = (__bf16)hi;
+    return __builtin_bit_cast(uint32_t, v);
 }
 
 // bf16 bits -> fp16 bits.  Exact for |x| in [2^-14, 65504] (fp16 carries more
@@ -41,9 +42,10 @@ __device__ __forceinline__ uint32_t bf16_to_f16_bits(uint32_t b, float mul) {
     return uint32_t(__builtin_bit_cast(uint16_t, h));
 }
 __device__ __forceinline__ uint32_t pack_f16x2(float lo, float hi) {
-    const uint32_t a = __builtin_bit_cast(uint16_t, (_Float16)lo);
-    const uint32_t b = __builtin_bit_cast(uint16_t, (_Float16)hi);
-    return a | (b << 16);
+    f16x2 v;
+    v.x = (_Float16)lo;
+    v.y = (_Float16)hi;
+    return __builtin_bit_cast(uint32_t, v);
 }
 
 // ---------------------------------------------------------------- MFMA
@@ -75,6 +77,16 @@ __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
     return v;
+}
+
+// Power-of-two factor s with max |s x| in [8, 16) given max |x| as fp32 bits;
+// 1 for zero or non-finite input.
+__device__ __forceinline__ float pow2_scale(const uint32_t* maxbits) {
+    const float mx = __uint_as_float(*maxbits);
+    if (!(mx > 0.f) || !isfinite(mx)) return 1.f;
+    int e;
+    frexpf(mx, &e);           // mx = f 2^e, f in [0.5, 1)
+    return ldexpf(1.f, max(-100, min(100, 4 - e)));
 }
 
 // ---------------------------------------------------------------- ring layout

@@ -68,8 +68,9 @@ struct AttnArgs {
     float* dq;
     float* dk;
     float* dv;
-    float* dk_col;         // bwd workspace [vcol_cap, d]
+    float* dk_col;         // bwd workspace [col segments, vcol_cap, d]
     float* dv_col;
+    int64_t vcol_cap;
     int32_t dq_accumulate;
     int32_t B, Hq, Hkv, Nq, Nk, d;
     int32_t nqb, nkb;
@@ -89,6 +90,8 @@ struct AttnArgs {
 };
 hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t s);
 hipError_t launch_attn_bwd(const AttnArgs& a, hipStream_t s);
+// query blocks per workgroup in the backward column pass
+constexpr int kColSeg = 512;
 
 struct MergeArgs {
     const float* o_part;

@@ -61,9 +61,9 @@ __device__ __forceinline__ void stage_rows(uint16_t* lds, const uint16_t* __rest
     }
 }
 
-// Transposed staging Xt[d][tpos(row)], converted to fp16 after multiplying by
-// `mul` (a power of two).
-template <int D, int NT, class Rows>
+// Transposed staging Xt[d][tpos(row)] (row stride TS elements), converted to
+// fp16 after multiplying by `mul` (a power of two).
+template <int D, int NT, class Rows, int TS = TileLds<D>::kTStride>
 __device__ __forceinline__ void stage_transposed_f16(uint16_t* lds, const uint16_t* __restrict__ src, Rows rows,
                                                      float mul, int tid) {
     constexpr int kItems = 16 * (D / 8);  // (4-row quad) x (8-wide d chunk)
@@ -85,8 +85,8 @@ __device__ __forceinline__ void stage_transposed_f16(uint16_t* lds, const uint16
             odd.x = bf16_to_f16_bits(r[0][e] >> 16, mul) | (bf16_to_f16_bits(r[1][e] >> 16, mul) << 16);
             odd.y = bf16_to_f16_bits(r[2][e] >> 16, mul) | (bf16_to_f16_bits(r[3][e] >> 16, mul) << 16);
             const int d0 = dc * 8 + 2 * e;
-            *reinterpret_cast<u32x2*>(lds + d0 * TileLds<D>::kTStride + pos) = even;
-            *reinterpret_cast<u32x2*>(lds + (d0 + 1) * TileLds<D>::kTStride + pos) = odd;
+            *reinterpret_cast<u32x2*>(lds + d0 * TS + pos) = even;
+            *reinterpret_cast<u32x2*>(lds + (d0 + 1) * TS + pos) = odd;
         }
     }
 }

@@ -65,7 +65,7 @@ def test_validation_before_launch():
     _bad(-1, L.msparse_index_count, ctypes.byref(d), iv, 10, iv, 10, ctypes.byref(r), ctypes.byref(ctypes.c_int64()),
          ctypes.byref(ctypes.c_int64()), ctypes.byref(ctypes.c_int64()), fake, 1 << 30, None)
     # a null index
-    _bad(-1, L.msparse_attn_fwd, ctypes.byref(d), fake, fake, fake, None, fake, fake, None, None)
+    _bad(-1, L.msparse_attn_fwd, ctypes.byref(d), fake, fake, fake, None, fake, fake, None, fake, 1 << 40, None)
 
 
 def test_index_capacity_needs_overflow_flag_or_bound():
