@@ -81,6 +81,104 @@ def cpu_baseline(wl, x, vi, si, rows_wanted: int):
                       f"{dt:.1f} s"}
 
 
+def ring_leg(x, v_idx, s_idx, wl, world: int, rank: int, steps: int):
+    """One worker's share of the striped ring (Section 4.2): its query shard
+    against every KV shard as sequential steps (forward with LSE merge, then
+    backward), plus the per-step and per-worker tile-work imbalance of the
+    striped and zigzag layouts from the index alone."""
+    import numpy as np
+    import torch
+    import paper_2510_18830_amd as ms
+    dev = x["q"].device
+    B, Hq, Hkv, N, d = wl.batch, wl.heads_q, wl.heads_kv, wl.seq, wl.head_dim
+    T = N // world
+    dims = ms.make_dims(B, T, Hq, Hkv, d)
+    lane = torch.arange(64, device=dev)
+
+    def rows_of(blk_global):
+        # the shard's tokens in local order, from the library's local -> global block map
+        return (blk_global.long()[:, None] * 64 + lane[None]).reshape(-1)
+
+    # work per (layout, worker, step) from the index counts: tiles + columns / 64
+    work = {}
+    idx_ws = ms._workspace(ms.index_workspace_bytes(dims, wl.k_v, wl.k_s, ms.make_ring(world, 0, 1)), dev)
+    for layout in ("striped", "zigzag"):
+        m = np.zeros((world, world))
+        for r in range(world):
+            for t in range(world):
+                blk, col, _ = ms.index_count(dims, v_idx, s_idx, ms.make_ring(world, r, t, layout),
+                                             workspace=idx_ws)
+                m[r, t] = blk + col / 64.0
+        work[layout] = m
+    # timed share of worker `rank`, striped (shard extraction stands in for the transfers)
+    shards, nnz = [], []
+    for t in range(world):
+        ring = ms.Ring(world, rank, t, ms.STRIPED)
+        blk, col, vcol = ms.index_count(dims, v_idx, s_idx, ring, workspace=idx_ws)
+        idx = ms.alloc_index(dims, blk, col, vcol, dev, world)
+        ms.build_index(dims, v_idx, s_idx, idx, ring, workspace=idx_ws)
+        kr = rows_of(idx["k_blk_global"])
+        shards.append((x["k"][:, :, kr].contiguous(), x["v"][:, :, kr].contiguous(), idx))
+        nnz.append((blk, col))
+    rr = rows_of(shards[0][2]["q_blk_global"])
+    q_loc = x["q"][:, :, rr].contiguous()
+    do_loc = x["do"][:, :, rr].contiguous()
+    o_acc = torch.empty(q_loc.shape, dtype=torch.float32, device=dev)
+    l_acc = torch.empty(q_loc.shape[:-1], dtype=torch.float32, device=dev)
+    part = torch.empty_like(o_acc)
+    lse_p = torch.empty_like(l_acc)
+    out = torch.empty_like(q_loc)
+    dq = torch.empty(q_loc.shape, dtype=torch.float32, device=dev)
+    dk = torch.empty(shards[0][0].shape, dtype=torch.float32, device=dev)
+    dv = torch.empty_like(dk)
+    bws = ms._workspace(max(ms.attn_bwd_workspace_bytes(dims, s[2].struct.vcol_cap) for s in shards), dev)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(world)]
+
+    def run(timed):
+        for t, (k_s, v_s, idx) in enumerate(shards):
+            if timed:
+                ev[t][0].record()
+            ms.attn_fwd(dims, q_loc, k_s, v_s, idx, lse=lse_p, out_f32=part, bf16_out=False)
+            ms.merge_out_lse(dims, part, lse_p, o_acc, l_acc, out if t == world - 1 else None, first=(t == 0))
+            if timed:
+                ev[t][1].record()
+        for t, (k_s, v_s, idx) in enumerate(shards):
+            if timed:
+                ev[t][2].record()
+            ms.attn_bwd(dims, q_loc, k_s, v_s, out, do_loc, l_acc, idx, dq, dk, dv, dq_accumulate=(t > 0),
+                        out_f32=o_acc, workspace=bws)
+            if timed:
+                ev[t][3].record()
+
+    run(False)
+    fwd_ms = np.zeros(world)
+    bwd_ms = np.zeros(world)
+    for _ in range(steps):
+        run(True)
+        torch.cuda.synchronize()
+        fwd_ms += [ev[t][0].elapsed_time(ev[t][1]) for t in range(world)]
+        bwd_ms += [ev[t][2].elapsed_time(ev[t][3]) for t in range(world)]
+    fwd_ms /= steps
+    bwd_ms /= steps
+    flops = np.array([3.5 * 4.0 * d * (4096.0 * b + 64.0 * c) for b, c in nnz])
+    total_ms = float(fwd_ms.sum() + bwd_ms.sum())
+
+    def imb(v):
+        v = np.asarray(v, dtype=np.float64)
+        return round(float(v.max() / v.mean()), 3)
+    return {
+        "workload": wl.name, "world": world, "rank": rank, "layout": "striped",
+        "step_ms_fwd": [round(float(v), 3) for v in fwd_ms], "step_ms_bwd": [round(float(v), 3) for v in bwd_ms],
+        "share_ms": round(total_ms, 2),
+        "share_tflops": round(float(flops.sum()) / (total_ms * 1e-3) / 1e12, 2),
+        "step_imbalance_time": imb(fwd_ms + bwd_ms),
+        "step_imbalance_work": {lay: imb(m[rank]) for lay, m in work.items()},
+        "worker_imbalance_work_mean_over_steps": {lay: round(float(np.mean([m[:, t].max() / m[:, t].mean()
+                                                                            for t in range(world)])), 3)
+                                                  for lay, m in work.items()},
+    }
+
+
 def torch_index(rows):
     import torch
     return torch.from_numpy(rows)
@@ -93,8 +191,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="layer_512k")
     ap.add_argument("--also", default="layer_128k", help="second workload timed the same way ('' to skip)")
-    ap.add_argument("--cpu-rows", type=int, default=64)
+    ap.add_argument("--cpu-rows", type=int, default=1024)
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--ring", type=int, default=1, help="also time worker 0's share of the 8-worker ring (512K)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (HBM counter calibration) and exit")
     args = ap.parse_args()
@@ -246,6 +345,13 @@ def main():
                 "tile_density_causal": round(r["density"], 4), "kernels": r["kernels"]}
             for n, r in results.items()},
     }
+    if args.ring and args.workload == "layer_512k":
+        rw = WORKLOADS["ring_512k_w8"]
+        print("[bench] ring share (worker 0 of 8, striped)", file=sys.stderr, flush=True)
+        vi_t = torch.from_numpy(main_r["v_idx"]).to(dev)
+        si_t = torch.from_numpy(main_r["s_idx"]).to(dev)
+        line["detail"]["ring_512k_w8"] = ring_leg(main_r["x"], vi_t, si_t, rw, rw.world, 0, max(1, args.steps // 2))
+        torch.cuda.empty_cache()
     if not args.no_cpu:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline(wl, main_r["x"], main_r["v_idx"], main_r["s_idx"], args.cpu_rows)

@@ -182,6 +182,6 @@ class Index:
 
 
 def imbalance(work) -> float:
-    """Imbalance degree max / mean (Section 5.3)."""
+    """Imbalance degree max / mean (Section 5.4, Workload Balance Analysis)."""
     w = np.asarray(work, dtype=np.float64)
     return float(w.max() / w.mean())

@@ -1,6 +1,6 @@
 """Seeded planted-pattern generator for the vertical-slash sparse-attention workloads.
 
-The paper trains Qwen2.5-3B / Llama-3.1-8B on ProLong at 512K tokens (Section 5.1);
+The paper trains Qwen2.5-3B / Llama-3.1-8B on ProLong at 512K tokens (Sections 5.1-5.2);
 neither the data nor the weights are available, so the benchmark inputs are
 synthetic tensors with the paper's shapes and a planted vertical-slash structure:
 
