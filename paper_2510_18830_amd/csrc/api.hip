@@ -365,15 +365,43 @@ msparse_status msparse_merge_out_lse(const msparse_dims* dims, const float* o_pa
     return check_hip(launch_merge(m, s), s, "merge out/lse");
 }
 
+// Backward workspace: Delta, max |dO|, the column work list and the per-item
+// column partials.
+static size_t carve_bwd(const msparse_dims* d, int64_t vcol_cap, char* base, AttnArgs* a) {
+    const int64_t bh = int64_t(d->batch) * d->heads_q;
+    const ColPlanSizes z = col_plan_sizes(bh, vcol_cap, d->seq_q / kBlock);
+    Carve c{base};
+    float* delta = c.take<float>(size_t(bh) * d->seq_q);
+    uint32_t* dmax = c.take<uint32_t>(1);
+    int32_t* choff = c.take<int32_t>(size_t(bh) + 1);
+    int64_t* e0 = c.take<int64_t>(size_t(z.chunk_cap));
+    int32_t* head = c.take<int32_t>(size_t(z.chunk_cap));
+    int32_t* qlo = c.take<int32_t>(size_t(z.chunk_cap));
+    int32_t* item = c.take<int32_t>(size_t(z.chunk_cap) + 1);
+    int32_t* span = c.take<int32_t>(1);
+    float* dkc = c.take<float>(size_t(z.slots) * kBlock * d->head_dim);
+    float* dvc = c.take<float>(size_t(z.slots) * kBlock * d->head_dim);
+    if (a) {
+        a->delta = delta;
+        a->dmax = dmax;
+        a->col_choff = choff;
+        a->col_e0 = e0;
+        a->col_head = head;
+        a->col_qlo = qlo;
+        a->col_item = item;
+        a->col_span = span;
+        a->col_chunk_cap = z.chunk_cap;
+        a->col_budget = z.budget;
+        a->col_slots = z.slots;
+        a->dk_col = dkc;
+        a->dv_col = dvc;
+    }
+    return c.off;
+}
+
 size_t msparse_attn_bwd_workspace(const msparse_dims* dims, int64_t vcol_cap) {
     if (check_dims(dims, false) || vcol_cap < 0) return 0;
-    const size_t segs = (size_t(dims->seq_q / kBlock) + kColSeg - 1) / kColSeg;
-    Carve c{nullptr};
-    c.take<float>(size_t(dims->batch) * dims->heads_q * dims->seq_q);
-    c.take<float>(segs * size_t(vcol_cap) * dims->head_dim);
-    c.take<float>(segs * size_t(vcol_cap) * dims->head_dim);
-    c.take<uint32_t>(1);
-    return c.off;
+    return carve_bwd(dims, vcol_cap, nullptr, nullptr);
 }
 
 msparse_status msparse_attn_bwd(const msparse_dims* dims, const void* q, const void* k, const void* v,
@@ -390,13 +418,8 @@ msparse_status msparse_attn_bwd(const msparse_dims* dims, const void* q, const v
     if (dims->seq_q == 0 && dims->seq_k == 0) return MSPARSE_OK;
     AttnArgs a{};
     fill_attn(dims, index, &a);
-    Carve c{static_cast<char*>(ws)};
-    a.delta = c.take<float>(size_t(dims->batch) * dims->heads_q * dims->seq_q);
-    const size_t segs = (size_t(dims->seq_q / kBlock) + kColSeg - 1) / kColSeg;
-    a.dk_col = c.take<float>(segs * size_t(index->vcol_cap) * dims->head_dim);
-    a.dv_col = c.take<float>(segs * size_t(index->vcol_cap) * dims->head_dim);
+    carve_bwd(dims, index->vcol_cap, static_cast<char*>(ws), &a);
     a.vcol_cap = index->vcol_cap;
-    a.dmax = c.take<uint32_t>(1);
     a.o_f32 = out_f32;
     a.q = static_cast<const uint16_t*>(q);
     a.k = static_cast<const uint16_t*>(k);

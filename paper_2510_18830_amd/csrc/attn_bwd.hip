@@ -13,11 +13,13 @@
 //               group and every query block that selected this key block (the
 //               transposed lists), S = Q K^T, dP = dO V^T, dV^T += dO^T P,
 //               dK^T += Q^T dZ (4 GEMMs); dK / dV of the block written once
-//   dkdv-col    the same tile body for the gathered vertical columns of one
-//               query head (64 per workgroup) against every query block that
-//               sees them outside its selected block-diagonals; per-head
-//               partials go to the workspace
-//   merge       adds the per-head column partials into dK / dV, heads in order.
+//   colplan     work list for the vertical columns: chunks of 64 entries of
+//               one head's vertical list, each cut into items of a few query
+//               blocks (one workgroup)
+//   dkdv-col    the same tile body for one item: the chunk's gathered columns
+//               against each of the item's query blocks that sees them outside
+//               its selected block-diagonals; partials go to the item's slot
+//   merge       adds the column partials into dK / dV, heads and items in order.
 // The second GEMM of each pair takes fp16 operands (P or dZ, and Q^T, K^T or
 // dO^T converted while staging): 3 more significand bits than bf16 at the same
 // MFMA rate.  dO is multiplied by a power of two s so that max |s dO| = 16,
@@ -368,27 +370,135 @@ __global__ void __launch_bounds__(kThreads) bwd_dkdv_kernel(AttnArgs a) {
 
 __device__ __forceinline__ bool dbit(const uint32_t* db, int32_t x) { return (db[x >> 5] >> (x & 31)) & 1u; }
 
-// Column pass: one workgroup per (head, 64 consecutive entries of the head's
-// vertical list, segment of kColSeg query blocks); grid.x covers
-// B * Hq * ceil(max verticals per head / 64) (surplus workgroups exit), grid.y
-// the segments.  Each writes the segment's partial dK / dV of its columns;
-// the merge kernel sums the segments in order.
+// ------------------------------------------------------------------ column pass
+// Work list: chunk = 64 consecutive entries of one head's vertical list.  The
+// query blocks that can see a chunk form a suffix of the local blocks (global
+// block numbers rise with the local block in both ring layouts), starting at
+// the first block at or after the chunk's smallest column; that suffix is cut
+// into items of `span` blocks.  One workgroup builds the list (plain scans, so
+// the list and hence the summation order are fixed by the index alone).
+constexpr int kPlanThreads = 1024;
+
+// Exclusive prefix sum over the 1024-thread workgroup; tmp holds 17 ints.
+__device__ int plan_scan(int v, int* tmp, int* total) {
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+    int x = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(x, o);
+        if (lane >= o) x += y;
+    }
+    if (lane == 63) tmp[wid] = x;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int run = 0;
+        for (int w = 0; w < kPlanThreads / 64; ++w) {
+            const int t = tmp[w];
+            tmp[w] = run;
+            run += t;
+        }
+        tmp[16] = run;
+    }
+    __syncthreads();
+    const int res = tmp[wid] + x - v;
+    *total = tmp[16];
+    __syncthreads();
+    return res;
+}
+
+__global__ void __launch_bounds__(kPlanThreads) bwd_colplan_kernel(AttnArgs a) {
+    __shared__ int tmp[17];
+    __shared__ long long part[kPlanThreads / 64];
+    const int tid = threadIdx.x;
+    const int BH = a.B * a.Hq;
+    // chunks per head (entries past the capacity are ignored)
+    int carry = 0;
+    for (int base = 0; base < BH; base += kPlanThreads) {
+        const int h = base + tid;
+        int n = 0;
+        if (h < BH) {
+            const int64_t v0 = min(a.vcol_ptr[h], a.vcol_cap), v1 = min(a.vcol_ptr[h + 1], a.vcol_cap);
+            n = v1 > v0 ? int((v1 - v0 + 63) / 64) : 0;
+        }
+        int tot;
+        const int ex = plan_scan(n, tmp, &tot);
+        if (h < BH) a.col_choff[h] = carry + ex;
+        carry += tot;
+    }
+    const int nc = carry;
+    if (tid == 0) a.col_choff[BH] = nc;
+    __syncthreads();
+    // per chunk: head, first entry, first candidate query block
+    long long cand = 0;
+    for (int g = tid; g < nc; g += kPlanThreads) {
+        int lo = 0, hi = BH;  // col_choff[lo] <= g < col_choff[hi]
+        while (hi - lo > 1) {
+            const int m = (lo + hi) >> 1;
+            if (a.col_choff[m] <= g) lo = m; else hi = m;
+        }
+        const int64_t e0 = a.vcol_ptr[lo] + int64_t(g - a.col_choff[lo]) * 64;
+        const int32_t cb = min(max(a.vcol_idx[e0], 0), a.Nk - 1) >> 6;
+        const int32_t cg = a.k_blk_global[cb];
+        int L = 0, R = a.nqb;  // first local query block with global block >= cg
+        while (L < R) {
+            const int m = (L + R) >> 1;
+            if (a.q_blk_global[m] < cg) L = m + 1; else R = m;
+        }
+        a.col_head[g] = lo;
+        a.col_e0[g] = e0;
+        a.col_qlo[g] = L;
+        cand += a.nqb - L;
+    }
+    for (int o = 32; o > 0; o >>= 1) cand += __shfl_xor(cand, o);
+    if ((tid & 63) == 0) part[tid >> 6] = cand;
+    __syncthreads();
+    long long total = 0;
+    for (int w = 0; w < kPlanThreads / 64; ++w) total += part[w];
+    const long long want = (total + a.col_budget - 1) / a.col_budget;
+    const int span = int(want > kColMinSpan ? want : kColMinSpan);
+    if (tid == 0) a.col_span[0] = span;
+    // items per chunk, scanned (chunk g was filled by this same thread above)
+    carry = 0;
+    for (int base = 0; base < nc; base += kPlanThreads) {
+        const int g = base + tid;
+        const int n = g < nc ? (a.nqb - a.col_qlo[g] + span - 1) / span : 0;
+        int tot;
+        const int ex = plan_scan(n, tmp, &tot);
+        if (g < nc) a.col_item[g] = carry + ex;
+        carry += tot;
+    }
+    if (tid == 0) a.col_item[nc] = carry;
+}
+
+// One workgroup per item: the item's chunk of verticals (64 key rows of one
+// query head, held in registers) against each query block of the item that
+// sees some of them outside its selected block-diagonals; the partial dK / dV
+// of the item go to its own slot (grid = item capacity; surplus workgroups
+// exit, consecutive items land on different XCDs).
 template <int D>
-__global__ void __launch_bounds__(kThreads) bwd_dkdv_col_kernel(AttnArgs a, int32_t chunks_per_head) {
+__global__ void __launch_bounds__(kThreads) bwd_dkdv_col_kernel(AttnArgs a) {
     constexpr int KD = D / 16, ND = D / 32;
     __shared__ KvLds<D> sm;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, l32 = lane & 31;
-    const int bh = int(blockIdx.x / chunks_per_head);
-    const int chunk = int(blockIdx.x % chunks_per_head);
-    const int seg = blockIdx.y;
-    const int64_t v0 = a.vcol_ptr[bh], v1 = a.vcol_ptr[bh + 1];
-    const int64_t e0 = v0 + int64_t(chunk) * 64;
-    if (e0 >= v1) return;
+    const int nc = a.col_choff[a.B * a.Hq];
+    const int item = int(blockIdx.x);
+    if (item >= a.col_item[nc]) return;
+    int g = 0, ghi = nc;  // col_item[g] <= item < col_item[ghi]
+    while (ghi - g > 1) {
+        const int m = (g + ghi) >> 1;
+        if (a.col_item[m] <= item) g = m; else ghi = m;
+    }
+    const int bh = a.col_head[g];
+    const int64_t e0 = a.col_e0[g];
+    const int64_t v1 = min(a.vcol_ptr[bh + 1], a.vcol_cap);
     const int cnt = int(min<int64_t>(64, v1 - e0));
+    const int span = a.col_span[0];
+    const int qb0 = a.col_qlo[g] + (item - a.col_item[g]) * span;
+    const int qb1 = min(a.nqb, qb0 + span);
     const int b = bh / a.Hq, hq = bh % a.Hq, hk = hq / (a.Hq / a.Hkv);
     const int key = 32 * w + l32;
     const bool valid = key < cnt;
-    const int32_t col = a.vcol_idx[e0 + (valid ? key : 0)];
+    const int32_t col = min(max(a.vcol_idx[e0 + (valid ? key : 0)], 0), a.Nk - 1);
     const int32_t cg = a.k_blk_global[col >> 6];
     const int32_t cin = col & 63;
     const int64_t krow = (int64_t(b) * a.Hkv + hk) * a.Nk + col;
@@ -407,12 +517,8 @@ __global__ void __launch_bounds__(kThreads) bwd_dkdv_col_kernel(AttnArgs a, int3
     const float c2 = a.scale * kLog2e;
     const float sc = dout_scale(a.dmax);
     const uint32_t* db = a.diag_bits + int64_t(bh) * a.dwords;
-    // the first column of the chunk has the smallest global block
-    const int32_t cg_min = a.k_blk_global[a.vcol_idx[e0] >> 6];
-    const int qb1 = min(a.nqb, (seg + 1) * kColSeg);
-    for (int qb = seg * kColSeg; qb < qb1; ++qb) {
+    for (int qb = qb0; qb < qb1; ++qb) {
         const int32_t qg = a.q_blk_global[qb];
-        if (qg < cg_min) continue;   // uniform across the workgroup
         const bool active = valid && qg >= cg && !dbit(db, qg - cg);
         const int lim = qg == cg ? cin : 0;
         // every column covered by a selected block-diagonal: nothing to do here
@@ -423,7 +529,7 @@ __global__ void __launch_bounds__(kThreads) bwd_dkdv_col_kernel(AttnArgs a, int3
         __syncthreads();
     }
     if (!valid) return;
-    const int64_t slot = int64_t(seg) * a.vcol_cap + e0 + key;
+    const int64_t slot = int64_t(item) * 64 + key;
     float* dkp = a.dk_col + slot * D;
     float* dvp = a.dv_col + slot * D;
     const float fk = a.scale / sc, fv = 1.f / sc;
@@ -445,8 +551,9 @@ __global__ void __launch_bounds__(kThreads) bwd_dkdv_col_kernel(AttnArgs a, int3
         }
 }
 
-// Adds the per-head column partials of key block kb into dK / dV: one
-// workgroup per (b, KV head, key block), query heads in order.
+// Adds the column partials of key block kb into dK / dV: one workgroup per
+// (b, KV head, key block); query heads in order, then each chunk's items in
+// order.
 __global__ void __launch_bounds__(128) bwd_colmerge_kernel(AttnArgs a) {
     const int BK = a.B * a.Hkv;
     const int bk = int(blockIdx.x % BK);
@@ -456,21 +563,26 @@ __global__ void __launch_bounds__(128) bwd_colmerge_kernel(AttnArgs a) {
     const int lo = kb * 64, hi = lo + 64;
     for (int g = 0; g < G; ++g) {
         const int bh = b * a.Hq + hk * G + g;
-        const int64_t v0 = a.vcol_ptr[bh], v1 = a.vcol_ptr[bh + 1];
+        const int64_t v0 = a.vcol_ptr[bh], v1 = min(a.vcol_ptr[bh + 1], a.vcol_cap);
+        if (v0 >= v1) continue;
         // first entry >= lo
         int64_t L = v0, R = v1;
         while (L < R) {
             const int64_t m = (L + R) >> 1;
             if (a.vcol_idx[m] < lo) L = m + 1; else R = m;
         }
-        const int segs = (a.nqb + kColSeg - 1) / kColSeg;
+        const int32_t c0 = a.col_choff[bh];
         for (int64_t e = L; e < v1 && a.vcol_idx[e] < hi; ++e) {
+            if (a.vcol_idx[e] < lo) continue;
+            const int64_t ch = c0 + (e - v0) / 64;
+            const int key = int((e - v0) % 64);
+            const int i0 = a.col_item[ch], i1 = a.col_item[ch + 1];
             const int64_t row = int64_t(bk) * a.Nk + a.vcol_idx[e];
             for (int j = threadIdx.x; j < a.d; j += blockDim.x) {
                 float sk = 0.f, sv = 0.f;
-                for (int sg = 0; sg < segs; ++sg) {
-                    sk += a.dk_col[(int64_t(sg) * a.vcol_cap + e) * a.d + j];
-                    sv += a.dv_col[(int64_t(sg) * a.vcol_cap + e) * a.d + j];
+                for (int it = i0; it < i1; ++it) {
+                    sk += a.dk_col[(int64_t(it) * 64 + key) * a.d + j];
+                    sv += a.dv_col[(int64_t(it) * 64 + key) * a.d + j];
                 }
                 a.dk[row * a.d + j] += sk;
                 a.dv[row * a.d + j] += sv;
@@ -497,15 +609,11 @@ hipError_t launch_bwd_d(const AttnArgs& a, hipStream_t s) {
     const int64_t kgrid = int64_t(a.B) * a.Hkv * a.nkb;
     if (kgrid > 0) { TraceScope _t("bwd_dkdv", s); hipLaunchKernelGGL(bwd_dkdv_kernel<D>, dim3(unsigned(kgrid)), dim3(kThreads), 0, s, a); }
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    // column chunks: a head has at most min(vcol_cap, Nk) verticals in a shard
-    const int64_t vmax = a.vcol_cap < int64_t(a.Nk) ? a.vcol_cap : int64_t(a.Nk);
-    const int32_t chunks = int32_t((vmax + 63) / 64);
-    const int64_t cgrid = int64_t(a.B) * a.Hq * chunks;
-    const int segs = (a.nqb + kColSeg - 1) / kColSeg;
-    if (cgrid > 0 && segs > 0) {
+    { TraceScope _t("bwd_colplan", s); hipLaunchKernelGGL(bwd_colplan_kernel, dim3(1), dim3(kPlanThreads), 0, s, a); }
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (a.col_slots > 0) {
         TraceScope _t("bwd_dkdv_col", s);
-        hipLaunchKernelGGL(bwd_dkdv_col_kernel<D>, dim3(unsigned(cgrid), unsigned(segs)), dim3(kThreads), 0, s, a,
-                           chunks);
+        hipLaunchKernelGGL(bwd_dkdv_col_kernel<D>, dim3(unsigned(a.col_slots)), dim3(kThreads), 0, s, a);
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (kgrid > 0) { TraceScope _t("bwd_colmerge", s); hipLaunchKernelGGL(bwd_colmerge_kernel, dim3(unsigned(kgrid)), dim3(128), 0, s, a); }

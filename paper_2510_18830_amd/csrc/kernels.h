@@ -68,9 +68,19 @@ struct AttnArgs {
     float* dq;
     float* dk;
     float* dv;
-    float* dk_col;         // bwd workspace [col segments, vcol_cap, d]
+    float* dk_col;         // bwd workspace [col_slots, 64, d]: per-item column partials
     float* dv_col;
     int64_t vcol_cap;
+    // bwd column-pass work list (workspace, written by the plan kernel)
+    int32_t* col_choff;    // [B*Hq + 1] first chunk of each head; last = chunk count
+    int64_t* col_e0;       // [col_chunk_cap] first vertical entry of each chunk
+    int32_t* col_head;     // [col_chunk_cap] head (b * Hq + h) of each chunk
+    int32_t* col_qlo;      // [col_chunk_cap] first local query block that may see the chunk
+    int32_t* col_item;     // [col_chunk_cap + 1] first item of each chunk; last = item count
+    int32_t* col_span;     // [1] query blocks per item
+    int64_t col_chunk_cap;
+    int64_t col_budget;    // items the span is chosen for
+    int64_t col_slots;     // item capacity (grid of the column kernel)
     int32_t dq_accumulate;
     int32_t B, Hq, Hkv, Nq, Nk, d;
     int32_t nqb, nkb;
@@ -90,8 +100,25 @@ struct AttnArgs {
 };
 hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t s);
 hipError_t launch_attn_bwd(const AttnArgs& a, hipStream_t s);
-// query blocks per workgroup in the backward column pass
-constexpr int kColSeg = 512;
+// Backward column pass: a chunk is 64 consecutive entries of one head's
+// vertical list; its candidate query blocks (a suffix of the local blocks) are
+// split into items of `span` blocks, one workgroup each.  span is the smallest
+// value >= kColMinSpan that keeps the item count within the budget.
+constexpr int kColItems = 4096;
+constexpr int kColMinSpan = 16;
+struct ColPlanSizes {
+    int64_t chunk_cap;  // bound on the chunk count: sum over heads of ceil(n_h / 64)
+    int64_t budget;
+    int64_t slots;      // bound on the item count: budget + chunk_cap
+};
+inline ColPlanSizes col_plan_sizes(int64_t bh, int64_t vcol_cap, int64_t nqb) {
+    ColPlanSizes z;
+    z.chunk_cap = (vcol_cap + 63) / 64 + bh;
+    const int64_t fine = z.chunk_cap * ((nqb + kColMinSpan - 1) / kColMinSpan);
+    z.budget = fine < kColItems ? fine : kColItems;
+    z.slots = z.budget + z.chunk_cap;
+    return z;
+}
 
 struct MergeArgs {
     const float* o_part;
