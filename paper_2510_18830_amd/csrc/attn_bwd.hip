@@ -105,10 +105,8 @@ __global__ void __launch_bounds__(kThreads) bwd_dq_kernel(AttnArgs a) {
     constexpr int KD = D / 16, ND = D / 32;
     __shared__ DqLds<D> sm;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, l32 = lane & 31;
-    const int BH = a.B * a.Hq;
-    const int64_t t = blockIdx.x;
-    const int bh = int(t % BH);
-    const int qb = a.nqb - 1 - int(t / BH);
+    int bh, qb;
+    query_tile_of(blockIdx.x, a.B, a.Hq, a.Hkv, a.nqb, bh, qb);
     const int b = bh / a.Hq, hq = bh % a.Hq, hk = hq / (a.Hq / a.Hkv);
     const int qrow = 32 * w + l32;
     const int64_t grow = int64_t(bh) * a.Nq + int64_t(qb) * 64 + qrow;

@@ -2,8 +2,14 @@
 // vertical columns (block_bar_sparse_attention_forward, Algorithm 2), and the
 // log-sum-exp merge of ring-step partials (merge_out_and_lse, Algorithm 2).
 //
-// One workgroup of two wavefronts per (batch, query head, 64-row query block);
-// wave w owns rows 32w .. 32w+31.  Per 64-key tile:
+// One workgroup of four wavefronts per (batch, query head, pair of consecutive
+// 64-row query blocks); waves 2j, 2j+1 own block j of the pair, 32 rows each.
+// The pair walks the union of its two block lists in ascending key order:
+// every key tile is staged once, and each half computes it only when its own
+// list selected it (the lists of neighbouring blocks share most of their
+// tiles: a run of selected diagonals x..x+r gives the pair r+2 distinct key
+// blocks for 2(r+1) block products).  Column tiles follow, per half.
+// Per 64-key tile, per wave:
 //   S^T = K Q^T       (A = K rows from LDS, B = the wave's Q rows in VGPRs),
 //   online softmax    (each lane owns one query row, the partner lane l^32
 //                      holds the other half of its keys),
@@ -11,7 +17,6 @@
 //                      from the S^T accumulator; this product runs in fp16,
 //                      whose 3 extra significand bits keep the rounding of P
 //                      well below the output tolerance at the same MFMA rate).
-// Block tiles come first, then the column list in chunks of 64 gathered keys.
 // Scores use exp2 with scale * log2(e) folded in; lse is stored as a natural log.
 #include "common.h"
 #include "kernels.h"
@@ -22,172 +27,232 @@ namespace msparse {
 
 namespace {
 
-constexpr int kFwdThreads = 128;
+constexpr int kFwdThreads = 256;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kSlack = 8.f;   // log2 units
 
 template <int D>
-struct FwdLds {
+struct FwdBuf {
     uint16_t k[TileLds<D>::kRowElems];
     uint16_t vt[TileLds<D>::kTElems];
+};
+template <int D>
+struct FwdLds {
+    FwdBuf<D> buf[2];  // double buffer: tile t+1 is stored while tile t is read
     int32_t kidx[64];
-    int32_t lim[64];   // key visible to in-block query row r iff r >= lim
+    int32_t lim[64];   // column tile: key visible to in-block query row r iff r >= lim
 };
 
-// Two waves per SIMD (at most 256 registers per lane): the staging of one
-// workgroup overlaps the MFMA work of the other.
+// Online-softmax state of one wave: 32 query rows, O^T accumulator.
+template <int D>
+struct FwdRows {
+    static constexpr int KD = D / 16;   // k-steps over head_dim
+    static constexpr int ND = D / 32;   // 32-wide output column blocks
+    u32x4 q[KD];
+    f32x16 o[ND];
+    float m = -INFINITY, l = 0.f;
+};
+
+// One 64-key tile for one wave.  mask: 0 none, 1 causal diagonal (key k
+// visible to row r iff r >= k), 2 per-key limits from LDS.
+template <int D>
+__device__ __forceinline__ void fwd_tile(const FwdBuf<D>& sm, const int32_t* lims, FwdRows<D>& st, int mask,
+                                         int qrow, int h, int l32, float c2) {
+    constexpr int KD = FwdRows<D>::KD, ND = FwdRows<D>::ND;
+    // ---- S^T for keys 0-31 (c = 0) and 32-63 (c = 1)
+    f32x16 sacc[2];
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+        sacc[c] = f32x16{};
+        const uint16_t* krow = sm.k + (32 * c + l32) * TileLds<D>::kRowStride + 8 * h;
+#pragma unroll
+        for (int s = 0; s < KD; ++s) sacc[c] = mfma32(lds_read16(krow + 16 * s), st.q[s], sacc[c]);
+    }
+    // ---- mask, tile max (raw logits; scale > 0 commutes with max)
+    if (mask) {
+#pragma unroll
+        for (int c = 0; c < 2; ++c)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int key = 32 * c + 8 * (r >> 2) + 4 * h + (r & 3);
+                const int lim = mask == 1 ? key : lims[key];
+                if (qrow < lim) sacc[c][r] = -INFINITY;
+            }
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[c][r]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32)) * c2;
+    // Lazy rescaling: keep the running maximum unless the tile exceeds it by
+    // more than kSlack (P then stays below 2^kSlack, well inside fp16), so the
+    // O accumulator is rescaled only on the rare tiles that raise the row
+    // maximum substantially.
+    const bool raise = mx > st.m + kSlack;
+    if (__any(raise)) {
+        const float m_new = raise ? mx : st.m;
+        const float alpha = st.m == -INFINITY ? 0.f : fast_exp2(st.m - m_new);
+        st.l *= alpha;
+#pragma unroll
+        for (int i = 0; i < ND; ++i) st.o[i] *= alpha;
+        st.m = m_new;
+    }
+    const float m_use = st.m == -INFINITY ? 0.f : st.m;
+    float rs = 0.f;
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const float p = fast_exp2(__builtin_fmaf(sacc[c][r], c2, -m_use));
+            sacc[c][r] = p;
+            rs += p;
+        }
+    st.l += rs + __shfl_xor(rs, 32);
+    // ---- O^T += V^T P^T
+    u32x4 pb[4];
+    pb[0] = pack8_f16<0>(sacc[0]);
+    pb[1] = pack8_f16<8>(sacc[0]);
+    pb[2] = pack8_f16<0>(sacc[1]);
+    pb[3] = pack8_f16<8>(sacc[1]);
+#pragma unroll
+    for (int i = 0; i < ND; ++i) {
+        const uint16_t* vrow = sm.vt + (32 * i + l32) * TileLds<D>::kTStride + 8 * h;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) st.o[i] = mfma32h(lds_read16(vrow + 16 * g), pb[g], st.o[i]);
+    }
+}
+
+// Two waves per SIMD (at most 256 registers per lane), two workgroups per CU:
+// the staging of one workgroup overlaps the MFMA work of the other.
 template <int D>
 __global__ void __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 attn_fwd_kernel(AttnArgs a) {
-    constexpr int KD = D / 16;   // k-steps over head_dim
-    constexpr int ND = D / 32;   // 32-wide output column blocks
+    constexpr int KD = FwdRows<D>::KD, ND = FwdRows<D>::ND;
     __shared__ FwdLds<D> sm;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int w = tid >> 6;
+    const int half = w >> 1;      // query block of the pair
     const int h = lane >> 5;      // lane half
     const int l32 = lane & 31;
 
-    const int BH = a.B * a.Hq;
-    const int64_t t = blockIdx.x;
-    const int bh = int(t % BH);
-    const int qb = a.nqb - 1 - int(t / BH);   // heaviest (latest) blocks first
+    const int npair = (a.nqb + 1) >> 1;
+    int bh, qp;
+    query_tile_of(blockIdx.x, a.B, a.Hq, a.Hkv, npair, bh, qp);
     const int b = bh / a.Hq;
     const int hq = bh % a.Hq;
     const int hk = hq / (a.Hq / a.Hkv);
-    const int qrow = 32 * w + l32;            // row inside the query block
+    const int qb0 = 2 * qp;
+    const bool has1 = qb0 + 1 < a.nqb;
+    const int qb = qb0 + (has1 ? half : 0);   // a lone block: both halves read it, half 1 stays idle
+    const bool live = half == 0 || has1;
+    const int qrow = 32 * (w & 1) + l32;      // row inside the query block
+    const int32_t qg = a.q_blk_global[qb];
 
-    const uint16_t* __restrict__ qp = a.q + (int64_t(bh) * a.Nq + int64_t(qb) * 64 + qrow) * D;
     const uint16_t* __restrict__ kp = a.k + (int64_t(b) * a.Hkv + hk) * int64_t(a.Nk) * D;
     const uint16_t* __restrict__ vp = a.v + (int64_t(b) * a.Hkv + hk) * int64_t(a.Nk) * D;
 
-    u32x4 qreg[KD];
+    FwdRows<D> st;
+    {
+        const uint16_t* __restrict__ qptr = a.q + (int64_t(bh) * a.Nq + int64_t(qb) * 64 + qrow) * D;
 #pragma unroll
-    for (int s = 0; s < KD; ++s) qreg[s] = *reinterpret_cast<const u32x4*>(qp + 16 * s + 8 * h);
-
-    f32x16 oacc[ND];
+        for (int s = 0; s < KD; ++s) st.q[s] = *reinterpret_cast<const u32x4*>(qptr + 16 * s + 8 * h);
+    }
 #pragma unroll
-    for (int i = 0; i < ND; ++i) oacc[i] = f32x16{};
-    float m_run = -INFINITY, l_run = 0.f;
+    for (int i = 0; i < ND; ++i) st.o[i] = f32x16{};
     const float c2 = a.scale * kLog2e;
 
-    const int64_t item = int64_t(bh) * a.nqb + qb;
-    const int64_t b0 = a.blk_ptr[item], b1 = a.blk_ptr[item + 1];
-    const int64_t c0 = a.col_ptr[item], c1 = a.col_ptr[item + 1];
-    const int nblk = int(b1 - b0);
-    const int ncolt = int((c1 - c0 + 63) / 64);
-    const int32_t qg = a.q_blk_global[qb];
-
-    for (int tt = 0; tt < nblk + ncolt; ++tt) {
-        // ---- tile metadata: key rows and per-key visibility limit
-        bool masked;
-        int kb = -1;
-        if (tt < nblk) {
-            kb = a.blk_idx[b0 + tt];
-            masked = a.k_blk_global[kb] == qg;    // diagonal tile: causal inside
-            if (masked && tid < 64) sm.lim[tid] = tid;
-        } else {
-            masked = true;
-            const int64_t cbase = c0 + int64_t(tt - nblk) * 64;
-            const int cnt = int(min<int64_t>(64, c1 - cbase));
-            if (tid < 64) {
-                const int j = tid < cnt ? tid : 0;
-                const int32_t col = a.col_idx[cbase + j];
-                sm.kidx[tid] = col;
-                sm.lim[tid] = tid < cnt ? (a.k_blk_global[col >> 6] == qg ? (col & 63) : 0) : 64;
-            }
-            __syncthreads();
+    // ---- block tiles: the union of the two ascending block lists, software
+    // pipelined (the loads of the next tile are in flight during this tile)
+    const int64_t item0 = int64_t(bh) * a.nqb + qb0;
+    const int64_t e00 = a.blk_ptr[item0], e01 = a.blk_ptr[item0 + 1];
+    const int64_t e11 = has1 ? a.blk_ptr[item0 + 2] : e01;
+    int64_t p0 = e00, p1 = e01;
+    auto next = [&](int32_t& kb, bool& in0, bool& in1) {
+        if (p0 >= e01 && p1 >= e11) return false;
+        const int32_t k0 = p0 < e01 ? a.blk_idx[p0] : INT32_MAX;
+        const int32_t k1 = p1 < e11 ? a.blk_idx[p1] : INT32_MAX;
+        kb = min(k0, k1);
+        in0 = k0 == kb;
+        in1 = k1 == kb;
+        p0 += in0;
+        p1 += in1;
+        return true;
+    };
+    RowRegs<D, kFwdThreads> kr;
+    TransRegs<D, kFwdThreads> vr;
+    int32_t kb = 0;
+    bool in0 = false, in1 = false;
+    bool have = next(kb, in0, in1);
+    if (have) {
+        const ContiguousRows rows{int64_t(kb) * 64};
+        load_rows<D, kFwdThreads>(kr, kp, rows, tid);
+        load_trans<D, kFwdThreads>(vr, vp, rows, tid);
+        store_rows<D, kFwdThreads>(sm.buf[0].k, kr, tid);
+        store_trans_f16<D, kFwdThreads>(sm.buf[0].vt, vr, 1.0f, tid);
+    }
+    __syncthreads();
+    int cur = 0;
+    while (have) {
+        int32_t kb2 = 0;
+        bool in0n = false, in1n = false;
+        const bool more = next(kb2, in0n, in1n);
+        if (more) {
+            const ContiguousRows rows{int64_t(kb2) * 64};
+            load_rows<D, kFwdThreads>(kr, kp, rows, tid);
+            load_trans<D, kFwdThreads>(vr, vp, rows, tid);
         }
-        if (kb >= 0) {
-            const ContiguousRows rows{int64_t(kb) * 64};
-            stage_rows<D, kFwdThreads>(sm.k, kp, rows, tid);
-            stage_transposed_f16<D, kFwdThreads>(sm.vt, vp, rows, 1.0f, tid);
-        } else {
-            stage_rows<D, kFwdThreads>(sm.k, kp, IndexedRows{sm.kidx}, tid);
-            stage_transposed_f16<D, kFwdThreads>(sm.vt, vp, IndexedRows{sm.kidx}, 1.0f, tid);
-        }
-        __syncthreads();
-
-        // ---- S^T for keys 0-31 (c = 0) and 32-63 (c = 1)
-        f32x16 sacc[2];
-#pragma unroll
-        for (int c = 0; c < 2; ++c) {
-            sacc[c] = f32x16{};
-            const uint16_t* krow = sm.k + (32 * c + l32) * TileLds<D>::kRowStride + 8 * h;
-#pragma unroll
-            for (int s = 0; s < KD; ++s) sacc[c] = mfma32(lds_read16(krow + 16 * s), qreg[s], sacc[c]);
-        }
-        // ---- mask, tile max (raw logits; scale > 0 commutes with max)
-        if (masked) {
-#pragma unroll
-            for (int c = 0; c < 2; ++c)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const int key = 32 * c + 8 * (r >> 2) + 4 * h + (r & 3);
-                    if (qrow < sm.lim[key]) sacc[c][r] = -INFINITY;
-                }
-        }
-        float mx = -INFINITY;
-#pragma unroll
-        for (int c = 0; c < 2; ++c)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[c][r]);
-        mx = fmaxf(mx, __shfl_xor(mx, 32)) * c2;
-        // Lazy rescaling: keep the running maximum unless the tile exceeds it
-        // by more than kSlack (P then stays below 2^kSlack, well inside fp16),
-        // so the O accumulator is rescaled only on the rare tiles that raise
-        // the row maximum substantially.
-        const bool raise = mx > m_run + kSlack;
-        if (__any(raise)) {
-            const float m_new = raise ? mx : m_run;
-            const float alpha = m_run == -INFINITY ? 0.f : fast_exp2(m_run - m_new);
-            l_run *= alpha;
-#pragma unroll
-            for (int i = 0; i < ND; ++i) oacc[i] *= alpha;
-            m_run = m_new;
-        }
-        const float m_use = m_run == -INFINITY ? 0.f : m_run;
-        float rs = 0.f;
-#pragma unroll
-        for (int c = 0; c < 2; ++c)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const float p = fast_exp2(__builtin_fmaf(sacc[c][r], c2, -m_use));
-                sacc[c][r] = p;
-                rs += p;
-            }
-        l_run += rs + __shfl_xor(rs, 32);
-
-        // ---- O^T += V^T P^T
-        u32x4 pb[4];
-        pb[0] = pack8_f16<0>(sacc[0]);
-        pb[1] = pack8_f16<8>(sacc[0]);
-        pb[2] = pack8_f16<0>(sacc[1]);
-        pb[3] = pack8_f16<8>(sacc[1]);
-#pragma unroll
-        for (int i = 0; i < ND; ++i) {
-            const uint16_t* vrow = sm.vt + (32 * i + l32) * TileLds<D>::kTStride + 8 * h;
-#pragma unroll
-            for (int g = 0; g < 4; ++g) oacc[i] = mfma32h(lds_read16(vrow + 16 * g), pb[g], oacc[i]);
+        if (half == 0 ? in0 : in1)
+            fwd_tile<D>(sm.buf[cur], sm.lim, st, a.k_blk_global[kb] == qg ? 1 : 0, qrow, h, l32, c2);
+        if (more) {
+            store_rows<D, kFwdThreads>(sm.buf[cur ^ 1].k, kr, tid);
+            store_trans_f16<D, kFwdThreads>(sm.buf[cur ^ 1].vt, vr, 1.0f, tid);
         }
         __syncthreads();
+        cur ^= 1;
+        kb = kb2;
+        in0 = in0n;
+        in1 = in1n;
+        have = more;
     }
 
+    // ---- column tiles, one half at a time (the lists differ only near the band)
+    for (int j = 0; j < 1 + int(has1); ++j) {
+        const int64_t c0 = a.col_ptr[item0 + j], c1 = a.col_ptr[item0 + j + 1];
+        const int32_t qgj = a.q_blk_global[qb0 + j];
+        for (int64_t cbase = c0; cbase < c1; cbase += 64) {
+            const int cnt = int(min<int64_t>(64, c1 - cbase));
+            if (tid < 64) {
+                const int32_t col = a.col_idx[cbase + (tid < cnt ? tid : 0)];
+                sm.kidx[tid] = col;
+                sm.lim[tid] = tid < cnt ? (a.k_blk_global[col >> 6] == qgj ? (col & 63) : 0) : 64;
+            }
+            __syncthreads();
+            stage_rows<D, kFwdThreads>(sm.buf[0].k, kp, IndexedRows{sm.kidx}, tid);
+            stage_transposed_f16<D, kFwdThreads>(sm.buf[0].vt, vp, IndexedRows{sm.kidx}, 1.0f, tid);
+            __syncthreads();
+            if (half == j) fwd_tile<D>(sm.buf[0], sm.lim, st, 2, qrow, h, l32, c2);
+            __syncthreads();
+        }
+    }
+    if (!live) return;
+
     // ---- epilogue: normalise, store bf16 out and natural-log lse
-    const bool empty = !(l_run > 0.f);
-    const float inv = empty ? 0.f : 1.f / l_run;
+    const bool empty = !(st.l > 0.f);
+    const float inv = empty ? 0.f : 1.f / st.l;
     const int64_t orow = (int64_t(bh) * a.Nq + int64_t(qb) * 64 + qrow) * D;
 #pragma unroll
     for (int i = 0; i < ND; ++i)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
             f32x4 o4;
-            o4.x = oacc[i][4 * g + 0] * inv;
-            o4.y = oacc[i][4 * g + 1] * inv;
-            o4.z = oacc[i][4 * g + 2] * inv;
-            o4.w = oacc[i][4 * g + 3] * inv;
+            o4.x = st.o[i][4 * g + 0] * inv;
+            o4.y = st.o[i][4 * g + 1] * inv;
+            o4.z = st.o[i][4 * g + 2] * inv;
+            o4.w = st.o[i][4 * g + 3] * inv;
             if (a.out) {
                 u32x2 pk;
                 pk.x = pack_bf16x2(o4.x, o4.y);
@@ -198,7 +263,7 @@ attn_fwd_kernel(AttnArgs a) {
         }
     if (h == 0) {
         float* lp = a.lse + int64_t(bh) * a.Nq + int64_t(qb) * 64 + qrow;
-        *lp = empty ? -INFINITY : (m_run + fast_log2(l_run)) * kLn2;
+        *lp = empty ? -INFINITY : (st.m + fast_log2(st.l)) * kLn2;
     }
 }
 
@@ -245,7 +310,8 @@ __global__ void merge_kernel(MergeArgs m) {
 }  // namespace
 
 hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t s) {
-    const int64_t grid = int64_t(a.B) * a.Hq * a.nqb;
+    const int64_t grid = int64_t(a.B) * a.Hq * ((a.nqb + 1) / 2);
+    if (grid == 0) return hipSuccess;
     if (a.d == 128)
         { TraceScope _t("attn_fwd", s); hipLaunchKernelGGL(attn_fwd_kernel<128>, dim3(unsigned(grid)), dim3(kFwdThreads), 0, s, a); }
     else

@@ -91,6 +91,112 @@ __device__ __forceinline__ void stage_transposed_f16(uint16_t* lds, const uint16
     }
 }
 
+// Two-phase staging for software pipelining: the global loads of a tile go to
+// registers first (issued before the current tile's compute), the LDS stores
+// (with the fp16 conversion of the transposed copy) follow after it.
+template <int D, int NT>
+struct RowRegs {
+    static constexpr int kChunks = D / 8;
+    static constexpr int kRowsPerPass = NT / kChunks;
+    static constexpr int kPasses = 64 / kRowsPerPass;
+    u32x4 r[kPasses];
+};
+template <int D, int NT, class Rows>
+__device__ __forceinline__ void load_rows(RowRegs<D, NT>& g, const uint16_t* __restrict__ src, Rows rows, int tid) {
+    using R = RowRegs<D, NT>;
+#pragma unroll
+    for (int p = 0; p < R::kPasses; ++p) {
+        const int r = p * R::kRowsPerPass + tid / R::kChunks;
+        g.r[p] = *reinterpret_cast<const u32x4*>(src + rows(r) * D + (tid % R::kChunks) * 8);
+    }
+}
+template <int D, int NT>
+__device__ __forceinline__ void store_rows(uint16_t* lds, const RowRegs<D, NT>& g, int tid) {
+    using R = RowRegs<D, NT>;
+#pragma unroll
+    for (int p = 0; p < R::kPasses; ++p) {
+        const int r = p * R::kRowsPerPass + tid / R::kChunks;
+        *reinterpret_cast<u32x4*>(lds + r * TileLds<D>::kRowStride + (tid % R::kChunks) * 8) = g.r[p];
+    }
+}
+// transposed staging: item = (4-row quad, 8-wide d chunk), 16 * D / 8 items
+template <int D, int NT>
+struct TransRegs {
+    static constexpr int kItems = 16 * (D / 8);
+    static constexpr int kPasses = (kItems + NT - 1) / NT;
+    u32x4 r[kPasses][4];
+};
+template <int D, int NT, class Rows>
+__device__ __forceinline__ void load_trans(TransRegs<D, NT>& g, const uint16_t* __restrict__ src, Rows rows, int tid) {
+    using R = TransRegs<D, NT>;
+#pragma unroll
+    for (int p = 0; p < R::kPasses; ++p) {
+        const int item = p * NT + tid;
+        if (R::kItems % NT != 0 && item >= R::kItems) break;
+        const int q4 = item & 15, dc = item >> 4;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) g.r[p][b] = *reinterpret_cast<const u32x4*>(src + rows(4 * q4 + b) * D + dc * 8);
+    }
+}
+template <int D, int NT, int TS = TileLds<D>::kTStride>
+__device__ __forceinline__ void store_trans_f16(uint16_t* lds, const TransRegs<D, NT>& g, float mul, int tid) {
+    using R = TransRegs<D, NT>;
+#pragma unroll
+    for (int p = 0; p < R::kPasses; ++p) {
+        const int item = p * NT + tid;
+        if (R::kItems % NT != 0 && item >= R::kItems) break;
+        const int q4 = item & 15, dc = item >> 4;
+        const int pos = tpos(4 * q4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const u32x4* r = g.r[p];
+            u32x2 even, odd;
+            even.x = bf16_to_f16_bits(r[0][e] & 0xffffu, mul) | (bf16_to_f16_bits(r[1][e] & 0xffffu, mul) << 16);
+            even.y = bf16_to_f16_bits(r[2][e] & 0xffffu, mul) | (bf16_to_f16_bits(r[3][e] & 0xffffu, mul) << 16);
+            odd.x = bf16_to_f16_bits(r[0][e] >> 16, mul) | (bf16_to_f16_bits(r[1][e] >> 16, mul) << 16);
+            odd.y = bf16_to_f16_bits(r[2][e] >> 16, mul) | (bf16_to_f16_bits(r[3][e] >> 16, mul) << 16);
+            const int d0 = dc * 8 + 2 * e;
+            *reinterpret_cast<u32x2*>(lds + d0 * TS + pos) = even;
+            *reinterpret_cast<u32x2*>(lds + (d0 + 1) * TS + pos) = odd;
+        }
+    }
+}
+
+#ifndef MS_ORDER
+#define MS_ORDER 1
+#endif
+#ifndef MS_XCHUNK
+#define MS_XCHUNK 64
+#endif
+// (head, query block) of workgroup t in a B*Hq*nqb grid.
+__device__ __forceinline__ void query_tile_of(int64_t t, int B, int Hq, int Hkv, int nqb, int& bh, int& qb) {
+    const int64_t BH = int64_t(B) * Hq;
+#if MS_ORDER == 0
+    bh = int(t % BH);
+    qb = nqb - 1 - int(t / BH);
+#else
+    const int64_t total = BH * nqb;
+    constexpr int64_t C = MS_XCHUNK;
+    const int64_t full = total / (8 * C) * (8 * C);
+    int64_t u = t;
+    if (t < full) {
+        const int64_t n = t >> 3, x = t & 7;
+        u = (n / C) * 8 * C + x * C + (n % C);
+    }
+#if MS_ORDER == 1
+    const int G = Hq / Hkv;
+    const int64_t per = int64_t(nqb) * G;
+    const int bg = int(u / per);
+    const int64_t r = u % per;
+    qb = nqb - 1 - int(r / G);
+    bh = (bg / Hkv) * Hq + (bg % Hkv) * G + int(r % G);
+#else
+    bh = int(u % BH);
+    qb = nqb - 1 - int(u / BH);
+#endif
+#endif
+}
+
 // 16-byte LDS read
 __device__ __forceinline__ u32x4 lds_read16(const uint16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
 
