@@ -189,7 +189,7 @@ MSPARSE_API msparse_status msparse_build_index(const msparse_dims* dims, const i
  * receives the unrounded output; msparse_attn_bwd computes
  * Delta = dO . O more accurately from it, and ring steps merge it.  out may be
  * NULL when out_f32 is given.  Workspace: msparse_attn_fwd_workspace(dims)
- * bytes (currently 0; NULL is accepted then). */
+ * bytes (it holds an fp16 copy of v, B * Hkv * seq_k * d * 2 bytes). */
 MSPARSE_API size_t msparse_attn_fwd_workspace(const msparse_dims* dims);
 MSPARSE_API msparse_status msparse_attn_fwd(const msparse_dims* dims, const void* q, const void* k, const void* v,
                                 const msparse_index* index, void* out, float* lse, float* out_f32,

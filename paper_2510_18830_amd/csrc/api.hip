@@ -318,9 +318,12 @@ static msparse_status fill_attn(const msparse_dims* d, const msparse_index* x, A
     return MSPARSE_OK;
 }
 
+// Forward workspace: the fp16 copy of V.
 size_t msparse_attn_fwd_workspace(const msparse_dims* dims) {
-    (void)dims;
-    return 0;
+    if (check_dims(dims, false)) return 0;
+    Carve c{nullptr};
+    c.take<uint16_t>(size_t(dims->batch) * dims->heads_kv * dims->seq_k * dims->head_dim);
+    return c.off;
 }
 
 msparse_status msparse_attn_fwd(const msparse_dims* dims, const void* q, const void* k, const void* v,
@@ -342,8 +345,14 @@ msparse_status msparse_attn_fwd(const msparse_dims* dims, const void* q, const v
     a.out = static_cast<uint16_t*>(out);
     a.out_f32 = out_f32;
     a.lse = lse;
+    Carve c{static_cast<char*>(ws)};
+    const size_t nkv = size_t(dims->batch) * dims->heads_kv * dims->seq_k * dims->head_dim;
+    uint16_t* v16 = c.take<uint16_t>(nkv);
+    a.v16 = v16;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    return check_hip(launch_attn_fwd(a, s), s, "attn fwd");
+    hipError_t e = launch_to_f16(a.v, v16, int64_t(nkv), nullptr, s);
+    if (e == hipSuccess) e = launch_attn_fwd(a, s);
+    return check_hip(e, s, "attn fwd");
 }
 
 msparse_status msparse_merge_out_lse(const msparse_dims* dims, const float* o_part, const float* lse_part, float* o_acc,

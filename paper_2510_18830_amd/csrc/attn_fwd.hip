@@ -13,10 +13,12 @@
 //   S^T = K Q^T       (A = K rows from LDS, B = the wave's Q rows in VGPRs),
 //   online softmax    (each lane owns one query row, the partner lane l^32
 //                      holds the other half of its keys),
-//   O^T += V^T P^T    (A = V^T from the transposed LDS copy, B = P straight
-//                      from the S^T accumulator; this product runs in fp16,
-//                      whose 3 extra significand bits keep the rounding of P
-//                      well below the output tolerance at the same MFMA rate).
+//   O^T += V^T P^T    (A = V^T read transposed from fp16 V rows in LDS,
+//                      B = P straight from the S^T accumulator; this product
+//                      runs in fp16, whose 3 extra significand bits keep the
+//                      rounding of P well below the output tolerance at the
+//                      same MFMA rate; the fp16 copy of V is made once per
+//                      call by a conversion pass).
 // Scores use exp2 with scale * log2(e) folded in; lse is stored as a natural log.
 #include "common.h"
 #include "kernels.h"
@@ -32,10 +34,16 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kSlack = 8.f;   // log2 units
 
+// V tile rows: fp16, row stride D + 16 elements (the transposing reads of a
+// 16-lane group then touch 4 rows x 32 bytes in distinct banks).
+template <int D>
+struct VTile {
+    static constexpr int kStride = D + 16;
+};
 template <int D>
 struct FwdBuf {
-    uint16_t k[TileLds<D>::kRowElems];
-    uint16_t vt[TileLds<D>::kTElems];
+    uint16_t k[TileLds<D>::kRowElems];      // bf16 K rows
+    uint16_t v[64 * VTile<D>::kStride];     // fp16 V rows
 };
 template <int D>
 struct FwdLds {
@@ -58,7 +66,8 @@ struct FwdRows {
 // visible to row r iff r >= k), 2 per-key limits from LDS.
 template <int D>
 __device__ __forceinline__ void fwd_tile(const FwdBuf<D>& sm, const int32_t* lims, FwdRows<D>& st, int mask,
-                                         int qrow, int h, int l32, float c2) {
+                                         int qrow, int lane, float c2) {
+    const int h = lane >> 5, l32 = lane & 31;
     constexpr int KD = FwdRows<D>::KD, ND = FwdRows<D>::ND;
     // ---- S^T for keys 0-31 (c = 0) and 32-63 (c = 1)
     f32x16 sacc[2];
@@ -110,18 +119,17 @@ __device__ __forceinline__ void fwd_tile(const FwdBuf<D>& sm, const int32_t* lim
             rs += p;
         }
     st.l += rs + __shfl_xor(rs, 32);
-    // ---- O^T += V^T P^T
+    // ---- O^T += V^T P^T (A = V^T read transposed from the fp16 V rows)
     u32x4 pb[4];
     pb[0] = pack8_f16<0>(sacc[0]);
     pb[1] = pack8_f16<8>(sacc[0]);
     pb[2] = pack8_f16<0>(sacc[1]);
     pb[3] = pack8_f16<8>(sacc[1]);
 #pragma unroll
-    for (int i = 0; i < ND; ++i) {
-        const uint16_t* vrow = sm.vt + (32 * i + l32) * TileLds<D>::kTStride + 8 * h;
+    for (int i = 0; i < ND; ++i)
 #pragma unroll
-        for (int g = 0; g < 4; ++g) st.o[i] = mfma32h(lds_read16(vrow + 16 * g), pb[g], st.o[i]);
-    }
+        for (int g = 0; g < 4; ++g)
+            st.o[i] = mfma32h(lds_read_tr_a<VTile<D>::kStride>(sm.v, 16 * g, 32 * i, lane), pb[g], st.o[i]);
 }
 
 // Two waves per SIMD (at most 256 registers per lane), two workgroups per CU:
@@ -153,7 +161,7 @@ attn_fwd_kernel(AttnArgs a) {
     const int32_t qg = a.q_blk_global[qb];
 
     const uint16_t* __restrict__ kp = a.k + (int64_t(b) * a.Hkv + hk) * int64_t(a.Nk) * D;
-    const uint16_t* __restrict__ vp = a.v + (int64_t(b) * a.Hkv + hk) * int64_t(a.Nk) * D;
+    const uint16_t* __restrict__ vp = a.v16 + (int64_t(b) * a.Hkv + hk) * int64_t(a.Nk) * D;
 
     FwdRows<D> st;
     {
@@ -182,17 +190,17 @@ attn_fwd_kernel(AttnArgs a) {
         p1 += in1;
         return true;
     };
-    RowRegs<D, kFwdThreads> kr;
-    TransRegs<D, kFwdThreads> vr;
+    RowRegs<D, kFwdThreads> kr, vr;
+    constexpr int VS = VTile<D>::kStride;
     int32_t kb = 0;
     bool in0 = false, in1 = false;
     bool have = next(kb, in0, in1);
     if (have) {
         const ContiguousRows rows{int64_t(kb) * 64};
         load_rows<D, kFwdThreads>(kr, kp, rows, tid);
-        load_trans<D, kFwdThreads>(vr, vp, rows, tid);
+        load_rows<D, kFwdThreads>(vr, vp, rows, tid);
         store_rows<D, kFwdThreads>(sm.buf[0].k, kr, tid);
-        store_trans_f16<D, kFwdThreads>(sm.buf[0].vt, vr, 1.0f, tid);
+        store_rows<D, kFwdThreads, VS>(sm.buf[0].v, vr, tid);
     }
     __syncthreads();
     int cur = 0;
@@ -203,13 +211,13 @@ attn_fwd_kernel(AttnArgs a) {
         if (more) {
             const ContiguousRows rows{int64_t(kb2) * 64};
             load_rows<D, kFwdThreads>(kr, kp, rows, tid);
-            load_trans<D, kFwdThreads>(vr, vp, rows, tid);
+            load_rows<D, kFwdThreads>(vr, vp, rows, tid);
         }
         if (half == 0 ? in0 : in1)
-            fwd_tile<D>(sm.buf[cur], sm.lim, st, a.k_blk_global[kb] == qg ? 1 : 0, qrow, h, l32, c2);
+            fwd_tile<D>(sm.buf[cur], sm.lim, st, a.k_blk_global[kb] == qg ? 1 : 0, qrow, lane, c2);
         if (more) {
             store_rows<D, kFwdThreads>(sm.buf[cur ^ 1].k, kr, tid);
-            store_trans_f16<D, kFwdThreads>(sm.buf[cur ^ 1].vt, vr, 1.0f, tid);
+            store_rows<D, kFwdThreads, VS>(sm.buf[cur ^ 1].v, vr, tid);
         }
         __syncthreads();
         cur ^= 1;
@@ -232,9 +240,9 @@ attn_fwd_kernel(AttnArgs a) {
             }
             __syncthreads();
             stage_rows<D, kFwdThreads>(sm.buf[0].k, kp, IndexedRows{sm.kidx}, tid);
-            stage_transposed_f16<D, kFwdThreads>(sm.buf[0].vt, vp, IndexedRows{sm.kidx}, 1.0f, tid);
+            stage_rows<D, kFwdThreads, IndexedRows, VS>(sm.buf[0].v, vp, IndexedRows{sm.kidx}, tid);
             __syncthreads();
-            if (half == j) fwd_tile<D>(sm.buf[0], sm.lim, st, 2, qrow, h, l32, c2);
+            if (half == j) fwd_tile<D>(sm.buf[0], sm.lim, st, 2, qrow, lane, c2);
             __syncthreads();
         }
     }

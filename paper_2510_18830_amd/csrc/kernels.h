@@ -57,6 +57,10 @@ struct AttnArgs {
     const uint16_t* q;     // bf16 [B,Hq,Nq,d]
     const uint16_t* k;     // bf16 [B,Hkv,Nk,d]
     const uint16_t* v;
+    const uint16_t* v16;   // fp16 copies of the second-GEMM operands (workspace):
+    const uint16_t* k16;   //   V (fwd), K (dQ), Q and s dO (dK / dV)
+    const uint16_t* q16;
+    const uint16_t* g16;
     const uint16_t* o;     // forward output (bwd)
     const uint16_t* dout;  // bf16 [B,Hq,Nq,d] (bwd)
     uint16_t* out;         // bf16 [B,Hq,Nq,d] (fwd)
@@ -99,6 +103,9 @@ struct AttnArgs {
     const int32_t* k_blk_global;
 };
 hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t s);
+// dst = fp16(src * mul) for n bf16 elements (n a multiple of 8); mul = 1, or
+// the power of two pow2_scale(maxbits) when maxbits is not NULL
+hipError_t launch_to_f16(const uint16_t* src, uint16_t* dst, int64_t n, const uint32_t* maxbits, hipStream_t s);
 hipError_t launch_attn_bwd(const AttnArgs& a, hipStream_t s);
 // Backward column pass: a chunk is 64 consecutive entries of one head's
 // vertical list; its candidate query blocks (a suffix of the local blocks) are

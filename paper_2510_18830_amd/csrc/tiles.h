@@ -48,7 +48,7 @@ struct ContiguousRows {
 };
 
 // Row-major staging of 64 rows x D bf16 (row length D in `src`).
-template <int D, int NT, class Rows>
+template <int D, int NT, class Rows, int RS = TileLds<D>::kRowStride>
 __device__ __forceinline__ void stage_rows(uint16_t* lds, const uint16_t* __restrict__ src, Rows rows, int tid) {
     constexpr int kChunks = D / 8;              // 16-byte chunks per row
     constexpr int kRowsPerPass = NT / kChunks;
@@ -57,7 +57,7 @@ __device__ __forceinline__ void stage_rows(uint16_t* lds, const uint16_t* __rest
         const int r = p * kRowsPerPass + tid / kChunks;
         const int c = tid % kChunks;
         const u32x4 v = *reinterpret_cast<const u32x4*>(src + rows(r) * D + c * 8);
-        *reinterpret_cast<u32x4*>(lds + r * TileLds<D>::kRowStride + c * 8) = v;
+        *reinterpret_cast<u32x4*>(lds + r * RS + c * 8) = v;
     }
 }
 
@@ -110,13 +110,13 @@ __device__ __forceinline__ void load_rows(RowRegs<D, NT>& g, const uint16_t* __r
         g.r[p] = *reinterpret_cast<const u32x4*>(src + rows(r) * D + (tid % R::kChunks) * 8);
     }
 }
-template <int D, int NT>
+template <int D, int NT, int RS = TileLds<D>::kRowStride>
 __device__ __forceinline__ void store_rows(uint16_t* lds, const RowRegs<D, NT>& g, int tid) {
     using R = RowRegs<D, NT>;
 #pragma unroll
     for (int p = 0; p < R::kPasses; ++p) {
         const int r = p * R::kRowsPerPass + tid / R::kChunks;
-        *reinterpret_cast<u32x4*>(lds + r * TileLds<D>::kRowStride + (tid % R::kChunks) * 8) = g.r[p];
+        *reinterpret_cast<u32x4*>(lds + r * RS + (tid % R::kChunks) * 8) = g.r[p];
     }
 }
 // transposed staging: item = (4-row quad, 8-wide d chunk), 16 * D / 8 items
@@ -195,6 +195,30 @@ __device__ __forceinline__ void query_tile_of(int64_t t, int B, int Hq, int Hkv,
     qb = nqb - 1 - int(u / BH);
 #endif
 #endif
+}
+
+// A operand of a 32x32x16 fp16 MFMA taken transposed from a row-major fp16
+// tile X[row][col] (row stride RS elements): A[m][k] = X[k0 + kperm(k)][m0 + m]
+// with kperm the key order of an accumulator-resident B operand (lane half h
+// supplies rows k0 + 4h + {0..3} and k0 + 8 + 4h + {0..3}).  Two
+// ds_read_b64_tr_b16: in each group of 16 lanes, lane s names 4 consecutive
+// elements of row (s / 4) and receives element s % 4 of the rows named by
+// lanes s / 4 + 4j, j = 0..3.
+template <int RS>
+__device__ __forceinline__ u32x4 lds_read_tr_a(const uint16_t* x, int k0, int m0, int lane) {
+    typedef short v4s __attribute__((ext_vector_type(4)));
+    const int row = k0 + 4 * (lane >> 5) + ((lane & 15) >> 2);
+    const int col = m0 + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+    const uint16_t* p = x + row * RS + col;
+    const v4s r0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4s*)(p));
+    const v4s r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4s*)(p + 8 * RS));
+    const u32x2 a = __builtin_bit_cast(u32x2, r0), b = __builtin_bit_cast(u32x2, r1);
+    u32x4 o;
+    o.x = a.x;
+    o.y = a.y;
+    o.z = b.x;
+    o.w = b.y;
+    return o;
 }
 
 // 16-byte LDS read
