@@ -380,6 +380,7 @@ static size_t carve_bwd(const msparse_dims* d, int64_t vcol_cap, char* base, Att
     const int64_t bh = int64_t(d->batch) * d->heads_q;
     const ColPlanSizes z = col_plan_sizes(bh, vcol_cap, d->seq_q / kBlock);
     Carve c{base};
+    uint16_t* k16 = c.take<uint16_t>(size_t(d->batch) * d->heads_kv * d->seq_k * d->head_dim);
     float* delta = c.take<float>(size_t(bh) * d->seq_q);
     uint32_t* dmax = c.take<uint32_t>(1);
     int32_t* choff = c.take<int32_t>(size_t(bh) + 1);
@@ -391,6 +392,7 @@ static size_t carve_bwd(const msparse_dims* d, int64_t vcol_cap, char* base, Att
     float* dkc = c.take<float>(size_t(z.slots) * kBlock * d->head_dim);
     float* dvc = c.take<float>(size_t(z.slots) * kBlock * d->head_dim);
     if (a) {
+        a->k16 = k16;
         a->delta = delta;
         a->dmax = dmax;
         a->col_choff = choff;

@@ -91,120 +91,192 @@ __global__ void __launch_bounds__(256) bwd_delta_kernel(AttnArgs a) {
 __device__ __forceinline__ float dout_scale(const uint32_t* dmax) { return pow2_scale(dmax); }
 
 // ------------------------------------------------------------------ dQ (query-major)
+// One workgroup of four waves per pair of consecutive query blocks (as in the
+// forward): the pair walks the union of its block lists with the next key
+// tile's loads in flight, then the column tiles of each block.  Per tile and
+// wave: S^T = K Q^T, dP^T = V dO^T (bf16, Q and dO rows in VGPRs),
+// dQ^T += K^T dZ^T (fp16; K^T read transposed from the fp16 copy of K).
+constexpr int kDqThreads = 256;
+
+template <int D>
+struct DqBuf {
+    uint16_t k[TileLds<D>::kRowElems];   // bf16 K rows
+    uint16_t v[TileLds<D>::kRowElems];   // bf16 V rows
+    uint16_t k16[F16Tile<D>::kElems];    // fp16 K rows
+};
 template <int D>
 struct DqLds {
-    uint16_t k[TileLds<D>::kRowElems];
-    uint16_t v[TileLds<D>::kRowElems];
-    uint16_t kt[TileLds<D>::kTElems];
+    DqBuf<D> buf[2];
     int32_t kidx[64];
     int32_t lim[64];
 };
 
 template <int D>
-__global__ void __launch_bounds__(kThreads) bwd_dq_kernel(AttnArgs a) {
-    constexpr int KD = D / 16, ND = D / 32;
-    __shared__ DqLds<D> sm;
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, l32 = lane & 31;
-    int bh, qb;
-    query_tile_of(blockIdx.x, a.B, a.Hq, a.Hkv, a.nqb, bh, qb);
-    const int b = bh / a.Hq, hq = bh % a.Hq, hk = hq / (a.Hq / a.Hkv);
-    const int qrow = 32 * w + l32;
-    const int64_t grow = int64_t(bh) * a.Nq + int64_t(qb) * 64 + qrow;
+struct DqRows {
+    static constexpr int KD = D / 16, ND = D / 32;
+    u32x4 q[KD], g[KD];
+    f32x16 acc[ND];
+    float lse2, dlt;
+};
 
-    const uint16_t* __restrict__ kp = a.k + (int64_t(b) * a.Hkv + hk) * int64_t(a.Nk) * D;
-    const uint16_t* __restrict__ vp = a.v + (int64_t(b) * a.Hkv + hk) * int64_t(a.Nk) * D;
-    u32x4 qreg[KD], dreg[KD];
+// mask: 0 none, 1 causal diagonal, 2 per-key limits
+template <int D>
+__device__ __forceinline__ void dq_tile(const DqBuf<D>& sm, const int32_t* lims, DqRows<D>& st, int mask, int qrow,
+                                        int lane, float c2, float sc) {
+    constexpr int KD = DqRows<D>::KD, ND = DqRows<D>::ND;
+    const int h = lane >> 5, l32 = lane & 31;
+    f32x16 sacc[2], pacc[2];
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+        sacc[c] = f32x16{};
+        pacc[c] = f32x16{};
+        const uint16_t* krow = sm.k + (32 * c + l32) * TileLds<D>::kRowStride + 8 * h;
+        const uint16_t* vrow = sm.v + (32 * c + l32) * TileLds<D>::kRowStride + 8 * h;
+#pragma unroll
+        for (int s = 0; s < KD; ++s) {
+            sacc[c] = mfma32(lds_read16(krow + 16 * s), st.q[s], sacc[c]);
+            pacc[c] = mfma32(lds_read16(vrow + 16 * s), st.g[s], pacc[c]);
+        }
+    }
+    // s dZ^T = P o (s dP^T - s Delta), P = exp2(c2 z - lse2) on visible entries
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            float p = fast_exp2(__builtin_fmaf(sacc[c][r], c2, -st.lse2));
+            if (mask) {
+                const int key = 32 * c + 8 * (r >> 2) + 4 * h + (r & 3);
+                const int lim = mask == 1 ? key : lims[key];
+                if (qrow < lim) p = 0.f;
+            }
+            sacc[c][r] = p * __builtin_fmaf(pacc[c][r], sc, -st.dlt);
+        }
+    u32x4 zb[4];
+    zb[0] = pack8_f16<0>(sacc[0]);
+    zb[1] = pack8_f16<8>(sacc[0]);
+    zb[2] = pack8_f16<0>(sacc[1]);
+    zb[3] = pack8_f16<8>(sacc[1]);
+#pragma unroll
+    for (int i = 0; i < ND; ++i)
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+            st.acc[i] = mfma32h(lds_read_tr_a<F16Tile<D>::kStride>(sm.k16, 16 * g, 32 * i, lane), zb[g], st.acc[i]);
+}
+
+template <int D>
+__global__ void __launch_bounds__(kDqThreads) bwd_dq_kernel(AttnArgs a) {
+    constexpr int KD = DqRows<D>::KD, ND = DqRows<D>::ND;
+    constexpr int FS = F16Tile<D>::kStride;
+    __shared__ DqLds<D> sm;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, half = w >> 1, h = lane >> 5, l32 = lane & 31;
+    const int npair = (a.nqb + 1) >> 1;
+    int bh, qp;
+    query_tile_of(blockIdx.x, a.B, a.Hq, a.Hkv, npair, bh, qp);
+    const int b = bh / a.Hq, hq = bh % a.Hq, hk = hq / (a.Hq / a.Hkv);
+    const int qb0 = 2 * qp;
+    const bool has1 = qb0 + 1 < a.nqb;
+    const int qb = qb0 + (has1 ? half : 0);
+    const bool live = half == 0 || has1;
+    const int qrow = 32 * (w & 1) + l32;
+    const int64_t grow = int64_t(bh) * a.Nq + int64_t(qb) * 64 + qrow;
+    const int32_t qg = a.q_blk_global[qb];
+
+    const int64_t kvoff = (int64_t(b) * a.Hkv + hk) * int64_t(a.Nk) * D;
+    const uint16_t* __restrict__ kp = a.k + kvoff;
+    const uint16_t* __restrict__ vp = a.v + kvoff;
+    const uint16_t* __restrict__ k16p = a.k16 + kvoff;
+    DqRows<D> st;
 #pragma unroll
     for (int s = 0; s < KD; ++s) {
-        qreg[s] = *reinterpret_cast<const u32x4*>(a.q + grow * D + 16 * s + 8 * h);
-        dreg[s] = *reinterpret_cast<const u32x4*>(a.dout + grow * D + 16 * s + 8 * h);
+        st.q[s] = *reinterpret_cast<const u32x4*>(a.q + grow * D + 16 * s + 8 * h);
+        st.g[s] = *reinterpret_cast<const u32x4*>(a.dout + grow * D + 16 * s + 8 * h);
     }
     const float c2 = a.scale * kLog2e;
     const float lse_n = a.lse[grow];
-    const float lse2 = lse_n == -INFINITY ? INFINITY : lse_n * kLog2e;   // empty row: P = 0
+    st.lse2 = lse_n == -INFINITY ? INFINITY : lse_n * kLog2e;   // empty row: P = 0
     const float sc = dout_scale(a.dmax);
-    const float dlt = a.delta[grow] * sc;
-
-    f32x16 acc[ND];
+    st.dlt = a.delta[grow] * sc;
 #pragma unroll
-    for (int i = 0; i < ND; ++i) acc[i] = f32x16{};
+    for (int i = 0; i < ND; ++i) st.acc[i] = f32x16{};
 
-    const int64_t item = int64_t(bh) * a.nqb + qb;
-    const int64_t b0 = a.blk_ptr[item], b1 = a.blk_ptr[item + 1];
-    const int64_t c0 = a.col_ptr[item], c1 = a.col_ptr[item + 1];
-    const int nblk = int(b1 - b0);
-    const int ncolt = int((c1 - c0 + 63) / 64);
-    const int32_t qg = a.q_blk_global[qb];
+    // ---- block tiles: union of the two ascending block lists, pipelined
+    const int64_t item0 = int64_t(bh) * a.nqb + qb0;
+    const int64_t e00 = a.blk_ptr[item0], e01 = a.blk_ptr[item0 + 1];
+    const int64_t e11 = has1 ? a.blk_ptr[item0 + 2] : e01;
+    int64_t p0 = e00, p1 = e01;
+    auto next = [&](int32_t& kb, bool& in0, bool& in1) {
+        if (p0 >= e01 && p1 >= e11) return false;
+        const int32_t k0 = p0 < e01 ? a.blk_idx[p0] : INT32_MAX;
+        const int32_t k1 = p1 < e11 ? a.blk_idx[p1] : INT32_MAX;
+        kb = min(k0, k1);
+        in0 = k0 == kb;
+        in1 = k1 == kb;
+        p0 += in0;
+        p1 += in1;
+        return true;
+    };
+    RowRegs<D, kDqThreads> kr, vr, k16r;
+    int32_t kb = 0;
+    bool in0 = false, in1 = false;
+    bool have = next(kb, in0, in1);
+    if (have) {
+        const ContiguousRows rows{int64_t(kb) * 64};
+        load_rows<D, kDqThreads>(kr, kp, rows, tid);
+        load_rows<D, kDqThreads>(vr, vp, rows, tid);
+        load_rows<D, kDqThreads>(k16r, k16p, rows, tid);
+        store_rows<D, kDqThreads>(sm.buf[0].k, kr, tid);
+        store_rows<D, kDqThreads>(sm.buf[0].v, vr, tid);
+        store_rows<D, kDqThreads, FS>(sm.buf[0].k16, k16r, tid);
+    }
+    __syncthreads();
+    int cur = 0;
+    while (have) {
+        int32_t kb2 = 0;
+        bool in0n = false, in1n = false;
+        const bool more = next(kb2, in0n, in1n);
+        if (more) {
+            const ContiguousRows rows{int64_t(kb2) * 64};
+            load_rows<D, kDqThreads>(kr, kp, rows, tid);
+            load_rows<D, kDqThreads>(vr, vp, rows, tid);
+            load_rows<D, kDqThreads>(k16r, k16p, rows, tid);
+        }
+        if (half == 0 ? in0 : in1)
+            dq_tile<D>(sm.buf[cur], sm.lim, st, a.k_blk_global[kb] == qg ? 1 : 0, qrow, lane, c2, sc);
+        if (more) {
+            store_rows<D, kDqThreads>(sm.buf[cur ^ 1].k, kr, tid);
+            store_rows<D, kDqThreads>(sm.buf[cur ^ 1].v, vr, tid);
+            store_rows<D, kDqThreads, FS>(sm.buf[cur ^ 1].k16, k16r, tid);
+        }
+        __syncthreads();
+        cur ^= 1;
+        kb = kb2;
+        in0 = in0n;
+        in1 = in1n;
+        have = more;
+    }
 
-    for (int tt = 0; tt < nblk + ncolt; ++tt) {
-        bool masked;
-        int kb = -1;
-        if (tt < nblk) {
-            kb = a.blk_idx[b0 + tt];
-            masked = a.k_blk_global[kb] == qg;
-            if (masked && tid < 64) sm.lim[tid] = tid;
-        } else {
-            masked = true;
-            const int64_t cbase = c0 + int64_t(tt - nblk) * 64;
+    // ---- column tiles, one half at a time
+    for (int j = 0; j < 1 + int(has1); ++j) {
+        const int64_t c0 = a.col_ptr[item0 + j], c1 = a.col_ptr[item0 + j + 1];
+        const int32_t qgj = a.q_blk_global[qb0 + j];
+        for (int64_t cbase = c0; cbase < c1; cbase += 64) {
             const int cnt = int(min<int64_t>(64, c1 - cbase));
             if (tid < 64) {
-                const int j = tid < cnt ? tid : 0;
-                const int32_t col = a.col_idx[cbase + j];
+                const int32_t col = a.col_idx[cbase + (tid < cnt ? tid : 0)];
                 sm.kidx[tid] = col;
-                sm.lim[tid] = tid < cnt ? (a.k_blk_global[col >> 6] == qg ? (col & 63) : 0) : 64;
+                sm.lim[tid] = tid < cnt ? (a.k_blk_global[col >> 6] == qgj ? (col & 63) : 0) : 64;
             }
             __syncthreads();
+            const IndexedRows rows{sm.kidx};
+            stage_rows<D, kDqThreads>(sm.buf[0].k, kp, rows, tid);
+            stage_rows<D, kDqThreads>(sm.buf[0].v, vp, rows, tid);
+            stage_rows<D, kDqThreads, IndexedRows, FS>(sm.buf[0].k16, k16p, rows, tid);
+            __syncthreads();
+            if (half == j) dq_tile<D>(sm.buf[0], sm.lim, st, 2, qrow, lane, c2, sc);
+            __syncthreads();
         }
-        if (kb >= 0) {
-            const ContiguousRows rows{int64_t(kb) * 64};
-            stage_rows<D, kThreads>(sm.k, kp, rows, tid);
-            stage_rows<D, kThreads>(sm.v, vp, rows, tid);
-            stage_transposed_f16<D, kThreads>(sm.kt, kp, rows, 1.0f, tid);
-        } else {
-            stage_rows<D, kThreads>(sm.k, kp, IndexedRows{sm.kidx}, tid);
-            stage_rows<D, kThreads>(sm.v, vp, IndexedRows{sm.kidx}, tid);
-            stage_transposed_f16<D, kThreads>(sm.kt, kp, IndexedRows{sm.kidx}, 1.0f, tid);
-        }
-        __syncthreads();
-
-        f32x16 sacc[2], pacc[2];
-#pragma unroll
-        for (int c = 0; c < 2; ++c) {
-            sacc[c] = f32x16{};
-            pacc[c] = f32x16{};
-            const uint16_t* krow = sm.k + (32 * c + l32) * TileLds<D>::kRowStride + 8 * h;
-            const uint16_t* vrow = sm.v + (32 * c + l32) * TileLds<D>::kRowStride + 8 * h;
-#pragma unroll
-            for (int s = 0; s < KD; ++s) {
-                sacc[c] = mfma32(lds_read16(krow + 16 * s), qreg[s], sacc[c]);
-                pacc[c] = mfma32(lds_read16(vrow + 16 * s), dreg[s], pacc[c]);
-            }
-        }
-        // s dZ^T = P o (s dP^T - s Delta), P = exp2(c2 z - lse2) on visible entries
-#pragma unroll
-        for (int c = 0; c < 2; ++c)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                float p = fast_exp2(__builtin_fmaf(sacc[c][r], c2, -lse2));
-                if (masked) {
-                    const int key = 32 * c + 8 * (r >> 2) + 4 * h + (r & 3);
-                    if (qrow < sm.lim[key]) p = 0.f;
-                }
-                sacc[c][r] = p * __builtin_fmaf(pacc[c][r], sc, -dlt);
-            }
-        u32x4 zb[4];
-        zb[0] = pack8_f16<0>(sacc[0]);
-        zb[1] = pack8_f16<8>(sacc[0]);
-        zb[2] = pack8_f16<0>(sacc[1]);
-        zb[3] = pack8_f16<8>(sacc[1]);
-#pragma unroll
-        for (int i = 0; i < ND; ++i) {
-            const uint16_t* trow = sm.kt + (32 * i + l32) * TileLds<D>::kTStride + 8 * h;
-#pragma unroll
-            for (int g = 0; g < 4; ++g) acc[i] = mfma32h(lds_read16(trow + 16 * g), zb[g], acc[i]);
-        }
-        __syncthreads();
     }
+    if (!live) return;
     float* dq = a.dq + grow * D;
     const float fin = a.scale / sc;
 #pragma unroll
@@ -212,10 +284,10 @@ __global__ void __launch_bounds__(kThreads) bwd_dq_kernel(AttnArgs a) {
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
             f32x4 val;
-            val.x = acc[i][4 * g + 0] * fin;
-            val.y = acc[i][4 * g + 1] * fin;
-            val.z = acc[i][4 * g + 2] * fin;
-            val.w = acc[i][4 * g + 3] * fin;
+            val.x = st.acc[i][4 * g + 0] * fin;
+            val.y = st.acc[i][4 * g + 1] * fin;
+            val.z = st.acc[i][4 * g + 2] * fin;
+            val.w = st.acc[i][4 * g + 3] * fin;
             f32x4* dst = reinterpret_cast<f32x4*>(dq + 32 * i + 8 * g + 4 * h);
             if (a.dq_accumulate) val += *dst;
             *dst = val;
@@ -601,8 +673,10 @@ hipError_t launch_bwd_d(const AttnArgs& a, hipStream_t s) {
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const int64_t qgrid = int64_t(a.B) * a.Hq * a.nqb;
-    if (qgrid > 0) { TraceScope _t("bwd_dq", s); hipLaunchKernelGGL(bwd_dq_kernel<D>, dim3(unsigned(qgrid)), dim3(kThreads), 0, s, a); }
+    const int64_t nkv = int64_t(a.B) * a.Hkv * a.Nk * a.d;
+    if ((e = launch_to_f16(a.k, a.k16, nkv, nullptr, s)) != hipSuccess) return e;
+    const int64_t qgrid = int64_t(a.B) * a.Hq * ((a.nqb + 1) / 2);
+    if (qgrid > 0) { TraceScope _t("bwd_dq", s); hipLaunchKernelGGL(bwd_dq_kernel<D>, dim3(unsigned(qgrid)), dim3(kDqThreads), 0, s, a); }
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const int64_t kgrid = int64_t(a.B) * a.Hkv * a.nkb;
     if (kgrid > 0) { TraceScope _t("bwd_dkdv", s); hipLaunchKernelGGL(bwd_dkdv_kernel<D>, dim3(unsigned(kgrid)), dim3(kThreads), 0, s, a); }

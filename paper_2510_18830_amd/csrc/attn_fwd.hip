@@ -34,16 +34,10 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kSlack = 8.f;   // log2 units
 
-// V tile rows: fp16, row stride D + 16 elements (the transposing reads of a
-// 16-lane group then touch 4 rows x 32 bytes in distinct banks).
-template <int D>
-struct VTile {
-    static constexpr int kStride = D + 16;
-};
 template <int D>
 struct FwdBuf {
     uint16_t k[TileLds<D>::kRowElems];      // bf16 K rows
-    uint16_t v[64 * VTile<D>::kStride];     // fp16 V rows
+    uint16_t v[F16Tile<D>::kElems];          // fp16 V rows
 };
 template <int D>
 struct FwdLds {
@@ -129,7 +123,7 @@ __device__ __forceinline__ void fwd_tile(const FwdBuf<D>& sm, const int32_t* lim
     for (int i = 0; i < ND; ++i)
 #pragma unroll
         for (int g = 0; g < 4; ++g)
-            st.o[i] = mfma32h(lds_read_tr_a<VTile<D>::kStride>(sm.v, 16 * g, 32 * i, lane), pb[g], st.o[i]);
+            st.o[i] = mfma32h(lds_read_tr_a<F16Tile<D>::kStride>(sm.v, 16 * g, 32 * i, lane), pb[g], st.o[i]);
 }
 
 // Two waves per SIMD (at most 256 registers per lane), two workgroups per CU:
@@ -191,7 +185,7 @@ attn_fwd_kernel(AttnArgs a) {
         return true;
     };
     RowRegs<D, kFwdThreads> kr, vr;
-    constexpr int VS = VTile<D>::kStride;
+    constexpr int VS = F16Tile<D>::kStride;
     int32_t kb = 0;
     bool in0 = false, in1 = false;
     bool have = next(kb, in0, in1);

@@ -57,10 +57,10 @@ struct AttnArgs {
     const uint16_t* q;     // bf16 [B,Hq,Nq,d]
     const uint16_t* k;     // bf16 [B,Hkv,Nk,d]
     const uint16_t* v;
-    const uint16_t* v16;   // fp16 copies of the second-GEMM operands (workspace):
-    const uint16_t* k16;   //   V (fwd), K (dQ), Q and s dO (dK / dV)
-    const uint16_t* q16;
-    const uint16_t* g16;
+    uint16_t* v16;         // fp16 copies of the second-GEMM operands (workspace):
+    uint16_t* k16;         //   V (fwd), K (dQ), Q and s dO (dK / dV)
+    uint16_t* q16;
+    uint16_t* g16;
     const uint16_t* o;     // forward output (bwd)
     const uint16_t* dout;  // bf16 [B,Hq,Nq,d] (bwd)
     uint16_t* out;         // bf16 [B,Hq,Nq,d] (fwd)

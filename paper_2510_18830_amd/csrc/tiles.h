@@ -30,6 +30,15 @@ struct TileLds {
     static constexpr int kTElems = D * kTStride;
 };
 
+// fp16 row-major tiles read through transposing loads: row stride D + 16
+// elements, so the reads of a 16-lane group (4 rows x 32 bytes) hit distinct
+// banks.
+template <int D>
+struct F16Tile {
+    static constexpr int kStride = D + 16;
+    static constexpr int kElems = 64 * kStride;
+};
+
 // position of row k (0..63) inside a transposed row
 __device__ __forceinline__ int tpos(int k) {
     const int a = (k >> 2) & 3;
