@@ -217,7 +217,9 @@ MSPARSE_API msparse_status msparse_merge_out_lse(const msparse_dims* dims, const
  * a bf16-rounded O moves large gradients by about 2^-9 of their size).
  * dq, dk, dv are fp32 and overwritten, except that dq_accumulate = 1 adds into
  * dq (ring steps after the first).
- * Workspace: msparse_attn_bwd_workspace(dims, vcol_cap) bytes. */
+ * Workspace: msparse_attn_bwd_workspace(dims, vcol_cap) bytes; it holds
+ * fp16 copies of k, q and dO (times a power of two), Delta, and the column
+ * pass's work list and per-item partials. */
 MSPARSE_API size_t msparse_attn_bwd_workspace(const msparse_dims* dims, int64_t vcol_cap);
 MSPARSE_API msparse_status msparse_attn_bwd(const msparse_dims* dims, const void* q, const void* k, const void* v,
                                 const void* out, const float* out_f32, const void* dout, const float* lse,

@@ -381,6 +381,8 @@ static size_t carve_bwd(const msparse_dims* d, int64_t vcol_cap, char* base, Att
     const ColPlanSizes z = col_plan_sizes(bh, vcol_cap, d->seq_q / kBlock);
     Carve c{base};
     uint16_t* k16 = c.take<uint16_t>(size_t(d->batch) * d->heads_kv * d->seq_k * d->head_dim);
+    uint16_t* q16 = c.take<uint16_t>(size_t(bh) * d->seq_q * d->head_dim);
+    uint16_t* g16 = c.take<uint16_t>(size_t(bh) * d->seq_q * d->head_dim);
     float* delta = c.take<float>(size_t(bh) * d->seq_q);
     uint32_t* dmax = c.take<uint32_t>(1);
     int32_t* choff = c.take<int32_t>(size_t(bh) + 1);
@@ -393,6 +395,8 @@ static size_t carve_bwd(const msparse_dims* d, int64_t vcol_cap, char* base, Att
     float* dvc = c.take<float>(size_t(z.slots) * kBlock * d->head_dim);
     if (a) {
         a->k16 = k16;
+        a->q16 = q16;
+        a->g16 = g16;
         a->delta = delta;
         a->dmax = dmax;
         a->col_choff = choff;

@@ -295,12 +295,14 @@ __global__ void __launch_bounds__(kDqThreads) bwd_dq_kernel(AttnArgs a) {
 }
 
 // ------------------------------------------------------------------ dK / dV (key-major)
+// A query tile as the key-major passes stage it: bf16 Q and dO rows for the
+// first GEMMs, fp16 Q and s dO rows read transposed for the second.
 template <int D>
-struct KvLds {
+struct KvBuf {
     uint16_t q[TileLds<D>::kRowElems];
-    uint16_t qt[TileLds<D>::kTElems];
     uint16_t g[TileLds<D>::kRowElems];    // dO
-    uint16_t gt[TileLds<D>::kTElems];
+    uint16_t q16[F16Tile<D>::kElems];     // fp16 Q
+    uint16_t g16[F16Tile<D>::kElems];     // fp16 s dO
     float lse2[64];
     float dlt[64];
 };
@@ -309,10 +311,10 @@ struct KvLds {
 // the per-key visibility: key visible to in-block query row r iff active and
 // r >= lim.
 template <int D>
-__device__ __forceinline__ void kv_tile(const KvLds<D>& sm, const u32x4* kreg, const u32x4* vreg, bool masked,
-                                        bool active, int lim, float c2, float sc, int h, int l32, f32x16* dv,
-                                        f32x16* dk) {
-    constexpr int KD = D / 16, ND = D / 32;
+__device__ __forceinline__ void kv_tile(const KvBuf<D>& sm, const u32x4* kreg, const u32x4* vreg, bool masked,
+                                        bool active, int lim, float c2, float sc, int lane, f32x16* dv, f32x16* dk) {
+    constexpr int KD = D / 16, ND = D / 32, FS = F16Tile<D>::kStride;
+    const int h = lane >> 5, l32 = lane & 31;
     f32x16 sacc[2], pacc[2];
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb) {
@@ -346,47 +348,84 @@ __device__ __forceinline__ void kv_tile(const KvLds<D>& sm, const u32x4* kreg, c
     zb[1] = pack8_f16<8>(pacc[0]);
     zb[2] = pack8_f16<0>(pacc[1]);
     zb[3] = pack8_f16<8>(pacc[1]);
+    // dV^T += (s dO)^T P, dK^T += Q^T (s dZ): A operands read transposed
 #pragma unroll
-    for (int i = 0; i < ND; ++i) {
-        const uint16_t* gt = sm.gt + (32 * i + l32) * TileLds<D>::kTStride + 8 * h;
-        const uint16_t* qt = sm.qt + (32 * i + l32) * TileLds<D>::kTStride + 8 * h;
+    for (int i = 0; i < ND; ++i)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-            dv[i] = mfma32h(lds_read16(gt + 16 * g), pb[g], dv[i]);
-            dk[i] = mfma32h(lds_read16(qt + 16 * g), zb[g], dk[i]);
+            dv[i] = mfma32h(lds_read_tr_a<FS>(sm.g16, 16 * g, 32 * i, lane), pb[g], dv[i]);
+            dk[i] = mfma32h(lds_read_tr_a<FS>(sm.q16, 16 * g, 32 * i, lane), zb[g], dk[i]);
         }
-    }
 }
 
-template <int D>
-__device__ __forceinline__ void kv_stage_query_tile(KvLds<D>& sm, const AttnArgs& a, int bh, int qb, float sc,
-                                                    int tid) {
+// Register copy of a query tile in flight (software pipelining).
+template <int D, int NT>
+struct KvRegs {
+    RowRegs<D, NT> q, g, q16, g16;
+    float lse, dlt;
+};
+template <int D, int NT>
+__device__ __forceinline__ void kv_load_query_tile(KvRegs<D, NT>& r, const AttnArgs& a, int bh, int qb, int tid) {
     const int64_t row0 = int64_t(bh) * a.Nq + int64_t(qb) * 64;
     const ContiguousRows rows{row0};
-    stage_rows<D, kThreads>(sm.q, a.q, rows, tid);
-    stage_transposed_f16<D, kThreads>(sm.qt, a.q, rows, 1.0f, tid);
-    stage_rows<D, kThreads>(sm.g, a.dout, rows, tid);
-    stage_transposed_f16<D, kThreads>(sm.gt, a.dout, rows, sc, tid);
+    load_rows<D, NT>(r.q, a.q, rows, tid);
+    load_rows<D, NT>(r.g, a.dout, rows, tid);
+    load_rows<D, NT>(r.q16, a.q16, rows, tid);
+    load_rows<D, NT>(r.g16, a.g16, rows, tid);
     if (tid < 64) {
-        const float l = a.lse[row0 + tid];
-        sm.lse2[tid] = l == -INFINITY ? INFINITY : l * kLog2e;
-        sm.dlt[tid] = a.delta[row0 + tid] * sc;
+        r.lse = a.lse[row0 + tid];
+        r.dlt = a.delta[row0 + tid];
     }
 }
+template <int D, int NT>
+__device__ __forceinline__ void kv_store_query_tile(KvBuf<D>& sm, const KvRegs<D, NT>& r, float sc, int tid) {
+    constexpr int FS = F16Tile<D>::kStride;
+    store_rows<D, NT>(sm.q, r.q, tid);
+    store_rows<D, NT>(sm.g, r.g, tid);
+    store_rows<D, NT, FS>(sm.q16, r.q16, tid);
+    store_rows<D, NT, FS>(sm.g16, r.g16, tid);
+    if (tid < 64) {
+        sm.lse2[tid] = r.lse == -INFINITY ? INFINITY : r.lse * kLog2e;
+        sm.dlt[tid] = r.dlt * sc;
+    }
+}
+template <int D, int NT>
+__device__ __forceinline__ void kv_stage_query_tile(KvBuf<D>& sm, const AttnArgs& a, int bh, int qb, float sc,
+                                                    int tid) {
+    KvRegs<D, NT> r;
+    kv_load_query_tile<D, NT>(r, a, bh, qb, tid);
+    kv_store_query_tile<D, NT>(sm, r, sc, tid);
+}
 
-// Key-major pass over 64-key blocks: grid = B * Hkv * nkb.
+// Key-major pass: one workgroup of four waves per (b, KV head, pair of
+// consecutive 64-key blocks); waves 2j, 2j+1 hold 32 keys each of block j of
+// the pair in VGPRs.  For every query head of the KV group the pair walks the
+// union of its two transposed lists (query blocks that selected the key
+// block), the next query tile's loads in flight during the current one.
+constexpr int kKvThreads = 256;
+
 template <int D>
-__global__ void __launch_bounds__(kThreads) bwd_dkdv_kernel(AttnArgs a) {
+struct KvLds {
+    KvBuf<D> buf[2];
+};
+
+template <int D>
+__global__ void __launch_bounds__(kKvThreads) bwd_dkdv_kernel(AttnArgs a) {
     constexpr int KD = D / 16, ND = D / 32;
     __shared__ KvLds<D> sm;
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, l32 = lane & 31;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, half = w >> 1, h = lane >> 5, l32 = lane & 31;
     const int BK = a.B * a.Hkv;
-    const int64_t t = blockIdx.x;
-    const int bk = int(t % BK);
-    const int kb = int(t / BK);
+    const int npair = (a.nkb + 1) >> 1;
+    const int64_t u = xcd_chunk(blockIdx.x, int64_t(BK) * npair);
+    const int bk = int(u / npair);
+    const int kp = int(u % npair);          // heaviest (earliest) pairs first
     const int b = bk / a.Hkv, hk = bk % a.Hkv;
     const int G = a.Hq / a.Hkv;
-    const int key = 32 * w + l32;  // this lane's key inside the block
+    const int kb0 = 2 * kp;
+    const bool has1 = kb0 + 1 < a.nkb;
+    const int kb = kb0 + (has1 ? half : 0);
+    const bool live = half == 0 || has1;
+    const int key = 32 * (w & 1) + l32;     // this lane's key inside the block
     const int64_t krow = int64_t(bk) * a.Nk + int64_t(kb) * 64 + key;
 
     u32x4 kreg[KD], vreg[KD];
@@ -404,37 +443,80 @@ __global__ void __launch_bounds__(kThreads) bwd_dkdv_kernel(AttnArgs a) {
     const float c2 = a.scale * kLog2e;
     const float sc = dout_scale(a.dmax);
     const int32_t kg = a.k_blk_global[kb];
-    for (int g = 0; g < G; ++g) {
-        const int bh = b * a.Hq + hk * G + g;
-        const int64_t item = int64_t(bh) * a.nkb + kb;
-        const int64_t p0 = a.kblk_ptr[item], p1 = a.kblk_ptr[item + 1];
-        for (int64_t p = p0; p < p1; ++p) {
-            const int qb = a.kblk_idx[p];
-            const bool masked = a.q_blk_global[qb] == kg;   // diagonal tile
-            kv_stage_query_tile<D>(sm, a, bh, qb, sc, tid);
-            __syncthreads();
-            kv_tile<D>(sm, kreg, vreg, masked, true, key, c2, sc, h, l32, dv, dk);
-            __syncthreads();
+
+    // walk: heads of the group in order, per head the union of the two lists
+    int g = 0;
+    int64_t p0 = 0, e0 = 0, p1 = 0, e1 = 0;
+    auto open_head = [&]() {
+        const int64_t item = int64_t(b * a.Hq + hk * G + g) * a.nkb + kb0;
+        p0 = a.kblk_ptr[item];
+        e0 = a.kblk_ptr[item + 1];
+        p1 = e0;
+        e1 = has1 ? a.kblk_ptr[item + 2] : e0;
+    };
+    open_head();
+    auto next = [&](int& bh, int& qb, bool& in0, bool& in1) {
+        while (p0 >= e0 && p1 >= e1) {
+            if (++g >= G) return false;
+            open_head();
         }
+        const int32_t q0 = p0 < e0 ? a.kblk_idx[p0] : INT32_MAX;
+        const int32_t q1 = p1 < e1 ? a.kblk_idx[p1] : INT32_MAX;
+        qb = min(q0, q1);
+        in0 = q0 == qb;
+        in1 = q1 == qb;
+        p0 += in0;
+        p1 += in1;
+        bh = b * a.Hq + hk * G + g;
+        return true;
+    };
+    KvRegs<D, kKvThreads> r;
+    int bh = 0, qb = 0;
+    bool in0 = false, in1 = false;
+    bool have = next(bh, qb, in0, in1);
+    if (have) {
+        kv_load_query_tile<D, kKvThreads>(r, a, bh, qb, tid);
+        kv_store_query_tile<D, kKvThreads>(sm.buf[0], r, sc, tid);
     }
+    __syncthreads();
+    int cur = 0;
+    while (have) {
+        int bh2 = 0, qb2 = 0;
+        bool in0n = false, in1n = false;
+        const bool more = next(bh2, qb2, in0n, in1n);
+        if (more) kv_load_query_tile<D, kKvThreads>(r, a, bh2, qb2, tid);
+        if (half == 0 ? in0 : in1) {
+            const bool masked = a.q_blk_global[qb] == kg;   // diagonal tile
+            kv_tile<D>(sm.buf[cur], kreg, vreg, masked, true, key, c2, sc, lane, dv, dk);
+        }
+        if (more) kv_store_query_tile<D, kKvThreads>(sm.buf[cur ^ 1], r, sc, tid);
+        __syncthreads();
+        cur ^= 1;
+        bh = bh2;
+        qb = qb2;
+        in0 = in0n;
+        in1 = in1n;
+        have = more;
+    }
+    if (!live) return;
     float* dkp = a.dk + krow * D;
     float* dvp = a.dv + krow * D;
     const float fk = a.scale / sc, fv = 1.f / sc;
 #pragma unroll
     for (int i = 0; i < ND; ++i)
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
+        for (int j = 0; j < 4; ++j) {
             f32x4 x, y;
-            x.x = dk[i][4 * g + 0] * fk;
-            x.y = dk[i][4 * g + 1] * fk;
-            x.z = dk[i][4 * g + 2] * fk;
-            x.w = dk[i][4 * g + 3] * fk;
-            y.x = dv[i][4 * g + 0] * fv;
-            y.y = dv[i][4 * g + 1] * fv;
-            y.z = dv[i][4 * g + 2] * fv;
-            y.w = dv[i][4 * g + 3] * fv;
-            *reinterpret_cast<f32x4*>(dkp + 32 * i + 8 * g + 4 * h) = x;
-            *reinterpret_cast<f32x4*>(dvp + 32 * i + 8 * g + 4 * h) = y;
+            x.x = dk[i][4 * j + 0] * fk;
+            x.y = dk[i][4 * j + 1] * fk;
+            x.z = dk[i][4 * j + 2] * fk;
+            x.w = dk[i][4 * j + 3] * fk;
+            y.x = dv[i][4 * j + 0] * fv;
+            y.y = dv[i][4 * j + 1] * fv;
+            y.z = dv[i][4 * j + 2] * fv;
+            y.w = dv[i][4 * j + 3] * fv;
+            *reinterpret_cast<f32x4*>(dkp + 32 * i + 8 * j + 4 * h) = x;
+            *reinterpret_cast<f32x4*>(dvp + 32 * i + 8 * j + 4 * h) = y;
         }
 }
 
@@ -548,7 +630,7 @@ __global__ void __launch_bounds__(kPlanThreads) bwd_colplan_kernel(AttnArgs a) {
 template <int D>
 __global__ void __launch_bounds__(kThreads) bwd_dkdv_col_kernel(AttnArgs a) {
     constexpr int KD = D / 16, ND = D / 32;
-    __shared__ KvLds<D> sm;
+    __shared__ KvBuf<D> sm;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, l32 = lane & 31;
     const int nc = a.col_choff[a.B * a.Hq];
     const int item = int(blockIdx.x);
@@ -593,9 +675,9 @@ __global__ void __launch_bounds__(kThreads) bwd_dkdv_col_kernel(AttnArgs a) {
         const int lim = qg == cg ? cin : 0;
         // every column covered by a selected block-diagonal: nothing to do here
         if (!__syncthreads_or(active)) continue;
-        kv_stage_query_tile<D>(sm, a, bh, qb, sc, tid);
+        kv_stage_query_tile<D, kThreads>(sm, a, bh, qb, sc, tid);
         __syncthreads();
-        kv_tile<D>(sm, kreg, vreg, true, active, lim, c2, sc, h, l32, dv, dk);
+        kv_tile<D>(sm, kreg, vreg, true, active, lim, c2, sc, lane, dv, dk);
         __syncthreads();
     }
     if (!valid) return;
@@ -678,8 +760,11 @@ hipError_t launch_bwd_d(const AttnArgs& a, hipStream_t s) {
     const int64_t qgrid = int64_t(a.B) * a.Hq * ((a.nqb + 1) / 2);
     if (qgrid > 0) { TraceScope _t("bwd_dq", s); hipLaunchKernelGGL(bwd_dq_kernel<D>, dim3(unsigned(qgrid)), dim3(kDqThreads), 0, s, a); }
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    const int64_t kgrid = int64_t(a.B) * a.Hkv * a.nkb;
-    if (kgrid > 0) { TraceScope _t("bwd_dkdv", s); hipLaunchKernelGGL(bwd_dkdv_kernel<D>, dim3(unsigned(kgrid)), dim3(kThreads), 0, s, a); }
+    const int64_t nq = int64_t(a.B) * a.Hq * a.Nq * a.d;
+    if ((e = launch_to_f16(a.q, a.q16, nq, nullptr, s)) != hipSuccess) return e;
+    if ((e = launch_to_f16(a.dout, a.g16, nq, a.dmax, s)) != hipSuccess) return e;
+    const int64_t kpgrid = int64_t(a.B) * a.Hkv * ((a.nkb + 1) / 2);
+    if (kpgrid > 0) { TraceScope _t("bwd_dkdv", s); hipLaunchKernelGGL(bwd_dkdv_kernel<D>, dim3(unsigned(kpgrid)), dim3(kKvThreads), 0, s, a); }
     if ((e = hipGetLastError()) != hipSuccess) return e;
     { TraceScope _t("bwd_colplan", s); hipLaunchKernelGGL(bwd_colplan_kernel, dim3(1), dim3(kPlanThreads), 0, s, a); }
     if ((e = hipGetLastError()) != hipSuccess) return e;
@@ -688,6 +773,7 @@ hipError_t launch_bwd_d(const AttnArgs& a, hipStream_t s) {
         hipLaunchKernelGGL(bwd_dkdv_col_kernel<D>, dim3(unsigned(a.col_slots)), dim3(kThreads), 0, s, a);
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
+    const int64_t kgrid = int64_t(a.B) * a.Hkv * a.nkb;
     if (kgrid > 0) { TraceScope _t("bwd_colmerge", s); hipLaunchKernelGGL(bwd_colmerge_kernel, dim3(unsigned(kgrid)), dim3(128), 0, s, a); }
     return hipGetLastError();
 }

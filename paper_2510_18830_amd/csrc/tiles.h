@@ -171,39 +171,31 @@ __device__ __forceinline__ void store_trans_f16(uint16_t* lds, const TransRegs<D
     }
 }
 
-#ifndef MS_ORDER
-#define MS_ORDER 1
-#endif
 #ifndef MS_XCHUNK
-#define MS_XCHUNK 64
+#define MS_XCHUNK 64   // logical items per XCD run
 #endif
-// (head, query block) of workgroup t in a B*Hq*nqb grid.
-__device__ __forceinline__ void query_tile_of(int64_t t, int B, int Hq, int Hkv, int nqb, int& bh, int& qb) {
-    const int64_t BH = int64_t(B) * Hq;
-#if MS_ORDER == 0
-    bh = int(t % BH);
-    qb = nqb - 1 - int(t / BH);
-#else
-    const int64_t total = BH * nqb;
+// Workgroup ids are dispatched round-robin over the 8 XCDs, each with its own
+// L2.  xcd_chunk maps id t to a logical index so that each XCD receives runs
+// of C consecutive logical items (the tail past the last full round of 8 runs
+// keeps its identity mapping); a bijection on [0, total).
+__device__ __forceinline__ int64_t xcd_chunk(int64_t t, int64_t total) {
     constexpr int64_t C = MS_XCHUNK;
     const int64_t full = total / (8 * C) * (8 * C);
-    int64_t u = t;
-    if (t < full) {
-        const int64_t n = t >> 3, x = t & 7;
-        u = (n / C) * 8 * C + x * C + (n % C);
-    }
-#if MS_ORDER == 1
+    if (t >= full) return t;
+    const int64_t n = t >> 3, x = t & 7;
+    return (n / C) * 8 * C + x * C + (n % C);
+}
+
+// (head, query block) of workgroup t in a B*Hq*nqb grid: KV-group-major
+// (the group's heads at one block are neighbours), latest blocks first.
+__device__ __forceinline__ void query_tile_of(int64_t t, int B, int Hq, int Hkv, int nqb, int& bh, int& qb) {
+    const int64_t u = xcd_chunk(t, int64_t(B) * Hq * nqb);
     const int G = Hq / Hkv;
     const int64_t per = int64_t(nqb) * G;
     const int bg = int(u / per);
     const int64_t r = u % per;
     qb = nqb - 1 - int(r / G);
     bh = (bg / Hkv) * Hq + (bg % Hkv) * G + int(r % G);
-#else
-    bh = int(u % BH);
-    qb = nqb - 1 - int(u / BH);
-#endif
-#endif
 }
 
 // A operand of a 32x32x16 fp16 MFMA taken transposed from a row-major fp16
