@@ -34,18 +34,6 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kSlack = 8.f;   // log2 units
 
-template <int D>
-struct FwdBuf {
-    uint16_t k[TileLds<D>::kRowElems];      // bf16 K rows
-    uint16_t v[F16Tile<D>::kElems];          // fp16 V rows
-};
-template <int D>
-struct FwdLds {
-    FwdBuf<D> buf[2];  // double buffer: tile t+1 is stored while tile t is read
-    int32_t kidx[64];
-    int32_t lim[64];   // column tile: key visible to in-block query row r iff r >= lim
-};
-
 // Online-softmax state of one wave: 32 query rows, O^T accumulator.
 template <int D>
 struct FwdRows {
@@ -59,8 +47,8 @@ struct FwdRows {
 // One 64-key tile for one wave.  mask: 0 none, 1 causal diagonal (key k
 // visible to row r iff r >= k), 2 per-key limits from LDS.
 template <int D>
-__device__ __forceinline__ void fwd_tile(const FwdBuf<D>& sm, const int32_t* lims, FwdRows<D>& st, int mask,
-                                         int qrow, int lane, float c2) {
+__device__ __forceinline__ void fwd_tile(const uint16_t* kt, const uint16_t* vt, const int32_t* lims, FwdRows<D>& st,
+                                         int mask, int qrow, int lane, float c2) {
     const int h = lane >> 5, l32 = lane & 31;
     constexpr int KD = FwdRows<D>::KD, ND = FwdRows<D>::ND;
     // ---- S^T for keys 0-31 (c = 0) and 32-63 (c = 1)
@@ -68,9 +56,9 @@ __device__ __forceinline__ void fwd_tile(const FwdBuf<D>& sm, const int32_t* lim
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
         sacc[c] = f32x16{};
-        const uint16_t* krow = sm.k + (32 * c + l32) * TileLds<D>::kRowStride + 8 * h;
 #pragma unroll
-        for (int s = 0; s < KD; ++s) sacc[c] = mfma32(lds_read16(krow + 16 * s), st.q[s], sacc[c]);
+        for (int s = 0; s < KD; ++s)
+            sacc[c] = mfma32(dma_read16<D, kRowPad>(kt, 32 * c + l32, h + 2 * s), st.q[s], sacc[c]);
     }
     // ---- mask, tile max (raw logits; scale > 0 commutes with max)
     if (mask) {
@@ -123,7 +111,7 @@ __device__ __forceinline__ void fwd_tile(const FwdBuf<D>& sm, const int32_t* lim
     for (int i = 0; i < ND; ++i)
 #pragma unroll
         for (int g = 0; g < 4; ++g)
-            st.o[i] = mfma32h(lds_read_tr_a<F16Tile<D>::kStride>(sm.v, 16 * g, 32 * i, lane), pb[g], st.o[i]);
+            st.o[i] = mfma32h(dma_read_tr<D, kTrPad>(vt, 16 * g, 32 * i, lane), pb[g], st.o[i]);
 }
 
 // Two waves per SIMD (at most 256 registers per lane), two workgroups per CU:
@@ -132,11 +120,14 @@ template <int D>
 __global__ void __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 attn_fwd_kernel(AttnArgs a) {
     constexpr int KD = FwdRows<D>::KD, ND = FwdRows<D>::ND;
-    __shared__ FwdLds<D> sm;
+    // two pipeline buffers as separate LDS objects (K bf16, V fp16 rows)
+    constexpr int KE = DmaTile<D, kRowPad>::kElems, VE = DmaTile<D, kTrPad>::kElems;
+    __shared__ uint16_t k0s[KE], v0s[VE], k1s[KE], v1s[VE];
+    __shared__ int32_t kidx[64], lims[64];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int w = tid >> 6;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index (uniform)
     const int half = w >> 1;      // query block of the pair
     const int h = lane >> 5;      // lane half
     const int l32 = lane & 31;
@@ -152,7 +143,7 @@ attn_fwd_kernel(AttnArgs a) {
     const int qb = qb0 + (has1 ? half : 0);   // a lone block: both halves read it, half 1 stays idle
     const bool live = half == 0 || has1;
     const int qrow = 32 * (w & 1) + l32;      // row inside the query block
-    const int32_t qg = a.q_blk_global[qb];
+    const int32_t qg = ldc(a.q_blk_global, qb);
 
     const uint16_t* __restrict__ kp = a.k + (int64_t(b) * a.Hkv + hk) * int64_t(a.Nk) * D;
     const uint16_t* __restrict__ vp = a.v16 + (int64_t(b) * a.Hkv + hk) * int64_t(a.Nk) * D;
@@ -170,13 +161,13 @@ attn_fwd_kernel(AttnArgs a) {
     // ---- block tiles: the union of the two ascending block lists, software
     // pipelined (the loads of the next tile are in flight during this tile)
     const int64_t item0 = int64_t(bh) * a.nqb + qb0;
-    const int64_t e00 = a.blk_ptr[item0], e01 = a.blk_ptr[item0 + 1];
-    const int64_t e11 = has1 ? a.blk_ptr[item0 + 2] : e01;
+    const int64_t e00 = ldc(a.blk_ptr, item0), e01 = ldc(a.blk_ptr, item0 + 1);
+    const int64_t e11 = has1 ? ldc(a.blk_ptr, item0 + 2) : e01;
     int64_t p0 = e00, p1 = e01;
     auto next = [&](int32_t& kb, bool& in0, bool& in1) {
         if (p0 >= e01 && p1 >= e11) return false;
-        const int32_t k0 = p0 < e01 ? a.blk_idx[p0] : INT32_MAX;
-        const int32_t k1 = p1 < e11 ? a.blk_idx[p1] : INT32_MAX;
+        const int32_t k0 = p0 < e01 ? ldc(a.blk_idx, p0) : INT32_MAX;
+        const int32_t k1 = p1 < e11 ? ldc(a.blk_idx, p1) : INT32_MAX;
         kb = min(k0, k1);
         in0 = k0 == kb;
         in1 = k1 == kb;
@@ -184,59 +175,57 @@ attn_fwd_kernel(AttnArgs a) {
         p1 += in1;
         return true;
     };
-    RowRegs<D, kFwdThreads> kr, vr;
-    constexpr int VS = F16Tile<D>::kStride;
     int32_t kb = 0;
     bool in0 = false, in1 = false;
     bool have = next(kb, in0, in1);
     if (have) {
         const ContiguousRows rows{int64_t(kb) * 64};
-        load_rows<D, kFwdThreads>(kr, kp, rows, tid);
-        load_rows<D, kFwdThreads>(vr, vp, rows, tid);
-        store_rows<D, kFwdThreads>(sm.buf[0].k, kr, tid);
-        store_rows<D, kFwdThreads, VS>(sm.buf[0].v, vr, tid);
+        dma_rows<D, kRowPad, 4>(k0s, kp, rows, w, lane);
+        dma_rows<D, kTrPad, 4>(v0s, vp, rows, w, lane);
     }
+    wait_vmem();
     __syncthreads();
-    int cur = 0;
-    while (have) {
+    // one tile: compute from (ck, cv) while the next tile lands in (nk, nv)
+    auto step = [&](const uint16_t* ck, const uint16_t* cv, uint16_t* nk, uint16_t* nv) {
         int32_t kb2 = 0;
         bool in0n = false, in1n = false;
         const bool more = next(kb2, in0n, in1n);
         if (more) {
             const ContiguousRows rows{int64_t(kb2) * 64};
-            load_rows<D, kFwdThreads>(kr, kp, rows, tid);
-            load_rows<D, kFwdThreads>(vr, vp, rows, tid);
+            dma_rows<D, kRowPad, 4>(nk, kp, rows, w, lane);
+            dma_rows<D, kTrPad, 4>(nv, vp, rows, w, lane);
         }
-        if (half == 0 ? in0 : in1)
-            fwd_tile<D>(sm.buf[cur], sm.lim, st, a.k_blk_global[kb] == qg ? 1 : 0, qrow, lane, c2);
-        if (more) {
-            store_rows<D, kFwdThreads>(sm.buf[cur ^ 1].k, kr, tid);
-            store_rows<D, kFwdThreads, VS>(sm.buf[cur ^ 1].v, vr, tid);
-        }
+        if (half == 0 ? in0 : in1) fwd_tile<D>(ck, cv, lims, st, ldc(a.k_blk_global, kb) == qg ? 1 : 0, qrow, lane, c2);
+        wait_vmem();
         __syncthreads();
-        cur ^= 1;
         kb = kb2;
         in0 = in0n;
         in1 = in1n;
         have = more;
+    };
+    while (have) {
+        step(k0s, v0s, k1s, v1s);
+        if (!have) break;
+        step(k1s, v1s, k0s, v0s);
     }
 
     // ---- column tiles, one half at a time (the lists differ only near the band)
     for (int j = 0; j < 1 + int(has1); ++j) {
-        const int64_t c0 = a.col_ptr[item0 + j], c1 = a.col_ptr[item0 + j + 1];
-        const int32_t qgj = a.q_blk_global[qb0 + j];
+        const int64_t c0 = ldc(a.col_ptr, item0 + j), c1 = ldc(a.col_ptr, item0 + j + 1);
+        const int32_t qgj = ldc(a.q_blk_global, qb0 + j);
         for (int64_t cbase = c0; cbase < c1; cbase += 64) {
             const int cnt = int(min<int64_t>(64, c1 - cbase));
             if (tid < 64) {
                 const int32_t col = a.col_idx[cbase + (tid < cnt ? tid : 0)];
-                sm.kidx[tid] = col;
-                sm.lim[tid] = tid < cnt ? (a.k_blk_global[col >> 6] == qgj ? (col & 63) : 0) : 64;
+                kidx[tid] = col;
+                lims[tid] = tid < cnt ? (a.k_blk_global[col >> 6] == qgj ? (col & 63) : 0) : 64;
             }
             __syncthreads();
-            stage_rows<D, kFwdThreads>(sm.buf[0].k, kp, IndexedRows{sm.kidx}, tid);
-            stage_rows<D, kFwdThreads, IndexedRows, VS>(sm.buf[0].v, vp, IndexedRows{sm.kidx}, tid);
+            dma_rows<D, kRowPad, 4>(k0s, kp, IndexedRows{kidx}, w, lane);
+            dma_rows<D, kTrPad, 4>(v0s, vp, IndexedRows{kidx}, w, lane);
+            wait_vmem();
             __syncthreads();
-            if (half == j) fwd_tile<D>(sm.buf[0], sm.lim, st, 2, qrow, lane, c2);
+            if (half == j) fwd_tile<D>(k0s, v0s, lims, st, 2, qrow, lane, c2);
             __syncthreads();
         }
     }

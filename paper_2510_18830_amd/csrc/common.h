@@ -48,6 +48,14 @@ __device__ __forceinline__ uint32_t pack_f16x2(float lo, float hi) {
     return __builtin_bit_cast(uint32_t, v);
 }
 
+// Read-only index data (lists, maps) through the constant address space: a
+// wave-uniform address then compiles to a scalar load, which does not share
+// the vector-memory counter with in-flight tile loads.
+template <class T>
+__device__ __forceinline__ T ldc(const T* p, int64_t i) {
+    return ((const __attribute__((address_space(4))) T*)(p))[i];
+}
+
 // ---------------------------------------------------------------- MFMA
 // D(32x32) += A(32x16) * B(16x32), bf16 inputs, fp32 accumulate.
 // Lane l supplies A[l%32][8*(l/32) .. +8] and B[8*(l/32) .. +8][l%32];

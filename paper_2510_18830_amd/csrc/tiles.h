@@ -171,6 +171,99 @@ __device__ __forceinline__ void store_trans_f16(uint16_t* lds, const TransRegs<D
     }
 }
 
+// ---------------------------------------------------------------- DMA tiles
+// 64 rows x D 16-bit elements filled by direct global->LDS loads.  One wave
+// instruction writes 64 lanes x 16 bytes contiguously (the lanes free to
+// gather any rows), i.e. RPI = 1024 / (2 D) whole rows.  Instruction g of a
+// tile carries rows g, g + NG, g + 2 NG, ... (NG = 64 / RPI groups) and the
+// groups lie 1024 + P bytes apart:
+//   byte offset of (row r, chunk c) = (r % NG) (1024 + P) + (r / NG) 2 D + 16 c.
+// Every operand read is then a per-lane base plus immediate offsets.  P = 16
+// spreads the 16 rows of a row-wise operand read over distinct banks; P = 64
+// does the same for the 4 rows x 32 bytes of each 16-lane group of a
+// transposing read (and for two such groups served together).
+template <int D, int P>
+struct DmaTile {
+    static constexpr int kRowBytes = 2 * D;
+    static constexpr int kRowsPerInst = 1024 / kRowBytes;   // 4 (D = 128) or 8 (D = 64)
+    static constexpr int kGroups = 64 / kRowsPerInst;       // 16 or 8
+    static constexpr int kGroupBytes = 1024 + P;
+    static constexpr int kBytes = kGroups * kGroupBytes;
+    static constexpr int kElems = kBytes / 2;
+    __device__ static constexpr int off(int r, int c) {      // element offset of chunk c of row r
+        return ((r % kGroups) * kGroupBytes + (r / kGroups) * kRowBytes + 16 * c) / 2;
+    }
+};
+constexpr int kRowPad = 16;   // tiles read row-wise
+constexpr int kTrPad = 64;    // tiles read through transposing loads
+
+typedef __attribute__((address_space(3))) void* lds_void_ptr;
+
+// LDS byte address of a pointer into a __shared__ object
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+    return uint32_t(reinterpret_cast<uintptr_t>((lds_void_ptr)(const_cast<void*>(p))));
+}
+
+// One global->LDS DMA instruction: each lane loads 16 bytes from its own
+// `src`; lane l's bytes land at LDS byte address `lds` + 16 l (`lds` uniform
+// across the wave).  Written as inline assembly so that the compiler adds no
+// waits of its own before LDS reads of other buffers; the consumer waits with
+// wait_vmem() and publishes the tile with a barrier.
+__device__ __forceinline__ void dma16(const void* src, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+                 :
+                 : "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds))
+                 : "memory", "m0");
+}
+
+// Issue the loads of one tile (rows(r), r = 0..63, row length D) into `tile`:
+// wave `wave` of NW issues instructions wave, wave + NW, ... < NG.  The data
+// lands asynchronously: wait_vmem() before the barrier that publishes it.
+template <int D, int P, int NW, class Rows>
+__device__ __forceinline__ void dma_rows(uint16_t* tile, const uint16_t* __restrict__ src, Rows rows, int wave,
+                                         int lane) {
+    using T = DmaTile<D, P>;
+    constexpr int NC = D / 8;
+#pragma unroll
+    for (int j = 0; j < (T::kGroups + NW - 1) / NW; ++j) {
+        const int g = wave + NW * j;
+        if (T::kGroups % NW != 0 && g >= T::kGroups) break;
+        const int r = g + T::kGroups * (lane / NC);
+        const int c = lane % NC;
+        dma16(src + rows(r) * D + c * 8, lds_addr(tile + g * (T::kGroupBytes / 2)));
+    }
+}
+
+// wait until this wave's outstanding vector-memory loads (tile DMA included) are done
+__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// 16 bytes of row r, chunk c of a DMA tile (row-wise MFMA operand)
+template <int D, int P>
+__device__ __forceinline__ u32x4 dma_read16(const uint16_t* tile, int r, int c) {
+    return *reinterpret_cast<const u32x4*>(tile + DmaTile<D, P>::off(r, c));
+}
+
+// A operand of a 32x32x16 fp16 MFMA read transposed from a DMA tile of fp16
+// rows (same operand as lds_read_tr_a: A[m][k] = X[k0 + kperm(k)][m0 + m]).
+template <int D, int P>
+__device__ __forceinline__ u32x4 dma_read_tr(const uint16_t* x, int k0, int m0, int lane) {
+    typedef short v4s __attribute__((ext_vector_type(4)));
+    using T = DmaTile<D, P>;
+    const int r0 = k0 + 4 * (lane >> 5) + ((lane & 15) >> 2);
+    const int e = m0 + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);   // element column
+    const uint16_t* p0 = x + T::off(r0, 0) + e;
+    const uint16_t* p1 = x + T::off(r0 + 8, 0) + e;
+    const v4s a0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4s*)(p0));
+    const v4s a1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4s*)(p1));
+    const u32x2 a = __builtin_bit_cast(u32x2, a0), b = __builtin_bit_cast(u32x2, a1);
+    u32x4 o;
+    o.x = a.x;
+    o.y = a.y;
+    o.z = b.x;
+    o.w = b.y;
+    return o;
+}
+
 #ifndef MS_XCHUNK
 #define MS_XCHUNK 64   // logical items per XCD run
 #endif
