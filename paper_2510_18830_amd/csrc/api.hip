@@ -384,6 +384,7 @@ static size_t carve_bwd(const msparse_dims* d, int64_t vcol_cap, char* base, Att
     uint16_t* q16 = c.take<uint16_t>(size_t(bh) * d->seq_q * d->head_dim);
     uint16_t* g16 = c.take<uint16_t>(size_t(bh) * d->seq_q * d->head_dim);
     float* delta = c.take<float>(size_t(bh) * d->seq_q);
+    float* lse2 = c.take<float>(size_t(bh) * d->seq_q);
     uint32_t* dmax = c.take<uint32_t>(1);
     int32_t* choff = c.take<int32_t>(size_t(bh) + 1);
     int64_t* e0 = c.take<int64_t>(size_t(z.chunk_cap));
@@ -398,6 +399,7 @@ static size_t carve_bwd(const msparse_dims* d, int64_t vcol_cap, char* base, Att
         a->q16 = q16;
         a->g16 = g16;
         a->delta = delta;
+        a->lse2 = lse2;
         a->dmax = dmax;
         a->col_choff = choff;
         a->col_e0 = e0;

@@ -90,26 +90,26 @@ __global__ void __launch_bounds__(256) bwd_delta_kernel(AttnArgs a) {
 
 __device__ __forceinline__ float dout_scale(const uint32_t* dmax) { return pow2_scale(dmax); }
 
+// Per-row values the tiles read: lse2 = lse log2(e) (+inf for a row without
+// keys, so its P is 0) and s Delta in place of Delta.
+__global__ void __launch_bounds__(256) bwd_rowprep_kernel(AttnArgs a) {
+    const int64_t rows = int64_t(a.B) * a.Hq * a.Nq;
+    const float sc = dout_scale(a.dmax);
+    for (int64_t n = int64_t(blockIdx.x) * 256 + threadIdx.x; n < rows; n += int64_t(gridDim.x) * 256) {
+        const float l = a.lse[n];
+        a.lse2[n] = l == -INFINITY ? INFINITY : l * kLog2e;
+        a.delta[n] *= sc;
+    }
+}
+
 // ------------------------------------------------------------------ dQ (query-major)
 // One workgroup of four waves per pair of consecutive query blocks (as in the
 // forward): the pair walks the union of its block lists with the next key
-// tile's loads in flight, then the column tiles of each block.  Per tile and
-// wave: S^T = K Q^T, dP^T = V dO^T (bf16, Q and dO rows in VGPRs),
-// dQ^T += K^T dZ^T (fp16; K^T read transposed from the fp16 copy of K).
+// tile in flight (direct global->LDS loads, double buffer), then the column
+// tiles of each block.  Per tile and wave: S^T = K Q^T, dP^T = V dO^T (bf16,
+// Q and dO rows in VGPRs), dQ^T += K^T dZ^T (fp16; K^T read transposed from
+// the fp16 copy of K).
 constexpr int kDqThreads = 256;
-
-template <int D>
-struct DqBuf {
-    uint16_t k[TileLds<D>::kRowElems];   // bf16 K rows
-    uint16_t v[TileLds<D>::kRowElems];   // bf16 V rows
-    uint16_t k16[F16Tile<D>::kElems];    // fp16 K rows
-};
-template <int D>
-struct DqLds {
-    DqBuf<D> buf[2];
-    int32_t kidx[64];
-    int32_t lim[64];
-};
 
 template <int D>
 struct DqRows {
@@ -121,8 +121,9 @@ struct DqRows {
 
 // mask: 0 none, 1 causal diagonal, 2 per-key limits
 template <int D>
-__device__ __forceinline__ void dq_tile(const DqBuf<D>& sm, const int32_t* lims, DqRows<D>& st, int mask, int qrow,
-                                        int lane, float c2, float sc) {
+__device__ __forceinline__ void dq_tile(const uint16_t* kt, const uint16_t* vt, const uint16_t* k16t,
+                                        const int32_t* lims, DqRows<D>& st, int mask, int qrow, int lane, float c2,
+                                        float sc) {
     constexpr int KD = DqRows<D>::KD, ND = DqRows<D>::ND;
     const int h = lane >> 5, l32 = lane & 31;
     f32x16 sacc[2], pacc[2];
@@ -130,12 +131,10 @@ __device__ __forceinline__ void dq_tile(const DqBuf<D>& sm, const int32_t* lims,
     for (int c = 0; c < 2; ++c) {
         sacc[c] = f32x16{};
         pacc[c] = f32x16{};
-        const uint16_t* krow = sm.k + (32 * c + l32) * TileLds<D>::kRowStride + 8 * h;
-        const uint16_t* vrow = sm.v + (32 * c + l32) * TileLds<D>::kRowStride + 8 * h;
 #pragma unroll
         for (int s = 0; s < KD; ++s) {
-            sacc[c] = mfma32(lds_read16(krow + 16 * s), st.q[s], sacc[c]);
-            pacc[c] = mfma32(lds_read16(vrow + 16 * s), st.g[s], pacc[c]);
+            sacc[c] = mfma32(dma_read16<D, kRowPad>(kt, 32 * c + l32, h + 2 * s), st.q[s], sacc[c]);
+            pacc[c] = mfma32(dma_read16<D, kRowPad>(vt, 32 * c + l32, h + 2 * s), st.g[s], pacc[c]);
         }
     }
     // s dZ^T = P o (s dP^T - s Delta), P = exp2(c2 z - lse2) on visible entries
@@ -160,15 +159,17 @@ __device__ __forceinline__ void dq_tile(const DqBuf<D>& sm, const int32_t* lims,
     for (int i = 0; i < ND; ++i)
 #pragma unroll
         for (int g = 0; g < 4; ++g)
-            st.acc[i] = mfma32h(lds_read_tr_a<F16Tile<D>::kStride>(sm.k16, 16 * g, 32 * i, lane), zb[g], st.acc[i]);
+            st.acc[i] = mfma32h(dma_read_tr<D, kTrPad>(k16t, 16 * g, 32 * i, lane), zb[g], st.acc[i]);
 }
 
 template <int D>
 __global__ void __launch_bounds__(kDqThreads) bwd_dq_kernel(AttnArgs a) {
     constexpr int KD = DqRows<D>::KD, ND = DqRows<D>::ND;
-    constexpr int FS = F16Tile<D>::kStride;
-    __shared__ DqLds<D> sm;
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, half = w >> 1, h = lane >> 5, l32 = lane & 31;
+    constexpr int RE = DmaTile<D, kRowPad>::kElems, TE = DmaTile<D, kTrPad>::kElems;
+    __shared__ uint16_t k0s[RE], v0s[RE], t0s[TE], k1s[RE], v1s[RE], t1s[TE];
+    __shared__ int32_t kidx[64], lims[64];
+    const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, l32 = lane & 31;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6), half = w >> 1;
     const int npair = (a.nqb + 1) >> 1;
     int bh, qp;
     query_tile_of(blockIdx.x, a.B, a.Hq, a.Hkv, npair, bh, qp);
@@ -179,7 +180,7 @@ __global__ void __launch_bounds__(kDqThreads) bwd_dq_kernel(AttnArgs a) {
     const bool live = half == 0 || has1;
     const int qrow = 32 * (w & 1) + l32;
     const int64_t grow = int64_t(bh) * a.Nq + int64_t(qb) * 64 + qrow;
-    const int32_t qg = a.q_blk_global[qb];
+    const int32_t qg = ldc(a.q_blk_global, qb);
 
     const int64_t kvoff = (int64_t(b) * a.Hkv + hk) * int64_t(a.Nk) * D;
     const uint16_t* __restrict__ kp = a.k + kvoff;
@@ -192,22 +193,21 @@ __global__ void __launch_bounds__(kDqThreads) bwd_dq_kernel(AttnArgs a) {
         st.g[s] = *reinterpret_cast<const u32x4*>(a.dout + grow * D + 16 * s + 8 * h);
     }
     const float c2 = a.scale * kLog2e;
-    const float lse_n = a.lse[grow];
-    st.lse2 = lse_n == -INFINITY ? INFINITY : lse_n * kLog2e;   // empty row: P = 0
+    st.lse2 = a.lse2[grow];
     const float sc = dout_scale(a.dmax);
-    st.dlt = a.delta[grow] * sc;
+    st.dlt = a.delta[grow];
 #pragma unroll
     for (int i = 0; i < ND; ++i) st.acc[i] = f32x16{};
 
     // ---- block tiles: union of the two ascending block lists, pipelined
     const int64_t item0 = int64_t(bh) * a.nqb + qb0;
-    const int64_t e00 = a.blk_ptr[item0], e01 = a.blk_ptr[item0 + 1];
-    const int64_t e11 = has1 ? a.blk_ptr[item0 + 2] : e01;
+    const int64_t e00 = ldc(a.blk_ptr, item0), e01 = ldc(a.blk_ptr, item0 + 1);
+    const int64_t e11 = has1 ? ldc(a.blk_ptr, item0 + 2) : e01;
     int64_t p0 = e00, p1 = e01;
     auto next = [&](int32_t& kb, bool& in0, bool& in1) {
         if (p0 >= e01 && p1 >= e11) return false;
-        const int32_t k0 = p0 < e01 ? a.blk_idx[p0] : INT32_MAX;
-        const int32_t k1 = p1 < e11 ? a.blk_idx[p1] : INT32_MAX;
+        const int32_t k0 = p0 < e01 ? ldc(a.blk_idx, p0) : INT32_MAX;
+        const int32_t k1 = p1 < e11 ? ldc(a.blk_idx, p1) : INT32_MAX;
         kb = min(k0, k1);
         in0 = k0 == kb;
         in1 = k1 == kb;
@@ -215,64 +215,54 @@ __global__ void __launch_bounds__(kDqThreads) bwd_dq_kernel(AttnArgs a) {
         p1 += in1;
         return true;
     };
-    RowRegs<D, kDqThreads> kr, vr, k16r;
+    auto load = [&](uint16_t* kt, uint16_t* vt, uint16_t* tt, auto rows) {
+        dma_rows<D, kRowPad, 4>(kt, kp, rows, w, lane);
+        dma_rows<D, kRowPad, 4>(vt, vp, rows, w, lane);
+        dma_rows<D, kTrPad, 4>(tt, k16p, rows, w, lane);
+    };
     int32_t kb = 0;
     bool in0 = false, in1 = false;
     bool have = next(kb, in0, in1);
-    if (have) {
-        const ContiguousRows rows{int64_t(kb) * 64};
-        load_rows<D, kDqThreads>(kr, kp, rows, tid);
-        load_rows<D, kDqThreads>(vr, vp, rows, tid);
-        load_rows<D, kDqThreads>(k16r, k16p, rows, tid);
-        store_rows<D, kDqThreads>(sm.buf[0].k, kr, tid);
-        store_rows<D, kDqThreads>(sm.buf[0].v, vr, tid);
-        store_rows<D, kDqThreads, FS>(sm.buf[0].k16, k16r, tid);
-    }
+    if (have) load(k0s, v0s, t0s, ContiguousRows{int64_t(kb) * 64});
+    wait_vmem();
     __syncthreads();
-    int cur = 0;
-    while (have) {
+    auto step = [&](const uint16_t* ck, const uint16_t* cv, const uint16_t* ct, uint16_t* nk, uint16_t* nv,
+                    uint16_t* nt) {
         int32_t kb2 = 0;
         bool in0n = false, in1n = false;
         const bool more = next(kb2, in0n, in1n);
-        if (more) {
-            const ContiguousRows rows{int64_t(kb2) * 64};
-            load_rows<D, kDqThreads>(kr, kp, rows, tid);
-            load_rows<D, kDqThreads>(vr, vp, rows, tid);
-            load_rows<D, kDqThreads>(k16r, k16p, rows, tid);
-        }
+        if (more) load(nk, nv, nt, ContiguousRows{int64_t(kb2) * 64});
         if (half == 0 ? in0 : in1)
-            dq_tile<D>(sm.buf[cur], sm.lim, st, a.k_blk_global[kb] == qg ? 1 : 0, qrow, lane, c2, sc);
-        if (more) {
-            store_rows<D, kDqThreads>(sm.buf[cur ^ 1].k, kr, tid);
-            store_rows<D, kDqThreads>(sm.buf[cur ^ 1].v, vr, tid);
-            store_rows<D, kDqThreads, FS>(sm.buf[cur ^ 1].k16, k16r, tid);
-        }
+            dq_tile<D>(ck, cv, ct, lims, st, ldc(a.k_blk_global, kb) == qg ? 1 : 0, qrow, lane, c2, sc);
+        wait_vmem();
         __syncthreads();
-        cur ^= 1;
         kb = kb2;
         in0 = in0n;
         in1 = in1n;
         have = more;
+    };
+    while (have) {
+        step(k0s, v0s, t0s, k1s, v1s, t1s);
+        if (!have) break;
+        step(k1s, v1s, t1s, k0s, v0s, t0s);
     }
 
     // ---- column tiles, one half at a time
     for (int j = 0; j < 1 + int(has1); ++j) {
-        const int64_t c0 = a.col_ptr[item0 + j], c1 = a.col_ptr[item0 + j + 1];
-        const int32_t qgj = a.q_blk_global[qb0 + j];
+        const int64_t c0 = ldc(a.col_ptr, item0 + j), c1 = ldc(a.col_ptr, item0 + j + 1);
+        const int32_t qgj = ldc(a.q_blk_global, qb0 + j);
         for (int64_t cbase = c0; cbase < c1; cbase += 64) {
             const int cnt = int(min<int64_t>(64, c1 - cbase));
             if (tid < 64) {
                 const int32_t col = a.col_idx[cbase + (tid < cnt ? tid : 0)];
-                sm.kidx[tid] = col;
-                sm.lim[tid] = tid < cnt ? (a.k_blk_global[col >> 6] == qgj ? (col & 63) : 0) : 64;
+                kidx[tid] = col;
+                lims[tid] = tid < cnt ? (a.k_blk_global[col >> 6] == qgj ? (col & 63) : 0) : 64;
             }
             __syncthreads();
-            const IndexedRows rows{sm.kidx};
-            stage_rows<D, kDqThreads>(sm.buf[0].k, kp, rows, tid);
-            stage_rows<D, kDqThreads>(sm.buf[0].v, vp, rows, tid);
-            stage_rows<D, kDqThreads, IndexedRows, FS>(sm.buf[0].k16, k16p, rows, tid);
+            load(k0s, v0s, t0s, IndexedRows{kidx});
+            wait_vmem();
             __syncthreads();
-            if (half == j) dq_tile<D>(sm.buf[0], sm.lim, st, 2, qrow, lane, c2, sc);
+            if (half == j) dq_tile<D>(k0s, v0s, t0s, lims, st, 2, qrow, lane, c2, sc);
             __syncthreads();
         }
     }
@@ -295,49 +285,73 @@ __global__ void __launch_bounds__(kDqThreads) bwd_dq_kernel(AttnArgs a) {
 }
 
 // ------------------------------------------------------------------ dK / dV (key-major)
-// A query tile as the key-major passes stage it: bf16 Q and dO rows for the
-// first GEMMs, fp16 Q and s dO rows read transposed for the second.
+// A query tile as the key-major passes stage it (DMA tiles): bf16 Q and dO
+// rows for the first GEMMs, fp16 Q and s dO rows read transposed for the
+// second, and the rows' lse2 and s Delta (64 floats each).
 template <int D>
-struct KvBuf {
-    uint16_t q[TileLds<D>::kRowElems];
-    uint16_t g[TileLds<D>::kRowElems];    // dO
-    uint16_t q16[F16Tile<D>::kElems];     // fp16 Q
-    uint16_t g16[F16Tile<D>::kElems];     // fp16 s dO
-    float lse2[64];
-    float dlt[64];
+struct KvTile {
+    static constexpr int kRow = DmaTile<D, kRowPad>::kElems;
+    static constexpr int kTr = DmaTile<D, kTrPad>::kElems;
+    static constexpr int kElems = 2 * kRow + 2 * kTr + 256;   // + 128 floats
+    // element offsets of the parts
+    static constexpr int kQ = 0, kG = kRow, kQ16 = 2 * kRow, kG16 = 2 * kRow + kTr, kRw = 2 * kRow + 2 * kTr;
 };
+
+// Issue the loads of query tile (bh, qb) into tile `t` (NW waves).
+template <int D, int NW>
+__device__ __forceinline__ void kv_load_query_tile(uint16_t* t, const AttnArgs& a, int bh, int qb, int wave,
+                                                   int lane) {
+    using T = KvTile<D>;
+    const int64_t row0 = int64_t(bh) * a.Nq + int64_t(qb) * 64;
+    const ContiguousRows rows{row0};
+    dma_rows<D, kRowPad, NW>(t + T::kQ, a.q, rows, wave, lane);
+    dma_rows<D, kRowPad, NW>(t + T::kG, a.dout, rows, wave, lane);
+    dma_rows<D, kTrPad, NW>(t + T::kQ16, a.q16, rows, wave, lane);
+    dma_rows<D, kTrPad, NW>(t + T::kG16, a.g16, rows, wave, lane);
+    if (wave == 0 && lane < 32) {   // lse2 -> floats 0..63, s Delta -> floats 64..127
+        const float* src = lane < 16 ? a.lse2 + row0 + 4 * lane : a.delta + row0 + 4 * (lane - 16);
+        dma16(src, lds_addr(t + T::kRw));
+    }
+}
 
 // One 64-row query tile against this wave's 32 keys.  `active` / `lim` give
 // the per-key visibility: key visible to in-block query row r iff active and
 // r >= lim.
 template <int D>
-__device__ __forceinline__ void kv_tile(const KvBuf<D>& sm, const u32x4* kreg, const u32x4* vreg, bool masked,
+__device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, const u32x4* vreg, bool masked,
                                         bool active, int lim, float c2, float sc, int lane, f32x16* dv, f32x16* dk) {
-    constexpr int KD = D / 16, ND = D / 32, FS = F16Tile<D>::kStride;
+    using T = KvTile<D>;
+    constexpr int KD = D / 16, ND = D / 32;
     const int h = lane >> 5, l32 = lane & 31;
+    const float* lse2 = reinterpret_cast<const float*>(t + T::kRw);
+    const float* dlt = lse2 + 64;
     f32x16 sacc[2], pacc[2];
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb) {
         sacc[rb] = f32x16{};
         pacc[rb] = f32x16{};
-        const uint16_t* qrow = sm.q + (32 * rb + l32) * TileLds<D>::kRowStride + 8 * h;
-        const uint16_t* grow = sm.g + (32 * rb + l32) * TileLds<D>::kRowStride + 8 * h;
 #pragma unroll
         for (int s = 0; s < KD; ++s) {
-            sacc[rb] = mfma32(lds_read16(qrow + 16 * s), kreg[s], sacc[rb]);
-            pacc[rb] = mfma32(lds_read16(grow + 16 * s), vreg[s], pacc[rb]);
+            sacc[rb] = mfma32(dma_read16<D, kRowPad>(t + T::kQ, 32 * rb + l32, h + 2 * s), kreg[s], sacc[rb]);
+            pacc[rb] = mfma32(dma_read16<D, kRowPad>(t + T::kG, 32 * rb + l32, h + 2 * s), vreg[s], pacc[rb]);
         }
     }
     // rows of acc element r: 32 rb + 8 (r/4) + 4 h + r%4; column = this lane's key
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const int row = 32 * rb + 8 * (r >> 2) + 4 * h + (r & 3);
-            float p = fast_exp2(__builtin_fmaf(sacc[rb][r], c2, -sm.lse2[row]));
-            if (masked && (!active || row < lim)) p = 0.f;
-            sacc[rb][r] = p;
-            pacc[rb][r] = p * __builtin_fmaf(pacc[rb][r], sc, -sm.dlt[row]);
+        for (int q4 = 0; q4 < 4; ++q4) {
+            const int row0 = 32 * rb + 8 * q4 + 4 * h;
+            const f32x4 l4 = *reinterpret_cast<const f32x4*>(lse2 + row0);
+            const f32x4 d4 = *reinterpret_cast<const f32x4*>(dlt + row0);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int r = 4 * q4 + e;
+                float p = fast_exp2(__builtin_fmaf(sacc[rb][r], c2, -l4[e]));
+                if (masked && (!active || row0 + e < lim)) p = 0.f;
+                sacc[rb][r] = p;
+                pacc[rb][r] = p * __builtin_fmaf(pacc[rb][r], sc, -d4[e]);
+            }
         }
     u32x4 pb[4], zb[4];
     pb[0] = pack8_f16<0>(sacc[0]);
@@ -353,67 +367,25 @@ __device__ __forceinline__ void kv_tile(const KvBuf<D>& sm, const u32x4* kreg, c
     for (int i = 0; i < ND; ++i)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-            dv[i] = mfma32h(lds_read_tr_a<FS>(sm.g16, 16 * g, 32 * i, lane), pb[g], dv[i]);
-            dk[i] = mfma32h(lds_read_tr_a<FS>(sm.q16, 16 * g, 32 * i, lane), zb[g], dk[i]);
+            dv[i] = mfma32h(dma_read_tr<D, kTrPad>(t + T::kG16, 16 * g, 32 * i, lane), pb[g], dv[i]);
+            dk[i] = mfma32h(dma_read_tr<D, kTrPad>(t + T::kQ16, 16 * g, 32 * i, lane), zb[g], dk[i]);
         }
-}
-
-// Register copy of a query tile in flight (software pipelining).
-template <int D, int NT>
-struct KvRegs {
-    RowRegs<D, NT> q, g, q16, g16;
-    float lse, dlt;
-};
-template <int D, int NT>
-__device__ __forceinline__ void kv_load_query_tile(KvRegs<D, NT>& r, const AttnArgs& a, int bh, int qb, int tid) {
-    const int64_t row0 = int64_t(bh) * a.Nq + int64_t(qb) * 64;
-    const ContiguousRows rows{row0};
-    load_rows<D, NT>(r.q, a.q, rows, tid);
-    load_rows<D, NT>(r.g, a.dout, rows, tid);
-    load_rows<D, NT>(r.q16, a.q16, rows, tid);
-    load_rows<D, NT>(r.g16, a.g16, rows, tid);
-    if (tid < 64) {
-        r.lse = a.lse[row0 + tid];
-        r.dlt = a.delta[row0 + tid];
-    }
-}
-template <int D, int NT>
-__device__ __forceinline__ void kv_store_query_tile(KvBuf<D>& sm, const KvRegs<D, NT>& r, float sc, int tid) {
-    constexpr int FS = F16Tile<D>::kStride;
-    store_rows<D, NT>(sm.q, r.q, tid);
-    store_rows<D, NT>(sm.g, r.g, tid);
-    store_rows<D, NT, FS>(sm.q16, r.q16, tid);
-    store_rows<D, NT, FS>(sm.g16, r.g16, tid);
-    if (tid < 64) {
-        sm.lse2[tid] = r.lse == -INFINITY ? INFINITY : r.lse * kLog2e;
-        sm.dlt[tid] = r.dlt * sc;
-    }
-}
-template <int D, int NT>
-__device__ __forceinline__ void kv_stage_query_tile(KvBuf<D>& sm, const AttnArgs& a, int bh, int qb, float sc,
-                                                    int tid) {
-    KvRegs<D, NT> r;
-    kv_load_query_tile<D, NT>(r, a, bh, qb, tid);
-    kv_store_query_tile<D, NT>(sm, r, sc, tid);
 }
 
 // Key-major pass: one workgroup of four waves per (b, KV head, pair of
 // consecutive 64-key blocks); waves 2j, 2j+1 hold 32 keys each of block j of
 // the pair in VGPRs.  For every query head of the KV group the pair walks the
 // union of its two transposed lists (query blocks that selected the key
-// block), the next query tile's loads in flight during the current one.
+// block), the next query tile in flight (direct global->LDS loads, double
+// buffer) during the current one.
 constexpr int kKvThreads = 256;
-
-template <int D>
-struct KvLds {
-    KvBuf<D> buf[2];
-};
 
 template <int D>
 __global__ void __launch_bounds__(kKvThreads) bwd_dkdv_kernel(AttnArgs a) {
     constexpr int KD = D / 16, ND = D / 32;
-    __shared__ KvLds<D> sm;
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, half = w >> 1, h = lane >> 5, l32 = lane & 31;
+    __shared__ __attribute__((aligned(16))) uint16_t t0s[KvTile<D>::kElems], t1s[KvTile<D>::kElems];
+    const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, l32 = lane & 31;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6), half = w >> 1;
     const int BK = a.B * a.Hkv;
     const int npair = (a.nkb + 1) >> 1;
     const int64_t u = xcd_chunk(blockIdx.x, int64_t(BK) * npair);
@@ -442,17 +414,17 @@ __global__ void __launch_bounds__(kKvThreads) bwd_dkdv_kernel(AttnArgs a) {
     }
     const float c2 = a.scale * kLog2e;
     const float sc = dout_scale(a.dmax);
-    const int32_t kg = a.k_blk_global[kb];
+    const int32_t kg = ldc(a.k_blk_global, kb);
 
     // walk: heads of the group in order, per head the union of the two lists
     int g = 0;
     int64_t p0 = 0, e0 = 0, p1 = 0, e1 = 0;
     auto open_head = [&]() {
         const int64_t item = int64_t(b * a.Hq + hk * G + g) * a.nkb + kb0;
-        p0 = a.kblk_ptr[item];
-        e0 = a.kblk_ptr[item + 1];
+        p0 = ldc(a.kblk_ptr, item);
+        e0 = ldc(a.kblk_ptr, item + 1);
         p1 = e0;
-        e1 = has1 ? a.kblk_ptr[item + 2] : e0;
+        e1 = has1 ? ldc(a.kblk_ptr, item + 2) : e0;
     };
     open_head();
     auto next = [&](int& bh, int& qb, bool& in0, bool& in1) {
@@ -460,8 +432,8 @@ __global__ void __launch_bounds__(kKvThreads) bwd_dkdv_kernel(AttnArgs a) {
             if (++g >= G) return false;
             open_head();
         }
-        const int32_t q0 = p0 < e0 ? a.kblk_idx[p0] : INT32_MAX;
-        const int32_t q1 = p1 < e1 ? a.kblk_idx[p1] : INT32_MAX;
+        const int32_t q0 = p0 < e0 ? ldc(a.kblk_idx, p0) : INT32_MAX;
+        const int32_t q1 = p1 < e1 ? ldc(a.kblk_idx, p1) : INT32_MAX;
         qb = min(q0, q1);
         in0 = q0 == qb;
         in1 = q1 == qb;
@@ -470,33 +442,33 @@ __global__ void __launch_bounds__(kKvThreads) bwd_dkdv_kernel(AttnArgs a) {
         bh = b * a.Hq + hk * G + g;
         return true;
     };
-    KvRegs<D, kKvThreads> r;
     int bh = 0, qb = 0;
     bool in0 = false, in1 = false;
     bool have = next(bh, qb, in0, in1);
-    if (have) {
-        kv_load_query_tile<D, kKvThreads>(r, a, bh, qb, tid);
-        kv_store_query_tile<D, kKvThreads>(sm.buf[0], r, sc, tid);
-    }
+    if (have) kv_load_query_tile<D, 4>(t0s, a, bh, qb, w, lane);
+    wait_vmem();
     __syncthreads();
-    int cur = 0;
-    while (have) {
+    auto step = [&](const uint16_t* ct, uint16_t* nt) {
         int bh2 = 0, qb2 = 0;
         bool in0n = false, in1n = false;
         const bool more = next(bh2, qb2, in0n, in1n);
-        if (more) kv_load_query_tile<D, kKvThreads>(r, a, bh2, qb2, tid);
+        if (more) kv_load_query_tile<D, 4>(nt, a, bh2, qb2, w, lane);
         if (half == 0 ? in0 : in1) {
-            const bool masked = a.q_blk_global[qb] == kg;   // diagonal tile
-            kv_tile<D>(sm.buf[cur], kreg, vreg, masked, true, key, c2, sc, lane, dv, dk);
+            const bool masked = ldc(a.q_blk_global, qb) == kg;   // diagonal tile
+            kv_tile<D>(ct, kreg, vreg, masked, true, key, c2, sc, lane, dv, dk);
         }
-        if (more) kv_store_query_tile<D, kKvThreads>(sm.buf[cur ^ 1], r, sc, tid);
+        wait_vmem();
         __syncthreads();
-        cur ^= 1;
         bh = bh2;
         qb = qb2;
         in0 = in0n;
         in1 = in1n;
         have = more;
+    };
+    while (have) {
+        step(t0s, t1s);
+        if (!have) break;
+        step(t1s, t0s);
     }
     if (!live) return;
     float* dkp = a.dk + krow * D;
@@ -630,8 +602,9 @@ __global__ void __launch_bounds__(kPlanThreads) bwd_colplan_kernel(AttnArgs a) {
 template <int D>
 __global__ void __launch_bounds__(kThreads) bwd_dkdv_col_kernel(AttnArgs a) {
     constexpr int KD = D / 16, ND = D / 32;
-    __shared__ KvBuf<D> sm;
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, l32 = lane & 31;
+    __shared__ __attribute__((aligned(16))) uint16_t ts[KvTile<D>::kElems];
+    const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, l32 = lane & 31;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int nc = a.col_choff[a.B * a.Hq];
     const int item = int(blockIdx.x);
     if (item >= a.col_item[nc]) return;
@@ -675,9 +648,10 @@ __global__ void __launch_bounds__(kThreads) bwd_dkdv_col_kernel(AttnArgs a) {
         const int lim = qg == cg ? cin : 0;
         // every column covered by a selected block-diagonal: nothing to do here
         if (!__syncthreads_or(active)) continue;
-        kv_stage_query_tile<D, kThreads>(sm, a, bh, qb, sc, tid);
+        kv_load_query_tile<D, 2>(ts, a, bh, qb, w, lane);
+        wait_vmem();
         __syncthreads();
-        kv_tile<D>(sm, kreg, vreg, true, active, lim, c2, sc, lane, dv, dk);
+        kv_tile<D>(ts, kreg, vreg, true, active, lim, c2, sc, lane, dv, dk);
         __syncthreads();
     }
     if (!valid) return;
@@ -755,6 +729,12 @@ hipError_t launch_bwd_d(const AttnArgs& a, hipStream_t s) {
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+    if (rows > 0) {
+        TraceScope _t("bwd_rowprep", s);
+        const int64_t want = (rows + 255) / 256;
+        hipLaunchKernelGGL(bwd_rowprep_kernel, dim3(unsigned(want < kDeltaBlocks ? want : int64_t(kDeltaBlocks))),
+                           dim3(256), 0, s, a);
+    }
     const int64_t nkv = int64_t(a.B) * a.Hkv * a.Nk * a.d;
     if ((e = launch_to_f16(a.k, a.k16, nkv, nullptr, s)) != hipSuccess) return e;
     const int64_t qgrid = int64_t(a.B) * a.Hq * ((a.nqb + 1) / 2);

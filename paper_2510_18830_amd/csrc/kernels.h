@@ -68,7 +68,8 @@ struct AttnArgs {
     const float* o_f32;    // optional fp32 forward output for Delta (bwd)
     uint32_t* dmax;        // bwd workspace: max |dO| as fp32 bits
     float* lse;            // fwd output / bwd input
-    float* delta;          // bwd workspace [B,Hq,Nq]
+    float* delta;          // bwd workspace [B,Hq,Nq]: Delta, then s * Delta after row prep
+    float* lse2;           // bwd workspace [B,Hq,Nq]: lse * log2(e) (+inf for a row without keys)
     float* dq;
     float* dk;
     float* dv;
