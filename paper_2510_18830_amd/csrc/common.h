@@ -34,13 +34,6 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     return __builtin_bit_cast(uint32_t, v);
 }
 
-// bf16 bits -> fp16 bits.  Exact for |x| in [2^-14, 65504] (fp16 carries more
-// significand bits than bf16); smaller magnitudes lose precision as fp16
-// subnormals.  `mul` is a power of two applied first (exact).
-__device__ __forceinline__ uint32_t bf16_to_f16_bits(uint32_t b, float mul) {
-    const _Float16 h = (_Float16)(__uint_as_float(b << 16) * mul);
-    return uint32_t(__builtin_bit_cast(uint16_t, h));
-}
 __device__ __forceinline__ uint32_t pack_f16x2(float lo, float hi) {
     f16x2 v;
     v.x = (_Float16)lo;

@@ -1,21 +1,19 @@
-// LDS staging of 64-row tiles shared by the attention kernels.
+// LDS tiles shared by the attention kernels.
 //
 // A tile is 64 rows of one head: a 64 x 64 block of the grid, or up to 64
-// gathered vertical columns (key rows named by an index list).  It is staged
-// two ways:
-//   row-major  X[row][d]        (operand whose contraction runs over d)
-//   transposed Xt[d][pos(row)]  (operand whose contraction runs over rows)
-// The transposed copy stores each 16-row group in the order
-//   rows 0-3, 8-11, 4-7, 12-15
-// because a 32x32 MFMA accumulator gives lane half h the rows
-// 8*(r/4) + 4*h + r%4; reading 8 consecutive positions at offset 8*h of a
-// 16-group then yields exactly the rows that the same lane holds in its
-// accumulator, so P (or dZ) feeds the next MFMA straight from registers.
-//
-// The transposed copy is converted to fp16 (times a power-of-two factor) for
-// the second GEMM of each pair (P V, P^T dO, dZ K, dZ^T Q): fp16 holds 3 more
-// significand bits than bf16, which keeps the rounding of P and dZ far below
-// the gradient tolerance at the same MFMA rate.
+// gathered vertical columns (key rows named by an index list).  The attention
+// kernels fill tiles with direct global->LDS loads (DMA tiles below) and read
+// them two ways:
+//   row-wise      16 bytes of one row per lane: an MFMA operand whose
+//                 contraction runs over d (K in S = Q K^T, Q and dO rows)
+//   transposed    ds_read_b64_tr_b16 over 16 rows x 32 columns: an MFMA A
+//                 operand whose contraction runs over the rows (V^T, K^T, Q^T,
+//                 dO^T), from fp16 copies of those tensors
+// A 32x32 MFMA accumulator gives lane half h the rows 8(r/4) + 4h + r%4; the
+// transposed reads fetch exactly that row order, so P (or dZ) feeds the next
+// MFMA straight from registers.  The second GEMM of each pair runs in fp16: 3
+// more significand bits than bf16 keep the rounding of P and dZ far below the
+// gradient tolerance at the same MFMA rate.
 #pragma once
 
 #include "common.h"
@@ -30,22 +28,6 @@ struct TileLds {
     static constexpr int kTElems = D * kTStride;
 };
 
-// fp16 row-major tiles read through transposing loads: row stride D + 16
-// elements, so the reads of a 16-lane group (4 rows x 32 bytes) hit distinct
-// banks.
-template <int D>
-struct F16Tile {
-    static constexpr int kStride = D + 16;
-    static constexpr int kElems = 64 * kStride;
-};
-
-// position of row k (0..63) inside a transposed row
-__device__ __forceinline__ int tpos(int k) {
-    const int a = (k >> 2) & 3;
-    const int sw = ((a & 1) << 1) | (a >> 1);
-    return (k & ~15) | (sw << 2) | (k & 3);
-}
-
 // Row sources: rows named by an LDS index list, or a contiguous run.
 struct IndexedRows {
     const int32_t* idx;
@@ -56,7 +38,8 @@ struct ContiguousRows {
     __device__ __forceinline__ int64_t operator()(int r) const { return base + r; }
 };
 
-// Row-major staging of 64 rows x D bf16 (row length D in `src`).
+// Row-major staging of 64 rows x D bf16 through registers (row length D in
+// `src`), padded rows of RS elements.
 template <int D, int NT, class Rows, int RS = TileLds<D>::kRowStride>
 __device__ __forceinline__ void stage_rows(uint16_t* lds, const uint16_t* __restrict__ src, Rows rows, int tid) {
     constexpr int kChunks = D / 8;              // 16-byte chunks per row
@@ -67,107 +50,6 @@ __device__ __forceinline__ void stage_rows(uint16_t* lds, const uint16_t* __rest
         const int c = tid % kChunks;
         const u32x4 v = *reinterpret_cast<const u32x4*>(src + rows(r) * D + c * 8);
         *reinterpret_cast<u32x4*>(lds + r * RS + c * 8) = v;
-    }
-}
-
-// Transposed staging Xt[d][tpos(row)] (row stride TS elements), converted to
-// fp16 after multiplying by `mul` (a power of two).
-template <int D, int NT, class Rows, int TS = TileLds<D>::kTStride>
-__device__ __forceinline__ void stage_transposed_f16(uint16_t* lds, const uint16_t* __restrict__ src, Rows rows,
-                                                     float mul, int tid) {
-    constexpr int kItems = 16 * (D / 8);  // (4-row quad) x (8-wide d chunk)
-#pragma unroll
-    for (int p = 0; p < (kItems + NT - 1) / NT; ++p) {
-        const int item = p * NT + tid;
-        if (kItems % NT != 0 && item >= kItems) break;
-        const int q4 = item & 15;
-        const int dc = item >> 4;
-        u32x4 r[4];
-#pragma unroll
-        for (int b = 0; b < 4; ++b) r[b] = *reinterpret_cast<const u32x4*>(src + rows(4 * q4 + b) * D + dc * 8);
-        const int pos = tpos(4 * q4);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            u32x2 even, odd;
-            even.x = bf16_to_f16_bits(r[0][e] & 0xffffu, mul) | (bf16_to_f16_bits(r[1][e] & 0xffffu, mul) << 16);
-            even.y = bf16_to_f16_bits(r[2][e] & 0xffffu, mul) | (bf16_to_f16_bits(r[3][e] & 0xffffu, mul) << 16);
-            odd.x = bf16_to_f16_bits(r[0][e] >> 16, mul) | (bf16_to_f16_bits(r[1][e] >> 16, mul) << 16);
-            odd.y = bf16_to_f16_bits(r[2][e] >> 16, mul) | (bf16_to_f16_bits(r[3][e] >> 16, mul) << 16);
-            const int d0 = dc * 8 + 2 * e;
-            *reinterpret_cast<u32x2*>(lds + d0 * TS + pos) = even;
-            *reinterpret_cast<u32x2*>(lds + (d0 + 1) * TS + pos) = odd;
-        }
-    }
-}
-
-// Two-phase staging for software pipelining: the global loads of a tile go to
-// registers first (issued before the current tile's compute), the LDS stores
-// (with the fp16 conversion of the transposed copy) follow after it.
-template <int D, int NT>
-struct RowRegs {
-    static constexpr int kChunks = D / 8;
-    static constexpr int kRowsPerPass = NT / kChunks;
-    static constexpr int kPasses = 64 / kRowsPerPass;
-    u32x4 r[kPasses];
-};
-template <int D, int NT, class Rows>
-__device__ __forceinline__ void load_rows(RowRegs<D, NT>& g, const uint16_t* __restrict__ src, Rows rows, int tid) {
-    using R = RowRegs<D, NT>;
-#pragma unroll
-    for (int p = 0; p < R::kPasses; ++p) {
-        const int r = p * R::kRowsPerPass + tid / R::kChunks;
-        g.r[p] = *reinterpret_cast<const u32x4*>(src + rows(r) * D + (tid % R::kChunks) * 8);
-    }
-}
-template <int D, int NT, int RS = TileLds<D>::kRowStride>
-__device__ __forceinline__ void store_rows(uint16_t* lds, const RowRegs<D, NT>& g, int tid) {
-    using R = RowRegs<D, NT>;
-#pragma unroll
-    for (int p = 0; p < R::kPasses; ++p) {
-        const int r = p * R::kRowsPerPass + tid / R::kChunks;
-        *reinterpret_cast<u32x4*>(lds + r * RS + (tid % R::kChunks) * 8) = g.r[p];
-    }
-}
-// transposed staging: item = (4-row quad, 8-wide d chunk), 16 * D / 8 items
-template <int D, int NT>
-struct TransRegs {
-    static constexpr int kItems = 16 * (D / 8);
-    static constexpr int kPasses = (kItems + NT - 1) / NT;
-    u32x4 r[kPasses][4];
-};
-template <int D, int NT, class Rows>
-__device__ __forceinline__ void load_trans(TransRegs<D, NT>& g, const uint16_t* __restrict__ src, Rows rows, int tid) {
-    using R = TransRegs<D, NT>;
-#pragma unroll
-    for (int p = 0; p < R::kPasses; ++p) {
-        const int item = p * NT + tid;
-        if (R::kItems % NT != 0 && item >= R::kItems) break;
-        const int q4 = item & 15, dc = item >> 4;
-#pragma unroll
-        for (int b = 0; b < 4; ++b) g.r[p][b] = *reinterpret_cast<const u32x4*>(src + rows(4 * q4 + b) * D + dc * 8);
-    }
-}
-template <int D, int NT, int TS = TileLds<D>::kTStride>
-__device__ __forceinline__ void store_trans_f16(uint16_t* lds, const TransRegs<D, NT>& g, float mul, int tid) {
-    using R = TransRegs<D, NT>;
-#pragma unroll
-    for (int p = 0; p < R::kPasses; ++p) {
-        const int item = p * NT + tid;
-        if (R::kItems % NT != 0 && item >= R::kItems) break;
-        const int q4 = item & 15, dc = item >> 4;
-        const int pos = tpos(4 * q4);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const u32x4* r = g.r[p];
-            u32x2 even, odd;
-            even.x = bf16_to_f16_bits(r[0][e] & 0xffffu, mul) | (bf16_to_f16_bits(r[1][e] & 0xffffu, mul) << 16);
-            even.y = bf16_to_f16_bits(r[2][e] & 0xffffu, mul) | (bf16_to_f16_bits(r[3][e] & 0xffffu, mul) << 16);
-            odd.x = bf16_to_f16_bits(r[0][e] >> 16, mul) | (bf16_to_f16_bits(r[1][e] >> 16, mul) << 16);
-            odd.y = bf16_to_f16_bits(r[2][e] >> 16, mul) | (bf16_to_f16_bits(r[3][e] >> 16, mul) << 16);
-            const int d0 = dc * 8 + 2 * e;
-            *reinterpret_cast<u32x2*>(lds + d0 * TS + pos) = even;
-            *reinterpret_cast<u32x2*>(lds + (d0 + 1) * TS + pos) = odd;
-        }
     }
 }
 
@@ -289,30 +171,6 @@ __device__ __forceinline__ void query_tile_of(int64_t t, int B, int Hq, int Hkv,
     const int64_t r = u % per;
     qb = nqb - 1 - int(r / G);
     bh = (bg / Hkv) * Hq + (bg % Hkv) * G + int(r % G);
-}
-
-// A operand of a 32x32x16 fp16 MFMA taken transposed from a row-major fp16
-// tile X[row][col] (row stride RS elements): A[m][k] = X[k0 + kperm(k)][m0 + m]
-// with kperm the key order of an accumulator-resident B operand (lane half h
-// supplies rows k0 + 4h + {0..3} and k0 + 8 + 4h + {0..3}).  Two
-// ds_read_b64_tr_b16: in each group of 16 lanes, lane s names 4 consecutive
-// elements of row (s / 4) and receives element s % 4 of the rows named by
-// lanes s / 4 + 4j, j = 0..3.
-template <int RS>
-__device__ __forceinline__ u32x4 lds_read_tr_a(const uint16_t* x, int k0, int m0, int lane) {
-    typedef short v4s __attribute__((ext_vector_type(4)));
-    const int row = k0 + 4 * (lane >> 5) + ((lane & 15) >> 2);
-    const int col = m0 + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-    const uint16_t* p = x + row * RS + col;
-    const v4s r0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4s*)(p));
-    const v4s r1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4s*)(p + 8 * RS));
-    const u32x2 a = __builtin_bit_cast(u32x2, r0), b = __builtin_bit_cast(u32x2, r1);
-    u32x4 o;
-    o.x = a.x;
-    o.y = a.y;
-    o.z = b.x;
-    o.w = b.y;
-    return o;
 }
 
 // 16-byte LDS read
