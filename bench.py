@@ -30,6 +30,38 @@ PEAK_BF16_TFLOPS = 2516.6     # MI355X dense bf16 / fp16 MFMA
 PEAK_HBM_GBS = 8000.0
 
 
+def kernel_source_hash() -> str:
+    """sha256 over the kernel library sources (csrc and the C header)."""
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2510_18830_amd", "csrc")
+    files = sorted(f for f in os.listdir(csrc) if f.endswith((".hip", ".h")))
+    for f in files + ["../../include/msparse.h"]:
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
+    return h.hexdigest()
+
+
+def hbm_traffic(workload: str, kernel: str):
+    """Bytes per launch of `kernel` from the committed PMC summary (FETCH_SIZE and
+    WRITE_SIZE, copy-calibrated), or None when there is none for this workload
+    or the kernel sources changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"{workload}_hbm_traffic.md")
+    if not os.path.exists(path):
+        return None
+    digest, table = None, {}
+    with open(path) as fh:
+        for line in fh:
+            tok = line.split()
+            if len(tok) == 2 and tok[0] == "source_sha256":
+                digest = tok[1]
+            elif len(tok) == 3 and tok[0] == "traffic":
+                table[tok[1]] = float(tok[2])
+    if digest != kernel_source_hash():
+        return None
+    return table.get(kernel)
+
+
 def kernel_flops(name: str, d: int, T: int, C: int, BH: int, N: int) -> float:
     """MFMA GEMM work each kernel must do on the computed blocks / columns."""
     pair = 2.0 * d            # one multiply-add over d per (row, key) per GEMM
@@ -317,8 +349,10 @@ def main():
     dom = max(kern, key=lambda n: kern[n]["avg_ms"] * kern[n]["launches_per_step"])
     dk_ = kern[dom]
     achieved = dk_["tflops"] if dk_["tflops"] is not None else 0.0
+    traffic = hbm_traffic(wl.name, f"{dom}_kernel<{wl.head_dim}>")
     roofline = {"bound": "mfma", "kernel": dom, "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None}
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                "traffic": None if traffic is None else round(traffic), "traffic_unit": "HBM bytes per launch"}
     line = {
         "metric": "sparse attn fwd+bwd TFLOP/s on computed blocks + ms/layer at 128K and 512K",
         "value": round(value, 2),
