@@ -119,11 +119,11 @@ struct DqRows {
     float lse2, dlt;
 };
 
-// mask: 0 none, 1 causal diagonal, 2 per-key limits
+// lims (LDS, or NULL for a tile without masking): key k visible to in-block
+// query row r iff r >= lims[k]; a rare uniform branch (see fwd_tile).
 template <int D>
 __device__ __forceinline__ void dq_tile(const uint16_t* kt, const uint16_t* vt, const uint16_t* k16t,
-                                        const int32_t* lims, DqRows<D>& st, int mask, int qrow, int lane, float c2,
-                                        float sc) {
+                                        const int32_t* lims, DqRows<D>& st, int qrow, int lane, float c2, float sc) {
     constexpr int KD = DqRows<D>::KD, ND = DqRows<D>::ND;
     const int h = lane >> 5, l32 = lane & 31;
     f32x16 sacc[2], pacc[2];
@@ -142,14 +142,21 @@ __device__ __forceinline__ void dq_tile(const uint16_t* kt, const uint16_t* vt, 
     for (int c = 0; c < 2; ++c)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-            float p = fast_exp2(__builtin_fmaf(sacc[c][r], c2, -st.lse2));
-            if (mask) {
-                const int key = 32 * c + 8 * (r >> 2) + 4 * h + (r & 3);
-                const int lim = mask == 1 ? key : lims[key];
-                if (qrow < lim) p = 0.f;
-            }
+            const float p = fast_exp2(__builtin_fmaf(sacc[c][r], c2, -st.lse2));
             sacc[c][r] = p * __builtin_fmaf(pacc[c][r], sc, -st.dlt);
         }
+    if (lims) {
+        keep_branch();
+#pragma unroll
+        for (int c = 0; c < 2; ++c)
+#pragma unroll
+            for (int q4 = 0; q4 < 4; ++q4) {
+                const i32x4 l4 = *reinterpret_cast<const i32x4*>(lims + 32 * c + 8 * q4 + 4 * h);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (qrow < l4[e]) sacc[c][4 * q4 + e] = 0.f;
+            }
+    }
     u32x4 zb[4];
     zb[0] = pack8_f16<0>(sacc[0]);
     zb[1] = pack8_f16<8>(sacc[0]);
@@ -167,10 +174,11 @@ __global__ void __launch_bounds__(kDqThreads) bwd_dq_kernel(AttnArgs a) {
     constexpr int KD = DqRows<D>::KD, ND = DqRows<D>::ND;
     constexpr int RE = DmaTile<D, kRowPad>::kElems, TE = DmaTile<D, kTrPad>::kElems;
     __shared__ uint16_t k0s[RE], v0s[RE], t0s[TE], k1s[RE], v1s[RE], t1s[TE];
-    __shared__ int32_t kidx[64], lims[64];
+    __shared__ int32_t kidx[64], lims[64], dlims[64];
     const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, l32 = lane & 31;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6), half = w >> 1;
     const int npair = (a.nqb + 1) >> 1;
+    if (tid < 64) dlims[tid] = tid;   // causal diagonal: key k visible to rows >= k
     int bh, qp;
     query_tile_of(blockIdx.x, a.B, a.Hq, a.Hkv, npair, bh, qp);
     const int b = bh / a.Hq, hq = bh % a.Hq, hk = hq / (a.Hq / a.Hkv);
@@ -233,7 +241,7 @@ __global__ void __launch_bounds__(kDqThreads) bwd_dq_kernel(AttnArgs a) {
         const bool more = next(kb2, in0n, in1n);
         if (more) load(nk, nv, nt, ContiguousRows{int64_t(kb2) * 64});
         if (half == 0 ? in0 : in1)
-            dq_tile<D>(ck, cv, ct, lims, st, ldc(a.k_blk_global, kb) == qg ? 1 : 0, qrow, lane, c2, sc);
+            dq_tile<D>(ck, cv, ct, ldc(a.k_blk_global, kb) == qg ? dlims : nullptr, st, qrow, lane, c2, sc);
         wait_vmem();
         __syncthreads();
         kb = kb2;
@@ -262,7 +270,7 @@ __global__ void __launch_bounds__(kDqThreads) bwd_dq_kernel(AttnArgs a) {
             load(k0s, v0s, t0s, IndexedRows{kidx});
             wait_vmem();
             __syncthreads();
-            if (half == j) dq_tile<D>(k0s, v0s, t0s, lims, st, 2, qrow, lane, c2, sc);
+            if (half == j) dq_tile<D>(k0s, v0s, t0s, lims, st, qrow, lane, c2, sc);
             __syncthreads();
         }
     }
@@ -314,12 +322,14 @@ __device__ __forceinline__ void kv_load_query_tile(uint16_t* t, const AttnArgs& 
     }
 }
 
-// One 64-row query tile against this wave's 32 keys.  `active` / `lim` give
-// the per-key visibility: key visible to in-block query row r iff active and
-// r >= lim.
+// One 64-row query tile against this wave's 32 keys (`key` = this lane's key
+// inside the 64-key block).  lims (LDS, or NULL for a tile without masking):
+// the key is visible to in-block query row r iff r >= lims[key] (64: not
+// visible); a rare uniform branch whose limit comes from LDS, so nothing of
+// it is hoisted into the loop.
 template <int D>
-__device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, const u32x4* vreg, bool masked,
-                                        bool active, int lim, float c2, float sc, int lane, f32x16* dv, f32x16* dk) {
+__device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, const u32x4* vreg, const int32_t* lims,
+                                        int key, float c2, float sc, int lane, f32x16* dv, f32x16* dk) {
     using T = KvTile<D>;
     constexpr int KD = D / 16, ND = D / 32;
     const int h = lane >> 5, l32 = lane & 31;
@@ -347,12 +357,23 @@ __device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, co
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 const int r = 4 * q4 + e;
-                float p = fast_exp2(__builtin_fmaf(sacc[rb][r], c2, -l4[e]));
-                if (masked && (!active || row0 + e < lim)) p = 0.f;
+                const float p = fast_exp2(__builtin_fmaf(sacc[rb][r], c2, -l4[e]));
                 sacc[rb][r] = p;
                 pacc[rb][r] = p * __builtin_fmaf(pacc[rb][r], sc, -d4[e]);
             }
         }
+    if (lims) {
+        keep_branch();
+        const int lim = lims[key] - 4 * h;   // row 32 rb + 8 (r/4) + 4 h + r%4 < lims[key]
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                if (32 * rb + 8 * (r >> 2) + (r & 3) < lim) {
+                    sacc[rb][r] = 0.f;
+                    pacc[rb][r] = 0.f;
+                }
+    }
     u32x4 pb[4], zb[4];
     pb[0] = pack8_f16<0>(sacc[0]);
     pb[1] = pack8_f16<8>(sacc[0]);
@@ -384,8 +405,10 @@ template <int D>
 __global__ void __launch_bounds__(kKvThreads) bwd_dkdv_kernel(AttnArgs a) {
     constexpr int KD = D / 16, ND = D / 32;
     __shared__ __attribute__((aligned(16))) uint16_t t0s[KvTile<D>::kElems], t1s[KvTile<D>::kElems];
+    __shared__ int32_t dlims[64];
     const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, l32 = lane & 31;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6), half = w >> 1;
+    if (tid < 64) dlims[tid] = tid;   // causal diagonal: key k visible to rows >= k
     const int BK = a.B * a.Hkv;
     const int npair = (a.nkb + 1) >> 1;
     const int64_t u = xcd_chunk(blockIdx.x, int64_t(BK) * npair);
@@ -454,8 +477,8 @@ __global__ void __launch_bounds__(kKvThreads) bwd_dkdv_kernel(AttnArgs a) {
         const bool more = next(bh2, qb2, in0n, in1n);
         if (more) kv_load_query_tile<D, 4>(nt, a, bh2, qb2, w, lane);
         if (half == 0 ? in0 : in1) {
-            const bool masked = ldc(a.q_blk_global, qb) == kg;   // diagonal tile
-            kv_tile<D>(ct, kreg, vreg, masked, true, key, c2, sc, lane, dv, dk);
+            const bool diag = ldc(a.q_blk_global, qb) == kg;
+            kv_tile<D>(ct, kreg, vreg, diag ? dlims : nullptr, key, c2, sc, lane, dv, dk);
         }
         wait_vmem();
         __syncthreads();
@@ -603,6 +626,7 @@ template <int D>
 __global__ void __launch_bounds__(kThreads) bwd_dkdv_col_kernel(AttnArgs a) {
     constexpr int KD = D / 16, ND = D / 32;
     __shared__ __attribute__((aligned(16))) uint16_t ts[KvTile<D>::kElems];
+    __shared__ int32_t clims[64];
     const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, l32 = lane & 31;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int nc = a.col_choff[a.B * a.Hq];
@@ -648,10 +672,11 @@ __global__ void __launch_bounds__(kThreads) bwd_dkdv_col_kernel(AttnArgs a) {
         const int lim = qg == cg ? cin : 0;
         // every column covered by a selected block-diagonal: nothing to do here
         if (!__syncthreads_or(active)) continue;
+        clims[key] = active ? lim : 64;
         kv_load_query_tile<D, 2>(ts, a, bh, qb, w, lane);
         wait_vmem();
         __syncthreads();
-        kv_tile<D>(ts, kreg, vreg, true, active, lim, c2, sc, lane, dv, dk);
+        kv_tile<D>(ts, kreg, vreg, clims, key, c2, sc, lane, dv, dk);
         __syncthreads();
     }
     if (!valid) return;

@@ -44,11 +44,13 @@ struct FwdRows {
     float m = -INFINITY, l = 0.f;
 };
 
-// One 64-key tile for one wave.  mask: 0 none, 1 causal diagonal (key k
-// visible to row r iff r >= k), 2 per-key limits from LDS.
+// One 64-key tile for one wave.  lims (LDS, or NULL for a tile without
+// masking): key k is visible to in-block query row r iff r >= lims[k] (the
+// causal diagonal uses lims[k] = k).  The masking is a rare uniform branch
+// whose limits come from LDS, so nothing of it is hoisted into the loop.
 template <int D>
 __device__ __forceinline__ void fwd_tile(const uint16_t* kt, const uint16_t* vt, const int32_t* lims, FwdRows<D>& st,
-                                         int mask, int qrow, int lane, float c2) {
+                                         int qrow, int lane, float c2) {
     const int h = lane >> 5, l32 = lane & 31;
     constexpr int KD = FwdRows<D>::KD, ND = FwdRows<D>::ND;
     // ---- S^T for keys 0-31 (c = 0) and 32-63 (c = 1)
@@ -61,14 +63,17 @@ __device__ __forceinline__ void fwd_tile(const uint16_t* kt, const uint16_t* vt,
             sacc[c] = mfma32(dma_read16<D, kRowPad>(kt, 32 * c + l32, h + 2 * s), st.q[s], sacc[c]);
     }
     // ---- mask, tile max (raw logits; scale > 0 commutes with max)
-    if (mask) {
+    if (lims) {
+        keep_branch();
 #pragma unroll
         for (int c = 0; c < 2; ++c)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int key = 32 * c + 8 * (r >> 2) + 4 * h + (r & 3);
-                const int lim = mask == 1 ? key : lims[key];
-                if (qrow < lim) sacc[c][r] = -INFINITY;
+            for (int q4 = 0; q4 < 4; ++q4) {
+                const int k0 = 32 * c + 8 * q4 + 4 * h;
+                const i32x4 l4 = *reinterpret_cast<const i32x4*>(lims + k0);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (qrow < l4[e]) sacc[c][4 * q4 + e] = -INFINITY;
             }
     }
     float mx = -INFINITY;
@@ -123,7 +128,7 @@ attn_fwd_kernel(AttnArgs a) {
     // two pipeline buffers as separate LDS objects (K bf16, V fp16 rows)
     constexpr int KE = DmaTile<D, kRowPad>::kElems, VE = DmaTile<D, kTrPad>::kElems;
     __shared__ uint16_t k0s[KE], v0s[VE], k1s[KE], v1s[VE];
-    __shared__ int32_t kidx[64], lims[64];
+    __shared__ int32_t kidx[64], lims[64], dlims[64];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -175,6 +180,7 @@ attn_fwd_kernel(AttnArgs a) {
         p1 += in1;
         return true;
     };
+    if (tid < 64) dlims[tid] = tid;   // causal diagonal: key k visible to rows >= k
     int32_t kb = 0;
     bool in0 = false, in1 = false;
     bool have = next(kb, in0, in1);
@@ -195,7 +201,7 @@ attn_fwd_kernel(AttnArgs a) {
             dma_rows<D, kRowPad, 4>(nk, kp, rows, w, lane);
             dma_rows<D, kTrPad, 4>(nv, vp, rows, w, lane);
         }
-        if (half == 0 ? in0 : in1) fwd_tile<D>(ck, cv, lims, st, ldc(a.k_blk_global, kb) == qg ? 1 : 0, qrow, lane, c2);
+        if (half == 0 ? in0 : in1) fwd_tile<D>(ck, cv, ldc(a.k_blk_global, kb) == qg ? dlims : nullptr, st, qrow, lane, c2);
         wait_vmem();
         __syncthreads();
         kb = kb2;
@@ -225,7 +231,7 @@ attn_fwd_kernel(AttnArgs a) {
             dma_rows<D, kTrPad, 4>(v0s, vp, IndexedRows{kidx}, w, lane);
             wait_vmem();
             __syncthreads();
-            if (half == j) fwd_tile<D>(k0s, v0s, lims, st, 2, qrow, lane, c2);
+            if (half == j) fwd_tile<D>(k0s, v0s, lims, st, qrow, lane, c2);
             __syncthreads();
         }
     }

@@ -17,6 +17,7 @@ typedef __attribute__((ext_vector_type(16))) float f32x16;
 typedef __attribute__((ext_vector_type(4))) float f32x4;
 typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
 typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
+typedef __attribute__((ext_vector_type(4))) int32_t i32x4;
 
 // ---------------------------------------------------------------- bf16 <-> fp32
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
@@ -48,6 +49,10 @@ template <class T>
 __device__ __forceinline__ T ldc(const T* p, int64_t i) {
     return ((const __attribute__((address_space(4))) T*)(p))[i];
 }
+
+// Marks a rarely taken branch as having a side effect, so the compiler keeps
+// it a branch instead of turning its body into unconditional selects.
+__device__ __forceinline__ void keep_branch() { asm volatile(""); }
 
 // ---------------------------------------------------------------- MFMA
 // D(32x32) += A(32x16) * B(16x32), bf16 inputs, fp32 accumulate.
