@@ -137,18 +137,18 @@ __device__ __forceinline__ void dq_tile(const uint16_t* kt, const uint16_t* vt, 
             pacc[c] = mfma32(dma_read16<D, kRowPad>(vt, 32 * c + l32, h + 2 * s), st.g[s], pacc[c]);
         }
     }
-    // s dZ^T = P o (s dP^T - s Delta), P = exp2(c2 z - lse2) on visible entries
+    // Per key half c: s dZ^T = P o (s dP^T - s Delta), P = exp2(c2 z - lse2) on
+    // visible entries, then that half's dQ k-steps (2c, 2c+1); the MFMAs of one
+    // half run while the other half's VALU work issues.
 #pragma unroll
-    for (int c = 0; c < 2; ++c)
+    for (int c = 0; c < 2; ++c) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             const float p = fast_exp2(__builtin_fmaf(sacc[c][r], c2, -st.lse2));
             sacc[c][r] = p * __builtin_fmaf(pacc[c][r], sc, -st.dlt);
         }
-    if (lims) {
-        keep_branch();
-#pragma unroll
-        for (int c = 0; c < 2; ++c)
+        if (lims) {
+            keep_branch();
 #pragma unroll
             for (int q4 = 0; q4 < 4; ++q4) {
                 const i32x4 l4 = *reinterpret_cast<const i32x4*>(lims + 32 * c + 8 * q4 + 4 * h);
@@ -156,17 +156,16 @@ __device__ __forceinline__ void dq_tile(const uint16_t* kt, const uint16_t* vt, 
                 for (int e = 0; e < 4; ++e)
                     if (qrow < l4[e]) sacc[c][4 * q4 + e] = 0.f;
             }
+        }
+        u32x4 zb[2];
+        zb[0] = pack8_f16<0>(sacc[c]);
+        zb[1] = pack8_f16<8>(sacc[c]);
+#pragma unroll
+        for (int i = 0; i < ND; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+                st.acc[i] = mfma32h(dma_read_tr<D, kTrPad>(k16t, 16 * (2 * c + j), 32 * i, lane), zb[j], st.acc[i]);
     }
-    u32x4 zb[4];
-    zb[0] = pack8_f16<0>(sacc[0]);
-    zb[1] = pack8_f16<8>(sacc[0]);
-    zb[2] = pack8_f16<0>(sacc[1]);
-    zb[3] = pack8_f16<8>(sacc[1]);
-#pragma unroll
-    for (int i = 0; i < ND; ++i)
-#pragma unroll
-        for (int g = 0; g < 4; ++g)
-            st.acc[i] = mfma32h(dma_read_tr<D, kTrPad>(k16t, 16 * g, 32 * i, lane), zb[g], st.acc[i]);
 }
 
 template <int D>
@@ -346,9 +345,12 @@ __device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, co
             pacc[rb] = mfma32(dma_read16<D, kRowPad>(t + T::kG, 32 * rb + l32, h + 2 * s), vreg[s], pacc[rb]);
         }
     }
-    // rows of acc element r: 32 rb + 8 (r/4) + 4 h + r%4; column = this lane's key
+    // Per half rb of the query rows: softmax terms, then that half's share of
+    // dV / dK (k-steps 2 rb, 2 rb + 1).  The second half's S / dP MFMAs and the
+    // first half's dV / dK MFMAs run while the other half's VALU work issues.
+    // Rows of acc element r: 32 rb + 8 (r/4) + 4 h + r%4; column = this lane's key.
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb)
+    for (int rb = 0; rb < 2; ++rb) {
 #pragma unroll
         for (int q4 = 0; q4 < 4; ++q4) {
             const int row0 = 32 * rb + 8 * q4 + 4 * h;
@@ -362,35 +364,31 @@ __device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, co
                 pacc[rb][r] = p * __builtin_fmaf(pacc[rb][r], sc, -d4[e]);
             }
         }
-    if (lims) {
-        keep_branch();
-        const int lim = lims[key] - 4 * h;   // row 32 rb + 8 (r/4) + 4 h + r%4 < lims[key]
-#pragma unroll
-        for (int rb = 0; rb < 2; ++rb)
+        if (lims) {
+            keep_branch();
+            const int lim = lims[key] - 4 * h - 32 * rb;   // row 32 rb + 8 (r/4) + 4 h + r%4 < lims[key]
 #pragma unroll
             for (int r = 0; r < 16; ++r)
-                if (32 * rb + 8 * (r >> 2) + (r & 3) < lim) {
+                if (8 * (r >> 2) + (r & 3) < lim) {
                     sacc[rb][r] = 0.f;
                     pacc[rb][r] = 0.f;
                 }
-    }
-    u32x4 pb[4], zb[4];
-    pb[0] = pack8_f16<0>(sacc[0]);
-    pb[1] = pack8_f16<8>(sacc[0]);
-    pb[2] = pack8_f16<0>(sacc[1]);
-    pb[3] = pack8_f16<8>(sacc[1]);
-    zb[0] = pack8_f16<0>(pacc[0]);
-    zb[1] = pack8_f16<8>(pacc[0]);
-    zb[2] = pack8_f16<0>(pacc[1]);
-    zb[3] = pack8_f16<8>(pacc[1]);
-    // dV^T += (s dO)^T P, dK^T += Q^T (s dZ): A operands read transposed
-#pragma unroll
-    for (int i = 0; i < ND; ++i)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-            dv[i] = mfma32h(dma_read_tr<D, kTrPad>(t + T::kG16, 16 * g, 32 * i, lane), pb[g], dv[i]);
-            dk[i] = mfma32h(dma_read_tr<D, kTrPad>(t + T::kQ16, 16 * g, 32 * i, lane), zb[g], dk[i]);
         }
+        u32x4 pb[2], zb[2];
+        pb[0] = pack8_f16<0>(sacc[rb]);
+        pb[1] = pack8_f16<8>(sacc[rb]);
+        zb[0] = pack8_f16<0>(pacc[rb]);
+        zb[1] = pack8_f16<8>(pacc[rb]);
+        // dV^T += (s dO)^T P, dK^T += Q^T (s dZ): A operands read transposed
+#pragma unroll
+        for (int i = 0; i < ND; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int g = 2 * rb + j;
+                dv[i] = mfma32h(dma_read_tr<D, kTrPad>(t + T::kG16, 16 * g, 32 * i, lane), pb[j], dv[i]);
+                dk[i] = mfma32h(dma_read_tr<D, kTrPad>(t + T::kQ16, 16 * g, 32 * i, lane), zb[j], dk[i]);
+            }
+    }
 }
 
 // Key-major pass: one workgroup of four waves per (b, KV head, pair of
