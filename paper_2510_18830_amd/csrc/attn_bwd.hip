@@ -169,7 +169,7 @@ __device__ __forceinline__ void dq_tile(const uint16_t* kt, const uint16_t* vt, 
 }
 
 template <int D>
-__global__ void __launch_bounds__(kDqThreads) bwd_dq_kernel(AttnArgs a) {
+__global__ void __launch_bounds__(kDqThreads) __attribute__((amdgpu_waves_per_eu(1, 1))) bwd_dq_kernel(AttnArgs a) {
     constexpr int KD = DqRows<D>::KD, ND = DqRows<D>::ND;
     constexpr int RE = DmaTile<D, kRowPad>::kElems, TE = DmaTile<D, kTrPad>::kElems;
     __shared__ uint16_t k0s[RE], v0s[RE], t0s[TE], k1s[RE], v1s[RE], t1s[TE];
@@ -211,7 +211,9 @@ __global__ void __launch_bounds__(kDqThreads) bwd_dq_kernel(AttnArgs a) {
     const int64_t e00 = ldc(a.blk_ptr, item0), e01 = ldc(a.blk_ptr, item0 + 1);
     const int64_t e11 = has1 ? ldc(a.blk_ptr, item0 + 2) : e01;
     int64_t p0 = e00, p1 = e01;
-    auto next = [&](int32_t& kb, bool& in0, bool& in1) {
+    // the diagonal test is made here, one tile ahead (no scalar load pending
+    // inside a tile)
+    auto next = [&](int32_t& kb, bool& in0, bool& in1, bool& diag) {
         if (p0 >= e01 && p1 >= e11) return false;
         const int32_t k0 = p0 < e01 ? ldc(a.blk_idx, p0) : INT32_MAX;
         const int32_t k1 = p1 < e11 ? ldc(a.blk_idx, p1) : INT32_MAX;
@@ -220,6 +222,7 @@ __global__ void __launch_bounds__(kDqThreads) bwd_dq_kernel(AttnArgs a) {
         in1 = k1 == kb;
         p0 += in0;
         p1 += in1;
+        diag = ldc(a.k_blk_global, kb) == qg;
         return true;
     };
     auto load = [&](uint16_t* kt, uint16_t* vt, uint16_t* tt, auto rows) {
@@ -228,24 +231,24 @@ __global__ void __launch_bounds__(kDqThreads) bwd_dq_kernel(AttnArgs a) {
         dma_rows<D, kTrPad, 4>(tt, k16p, rows, w, lane);
     };
     int32_t kb = 0;
-    bool in0 = false, in1 = false;
-    bool have = next(kb, in0, in1);
+    bool in0 = false, in1 = false, diag = false;
+    bool have = next(kb, in0, in1, diag);
     if (have) load(k0s, v0s, t0s, ContiguousRows{int64_t(kb) * 64});
     wait_vmem();
     __syncthreads();
     auto step = [&](const uint16_t* ck, const uint16_t* cv, const uint16_t* ct, uint16_t* nk, uint16_t* nv,
                     uint16_t* nt) {
         int32_t kb2 = 0;
-        bool in0n = false, in1n = false;
-        const bool more = next(kb2, in0n, in1n);
+        bool in0n = false, in1n = false, diagn = false;
+        const bool more = next(kb2, in0n, in1n, diagn);
         if (more) load(nk, nv, nt, ContiguousRows{int64_t(kb2) * 64});
-        if (half == 0 ? in0 : in1)
-            dq_tile<D>(ck, cv, ct, ldc(a.k_blk_global, kb) == qg ? dlims : nullptr, st, qrow, lane, c2, sc);
+        if (half == 0 ? in0 : in1) dq_tile<D>(ck, cv, ct, diag ? dlims : nullptr, st, qrow, lane, c2, sc);
         wait_vmem();
         __syncthreads();
         kb = kb2;
         in0 = in0n;
         in1 = in1n;
+        diag = diagn;
         have = more;
     };
     while (have) {
@@ -339,11 +342,36 @@ __device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, co
     for (int rb = 0; rb < 2; ++rb) {
         sacc[rb] = f32x16{};
         pacc[rb] = f32x16{};
+    }
+    // Four independent accumulation chains.  Operands are read in groups of two
+    // k-steps (8 LDS reads) into two register sets: group g + 1 is read before
+    // group g's MFMAs issue (scheduling fences keep that order), so LDS
+    // latency overlaps the MFMAs (the default schedule waits for every read
+    // right before its MFMA).
+    u32x4 fq[2][2][2], fg[2][2][2];   // [set][k-step of group][rb]
+    auto read_group = [&](int set, int s0) {
 #pragma unroll
-        for (int s = 0; s < KD; ++s) {
-            sacc[rb] = mfma32(dma_read16<D, kRowPad>(t + T::kQ, 32 * rb + l32, h + 2 * s), kreg[s], sacc[rb]);
-            pacc[rb] = mfma32(dma_read16<D, kRowPad>(t + T::kG, 32 * rb + l32, h + 2 * s), vreg[s], pacc[rb]);
-        }
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int rb = 0; rb < 2; ++rb) {
+                fq[set][j][rb] = dma_read16<D, kRowPad>(t + T::kQ, 32 * rb + l32, h + 2 * (s0 + j));
+                fg[set][j][rb] = dma_read16<D, kRowPad>(t + T::kG, 32 * rb + l32, h + 2 * (s0 + j));
+            }
+    };
+    read_group(0, 0);
+#pragma unroll
+    for (int s0 = 0; s0 < KD; s0 += 2) {
+        const int set = (s0 >> 1) & 1;
+        if (s0 + 2 < KD) read_group(set ^ 1, s0 + 2);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int rb = 0; rb < 2; ++rb) {
+                sacc[rb] = mfma32(fq[set][j][rb], kreg[s0 + j], sacc[rb]);
+                pacc[rb] = mfma32(fg[set][j][rb], vreg[s0 + j], pacc[rb]);
+            }
+        __builtin_amdgcn_sched_barrier(0);
     }
     // Per half rb of the query rows: softmax terms, then that half's share of
     // dV / dK (k-steps 2 rb, 2 rb + 1).  The second half's S / dP MFMAs and the
@@ -400,7 +428,7 @@ __device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, co
 constexpr int kKvThreads = 256;
 
 template <int D>
-__global__ void __launch_bounds__(kKvThreads) bwd_dkdv_kernel(AttnArgs a) {
+__global__ void __launch_bounds__(kKvThreads) __attribute__((amdgpu_waves_per_eu(1, 1))) bwd_dkdv_kernel(AttnArgs a) {
     constexpr int KD = D / 16, ND = D / 32;
     __shared__ __attribute__((aligned(16))) uint16_t t0s[KvTile<D>::kElems], t1s[KvTile<D>::kElems];
     __shared__ int32_t dlims[64];
@@ -448,7 +476,9 @@ __global__ void __launch_bounds__(kKvThreads) bwd_dkdv_kernel(AttnArgs a) {
         e1 = has1 ? ldc(a.kblk_ptr, item + 2) : e0;
     };
     open_head();
-    auto next = [&](int& bh, int& qb, bool& in0, bool& in1) {
+    // the diagonal test is made here, one tile ahead, so that no scalar load
+    // is pending inside a tile (it would force the LDS waits to drain fully)
+    auto next = [&](int& bh, int& qb, bool& in0, bool& in1, bool& diag) {
         while (p0 >= e0 && p1 >= e1) {
             if (++g >= G) return false;
             open_head();
@@ -461,29 +491,28 @@ __global__ void __launch_bounds__(kKvThreads) bwd_dkdv_kernel(AttnArgs a) {
         p0 += in0;
         p1 += in1;
         bh = b * a.Hq + hk * G + g;
+        diag = ldc(a.q_blk_global, qb) == kg;
         return true;
     };
     int bh = 0, qb = 0;
-    bool in0 = false, in1 = false;
-    bool have = next(bh, qb, in0, in1);
+    bool in0 = false, in1 = false, diag = false;
+    bool have = next(bh, qb, in0, in1, diag);
     if (have) kv_load_query_tile<D, 4>(t0s, a, bh, qb, w, lane);
     wait_vmem();
     __syncthreads();
     auto step = [&](const uint16_t* ct, uint16_t* nt) {
         int bh2 = 0, qb2 = 0;
-        bool in0n = false, in1n = false;
-        const bool more = next(bh2, qb2, in0n, in1n);
+        bool in0n = false, in1n = false, diagn = false;
+        const bool more = next(bh2, qb2, in0n, in1n, diagn);
         if (more) kv_load_query_tile<D, 4>(nt, a, bh2, qb2, w, lane);
-        if (half == 0 ? in0 : in1) {
-            const bool diag = ldc(a.q_blk_global, qb) == kg;
-            kv_tile<D>(ct, kreg, vreg, diag ? dlims : nullptr, key, c2, sc, lane, dv, dk);
-        }
+        if (half == 0 ? in0 : in1) kv_tile<D>(ct, kreg, vreg, diag ? dlims : nullptr, key, c2, sc, lane, dv, dk);
         wait_vmem();
         __syncthreads();
         bh = bh2;
         qb = qb2;
         in0 = in0n;
         in1 = in1n;
+        diag = diagn;
         have = more;
     };
     while (have) {
@@ -621,7 +650,7 @@ __global__ void __launch_bounds__(kPlanThreads) bwd_colplan_kernel(AttnArgs a) {
 // of the item go to its own slot (grid = item capacity; surplus workgroups
 // exit, consecutive items land on different XCDs).
 template <int D>
-__global__ void __launch_bounds__(kThreads) bwd_dkdv_col_kernel(AttnArgs a) {
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))) bwd_dkdv_col_kernel(AttnArgs a) {
     constexpr int KD = D / 16, ND = D / 32;
     __shared__ __attribute__((aligned(16))) uint16_t ts[KvTile<D>::kElems];
     __shared__ int32_t clims[64];
