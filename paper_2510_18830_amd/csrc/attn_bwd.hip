@@ -131,17 +131,49 @@ __device__ __forceinline__ void dq_tile(const uint16_t* kt, const uint16_t* vt, 
     for (int c = 0; c < 2; ++c) {
         sacc[c] = f32x16{};
         pacc[c] = f32x16{};
+    }
+    // S^T and dP^T: four accumulation chains, operands read in groups of two
+    // k-steps into two register sets, group g + 1 before group g's MFMAs
+    // (scheduling fences keep that order; see kv_tile).
+    u32x4 fk[2][2][2], fv[2][2][2];   // [set][k-step of group][c]
+    auto read_group = [&](int set, int s0) {
 #pragma unroll
-        for (int s = 0; s < KD; ++s) {
-            sacc[c] = mfma32(dma_read16<D, kRowPad>(kt, 32 * c + l32, h + 2 * s), st.q[s], sacc[c]);
-            pacc[c] = mfma32(dma_read16<D, kRowPad>(vt, 32 * c + l32, h + 2 * s), st.g[s], pacc[c]);
-        }
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int c = 0; c < 2; ++c) {
+                fk[set][j][c] = dma_read16<D, kRowPad>(kt, 32 * c + l32, h + 2 * (s0 + j));
+                fv[set][j][c] = dma_read16<D, kRowPad>(vt, 32 * c + l32, h + 2 * (s0 + j));
+            }
+    };
+    read_group(0, 0);
+#pragma unroll
+    for (int s0 = 0; s0 < KD; s0 += 2) {
+        const int set = (s0 >> 1) & 1;
+        if (s0 + 2 < KD) read_group(set ^ 1, s0 + 2);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int c = 0; c < 2; ++c) {
+                sacc[c] = mfma32(fk[set][j][c], st.q[s0 + j], sacc[c]);
+                pacc[c] = mfma32(fv[set][j][c], st.g[s0 + j], pacc[c]);
+            }
+        __builtin_amdgcn_sched_barrier(0);
     }
     // Per key half c: s dZ^T = P o (s dP^T - s Delta), P = exp2(c2 z - lse2) on
-    // visible entries, then that half's dQ k-steps (2c, 2c+1); the MFMAs of one
-    // half run while the other half's VALU work issues.
+    // visible entries, then that half's dQ k-steps (2c, 2c+1), K^T read
+    // transposed in groups of two d blocks into two register sets.
+    u32x4 ak[2][2][2];   // [set][i of group][j]
+    auto read_tr = [&](int set, int c, int i0) {
+#pragma unroll
+        for (int ii = 0; ii < 2; ++ii)
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+                ak[set][ii][j] = dma_read_tr<D, kTrPad>(k16t, 16 * (2 * c + j), 32 * (i0 + ii), lane);
+    };
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
+        read_tr(0, c, 0);
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             const float p = fast_exp2(__builtin_fmaf(sacc[c][r], c2, -st.lse2));
@@ -161,10 +193,16 @@ __device__ __forceinline__ void dq_tile(const uint16_t* kt, const uint16_t* vt, 
         zb[0] = pack8_f16<0>(sacc[c]);
         zb[1] = pack8_f16<8>(sacc[c]);
 #pragma unroll
-        for (int i = 0; i < ND; ++i)
+        for (int i0 = 0; i0 < ND; i0 += 2) {
+            const int set = (i0 >> 1) & 1;
+            if (i0 + 2 < ND) read_tr(set ^ 1, c, i0 + 2);
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-            for (int j = 0; j < 2; ++j)
-                st.acc[i] = mfma32h(dma_read_tr<D, kTrPad>(k16t, 16 * (2 * c + j), 32 * i, lane), zb[j], st.acc[i]);
+            for (int ii = 0; ii < 2; ++ii)
+#pragma unroll
+                for (int j = 0; j < 2; ++j) st.acc[i0 + ii] = mfma32h(ak[set][ii][j], zb[j], st.acc[i0 + ii]);
+            __builtin_amdgcn_sched_barrier(0);
+        }
     }
 }
 
@@ -377,8 +415,20 @@ __device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, co
     // dV / dK (k-steps 2 rb, 2 rb + 1).  The second half's S / dP MFMAs and the
     // first half's dV / dK MFMAs run while the other half's VALU work issues.
     // Rows of acc element r: 32 rb + 8 (r/4) + 4 h + r%4; column = this lane's key.
+    // dV^T += (s dO)^T P, dK^T += Q^T (s dZ) for half rb: A operands read
+    // transposed, in groups (one 32-wide d block i: 4 operands, 8 reads) into
+    // two register sets, the first group before the softmax VALU work.
+    u32x4 av[2][2], ak[2][2];   // [set][j]
+    auto read_tr = [&](int set, int rb, int i) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            av[set][j] = dma_read_tr<D, kTrPad>(t + T::kG16, 16 * (2 * rb + j), 32 * i, lane);
+            ak[set][j] = dma_read_tr<D, kTrPad>(t + T::kQ16, 16 * (2 * rb + j), 32 * i, lane);
+        }
+    };
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb) {
+        read_tr(0, rb, 0);
 #pragma unroll
         for (int q4 = 0; q4 < 4; ++q4) {
             const int row0 = 32 * rb + 8 * q4 + 4 * h;
@@ -407,15 +457,18 @@ __device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, co
         pb[1] = pack8_f16<8>(sacc[rb]);
         zb[0] = pack8_f16<0>(pacc[rb]);
         zb[1] = pack8_f16<8>(pacc[rb]);
-        // dV^T += (s dO)^T P, dK^T += Q^T (s dZ): A operands read transposed
 #pragma unroll
-        for (int i = 0; i < ND; ++i)
+        for (int i = 0; i < ND; ++i) {
+            const int set = i & 1;
+            if (i + 1 < ND) read_tr(set ^ 1, rb, i + 1);
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int j = 0; j < 2; ++j) {
-                const int g = 2 * rb + j;
-                dv[i] = mfma32h(dma_read_tr<D, kTrPad>(t + T::kG16, 16 * g, 32 * i, lane), pb[j], dv[i]);
-                dk[i] = mfma32h(dma_read_tr<D, kTrPad>(t + T::kQ16, 16 * g, 32 * i, lane), zb[j], dk[i]);
+                dv[i] = mfma32h(av[set][j], pb[j], dv[i]);
+                dk[i] = mfma32h(ak[set][j], zb[j], dk[i]);
             }
+            __builtin_amdgcn_sched_barrier(0);
+        }
     }
 }
 
