@@ -54,13 +54,30 @@ __device__ __forceinline__ void fwd_tile(const uint16_t* kt, const uint16_t* vt,
     const int h = lane >> 5, l32 = lane & 31;
     constexpr int KD = FwdRows<D>::KD, ND = FwdRows<D>::ND;
     // ---- S^T for keys 0-31 (c = 0) and 32-63 (c = 1)
+    // operands read in groups of two k-steps into two register sets, group
+    // g + 1 before group g's MFMAs (scheduling fences keep that order), so the
+    // LDS latency overlaps the MFMAs
     f32x16 sacc[2];
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
-        sacc[c] = f32x16{};
+    for (int c = 0; c < 2; ++c) sacc[c] = f32x16{};
+    u32x4 fk[2][2][2];   // [set][k-step of group][c]
+    auto read_group = [&](int set, int s0) {
 #pragma unroll
-        for (int s = 0; s < KD; ++s)
-            sacc[c] = mfma32(dma_read16<D, kRowPad>(kt, 32 * c + l32, h + 2 * s), st.q[s], sacc[c]);
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int c = 0; c < 2; ++c) fk[set][j][c] = dma_read16<D, kRowPad>(kt, 32 * c + l32, h + 2 * (s0 + j));
+    };
+    read_group(0, 0);
+#pragma unroll
+    for (int s0 = 0; s0 < KD; s0 += 2) {
+        const int set = (s0 >> 1) & 1;
+        if (s0 + 2 < KD) read_group(set ^ 1, s0 + 2);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int c = 0; c < 2; ++c) sacc[c] = mfma32(fk[set][j][c], st.q[s0 + j], sacc[c]);
+        __builtin_amdgcn_sched_barrier(0);
     }
     // ---- mask, tile max (raw logits; scale > 0 commutes with max)
     if (lims) {
@@ -112,11 +129,22 @@ __device__ __forceinline__ void fwd_tile(const uint16_t* kt, const uint16_t* vt,
     pb[1] = pack8_f16<8>(sacc[0]);
     pb[2] = pack8_f16<0>(sacc[1]);
     pb[3] = pack8_f16<8>(sacc[1]);
+    // V^T operands in groups of one d block (4 operands) into two register sets
+    u32x4 av[2][4];
+    auto read_tr = [&](int set, int i) {
 #pragma unroll
-    for (int i = 0; i < ND; ++i)
+        for (int g = 0; g < 4; ++g) av[set][g] = dma_read_tr<D, kTrPad>(vt, 16 * g, 32 * i, lane);
+    };
+    read_tr(0, 0);
 #pragma unroll
-        for (int g = 0; g < 4; ++g)
-            st.o[i] = mfma32h(dma_read_tr<D, kTrPad>(vt, 16 * g, 32 * i, lane), pb[g], st.o[i]);
+    for (int i = 0; i < ND; ++i) {
+        const int set = i & 1;
+        if (i + 1 < ND) read_tr(set ^ 1, i + 1);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int g = 0; g < 4; ++g) st.o[i] = mfma32h(av[set][g], pb[g], st.o[i]);
+        __builtin_amdgcn_sched_barrier(0);
+    }
 }
 
 // Two waves per SIMD (at most 256 registers per lane), two workgroups per CU:
