@@ -189,7 +189,8 @@ MSPARSE_API msparse_status msparse_build_index(const msparse_dims* dims, const i
  * receives the unrounded output; msparse_attn_bwd computes
  * Delta = dO . O more accurately from it, and ring steps merge it.  out may be
  * NULL when out_f32 is given.  Workspace: msparse_attn_fwd_workspace(dims)
- * bytes (it holds an fp16 copy of v, B * Hkv * seq_k * d * 2 bytes). */
+ * bytes (it holds an fp16 copy of v times a power of two, B * Hkv * seq_k *
+ * d * 2 bytes, and a few words). */
 MSPARSE_API size_t msparse_attn_fwd_workspace(const msparse_dims* dims);
 MSPARSE_API msparse_status msparse_attn_fwd(const msparse_dims* dims, const void* q, const void* k, const void* v,
                                 const msparse_index* index, void* out, float* lse, float* out_f32,
@@ -218,8 +219,8 @@ MSPARSE_API msparse_status msparse_merge_out_lse(const msparse_dims* dims, const
  * dq, dk, dv are fp32 and overwritten, except that dq_accumulate = 1 adds into
  * dq (ring steps after the first).
  * Workspace: msparse_attn_bwd_workspace(dims, vcol_cap) bytes; it holds
- * fp16 copies of k, q and dO (times a power of two), Delta, and the column
- * pass's work list and per-item partials. */
+ * fp16 copies of q, k, v and dO (each times a power of two), Delta, lse, and
+ * the column pass's work list and per-item partials. */
 MSPARSE_API size_t msparse_attn_bwd_workspace(const msparse_dims* dims, int64_t vcol_cap);
 MSPARSE_API msparse_status msparse_attn_bwd(const msparse_dims* dims, const void* q, const void* k, const void* v,
                                 const void* out, const float* out_f32, const void* dout, const float* lse,

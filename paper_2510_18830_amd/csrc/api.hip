@@ -318,12 +318,21 @@ static msparse_status fill_attn(const msparse_dims* d, const msparse_index* x, A
     return MSPARSE_OK;
 }
 
-// Forward workspace: the fp16 copy of V.
+// Forward workspace: the scaled fp16 copy of V and the max words.
+static size_t carve_fwd(const msparse_dims* d, char* base, AttnArgs* a) {
+    Carve c{base};
+    uint16_t* v16 = c.take<uint16_t>(size_t(d->batch) * d->heads_kv * d->seq_k * d->head_dim);
+    uint32_t* mx = c.take<uint32_t>(3);
+    if (a) {
+        a->v16 = v16;
+        a->qkvmax = mx;
+    }
+    return c.off;
+}
+
 size_t msparse_attn_fwd_workspace(const msparse_dims* dims) {
     if (check_dims(dims, false)) return 0;
-    Carve c{nullptr};
-    c.take<uint16_t>(size_t(dims->batch) * dims->heads_kv * dims->seq_k * dims->head_dim);
-    return c.off;
+    return carve_fwd(dims, nullptr, nullptr);
 }
 
 msparse_status msparse_attn_fwd(const msparse_dims* dims, const void* q, const void* k, const void* v,
@@ -345,14 +354,9 @@ msparse_status msparse_attn_fwd(const msparse_dims* dims, const void* q, const v
     a.out = static_cast<uint16_t*>(out);
     a.out_f32 = out_f32;
     a.lse = lse;
-    Carve c{static_cast<char*>(ws)};
-    const size_t nkv = size_t(dims->batch) * dims->heads_kv * dims->seq_k * dims->head_dim;
-    uint16_t* v16 = c.take<uint16_t>(nkv);
-    a.v16 = v16;
+    carve_fwd(dims, static_cast<char*>(ws), &a);
     hipStream_t s = static_cast<hipStream_t>(stream);
-    hipError_t e = launch_to_f16(a.v, v16, int64_t(nkv), nullptr, s);
-    if (e == hipSuccess) e = launch_attn_fwd(a, s);
-    return check_hip(e, s, "attn fwd");
+    return check_hip(launch_attn_fwd(a, s), s, "attn fwd");
 }
 
 msparse_status msparse_merge_out_lse(const msparse_dims* dims, const float* o_part, const float* lse_part, float* o_acc,
@@ -374,18 +378,19 @@ msparse_status msparse_merge_out_lse(const msparse_dims* dims, const float* o_pa
     return check_hip(launch_merge(m, s), s, "merge out/lse");
 }
 
-// Backward workspace: Delta, max |dO|, the column work list and the per-item
-// column partials.
+// Backward workspace: scaled fp16 copies of K, V, Q and dO, Delta, lse2, the
+// max words, the column work list and the per-item column partials.
 static size_t carve_bwd(const msparse_dims* d, int64_t vcol_cap, char* base, AttnArgs* a) {
     const int64_t bh = int64_t(d->batch) * d->heads_q;
     const ColPlanSizes z = col_plan_sizes(bh, vcol_cap, d->seq_q / kBlock);
     Carve c{base};
     uint16_t* k16 = c.take<uint16_t>(size_t(d->batch) * d->heads_kv * d->seq_k * d->head_dim);
+    uint16_t* v16 = c.take<uint16_t>(size_t(d->batch) * d->heads_kv * d->seq_k * d->head_dim);
     uint16_t* q16 = c.take<uint16_t>(size_t(bh) * d->seq_q * d->head_dim);
     uint16_t* g16 = c.take<uint16_t>(size_t(bh) * d->seq_q * d->head_dim);
     float* delta = c.take<float>(size_t(bh) * d->seq_q);
     float* lse2 = c.take<float>(size_t(bh) * d->seq_q);
-    uint32_t* dmax = c.take<uint32_t>(1);
+    uint32_t* dmax = c.take<uint32_t>(4);   // max |dO|, |Q|, |K|, |V|
     int32_t* choff = c.take<int32_t>(size_t(bh) + 1);
     int64_t* e0 = c.take<int64_t>(size_t(z.chunk_cap));
     int32_t* head = c.take<int32_t>(size_t(z.chunk_cap));
@@ -396,11 +401,13 @@ static size_t carve_bwd(const msparse_dims* d, int64_t vcol_cap, char* base, Att
     float* dvc = c.take<float>(size_t(z.slots) * kBlock * d->head_dim);
     if (a) {
         a->k16 = k16;
+        a->v16 = v16;
         a->q16 = q16;
         a->g16 = g16;
         a->delta = delta;
         a->lse2 = lse2;
         a->dmax = dmax;
+        a->qkvmax = dmax + 1;
         a->col_choff = choff;
         a->col_e0 = e0;
         a->col_head = head;

@@ -39,7 +39,7 @@ constexpr float kLog2e = 1.4426950408889634f;
 
 // ------------------------------------------------------------------ Delta
 __global__ void bwd_init_kernel(AttnArgs a) {
-    if (threadIdx.x == 0) *a.dmax = 0u;
+    if (threadIdx.x < 4) (threadIdx.x == 0 ? a.dmax : a.qkvmax + threadIdx.x - 1)[0] = 0u;
 }
 
 constexpr int kDeltaBlocks = 2048;
@@ -106,9 +106,10 @@ __global__ void __launch_bounds__(256) bwd_rowprep_kernel(AttnArgs a) {
 // One workgroup of four waves per pair of consecutive query blocks (as in the
 // forward): the pair walks the union of its block lists with the next key
 // tile in flight (direct global->LDS loads, double buffer), then the column
-// tiles of each block.  Per tile and wave: S^T = K Q^T, dP^T = V dO^T (bf16,
-// Q and dO rows in VGPRs), dQ^T += K^T dZ^T (fp16; K^T read transposed from
-// the fp16 copy of K).
+// tiles of each block.  Everything runs on the scaled fp16 copies (sq Q,
+// sk K, sv V, s dO; powers of two, folded back exactly).  Per tile and wave:
+// S^T = K Q^T, dP^T = V dO^T (K, V rows from LDS, Q and dO rows in VGPRs),
+// dQ^T += K^T dZ^T (K^T read transposed from the same K tile).
 constexpr int kDqThreads = 256;
 
 template <int D>
@@ -121,9 +122,10 @@ struct DqRows {
 
 // lims (LDS, or NULL for a tile without masking): key k visible to in-block
 // query row r iff r >= lims[k]; a rare uniform branch (see fwd_tile).
+// c2 = scale log2(e) / (sq sk); isv = 1 / sv (turns the dP^T accumulator into s dP^T)
 template <int D>
-__device__ __forceinline__ void dq_tile(const uint16_t* kt, const uint16_t* vt, const uint16_t* k16t,
-                                        const int32_t* lims, DqRows<D>& st, int qrow, int lane, float c2, float sc) {
+__device__ __forceinline__ void dq_tile(const uint16_t* kt, const uint16_t* vt, const int32_t* lims, DqRows<D>& st,
+                                        int qrow, int lane, float c2, float isv) {
     constexpr int KD = DqRows<D>::KD, ND = DqRows<D>::ND;
     const int h = lane >> 5, l32 = lane & 31;
     f32x16 sacc[2], pacc[2];
@@ -141,8 +143,8 @@ __device__ __forceinline__ void dq_tile(const uint16_t* kt, const uint16_t* vt, 
         for (int j = 0; j < 2; ++j)
 #pragma unroll
             for (int c = 0; c < 2; ++c) {
-                fk[set][j][c] = dma_read16<D, kRowPad>(kt, 32 * c + l32, h + 2 * (s0 + j));
-                fv[set][j][c] = dma_read16<D, kRowPad>(vt, 32 * c + l32, h + 2 * (s0 + j));
+                fk[set][j][c] = dma_read16<D, kDualPad>(kt, 32 * c + l32, h + 2 * (s0 + j));
+                fv[set][j][c] = dma_read16<D, kDualPad>(vt, 32 * c + l32, h + 2 * (s0 + j));
             }
     };
     read_group(0, 0);
@@ -155,8 +157,8 @@ __device__ __forceinline__ void dq_tile(const uint16_t* kt, const uint16_t* vt, 
         for (int j = 0; j < 2; ++j)
 #pragma unroll
             for (int c = 0; c < 2; ++c) {
-                sacc[c] = mfma32(fk[set][j][c], st.q[s0 + j], sacc[c]);
-                pacc[c] = mfma32(fv[set][j][c], st.g[s0 + j], pacc[c]);
+                sacc[c] = mfma32h(fk[set][j][c], st.q[s0 + j], sacc[c]);
+                pacc[c] = mfma32h(fv[set][j][c], st.g[s0 + j], pacc[c]);
             }
         __builtin_amdgcn_sched_barrier(0);
     }
@@ -169,7 +171,7 @@ __device__ __forceinline__ void dq_tile(const uint16_t* kt, const uint16_t* vt, 
         for (int ii = 0; ii < 2; ++ii)
 #pragma unroll
             for (int j = 0; j < 2; ++j)
-                ak[set][ii][j] = dma_read_tr<D, kTrPad>(k16t, 16 * (2 * c + j), 32 * (i0 + ii), lane);
+                ak[set][ii][j] = dma_read_tr<D, kDualPad>(kt, 16 * (2 * c + j), 32 * (i0 + ii), lane);
     };
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
@@ -177,7 +179,7 @@ __device__ __forceinline__ void dq_tile(const uint16_t* kt, const uint16_t* vt, 
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             const float p = fast_exp2(__builtin_fmaf(sacc[c][r], c2, -st.lse2));
-            sacc[c][r] = p * __builtin_fmaf(pacc[c][r], sc, -st.dlt);
+            sacc[c][r] = p * __builtin_fmaf(pacc[c][r], isv, -st.dlt);
         }
         if (lims) {
             keep_branch();
@@ -209,8 +211,8 @@ __device__ __forceinline__ void dq_tile(const uint16_t* kt, const uint16_t* vt, 
 template <int D>
 __global__ void __launch_bounds__(kDqThreads) __attribute__((amdgpu_waves_per_eu(1, 1))) bwd_dq_kernel(AttnArgs a) {
     constexpr int KD = DqRows<D>::KD, ND = DqRows<D>::ND;
-    constexpr int RE = DmaTile<D, kRowPad>::kElems, TE = DmaTile<D, kTrPad>::kElems;
-    __shared__ uint16_t k0s[RE], v0s[RE], t0s[TE], k1s[RE], v1s[RE], t1s[TE];
+    constexpr int TE = DmaTile<D, kDualPad>::kElems;
+    __shared__ uint16_t k0s[TE], v0s[TE], k1s[TE], v1s[TE];
     __shared__ int32_t kidx[64], lims[64], dlims[64];
     const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, l32 = lane & 31;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6), half = w >> 1;
@@ -228,16 +230,17 @@ __global__ void __launch_bounds__(kDqThreads) __attribute__((amdgpu_waves_per_eu
     const int32_t qg = ldc(a.q_blk_global, qb);
 
     const int64_t kvoff = (int64_t(b) * a.Hkv + hk) * int64_t(a.Nk) * D;
-    const uint16_t* __restrict__ kp = a.k + kvoff;
-    const uint16_t* __restrict__ vp = a.v + kvoff;
-    const uint16_t* __restrict__ k16p = a.k16 + kvoff;
+    const uint16_t* __restrict__ kp = a.k16 + kvoff;
+    const uint16_t* __restrict__ vp = a.v16 + kvoff;
     DqRows<D> st;
 #pragma unroll
     for (int s = 0; s < KD; ++s) {
-        st.q[s] = *reinterpret_cast<const u32x4*>(a.q + grow * D + 16 * s + 8 * h);
-        st.g[s] = *reinterpret_cast<const u32x4*>(a.dout + grow * D + 16 * s + 8 * h);
+        st.q[s] = *reinterpret_cast<const u32x4*>(a.q16 + grow * D + 16 * s + 8 * h);
+        st.g[s] = *reinterpret_cast<const u32x4*>(a.g16 + grow * D + 16 * s + 8 * h);
     }
-    const float c2 = a.scale * kLog2e;
+    const float sq = operand_scale(a.qkvmax), sk = operand_scale(a.qkvmax + 1);
+    const float isv = 1.f / operand_scale(a.qkvmax + 2);
+    const float c2 = a.scale * kLog2e / (sq * sk);
     st.lse2 = a.lse2[grow];
     const float sc = dout_scale(a.dmax);
     st.dlt = a.delta[grow];
@@ -263,24 +266,22 @@ __global__ void __launch_bounds__(kDqThreads) __attribute__((amdgpu_waves_per_eu
         diag = ldc(a.k_blk_global, kb) == qg;
         return true;
     };
-    auto load = [&](uint16_t* kt, uint16_t* vt, uint16_t* tt, auto rows) {
-        dma_rows<D, kRowPad, 4>(kt, kp, rows, w, lane);
-        dma_rows<D, kRowPad, 4>(vt, vp, rows, w, lane);
-        dma_rows<D, kTrPad, 4>(tt, k16p, rows, w, lane);
+    auto load = [&](uint16_t* kt, uint16_t* vt, auto rows) {
+        dma_rows<D, kDualPad, 4>(kt, kp, rows, w, lane);
+        dma_rows<D, kDualPad, 4>(vt, vp, rows, w, lane);
     };
     int32_t kb = 0;
     bool in0 = false, in1 = false, diag = false;
     bool have = next(kb, in0, in1, diag);
-    if (have) load(k0s, v0s, t0s, ContiguousRows{int64_t(kb) * 64});
+    if (have) load(k0s, v0s, ContiguousRows{int64_t(kb) * 64});
     wait_vmem();
     __syncthreads();
-    auto step = [&](const uint16_t* ck, const uint16_t* cv, const uint16_t* ct, uint16_t* nk, uint16_t* nv,
-                    uint16_t* nt) {
+    auto step = [&](const uint16_t* ck, const uint16_t* cv, uint16_t* nk, uint16_t* nv) {
         int32_t kb2 = 0;
         bool in0n = false, in1n = false, diagn = false;
         const bool more = next(kb2, in0n, in1n, diagn);
-        if (more) load(nk, nv, nt, ContiguousRows{int64_t(kb2) * 64});
-        if (half == 0 ? in0 : in1) dq_tile<D>(ck, cv, ct, diag ? dlims : nullptr, st, qrow, lane, c2, sc);
+        if (more) load(nk, nv, ContiguousRows{int64_t(kb2) * 64});
+        if (half == 0 ? in0 : in1) dq_tile<D>(ck, cv, diag ? dlims : nullptr, st, qrow, lane, c2, isv);
         wait_vmem();
         __syncthreads();
         kb = kb2;
@@ -290,9 +291,9 @@ __global__ void __launch_bounds__(kDqThreads) __attribute__((amdgpu_waves_per_eu
         have = more;
     };
     while (have) {
-        step(k0s, v0s, t0s, k1s, v1s, t1s);
+        step(k0s, v0s, k1s, v1s);
         if (!have) break;
-        step(k1s, v1s, t1s, k0s, v0s, t0s);
+        step(k1s, v1s, k0s, v0s);
     }
 
     // ---- column tiles, one half at a time
@@ -307,16 +308,16 @@ __global__ void __launch_bounds__(kDqThreads) __attribute__((amdgpu_waves_per_eu
                 lims[tid] = tid < cnt ? (a.k_blk_global[col >> 6] == qgj ? (col & 63) : 0) : 64;
             }
             __syncthreads();
-            load(k0s, v0s, t0s, IndexedRows{kidx});
+            load(k0s, v0s, IndexedRows{kidx});
             wait_vmem();
             __syncthreads();
-            if (half == j) dq_tile<D>(k0s, v0s, t0s, lims, st, qrow, lane, c2, sc);
+            if (half == j) dq_tile<D>(k0s, v0s, lims, st, qrow, lane, c2, isv);
             __syncthreads();
         }
     }
     if (!live) return;
     float* dq = a.dq + grow * D;
-    const float fin = a.scale / sc;
+    const float fin = a.scale / (sc * sk);
 #pragma unroll
     for (int i = 0; i < ND; ++i)
 #pragma unroll
@@ -333,16 +334,15 @@ __global__ void __launch_bounds__(kDqThreads) __attribute__((amdgpu_waves_per_eu
 }
 
 // ------------------------------------------------------------------ dK / dV (key-major)
-// A query tile as the key-major passes stage it (DMA tiles): bf16 Q and dO
-// rows for the first GEMMs, fp16 Q and s dO rows read transposed for the
+// A query tile as the key-major passes stage it (DMA tiles): the scaled fp16
+// Q and dO rows, read row-wise for the first GEMMs and transposed for the
 // second, and the rows' lse2 and s Delta (64 floats each).
 template <int D>
 struct KvTile {
-    static constexpr int kRow = DmaTile<D, kRowPad>::kElems;
-    static constexpr int kTr = DmaTile<D, kTrPad>::kElems;
-    static constexpr int kElems = 2 * kRow + 2 * kTr + 256;   // + 128 floats
+    static constexpr int kPart = DmaTile<D, kDualPad>::kElems;
+    static constexpr int kElems = 2 * kPart + 256;   // + 128 floats
     // element offsets of the parts
-    static constexpr int kQ = 0, kG = kRow, kQ16 = 2 * kRow, kG16 = 2 * kRow + kTr, kRw = 2 * kRow + 2 * kTr;
+    static constexpr int kQ16 = 0, kG16 = kPart, kRw = 2 * kPart;
 };
 
 // Issue the loads of query tile (bh, qb) into tile `t` (NW waves).
@@ -352,10 +352,8 @@ __device__ __forceinline__ void kv_load_query_tile(uint16_t* t, const AttnArgs& 
     using T = KvTile<D>;
     const int64_t row0 = int64_t(bh) * a.Nq + int64_t(qb) * 64;
     const ContiguousRows rows{row0};
-    dma_rows<D, kRowPad, NW>(t + T::kQ, a.q, rows, wave, lane);
-    dma_rows<D, kRowPad, NW>(t + T::kG, a.dout, rows, wave, lane);
-    dma_rows<D, kTrPad, NW>(t + T::kQ16, a.q16, rows, wave, lane);
-    dma_rows<D, kTrPad, NW>(t + T::kG16, a.g16, rows, wave, lane);
+    dma_rows<D, kDualPad, NW>(t + T::kQ16, a.q16, rows, wave, lane);
+    dma_rows<D, kDualPad, NW>(t + T::kG16, a.g16, rows, wave, lane);
     if (wave == 0 && lane < 32) {   // lse2 -> floats 0..63, s Delta -> floats 64..127
         const float* src = lane < 16 ? a.lse2 + row0 + 4 * lane : a.delta + row0 + 4 * (lane - 16);
         dma16(src, lds_addr(t + T::kRw));
@@ -363,13 +361,14 @@ __device__ __forceinline__ void kv_load_query_tile(uint16_t* t, const AttnArgs& 
 }
 
 // One 64-row query tile against this wave's 32 keys (`key` = this lane's key
-// inside the 64-key block).  lims (LDS, or NULL for a tile without masking):
+// inside the 64-key block; kreg, vreg its scaled fp16 K and V rows).  c2 =
+// scale log2(e) / (sq sk); isv = 1 / sv turns the dP accumulator into s dP.  lims (LDS, or NULL for a tile without masking):
 // the key is visible to in-block query row r iff r >= lims[key] (64: not
 // visible); a rare uniform branch whose limit comes from LDS, so nothing of
 // it is hoisted into the loop.
 template <int D>
 __device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, const u32x4* vreg, const int32_t* lims,
-                                        int key, float c2, float sc, int lane, f32x16* dv, f32x16* dk) {
+                                        int key, float c2, float isv, int lane, f32x16* dv, f32x16* dk) {
     using T = KvTile<D>;
     constexpr int KD = D / 16, ND = D / 32;
     const int h = lane >> 5, l32 = lane & 31;
@@ -392,8 +391,8 @@ __device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, co
         for (int j = 0; j < 2; ++j)
 #pragma unroll
             for (int rb = 0; rb < 2; ++rb) {
-                fq[set][j][rb] = dma_read16<D, kRowPad>(t + T::kQ, 32 * rb + l32, h + 2 * (s0 + j));
-                fg[set][j][rb] = dma_read16<D, kRowPad>(t + T::kG, 32 * rb + l32, h + 2 * (s0 + j));
+                fq[set][j][rb] = dma_read16<D, kDualPad>(t + T::kQ16, 32 * rb + l32, h + 2 * (s0 + j));
+                fg[set][j][rb] = dma_read16<D, kDualPad>(t + T::kG16, 32 * rb + l32, h + 2 * (s0 + j));
             }
     };
     read_group(0, 0);
@@ -406,8 +405,8 @@ __device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, co
         for (int j = 0; j < 2; ++j)
 #pragma unroll
             for (int rb = 0; rb < 2; ++rb) {
-                sacc[rb] = mfma32(fq[set][j][rb], kreg[s0 + j], sacc[rb]);
-                pacc[rb] = mfma32(fg[set][j][rb], vreg[s0 + j], pacc[rb]);
+                sacc[rb] = mfma32h(fq[set][j][rb], kreg[s0 + j], sacc[rb]);
+                pacc[rb] = mfma32h(fg[set][j][rb], vreg[s0 + j], pacc[rb]);
             }
         __builtin_amdgcn_sched_barrier(0);
     }
@@ -422,8 +421,8 @@ __device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, co
     auto read_tr = [&](int set, int rb, int i) {
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
-            av[set][j] = dma_read_tr<D, kTrPad>(t + T::kG16, 16 * (2 * rb + j), 32 * i, lane);
-            ak[set][j] = dma_read_tr<D, kTrPad>(t + T::kQ16, 16 * (2 * rb + j), 32 * i, lane);
+            av[set][j] = dma_read_tr<D, kDualPad>(t + T::kG16, 16 * (2 * rb + j), 32 * i, lane);
+            ak[set][j] = dma_read_tr<D, kDualPad>(t + T::kQ16, 16 * (2 * rb + j), 32 * i, lane);
         }
     };
 #pragma unroll
@@ -439,7 +438,7 @@ __device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, co
                 const int r = 4 * q4 + e;
                 const float p = fast_exp2(__builtin_fmaf(sacc[rb][r], c2, -l4[e]));
                 sacc[rb][r] = p;
-                pacc[rb][r] = p * __builtin_fmaf(pacc[rb][r], sc, -d4[e]);
+                pacc[rb][r] = p * __builtin_fmaf(pacc[rb][r], isv, -d4[e]);
             }
         }
         if (lims) {
@@ -505,8 +504,8 @@ __global__ void __launch_bounds__(kKvThreads) __attribute__((amdgpu_waves_per_eu
     u32x4 kreg[KD], vreg[KD];
 #pragma unroll
     for (int s = 0; s < KD; ++s) {
-        kreg[s] = *reinterpret_cast<const u32x4*>(a.k + krow * D + 16 * s + 8 * h);
-        vreg[s] = *reinterpret_cast<const u32x4*>(a.v + krow * D + 16 * s + 8 * h);
+        kreg[s] = *reinterpret_cast<const u32x4*>(a.k16 + krow * D + 16 * s + 8 * h);
+        vreg[s] = *reinterpret_cast<const u32x4*>(a.v16 + krow * D + 16 * s + 8 * h);
     }
     f32x16 dv[ND], dk[ND];
 #pragma unroll
@@ -514,7 +513,9 @@ __global__ void __launch_bounds__(kKvThreads) __attribute__((amdgpu_waves_per_eu
         dv[i] = f32x16{};
         dk[i] = f32x16{};
     }
-    const float c2 = a.scale * kLog2e;
+    const float sq = operand_scale(a.qkvmax), sk = operand_scale(a.qkvmax + 1);
+    const float isv = 1.f / operand_scale(a.qkvmax + 2);
+    const float c2 = a.scale * kLog2e / (sq * sk);
     const float sc = dout_scale(a.dmax);
     const int32_t kg = ldc(a.k_blk_global, kb);
 
@@ -558,7 +559,7 @@ __global__ void __launch_bounds__(kKvThreads) __attribute__((amdgpu_waves_per_eu
         bool in0n = false, in1n = false, diagn = false;
         const bool more = next(bh2, qb2, in0n, in1n, diagn);
         if (more) kv_load_query_tile<D, 4>(nt, a, bh2, qb2, w, lane);
-        if (half == 0 ? in0 : in1) kv_tile<D>(ct, kreg, vreg, diag ? dlims : nullptr, key, c2, sc, lane, dv, dk);
+        if (half == 0 ? in0 : in1) kv_tile<D>(ct, kreg, vreg, diag ? dlims : nullptr, key, c2, isv, lane, dv, dk);
         wait_vmem();
         __syncthreads();
         bh = bh2;
@@ -576,7 +577,7 @@ __global__ void __launch_bounds__(kKvThreads) __attribute__((amdgpu_waves_per_eu
     if (!live) return;
     float* dkp = a.dk + krow * D;
     float* dvp = a.dv + krow * D;
-    const float fk = a.scale / sc, fv = 1.f / sc;
+    const float fk = a.scale / (sc * sq), fv = 1.f / sc;
 #pragma unroll
     for (int i = 0; i < ND; ++i)
 #pragma unroll
@@ -734,8 +735,8 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1
     u32x4 kreg[KD], vreg[KD];
 #pragma unroll
     for (int s = 0; s < KD; ++s) {
-        kreg[s] = *reinterpret_cast<const u32x4*>(a.k + krow * D + 16 * s + 8 * h);
-        vreg[s] = *reinterpret_cast<const u32x4*>(a.v + krow * D + 16 * s + 8 * h);
+        kreg[s] = *reinterpret_cast<const u32x4*>(a.k16 + krow * D + 16 * s + 8 * h);
+        vreg[s] = *reinterpret_cast<const u32x4*>(a.v16 + krow * D + 16 * s + 8 * h);
     }
     f32x16 dv[ND], dk[ND];
 #pragma unroll
@@ -743,7 +744,9 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1
         dv[i] = f32x16{};
         dk[i] = f32x16{};
     }
-    const float c2 = a.scale * kLog2e;
+    const float sq = operand_scale(a.qkvmax), sk = operand_scale(a.qkvmax + 1);
+    const float isv = 1.f / operand_scale(a.qkvmax + 2);
+    const float c2 = a.scale * kLog2e / (sq * sk);
     const float sc = dout_scale(a.dmax);
     const uint32_t* db = a.diag_bits + int64_t(bh) * a.dwords;
     for (int qb = qb0; qb < qb1; ++qb) {
@@ -756,14 +759,14 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1
         kv_load_query_tile<D, 2>(ts, a, bh, qb, w, lane);
         wait_vmem();
         __syncthreads();
-        kv_tile<D>(ts, kreg, vreg, clims, key, c2, sc, lane, dv, dk);
+        kv_tile<D>(ts, kreg, vreg, clims, key, c2, isv, lane, dv, dk);
         __syncthreads();
     }
     if (!valid) return;
     const int64_t slot = int64_t(item) * 64 + key;
     float* dkp = a.dk_col + slot * D;
     float* dvp = a.dv_col + slot * D;
-    const float fk = a.scale / sc, fv = 1.f / sc;
+    const float fk = a.scale / (sc * sq), fv = 1.f / sc;
 #pragma unroll
     for (int i = 0; i < ND; ++i)
 #pragma unroll
@@ -840,14 +843,19 @@ hipError_t launch_bwd_d(const AttnArgs& a, hipStream_t s) {
         hipLaunchKernelGGL(bwd_rowprep_kernel, dim3(unsigned(want < kDeltaBlocks ? want : int64_t(kDeltaBlocks))),
                            dim3(256), 0, s, a);
     }
+    // scaled fp16 copies: Q, K, V to max in [2^14, 2^15), dO to [8, 16)
     const int64_t nkv = int64_t(a.B) * a.Hkv * a.Nk * a.d;
-    if ((e = launch_to_f16(a.k, a.k16, nkv, nullptr, s)) != hipSuccess) return e;
+    const int64_t nq = int64_t(a.B) * a.Hq * a.Nq * a.d;
+    if ((e = launch_absmax(a.q, nq, a.qkvmax, s)) != hipSuccess) return e;
+    if ((e = launch_absmax(a.k, nkv, a.qkvmax + 1, s)) != hipSuccess) return e;
+    if ((e = launch_absmax(a.v, nkv, a.qkvmax + 2, s)) != hipSuccess) return e;
+    if ((e = launch_to_f16(a.q, a.q16, nq, a.qkvmax, kOperandExp, s)) != hipSuccess) return e;
+    if ((e = launch_to_f16(a.k, a.k16, nkv, a.qkvmax + 1, kOperandExp, s)) != hipSuccess) return e;
+    if ((e = launch_to_f16(a.v, a.v16, nkv, a.qkvmax + 2, kOperandExp, s)) != hipSuccess) return e;
+    if ((e = launch_to_f16(a.dout, a.g16, nq, a.dmax, 4, s)) != hipSuccess) return e;
     const int64_t qgrid = int64_t(a.B) * a.Hq * ((a.nqb + 1) / 2);
     if (qgrid > 0) { TraceScope _t("bwd_dq", s); hipLaunchKernelGGL(bwd_dq_kernel<D>, dim3(unsigned(qgrid)), dim3(kDqThreads), 0, s, a); }
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    const int64_t nq = int64_t(a.B) * a.Hq * a.Nq * a.d;
-    if ((e = launch_to_f16(a.q, a.q16, nq, nullptr, s)) != hipSuccess) return e;
-    if ((e = launch_to_f16(a.dout, a.g16, nq, a.dmax, s)) != hipSuccess) return e;
     const int64_t kpgrid = int64_t(a.B) * a.Hkv * ((a.nkb + 1) / 2);
     if (kpgrid > 0) { TraceScope _t("bwd_dkdv", s); hipLaunchKernelGGL(bwd_dkdv_kernel<D>, dim3(unsigned(kpgrid)), dim3(kKvThreads), 0, s, a); }
     if ((e = hipGetLastError()) != hipSuccess) return e;

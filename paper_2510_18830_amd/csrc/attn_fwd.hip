@@ -17,8 +17,9 @@
 //                      B = P straight from the S^T accumulator; this product
 //                      runs in fp16, whose 3 extra significand bits keep the
 //                      rounding of P well below the output tolerance at the
-//                      same MFMA rate; the fp16 copy of V is made once per
-//                      call by a conversion pass).
+//                      same MFMA rate; the fp16 copy of V, times a power of
+//                      two sv from max |V|, is made once per call by a
+//                      conversion pass and 1/sv applied at the end).
 // Scores use exp2 with scale * log2(e) folded in; lse is stored as a natural log.
 #include "common.h"
 #include "kernels.h"
@@ -265,9 +266,10 @@ attn_fwd_kernel(AttnArgs a) {
     }
     if (!live) return;
 
-    // ---- epilogue: normalise, store bf16 out and natural-log lse
+    // ---- epilogue: normalise (V carried the factor sv), store bf16 out and
+    // natural-log lse
     const bool empty = !(st.l > 0.f);
-    const float inv = empty ? 0.f : 1.f / st.l;
+    const float inv = empty ? 0.f : 1.f / (st.l * operand_scale(a.qkvmax + 2));
     const int64_t orow = (int64_t(bh) * a.Nq + int64_t(qb) * 64 + qrow) * D;
 #pragma unroll
     for (int i = 0; i < ND; ++i)
@@ -290,6 +292,10 @@ attn_fwd_kernel(AttnArgs a) {
         float* lp = a.lse + int64_t(bh) * a.Nq + int64_t(qb) * 64 + qrow;
         *lp = empty ? -INFINITY : (st.m + fast_log2(st.l)) * kLn2;
     }
+}
+
+__global__ void fwd_prep_kernel(AttnArgs a) {
+    if (threadIdx.x == 0) a.qkvmax[2] = 0u;
 }
 
 __global__ void merge_kernel(MergeArgs m) {
@@ -337,6 +343,12 @@ __global__ void merge_kernel(MergeArgs m) {
 hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t s) {
     const int64_t grid = int64_t(a.B) * a.Hq * ((a.nqb + 1) / 2);
     if (grid == 0) return hipSuccess;
+    // fp16 copy of V times a power of two from max |V|
+    hipLaunchKernelGGL(fwd_prep_kernel, dim3(1), dim3(64), 0, s, a);
+    const int64_t nkv = int64_t(a.B) * a.Hkv * a.Nk * a.d;
+    hipError_t e = launch_absmax(a.v, nkv, a.qkvmax + 2, s);
+    if (e == hipSuccess) e = launch_to_f16(a.v, a.v16, nkv, a.qkvmax + 2, kOperandExp, s);
+    if (e != hipSuccess) return e;
     if (a.d == 128)
         { TraceScope _t("attn_fwd", s); hipLaunchKernelGGL(attn_fwd_kernel<128>, dim3(unsigned(grid)), dim3(kFwdThreads), 0, s, a); }
     else

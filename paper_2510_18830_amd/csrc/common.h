@@ -107,13 +107,22 @@ __device__ __forceinline__ float wave_sum(float v) {
 
 // Power-of-two factor s with max |s x| in [8, 16) given max |x| as fp32 bits;
 // 1 for zero or non-finite input.
-__device__ __forceinline__ float pow2_scale(const uint32_t* maxbits) {
+// Power of two s with max * s in [2^(E-1), 2^E), from the fp32 bits of a
+// non-negative max (1 when it is 0 or not finite).  Multiplying by s is exact.
+template <int E>
+__device__ __forceinline__ float pow2_scale_to(const uint32_t* maxbits) {
     const float mx = __uint_as_float(*maxbits);
     if (!(mx > 0.f) || !isfinite(mx)) return 1.f;
     int e;
     frexpf(mx, &e);           // mx = f 2^e, f in [0.5, 1)
-    return ldexpf(1.f, max(-100, min(100, 4 - e)));
+    return ldexpf(1.f, max(-100, min(100, E - e)));
 }
+// dO: max |s dO| in [8, 16), so s dP, s Delta and s dZ stay inside fp16
+__device__ __forceinline__ float pow2_scale(const uint32_t* maxbits) { return pow2_scale_to<4>(maxbits); }
+// fp16 copies of Q, K, V: max in [2^14, 2^15) (exact conversion of every bf16
+// value down to 2^-29 of the max; products stay far inside fp32)
+constexpr int kOperandExp = 15;
+__device__ __forceinline__ float operand_scale(const uint32_t* maxbits) { return pow2_scale_to<kOperandExp>(maxbits); }
 
 // ---------------------------------------------------------------- ring layout
 // Global 64-token blocks are dealt to `world` workers (Section 4.2).

@@ -67,6 +67,7 @@ struct AttnArgs {
     float* out_f32;        // optional fp32 copy of out (fwd)
     const float* o_f32;    // optional fp32 forward output for Delta (bwd)
     uint32_t* dmax;        // bwd workspace: max |dO| as fp32 bits
+    uint32_t* qkvmax;      // workspace: max |Q|, |K|, |V| as fp32 bits (the fwd uses [2])
     float* lse;            // fwd output / bwd input
     float* delta;          // bwd workspace [B,Hq,Nq]: Delta, then s * Delta after row prep
     float* lse2;           // bwd workspace [B,Hq,Nq]: lse * log2(e) (+inf for a row without keys)
@@ -104,9 +105,14 @@ struct AttnArgs {
     const int32_t* k_blk_global;
 };
 hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t s);
-// dst = fp16(src * mul) for n bf16 elements (n a multiple of 8); mul = 1, or
-// the power of two pow2_scale(maxbits) when maxbits is not NULL
-hipError_t launch_to_f16(const uint16_t* src, uint16_t* dst, int64_t n, const uint32_t* maxbits, hipStream_t s);
+// *maxbits = max(*maxbits, max |src|) as fp32 bits, n bf16 elements (n a
+// multiple of 8)
+hipError_t launch_absmax(const uint16_t* src, int64_t n, uint32_t* maxbits, hipStream_t s);
+// dst = fp16(src * mul) for n bf16 elements (n a multiple of 8); mul = 1 when
+// maxbits is NULL, else the power of two pow2_scale_to<exp>(maxbits) (exp 4
+// for dO, kOperandExp for Q, K, V)
+hipError_t launch_to_f16(const uint16_t* src, uint16_t* dst, int64_t n, const uint32_t* maxbits, int exp,
+                         hipStream_t s);
 hipError_t launch_attn_bwd(const AttnArgs& a, hipStream_t s);
 // Backward column pass: a chunk is 64 consecutive entries of one head's
 // vertical list; its candidate query blocks (a suffix of the local blocks) are

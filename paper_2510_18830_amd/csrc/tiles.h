@@ -78,6 +78,8 @@ struct DmaTile {
 };
 constexpr int kRowPad = 16;   // tiles read row-wise
 constexpr int kTrPad = 64;    // tiles read through transposing loads
+constexpr int kDualPad = 48;  // tiles read both ways (48 g mod 256 is distinct for
+                              // g = 0..15, and 4 groups x 64 bytes do not overlap)
 
 typedef __attribute__((address_space(3))) void* lds_void_ptr;
 
