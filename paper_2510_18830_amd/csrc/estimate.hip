@@ -69,8 +69,10 @@ __global__ void __launch_bounds__(kThreads) est_pass1_kernel(EstArgs a) {
     __shared__ Pass1Lds<D> sm;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, l32 = lane & 31;
     const int nb = a.N / kBlock;
-    const int bh = blockIdx.x / a.nchunk;
-    const int chunk = blockIdx.x % a.nchunk;
+    // KV-group-major order, XCD-chunked: the group's heads read each K chunk
+    // together from one L2
+    int bh, chunk;
+    query_tile_of(blockIdx.x, a.B, a.Hq, a.Hkv, a.nchunk, bh, chunk);
     const int b = bh / a.Hq, hq = bh % a.Hq, hk = hq / (a.Hq / a.Hkv);
     const int row = 32 * w + l32;   // in the last block
     const uint16_t* qp = a.q + (int64_t(bh) * a.N + a.N - kBlock + row) * D;
@@ -125,17 +127,31 @@ __global__ void __launch_bounds__(kThreads) est_pass1_kernel(EstArgs a) {
     }
 }
 
-__global__ void __launch_bounds__(64) est_combine_kernel(EstArgs a) {
-    const int bh = blockIdx.x, r = threadIdx.x;
+// One workgroup per head: thread (r, j) reduces chunks j, j + 16, ... of row
+// r; the 16 partials of a row are combined in a fixed order.
+constexpr int kCombineSplit = 16;
+__global__ void __launch_bounds__(64 * kCombineSplit) est_combine_kernel(EstArgs a) {
+    __shared__ float pm_s[kCombineSplit][64], ps_s[kCombineSplit][64];
+    const int bh = blockIdx.x, r = threadIdx.x & 63, j = threadIdx.x >> 6;
     float M = -INFINITY;
-    for (int c = 0; c < a.nchunk; ++c) M = fmaxf(M, a.part_max[(int64_t(bh) * a.nchunk + c) * kBlock + r]);
+    for (int c = j; c < a.nchunk; c += kCombineSplit) M = fmaxf(M, a.part_max[(int64_t(bh) * a.nchunk + c) * kBlock + r]);
     float S = 0.f;
-    for (int c = 0; c < a.nchunk; ++c) {
+    for (int c = j; c < a.nchunk; c += kCombineSplit) {
         const int64_t o = (int64_t(bh) * a.nchunk + c) * kBlock + r;
         const float pm = a.part_max[o];
         if (pm != -INFINITY) S += a.part_sum[o] * fast_exp2(pm - M);
     }
-    a.row_lse[bh * kBlock + r] = M + fast_log2(S);
+    pm_s[j][r] = M;
+    ps_s[j][r] = S;
+    __syncthreads();
+    if (j == 0) {
+        float MM = -INFINITY;
+        for (int t = 0; t < kCombineSplit; ++t) MM = fmaxf(MM, pm_s[t][r]);
+        float SS = 0.f;
+        for (int t = 0; t < kCombineSplit; ++t)
+            if (pm_s[t][r] != -INFINITY) SS += ps_s[t][r] * fast_exp2(pm_s[t][r] - MM);
+        a.row_lse[bh * kBlock + r] = MM + fast_log2(SS);
+    }
 }
 
 template <int D>
@@ -151,8 +167,8 @@ __global__ void __launch_bounds__(kThreads) est_pass2_kernel(EstArgs a) {
     __shared__ Pass2Lds<D> sm;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, l32 = lane & 31;
     const int nb = a.N / kBlock;
-    const int bh = blockIdx.x / a.nchunk;
-    const int chunk = blockIdx.x % a.nchunk;
+    int bh, chunk;   // order as in pass 1
+    query_tile_of(blockIdx.x, a.B, a.Hq, a.Hkv, a.nchunk, bh, chunk);
     const int b = bh / a.Hq, hq = bh % a.Hq, hk = hq / (a.Hq / a.Hkv);
     // A operand: this wave's 32 query rows
     const uint16_t* qp = a.q + (int64_t(bh) * a.N + a.N - kBlock + 32 * w + l32) * D;
@@ -225,52 +241,55 @@ __global__ void __launch_bounds__(256) est_diag_kernel(EstArgs a) {
 // ---------------------------------------------------------------- top-k
 constexpr int kTopkThreads = 1024;
 
-__device__ int64_t block_excl_scan(int64_t v, int64_t* tmp, int64_t* total) {
-    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-    int64_t x = v;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const int64_t y = __shfl_up(x, o);
-        if (lane >= o) x += y;
-    }
-    if (lane == 63) tmp[wid] = x;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        int64_t run = 0;
-        for (int k = 0; k < kTopkThreads / 64; ++k) {
-            const int64_t t = tmp[k];
-            tmp[k] = run;
-            run += t;
-        }
-        tmp[16] = run;
-    }
-    __syncthreads();
-    const int64_t r = tmp[wid] + x - v;
-    *total = tmp[16];
-    __syncthreads();
-    return r;
-}
 
+// Histograms are private per wave (16 copies, stride 257 words so the copies
+// sit on different banks): scores of one list share few exponents, and one
+// shared histogram would serialise nearly every atomic on the same bins.
+// Scores are read 4 at a time (16-byte loads, N % 64 == 0), several loads in
+// flight per thread.
+constexpr int kHistStride = 257;
+constexpr int kTopkWaves = kTopkThreads / 64;
 __global__ void __launch_bounds__(kTopkThreads) est_topk_kernel(EstArgs a) {
+    __shared__ uint32_t whist[kTopkWaves * kHistStride];
     __shared__ uint32_t hist[256];
-    __shared__ int64_t tmp[17];
     __shared__ uint32_t s_prefix, s_krem;
+    __shared__ int64_t wgt[kTopkWaves], weq[kTopkWaves];
     const int BH = a.B * a.Hq;
     const bool is_v = blockIdx.x < BH;
     const int bh = is_v ? blockIdx.x : blockIdx.x - BH;
     const int k = is_v ? a.k_v : a.k_s;
     const uint32_t* sc = reinterpret_cast<const uint32_t*>((is_v ? a.v_score : a.s_score) + int64_t(bh) * a.N);
     int32_t* out = (is_v ? a.v_idx : a.s_idx) + int64_t(bh) * k;
-    const int tid = threadIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int N = a.N;
+    const int n4 = N / 4;
+    const u32x4* sc4 = reinterpret_cast<const u32x4*>(sc);
 
     uint32_t prefix = 0, mask = 0, krem = uint32_t(k);
     for (int shift = 24; shift >= 0; shift -= 8) {
-        for (int i = tid; i < 256; i += kTopkThreads) hist[i] = 0;
+        for (int i = tid; i < kTopkWaves * kHistStride; i += kTopkThreads) whist[i] = 0;
         __syncthreads();
-        for (int i = tid; i < N; i += kTopkThreads) {
-            const uint32_t x = sc[i];
-            if ((x & mask) == prefix) atomicAdd(&hist[(x >> shift) & 255u], 1u);
+        uint32_t* wh = whist + wv * kHistStride;
+        for (int i0 = tid; i0 < n4; i0 += 4 * kTopkThreads) {
+            u32x4 x[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int i = i0 + u * kTopkThreads;
+                x[u] = i < n4 ? sc4[i] : u32x4{~0u, ~0u, ~0u, ~0u};
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                if (i0 + u * kTopkThreads >= n4) break;
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if ((x[u][e] & mask) == prefix) atomicAdd(&wh[(x[u][e] >> shift) & 255u], 1u);
+            }
+        }
+        __syncthreads();
+        for (int bb = tid; bb < 256; bb += kTopkThreads) {
+            uint32_t t = 0;
+            for (int w = 0; w < kTopkWaves; ++w) t += whist[w * kHistStride + bb];
+            hist[bb] = t;
         }
         __syncthreads();
         if (tid == 0) {
@@ -293,26 +312,39 @@ __global__ void __launch_bounds__(kTopkThreads) est_topk_kernel(EstArgs a) {
         __syncthreads();
     }
     // prefix = bit pattern of the k-th largest; take all above it and the
-    // first krem equal ones, in index order
-    const int per = (N + kTopkThreads - 1) / kTopkThreads;
-    const int i0 = min(N, tid * per), i1 = min(N, i0 + per);
+    // first krem equal ones, in index order.  Wave wv owns the contiguous
+    // slice [wv C, (wv + 1) C) and reads it 64 scores at a time (coalesced);
+    // ballots give the counts and ranks, one scan over the waves the offsets.
+    const int C = ((N + kTopkWaves * 64 - 1) / (kTopkWaves * 64)) * 64;
+    const int lo = wv * C, hi = min(N, lo + C);
+    const uint64_t below = (1ull << lane) - 1ull;
     int64_t gt = 0, eq = 0;
-    for (int i = i0; i < i1; ++i) {
-        const uint32_t x = sc[i];
-        gt += x > prefix;
-        eq += x == prefix;
+    for (int i0 = lo; i0 < hi; i0 += 64) {
+        const int i = i0 + lane;
+        const uint32_t x = i < hi ? sc[i] : 0u;
+        gt += __popcll(__ballot(i < hi && x > prefix));
+        eq += __popcll(__ballot(i < hi && x == prefix));
     }
-    int64_t tot;
-    const int64_t eq_before = block_excl_scan(eq, tmp, &tot);
-    const int64_t eq_take = max<int64_t>(0, min<int64_t>(eq, int64_t(krem) - eq_before));
-    int64_t pos = block_excl_scan(gt + eq_take, tmp, &tot);
-    int64_t taken_eq = 0;
-    for (int i = i0; i < i1; ++i) {
-        const uint32_t x = sc[i];
-        if (x > prefix || (x == prefix && taken_eq < eq_take)) {
-            if (x == prefix) ++taken_eq;
-            out[pos++] = i;
-        }
+    if (lane == 0) {
+        wgt[wv] = gt;
+        weq[wv] = eq;
+    }
+    __syncthreads();
+    int64_t off = 0, eq_before = 0;
+    for (int w = 0; w < wv; ++w) {
+        off += wgt[w] + min<int64_t>(weq[w], max<int64_t>(0, int64_t(krem) - eq_before));
+        eq_before += weq[w];
+    }
+    for (int i0 = lo; i0 < hi; i0 += 64) {
+        const int i = i0 + lane;
+        const uint32_t x = i < hi ? sc[i] : 0u;
+        const bool e = i < hi && x == prefix;
+        const uint64_t me = __ballot(e);
+        const bool take = (i < hi && x > prefix) || (e && eq_before + __popcll(me & below) < int64_t(krem));
+        const uint64_t mt = __ballot(take);
+        if (take) out[off + __popcll(mt & below)] = i;
+        off += __popcll(mt);
+        eq_before += __popcll(me);
     }
 }
 
@@ -320,7 +352,7 @@ template <int D>
 hipError_t launch_d(const EstArgs& a, hipStream_t s) {
     const int BH = a.B * a.Hq;
     { TraceScope _t("est_pass1", s); hipLaunchKernelGGL(est_pass1_kernel<D>, dim3(BH * a.nchunk), dim3(kThreads), 0, s, a); }
-    { TraceScope _t("est_combine", s); hipLaunchKernelGGL(est_combine_kernel, dim3(BH), dim3(64), 0, s, a); }
+    { TraceScope _t("est_combine", s); hipLaunchKernelGGL(est_combine_kernel, dim3(BH), dim3(64 * kCombineSplit), 0, s, a); }
     { TraceScope _t("est_pass2", s); hipLaunchKernelGGL(est_pass2_kernel<D>, dim3(BH * a.nchunk), dim3(kThreads), 0, s, a); }
     const int64_t n = int64_t(BH) * a.N;
     { TraceScope _t("est_diag", s); hipLaunchKernelGGL(est_diag_kernel, dim3(unsigned((n + 255) / 256)), dim3(256), 0, s, a); }
