@@ -213,12 +213,18 @@ __global__ void __launch_bounds__(kThreads) est_pass2_kernel(EstArgs a) {
         __syncthreads();
         if (tid < 64) a.v_score[int64_t(bh) * a.N + int64_t(j) * kBlock + tid] = sm.col[0][tid] + sm.col[1][tid];
         if (tid < 127) {
-            // delta_local = r - c = tid - 63
+            // delta_local = r - c = tid - 63: a fixed 64-step walk, masked at
+            // the ends, four accumulators (the reads pipeline; neighbouring
+            // threads read neighbouring words)
             const int dl = tid - 63;
-            const int r0 = max(0, dl), r1 = min(63, 63 + dl);
-            float s = 0.f;
-            for (int r = r0; r <= r1; ++r) s += sm.p[r][r - dl];
-            a.diag_part[(int64_t(bh) * nb + j) * 128 + tid] = s;
+            float s4[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int r = 0; r < 64; ++r) {
+                const int c = r - dl;
+                const float v = sm.p[r][c & 63];
+                s4[r & 3] += (c >= 0 && c < 64) ? v : 0.f;
+            }
+            a.diag_part[(int64_t(bh) * nb + j) * 128 + tid] = (s4[0] + s4[1]) + (s4[2] + s4[3]);
         }
         __syncthreads();
     }
