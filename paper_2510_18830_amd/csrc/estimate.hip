@@ -255,6 +255,27 @@ constexpr int kTopkThreads = 1024;
 // flight per thread.
 constexpr int kHistStride = 257;
 constexpr int kTopkWaves = kTopkThreads / 64;
+
+// Adds 1 to bin `bin` of the wave's histogram for every lane with `on`.  The
+// lanes sharing the first pending lane's bin are counted with a ballot and
+// added by one lane, up to 4 rounds (the scores of a list share few
+// exponents, so most digits fall in a handful of bins); the rest add singly.
+__device__ __forceinline__ void hist_add(uint32_t* wh, uint32_t bin, bool on) {
+    const int lane = threadIdx.x & 63;
+    bool pending = on;
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+        const uint64_t pm = __ballot(pending);
+        if (pm == 0) return;
+        const int first = __builtin_ctzll(pm);
+        const uint32_t lb = uint32_t(__shfl(int(bin), first));
+        const bool same = pending && bin == lb;
+        const uint64_t sm = __ballot(same);
+        if (lane == first) atomicAdd(&wh[lb], uint32_t(__popcll(sm)));
+        pending = pending && !same;
+    }
+    if (pending) atomicAdd(&wh[bin], 1u);
+}
 __global__ void __launch_bounds__(kTopkThreads) est_topk_kernel(EstArgs a) {
     __shared__ uint32_t whist[kTopkWaves * kHistStride];
     __shared__ uint32_t hist[256];
@@ -285,10 +306,9 @@ __global__ void __launch_bounds__(kTopkThreads) est_topk_kernel(EstArgs a) {
             }
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
-                if (i0 + u * kTopkThreads >= n4) break;
+                const bool in = i0 + u * kTopkThreads < n4;
 #pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    if ((x[u][e] & mask) == prefix) atomicAdd(&wh[(x[u][e] >> shift) & 255u], 1u);
+                for (int e = 0; e < 4; ++e) hist_add(wh, (x[u][e] >> shift) & 255u, in && (x[u][e] & mask) == prefix);
             }
         }
         __syncthreads();
