@@ -62,6 +62,42 @@ def hbm_traffic(workload: str, kernel: str):
     return table.get(kernel)
 
 
+def estimation_and_index_report(r) -> dict:
+    """Estimation and index build against their rooflines.  Estimation: HBM
+    fraction on algorithmic bytes (K once, the last query rows, the two score
+    vectors written and read back, the selected indices), MFMA fraction on the
+    two passes' FLOPs, and the measured HBM bytes of the estimation kernels
+    from the committed counters (None when stale).  Index: HBM fraction on the
+    bytes it reads (index lists) and writes (CSR entries and offsets)."""
+    wl = r["wl"]
+    B, Hq, Hkv, N, d, L = wl.batch, wl.heads_q, wl.heads_kv, wl.seq, wl.head_dim, wl.last_q
+    est_bytes = (B * Hkv * N * d * 2 + B * Hq * L * d * 2 + 2 * (2 * B * Hq * N * 4)
+                 + B * Hq * (wl.k_v + wl.k_s) * 4)
+    est_flops = 2 * 2.0 * L * B * Hq * N * d
+    t_est = r["stage_ms"]["estimate"] * 1e-3
+    measured = None
+    names = [f"est_pass1_kernel<{d}>", f"est_pass2_kernel<{d}>", "est_combine_kernel", "est_diag_kernel",
+             "est_topk_kernel"]
+    vals = [hbm_traffic(wl.name, n) for n in names]
+    if all(v is not None for v in vals):
+        measured = round(sum(vals))
+    nqb = N // 64
+    idx_bytes = (B * Hq * (wl.k_v + wl.k_s) * 4                       # read the selected indices
+                 + 4 * (2 * r["T"] + r["C"] + r["vcol"])             # block, transposed, column, vertical entries
+                 + 8 * (2 * B * Hq * nqb + B * Hq * (N // 64) + B * Hq))   # offsets
+    t_idx = r["stage_ms"]["index"] * 1e-3
+    return {
+        "estimation_ms": round(t_est * 1e3, 3),
+        "estimation_algorithmic_bytes": int(est_bytes),
+        "estimation_hbm_frac": round(est_bytes / t_est / (PEAK_HBM_GBS * 1e9), 4),
+        "estimation_mfma_frac": round(est_flops / t_est / (PEAK_BF16_TFLOPS * 1e12), 4),
+        "estimation_measured_hbm_bytes": measured,
+        "index_ms": round(t_idx * 1e3, 3),
+        "index_algorithmic_bytes": int(idx_bytes),
+        "index_hbm_frac": round(idx_bytes / t_idx / (PEAK_HBM_GBS * 1e9), 4),
+    }
+
+
 def kernel_flops(name: str, d: int, T: int, C: int, BH: int, N: int) -> float:
     """MFMA GEMM work each kernel must do on the computed blocks / columns."""
     pair = 2.0 * d            # one multiply-add over d per (row, key) per GEMM
@@ -299,6 +335,7 @@ def main():
             ms.attn_bwd(dims, q, k, v, out, do, lse, idx, dq, dk, dv, out_f32=out32, workspace=bwd_ws)
             mark("bwd", 1)
             state["nnz"] = (blk, col)
+            state["vcol"] = vcol
             if timed:
                 torch.cuda.synchronize()
                 for s, (a, b) in ev.items():
@@ -332,7 +369,7 @@ def main():
         nb = N // 64
         results[name] = dict(
             wl=wl, ms_per_step=ms_step, wall_ms_per_step=wall, stage_ms=step_ms, kernels=per_kernel,
-            fwd_flops=fwd_flops, T=T, C=C,
+            fwd_flops=fwd_flops, T=T, C=C, vcol=state["vcol"],
             density=T / (B * Hq * nb * (nb + 1) / 2.0),
             v_idx=v_idx.cpu().numpy(), s_idx=s_idx.cpu().numpy(), x=x if name == args.workload else None)
         print(f"[bench] {name}: {ms_step:.2f} ms/step {json.dumps(step_ms)}", file=sys.stderr, flush=True)
@@ -350,6 +387,8 @@ def main():
     dk_ = kern[dom]
     achieved = dk_["tflops"] if dk_["tflops"] is not None else 0.0
     traffic = hbm_traffic(wl.name, f"{dom}_kernel<{wl.head_dim}>")
+    for r in results.values():
+        r["est_idx"] = estimation_and_index_report(r)
     roofline = {"bound": "mfma", "kernel": dom, "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                 "traffic": None if traffic is None else round(traffic), "traffic_unit": "HBM bytes per launch"}
@@ -376,6 +415,7 @@ def main():
                 "bwd_tflops_kernel": round(2.5 * r["fwd_flops"] / (r["stage_ms"]["bwd"] * 1e-3) / 1e12, 2),
                 "fwd_bwd_tflops_step": round(3.5 * r["fwd_flops"] / (r["ms_per_step"] * 1e-3) / 1e12, 2),
                 "counted_tiles": int(r["T"]), "counted_col_pairs": int(r["C"]),
+                "estimation_and_index": r["est_idx"],
                 "tile_density_causal": round(r["density"], 4), "kernels": r["kernels"]}
             for n, r in results.items()},
     }
