@@ -30,7 +30,6 @@ namespace msparse {
 
 namespace {
 
-constexpr int kFwdThreads = 256;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kSlack = 8.f;   // log2 units
@@ -148,12 +147,23 @@ __device__ __forceinline__ void fwd_tile(const uint16_t* kt, const uint16_t* vt,
     }
 }
 
-// Two waves per SIMD (at most 256 registers per lane), two workgroups per CU:
-// the staging of one workgroup overlaps the MFMA work of the other.
+#ifndef MS_FWD_NB
+#define MS_FWD_NB 2
+#endif
+constexpr int kFwdBlocks = MS_FWD_NB;            // query blocks per workgroup
+constexpr int kFwdThreads = 128 * kFwdBlocks;    // two waves per block
+
+// Two waves per SIMD (at most 256 registers per lane): the staging and
+// barrier waits of one set of waves overlap the MFMA work of another.
+// Workgroup = kFwdBlocks consecutive query blocks of one head; the blocks
+// walk the union of their ascending block lists (each key tile staged once,
+// computed by the blocks whose list selected it), then each block's column
+// tiles.
 template <int D>
 __global__ void __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 attn_fwd_kernel(AttnArgs a) {
     constexpr int KD = FwdRows<D>::KD, ND = FwdRows<D>::ND;
+    constexpr int NB = kFwdBlocks, NW = 2 * NB;
     // two pipeline buffers as separate LDS objects (K bf16, V fp16 rows)
     constexpr int KE = DmaTile<D, kRowPad>::kElems, VE = DmaTile<D, kTrPad>::kElems;
     __shared__ uint16_t k0s[KE], v0s[VE], k1s[KE], v1s[VE];
@@ -162,21 +172,21 @@ attn_fwd_kernel(AttnArgs a) {
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index (uniform)
-    const int half = w >> 1;      // query block of the pair
+    const int blk = w >> 1;       // this wave's query block in the group
     const int h = lane >> 5;      // lane half
     const int l32 = lane & 31;
 
-    const int npair = (a.nqb + 1) >> 1;
-    int bh, qp;
-    query_tile_of(blockIdx.x, a.B, a.Hq, a.Hkv, npair, bh, qp);
+    const int ngroup = (a.nqb + NB - 1) / NB;
+    int bh, qgi;
+    query_tile_of(blockIdx.x, a.B, a.Hq, a.Hkv, ngroup, bh, qgi);
     const int b = bh / a.Hq;
     const int hq = bh % a.Hq;
     const int hk = hq / (a.Hq / a.Hkv);
-    const int qb0 = 2 * qp;
-    const bool has1 = qb0 + 1 < a.nqb;
-    const int qb = qb0 + (has1 ? half : 0);   // a lone block: both halves read it, half 1 stays idle
-    const bool live = half == 0 || has1;
-    const int qrow = 32 * (w & 1) + l32;      // row inside the query block
+    const int qb0 = NB * qgi;
+    const int nblk = min(NB, a.nqb - qb0);                    // blocks present in the group
+    const bool live = blk < nblk;
+    const int qb = qb0 + (live ? blk : 0);                   // an absent block's waves read block 0 and stay idle
+    const int qrow = 32 * (w & 1) + l32;                     // row inside the query block
     const int32_t qg = ldc(a.q_blk_global, qb);
 
     const uint16_t* __restrict__ kp = a.k + (int64_t(b) * a.Hkv + hk) * int64_t(a.Nk) * D;
@@ -192,50 +202,63 @@ attn_fwd_kernel(AttnArgs a) {
     for (int i = 0; i < ND; ++i) st.o[i] = f32x16{};
     const float c2 = a.scale * kLog2e;
 
-    // ---- block tiles: the union of the two ascending block lists, software
+    // ---- block tiles: the union of the NB ascending block lists, software
     // pipelined (the loads of the next tile are in flight during this tile)
     const int64_t item0 = int64_t(bh) * a.nqb + qb0;
-    const int64_t e00 = ldc(a.blk_ptr, item0), e01 = ldc(a.blk_ptr, item0 + 1);
-    const int64_t e11 = has1 ? ldc(a.blk_ptr, item0 + 2) : e01;
-    int64_t p0 = e00, p1 = e01;
-    auto next = [&](int32_t& kb, bool& in0, bool& in1) {
-        if (p0 >= e01 && p1 >= e11) return false;
-        const int32_t k0 = p0 < e01 ? ldc(a.blk_idx, p0) : INT32_MAX;
-        const int32_t k1 = p1 < e11 ? ldc(a.blk_idx, p1) : INT32_MAX;
-        kb = min(k0, k1);
-        in0 = k0 == kb;
-        in1 = k1 == kb;
-        p0 += in0;
-        p1 += in1;
+    int64_t p[NB], e[NB];
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+        p[j] = j < nblk ? ldc(a.blk_ptr, item0 + j) : 0;
+        e[j] = j < nblk ? ldc(a.blk_ptr, item0 + j + 1) : 0;
+    }
+    // next key tile of the union: kb, the blocks that selected it (bit j), and
+    // its global key block (for the diagonal tests; read one tile ahead)
+    auto next = [&](int32_t& kb, uint32_t& sel, int32_t& kg) {
+        int32_t k[NB];
+        kb = INT32_MAX;
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+            k[j] = p[j] < e[j] ? ldc(a.blk_idx, p[j]) : INT32_MAX;
+            kb = min(kb, k[j]);
+        }
+        if (kb == INT32_MAX) return false;
+        sel = 0;
+#pragma unroll
+        for (int j = 0; j < NB; ++j)
+            if (k[j] == kb) {
+                sel |= 1u << j;
+                ++p[j];
+            }
+        kg = ldc(a.k_blk_global, kb);
         return true;
     };
     if (tid < 64) dlims[tid] = tid;   // causal diagonal: key k visible to rows >= k
-    int32_t kb = 0;
-    bool in0 = false, in1 = false;
-    bool have = next(kb, in0, in1);
+    int32_t kb = 0, kg = 0;
+    uint32_t sel = 0;
+    bool have = next(kb, sel, kg);
     if (have) {
         const ContiguousRows rows{int64_t(kb) * 64};
-        dma_rows<D, kRowPad, 4>(k0s, kp, rows, w, lane);
-        dma_rows<D, kTrPad, 4>(v0s, vp, rows, w, lane);
+        dma_rows<D, kRowPad, NW>(k0s, kp, rows, w, lane);
+        dma_rows<D, kTrPad, NW>(v0s, vp, rows, w, lane);
     }
     wait_vmem();
     __syncthreads();
     // one tile: compute from (ck, cv) while the next tile lands in (nk, nv)
     auto step = [&](const uint16_t* ck, const uint16_t* cv, uint16_t* nk, uint16_t* nv) {
-        int32_t kb2 = 0;
-        bool in0n = false, in1n = false;
-        const bool more = next(kb2, in0n, in1n);
+        int32_t kb2 = 0, kg2 = 0;
+        uint32_t sel2 = 0;
+        const bool more = next(kb2, sel2, kg2);
         if (more) {
             const ContiguousRows rows{int64_t(kb2) * 64};
-            dma_rows<D, kRowPad, 4>(nk, kp, rows, w, lane);
-            dma_rows<D, kTrPad, 4>(nv, vp, rows, w, lane);
+            dma_rows<D, kRowPad, NW>(nk, kp, rows, w, lane);
+            dma_rows<D, kTrPad, NW>(nv, vp, rows, w, lane);
         }
-        if (half == 0 ? in0 : in1) fwd_tile<D>(ck, cv, ldc(a.k_blk_global, kb) == qg ? dlims : nullptr, st, qrow, lane, c2);
+        if ((sel >> blk) & 1u) fwd_tile<D>(ck, cv, kg == qg ? dlims : nullptr, st, qrow, lane, c2);
         wait_vmem();
         __syncthreads();
         kb = kb2;
-        in0 = in0n;
-        in1 = in1n;
+        kg = kg2;
+        sel = sel2;
         have = more;
     };
     while (have) {
@@ -244,8 +267,8 @@ attn_fwd_kernel(AttnArgs a) {
         step(k1s, v1s, k0s, v0s);
     }
 
-    // ---- column tiles, one half at a time (the lists differ only near the band)
-    for (int j = 0; j < 1 + int(has1); ++j) {
+    // ---- column tiles, one block at a time (the lists differ only near the band)
+    for (int j = 0; j < nblk; ++j) {
         const int64_t c0 = ldc(a.col_ptr, item0 + j), c1 = ldc(a.col_ptr, item0 + j + 1);
         const int32_t qgj = ldc(a.q_blk_global, qb0 + j);
         for (int64_t cbase = c0; cbase < c1; cbase += 64) {
@@ -256,11 +279,11 @@ attn_fwd_kernel(AttnArgs a) {
                 lims[tid] = tid < cnt ? (a.k_blk_global[col >> 6] == qgj ? (col & 63) : 0) : 64;
             }
             __syncthreads();
-            dma_rows<D, kRowPad, 4>(k0s, kp, IndexedRows{kidx}, w, lane);
-            dma_rows<D, kTrPad, 4>(v0s, vp, IndexedRows{kidx}, w, lane);
+            dma_rows<D, kRowPad, NW>(k0s, kp, IndexedRows{kidx}, w, lane);
+            dma_rows<D, kTrPad, NW>(v0s, vp, IndexedRows{kidx}, w, lane);
             wait_vmem();
             __syncthreads();
-            if (half == j) fwd_tile<D>(k0s, v0s, lims, st, qrow, lane, c2);
+            if (blk == j) fwd_tile<D>(k0s, v0s, lims, st, qrow, lane, c2);
             __syncthreads();
         }
     }
@@ -341,7 +364,7 @@ __global__ void merge_kernel(MergeArgs m) {
 }  // namespace
 
 hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t s) {
-    const int64_t grid = int64_t(a.B) * a.Hq * ((a.nqb + 1) / 2);
+    const int64_t grid = int64_t(a.B) * a.Hq * ((a.nqb + kFwdBlocks - 1) / kFwdBlocks);
     if (grid == 0) return hipSuccess;
     // fp16 copy of V times a power of two from max |V|
     hipLaunchKernelGGL(fwd_prep_kernel, dim3(1), dim3(64), 0, s, a);

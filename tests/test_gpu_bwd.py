@@ -19,6 +19,10 @@ SMALL = {
     "gqa_8k_g4": WORKLOADS["layer_128k"].resized(seq=8192, heads_q=4, heads_kv=1, k_v=150, k_s=700),
     "d64_b2": WORKLOADS["layer_32k"].resized(batch=2, seq=3072, heads_q=2, heads_kv=1, head_dim=64, k_v=70,
                                              k_s=130),
+    # odd block counts: lone query block (dQ) and lone key block (dK/dV) per pair
+    "odd_65_blocks_d64": WORKLOADS["layer_32k"].resized(seq=4160, heads_q=2, heads_kv=1, head_dim=64, k_v=90,
+                                                        k_s=300),
+    "odd_17_blocks_d128": WORKLOADS["layer_32k"].resized(seq=1088, heads_q=2, heads_kv=2, k_v=40, k_s=200),
 }
 
 

@@ -18,6 +18,10 @@ SMALL = {
     "gqa_4k_d128": WORKLOADS["layer_32k"].resized(seq=4096, heads_q=4, heads_kv=2, k_v=100, k_s=600),
     "gqa_8k_b2": WORKLOADS["layer_128k"].resized(batch=2, seq=8192, heads_q=4, heads_kv=1, k_v=150, k_s=700),
     "d64_sparse": WORKLOADS["layer_32k"].resized(seq=6144, heads_q=2, heads_kv=2, head_dim=64, k_v=70, k_s=130),
+    # odd block counts: the last workgroup of a block pair holds a lone block
+    "odd_65_blocks_d64": WORKLOADS["layer_32k"].resized(seq=4160, heads_q=2, heads_kv=1, head_dim=64, k_v=90,
+                                                        k_s=300),
+    "odd_17_blocks_d128": WORKLOADS["layer_32k"].resized(seq=1088, heads_q=2, heads_kv=2, k_v=40, k_s=200),
 }
 
 
@@ -71,9 +75,10 @@ def test_fwd_dense_budget(gpu):
     assert_lse_close(gl, rl)
 
 
-@pytest.mark.parametrize("layout,W", [("striped", 4), ("zigzag", 4)])
-def test_fwd_ring_steps_merge(gpu, layout, W):
-    wl = SMALL["gqa_8k_b2"].resized(batch=1)
+# (striped, 2, 4480): 35 local blocks per shard, so the pair kernels see a lone block
+@pytest.mark.parametrize("layout,W,seq", [("striped", 4, 8192), ("zigzag", 4, 8192), ("striped", 2, 4480)])
+def test_fwd_ring_steps_merge(gpu, layout, W, seq):
+    wl = SMALL["gqa_8k_b2"].resized(batch=1, seq=seq)
     x = make_inputs(wl, "cpu", with_do=False)
     f = inputs_f64(x)
     vi, si, _, _ = oracle_indices(f, wl)
