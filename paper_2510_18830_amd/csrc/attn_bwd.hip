@@ -134,53 +134,38 @@ __device__ __forceinline__ void dq_tile(const uint16_t* kt, const uint16_t* vt, 
         sacc[c] = f32x16{};
         pacc[c] = f32x16{};
     }
-    // S^T and dP^T: four accumulation chains, operands read in groups of two
-    // k-steps into two register sets, group g + 1 before group g's MFMAs
-    // (scheduling fences keep that order; see kv_tile).
-    u32x4 fk[2][2][2], fv[2][2][2];   // [set][k-step of group][c]
-    auto read_group = [&](int set, int s0) {
+    // Same phase schedule as kv_tile, over the two key halves c:
+    //   A  S^T, dP^T of keys 32 c .. for c = 0
+    //   B  S^T, dP^T of c = 1, interleaved with c = 0's dZ terms
+    //   C  dQ k-steps of c = 0, interleaved with c = 1's dZ terms
+    //   D  dQ k-steps of c = 1
+    // with operands read one group ahead into two register sets.
+    u32x4 fk[2][2], fv[2][2];   // [set][k-step of group]
+    auto read_sd = [&](int set, int c, int s0) {
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-            for (int c = 0; c < 2; ++c) {
-                fk[set][j][c] = dma_read16<D, kDualPad>(kt, 32 * c + l32, h + 2 * (s0 + j));
-                fv[set][j][c] = dma_read16<D, kDualPad>(vt, 32 * c + l32, h + 2 * (s0 + j));
-            }
+        for (int j = 0; j < 2; ++j) {
+            fk[set][j] = dma_read16<D, kDualPad>(kt, 32 * c + l32, h + 2 * (s0 + j));
+            fv[set][j] = dma_read16<D, kDualPad>(vt, 32 * c + l32, h + 2 * (s0 + j));
+        }
     };
-    read_group(0, 0);
+    auto mfma_sd = [&](int set, int c, int s0) {
 #pragma unroll
-    for (int s0 = 0; s0 < KD; s0 += 2) {
-        const int set = (s0 >> 1) & 1;
-        if (s0 + 2 < KD) read_group(set ^ 1, s0 + 2);
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-            for (int c = 0; c < 2; ++c) {
-                sacc[c] = mfma32h(fk[set][j][c], st.q[s0 + j], sacc[c]);
-                pacc[c] = mfma32h(fv[set][j][c], st.g[s0 + j], pacc[c]);
-            }
-        __builtin_amdgcn_sched_barrier(0);
-    }
-    // Per key half c: s dZ^T = P o (s dP^T - s Delta), P = exp2(c2 z - lse2) on
-    // visible entries, then that half's dQ k-steps (2c, 2c+1), K^T read
-    // transposed in groups of two d blocks into two register sets.
-    u32x4 ak[2][2][2];   // [set][i of group][j]
-    auto read_tr = [&](int set, int c, int i0) {
-#pragma unroll
-        for (int ii = 0; ii < 2; ++ii)
-#pragma unroll
-            for (int j = 0; j < 2; ++j)
-                ak[set][ii][j] = dma_read_tr<D, kDualPad>(kt, 16 * (2 * c + j), 32 * (i0 + ii), lane);
+        for (int j = 0; j < 2; ++j) {
+            sacc[c] = mfma32h(fk[set][j], st.q[s0 + j], sacc[c]);
+            pacc[c] = mfma32h(fv[set][j], st.g[s0 + j], pacc[c]);
+        }
     };
+    // s dZ^T = P o (s dP^T - s Delta), P = exp2(c2 z - lse2), for accumulator
+    // elements 4 q4 .. 4 q4 + 3 (keys 32 c + 8 q4 + 4 h + 0..3)
+    auto soft = [&](int c, int q4) {
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
-        read_tr(0, c, 0);
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
+        for (int e = 0; e < 4; ++e) {
+            const int r = 4 * q4 + e;
             const float p = fast_exp2(__builtin_fmaf(sacc[c][r], c2, -st.lse2));
             sacc[c][r] = p * __builtin_fmaf(pacc[c][r], isv, -st.dlt);
         }
+    };
+    auto mask = [&](int c) {
         if (lims) {
             keep_branch();
 #pragma unroll
@@ -191,20 +176,73 @@ __device__ __forceinline__ void dq_tile(const uint16_t* kt, const uint16_t* vt, 
                     if (qrow < l4[e]) sacc[c][4 * q4 + e] = 0.f;
             }
         }
-        u32x4 zb[2];
+    };
+    u32x4 zb[2];
+    auto pack = [&](int c) {
         zb[0] = pack8_f16<0>(sacc[c]);
         zb[1] = pack8_f16<8>(sacc[c]);
+    };
+    // dQ += (s dZ) K for key half c, d block i: K^T read transposed
+    u32x4 ak[2][2];   // [set][j]
+    auto read_tr = [&](int set, int c, int i) {
 #pragma unroll
-        for (int i0 = 0; i0 < ND; i0 += 2) {
-            const int set = (i0 >> 1) & 1;
-            if (i0 + 2 < ND) read_tr(set ^ 1, c, i0 + 2);
-            __builtin_amdgcn_sched_barrier(0);
+        for (int j = 0; j < 2; ++j) ak[set][j] = dma_read_tr<D, kDualPad>(kt, 16 * (2 * c + j), 32 * i, lane);
+    };
+    auto mfma_q = [&](int set, int i) {
 #pragma unroll
-            for (int ii = 0; ii < 2; ++ii)
+        for (int j = 0; j < 2; ++j) st.acc[i] = mfma32h(ak[set][j], zb[j], st.acc[i]);
+    };
+    constexpr int NG = KD / 2;
+    // ---- A
+    read_sd(0, 0, 0);
 #pragma unroll
-                for (int j = 0; j < 2; ++j) st.acc[i0 + ii] = mfma32h(ak[set][ii][j], zb[j], st.acc[i0 + ii]);
-            __builtin_amdgcn_sched_barrier(0);
-        }
+    for (int g = 0; g < NG; ++g) {
+        const int set = g & 1;
+        if (g + 1 < NG) read_sd(set ^ 1, 0, 2 * (g + 1));
+        else read_sd(set ^ 1, 1, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        mfma_sd(set, 0, 2 * g);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    // ---- B
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+        const int set = (NG + g) & 1;
+        if (g + 1 < NG) read_sd(set ^ 1, 1, 2 * (g + 1));
+        else read_tr(set ^ 1, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        mfma_sd(set, 1, 2 * g);
+        if (g < 4) soft(0, g);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int q4 = NG; q4 < 4; ++q4) soft(0, q4);   // d = 64: two groups per half
+    mask(0);
+    pack(0);
+    // ---- C
+    constexpr int S0 = (2 * NG) & 1;   // register set holding c = 0's first dQ operands
+#pragma unroll
+    for (int i = 0; i < ND; ++i) {
+        const int set = (S0 + i) & 1;
+        if (i + 1 < ND) read_tr(set ^ 1, 0, i + 1);
+        else read_tr(set ^ 1, 1, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        mfma_q(set, i);
+        if (i < 4) soft(1, i);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int q4 = ND; q4 < 4; ++q4) soft(1, q4);
+    mask(1);
+    pack(1);
+    // ---- D
+#pragma unroll
+    for (int i = 0; i < ND; ++i) {
+        const int set = (S0 + ND + i) & 1;
+        if (i + 1 < ND) read_tr(set ^ 1, 1, i + 1);
+        __builtin_amdgcn_sched_barrier(0);
+        mfma_q(set, i);
+        __builtin_amdgcn_sched_barrier(0);
     }
 }
 
@@ -380,67 +418,45 @@ __device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, co
         sacc[rb] = f32x16{};
         pacc[rb] = f32x16{};
     }
-    // Four independent accumulation chains.  Operands are read in groups of two
-    // k-steps (8 LDS reads) into two register sets: group g + 1 is read before
-    // group g's MFMAs issue (scheduling fences keep that order), so LDS
-    // latency overlaps the MFMAs (the default schedule waits for every read
-    // right before its MFMA).
-    u32x4 fq[2][2][2], fg[2][2][2];   // [set][k-step of group][rb]
-    auto read_group = [&](int set, int s0) {
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-            for (int rb = 0; rb < 2; ++rb) {
-                fq[set][j][rb] = dma_read16<D, kDualPad>(t + T::kQ16, 32 * rb + l32, h + 2 * (s0 + j));
-                fg[set][j][rb] = dma_read16<D, kDualPad>(t + T::kG16, 32 * rb + l32, h + 2 * (s0 + j));
-            }
-    };
-    read_group(0, 0);
-#pragma unroll
-    for (int s0 = 0; s0 < KD; s0 += 2) {
-        const int set = (s0 >> 1) & 1;
-        if (s0 + 2 < KD) read_group(set ^ 1, s0 + 2);
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-            for (int rb = 0; rb < 2; ++rb) {
-                sacc[rb] = mfma32h(fq[set][j][rb], kreg[s0 + j], sacc[rb]);
-                pacc[rb] = mfma32h(fg[set][j][rb], vreg[s0 + j], pacc[rb]);
-            }
-        __builtin_amdgcn_sched_barrier(0);
-    }
-    // Per half rb of the query rows: softmax terms, then that half's share of
-    // dV / dK (k-steps 2 rb, 2 rb + 1).  The second half's S / dP MFMAs and the
-    // first half's dV / dK MFMAs run while the other half's VALU work issues.
+    // Schedule (one wave per SIMD, so MFMA and VALU overlap only inside the
+    // wave's own instruction stream):
+    //   A  S, dP of row half 0
+    //   B  S, dP of row half 1, interleaved with half 0's softmax terms
+    //   C  dV, dK of half 0, interleaved with half 1's softmax terms
+    //   D  dV, dK of half 1
+    // MFMA operands are read from LDS one group ahead into two register sets;
+    // scheduling fences separate the groups (the default schedule waits for
+    // every read right before its MFMA and runs the phases back to back).
     // Rows of acc element r: 32 rb + 8 (r/4) + 4 h + r%4; column = this lane's key.
-    // dV^T += (s dO)^T P, dK^T += Q^T (s dZ) for half rb: A operands read
-    // transposed, in groups (one 32-wide d block i: 4 operands, 8 reads) into
-    // two register sets, the first group before the softmax VALU work.
-    u32x4 av[2][2], ak[2][2];   // [set][j]
-    auto read_tr = [&](int set, int rb, int i) {
+    u32x4 fq[2][2], fg[2][2];   // [set][k-step of group]
+    auto read_sd = [&](int set, int rb, int s0) {
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
-            av[set][j] = dma_read_tr<D, kDualPad>(t + T::kG16, 16 * (2 * rb + j), 32 * i, lane);
-            ak[set][j] = dma_read_tr<D, kDualPad>(t + T::kQ16, 16 * (2 * rb + j), 32 * i, lane);
+            fq[set][j] = dma_read16<D, kDualPad>(t + T::kQ16, 32 * rb + l32, h + 2 * (s0 + j));
+            fg[set][j] = dma_read16<D, kDualPad>(t + T::kG16, 32 * rb + l32, h + 2 * (s0 + j));
         }
     };
+    auto mfma_sd = [&](int set, int rb, int s0) {
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb) {
-        read_tr(0, rb, 0);
-#pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-            const int row0 = 32 * rb + 8 * q4 + 4 * h;
-            const f32x4 l4 = *reinterpret_cast<const f32x4*>(lse2 + row0);
-            const f32x4 d4 = *reinterpret_cast<const f32x4*>(dlt + row0);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int r = 4 * q4 + e;
-                const float p = fast_exp2(__builtin_fmaf(sacc[rb][r], c2, -l4[e]));
-                sacc[rb][r] = p;
-                pacc[rb][r] = p * __builtin_fmaf(pacc[rb][r], isv, -d4[e]);
-            }
+        for (int j = 0; j < 2; ++j) {
+            sacc[rb] = mfma32h(fq[set][j], kreg[s0 + j], sacc[rb]);
+            pacc[rb] = mfma32h(fg[set][j], vreg[s0 + j], pacc[rb]);
         }
+    };
+    // softmax terms of rows 32 rb + 8 q4 + 4 h + 0..3
+    auto soft = [&](int rb, int q4) {
+        const int row0 = 32 * rb + 8 * q4 + 4 * h;
+        const f32x4 l4 = *reinterpret_cast<const f32x4*>(lse2 + row0);
+        const f32x4 d4 = *reinterpret_cast<const f32x4*>(dlt + row0);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int r = 4 * q4 + e;
+            const float p = fast_exp2(__builtin_fmaf(sacc[rb][r], c2, -l4[e]));
+            sacc[rb][r] = p;
+            pacc[rb][r] = p * __builtin_fmaf(pacc[rb][r], isv, -d4[e]);
+        }
+    };
+    auto mask = [&](int rb) {
         if (lims) {
             keep_branch();
             const int lim = lims[key] - 4 * h - 32 * rb;   // row 32 rb + 8 (r/4) + 4 h + r%4 < lims[key]
@@ -451,23 +467,81 @@ __device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, co
                     pacc[rb][r] = 0.f;
                 }
         }
-        u32x4 pb[2], zb[2];
+    };
+    // transposed A operands of dV (s dO)^T and dK Q^T for one 32-wide d block
+    u32x4 av[2][2], ak[2][2];   // [set][j]
+    auto read_tr = [&](int set, int rb, int i) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            av[set][j] = dma_read_tr<D, kDualPad>(t + T::kG16, 16 * (2 * rb + j), 32 * i, lane);
+            ak[set][j] = dma_read_tr<D, kDualPad>(t + T::kQ16, 16 * (2 * rb + j), 32 * i, lane);
+        }
+    };
+    u32x4 pb[2], zb[2];
+    auto pack = [&](int rb) {
         pb[0] = pack8_f16<0>(sacc[rb]);
         pb[1] = pack8_f16<8>(sacc[rb]);
         zb[0] = pack8_f16<0>(pacc[rb]);
         zb[1] = pack8_f16<8>(pacc[rb]);
+    };
+    auto mfma_kv = [&](int set, int i) {
 #pragma unroll
-        for (int i = 0; i < ND; ++i) {
-            const int set = i & 1;
-            if (i + 1 < ND) read_tr(set ^ 1, rb, i + 1);
-            __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                dv[i] = mfma32h(av[set][j], pb[j], dv[i]);
-                dk[i] = mfma32h(ak[set][j], zb[j], dk[i]);
-            }
-            __builtin_amdgcn_sched_barrier(0);
+        for (int j = 0; j < 2; ++j) {
+            dv[i] = mfma32h(av[set][j], pb[j], dv[i]);
+            dk[i] = mfma32h(ak[set][j], zb[j], dk[i]);
         }
+    };
+    static_assert(KD == 2 * ND, "four S/dP groups and four dV/dK groups per half");
+    constexpr int NG = KD / 2;   // groups per half (4 for d = 128)
+    // ---- A
+    read_sd(0, 0, 0);
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+        const int set = g & 1;
+        if (g + 1 < NG) read_sd(set ^ 1, 0, 2 * (g + 1));
+        else read_sd(set ^ 1, 1, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        mfma_sd(set, 0, 2 * g);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    // ---- B
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+        const int set = (NG + g) & 1;
+        if (g + 1 < NG) read_sd(set ^ 1, 1, 2 * (g + 1));
+        __builtin_amdgcn_sched_barrier(0);
+        mfma_sd(set, 1, 2 * g);
+        if (g < 4) soft(0, g);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int q4 = NG; q4 < 4; ++q4) soft(0, q4);   // d = 64: two groups per half
+    mask(0);
+    pack(0);
+    // ---- C
+    read_tr(0, 0, 0);
+#pragma unroll
+    for (int i = 0; i < ND; ++i) {
+        const int set = i & 1;
+        if (i + 1 < ND) read_tr(set ^ 1, 0, i + 1);
+        else read_tr(set ^ 1, 1, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        mfma_kv(set, i);
+        if (i < 4) soft(1, i);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int q4 = ND; q4 < 4; ++q4) soft(1, q4);
+    mask(1);
+    pack(1);
+    // ---- D
+#pragma unroll
+    for (int i = 0; i < ND; ++i) {
+        const int set = (ND + i) & 1;
+        if (i + 1 < ND) read_tr(set ^ 1, 1, i + 1);
+        __builtin_amdgcn_sched_barrier(0);
+        mfma_kv(set, i);
+        __builtin_amdgcn_sched_barrier(0);
     }
 }
 
