@@ -15,6 +15,9 @@ and the selected slash offsets S (delta = n - m):
   * cols(i)   = {v in V : v <= 64 i + 63, (i - floor(v/64)) not in D}, ascending:
     the verticals that the selected tiles of row block i do not already cover.
 
+Negative entries of v_idx / s_idx are the unused slots of a top-p list (whose
+length varies per head) and are dropped.
+
 Ring shards (Section 4.2 for the striped layout; the zigzag layout is the
 baseline the paper compares with): the global 64-token block g belongs to
   striped: worker g mod W;
@@ -32,6 +35,8 @@ BLOCK = 64
 def diag_set(s_idx, nb: int) -> np.ndarray:
     out = set()
     for delta in np.asarray(s_idx).tolist():
+        if delta < 0:          # unused slot
+            continue
         for x in (delta // BLOCK, -(-delta // BLOCK)):
             if x < nb:
                 out.add(x)
@@ -58,6 +63,7 @@ def head_lists(v_idx, s_idx, N: int):
     in_d = np.zeros(nb, dtype=bool)
     in_d[D] = True
     V = np.unique(np.asarray(v_idx, dtype=np.int64))   # ascending, duplicates count once
+    V = V[V >= 0]                                         # unused slots
     blocks, cols = [], []
     for i in range(nb):
         blocks.append(np.sort(i - D[D <= i]))
@@ -119,6 +125,7 @@ class Index:
             self.blocks.append(hb)
             self.cols.append(hc)
             V = np.unique(v2[bh].astype(np.int64))
+            V = V[V >= 0]
             if W == 1:
                 self.vcols.append(V)
                 continue

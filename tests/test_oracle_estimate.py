@@ -127,3 +127,87 @@ def test_layer_estimate_gqa_mapping():
             np.testing.assert_array_equal(vs[b, h], v1)
             assert vi[b, h].tolist() == E.topk_lower(v1, 5).tolist()
             assert si[b, h].tolist() == E.topk_lower(s1, 7).tolist()
+
+
+# ---- top-p budget (score_cover of Algorithm 1)
+
+def test_score_cover_zero_query_exact_rational():
+    # q = 0: v_score[m] = H_N - H_{N-L} =: c0 for every m <= N - L (N - L + 1 equal
+    # entries), and the total mass is L.  While p L <= (N - L + 1) c0 the budget
+    # is ceil(p L / c0), computed here in exact rationals.
+    from fractions import Fraction as Fr
+    N, L, d = 200, 16, 8
+    rng = np.random.default_rng(4)
+    vs, ss = E.vs_scores(np.zeros((L, d)), rng.standard_normal((N, d)), 1 / math.sqrt(d))
+    c0 = sum(Fr(1, n + 1) for n in range(N - L, N))
+    for p in (Fr(1, 10), Fr(3, 10), Fr(1, 2), Fr(77, 100), Fr(9, 10)):
+        want = math.ceil(p * L / c0)
+        assert want <= N - L + 1
+        assert E.score_cover(vs, float(p)) == want
+        assert E.score_cover(ss, float(p)) == want   # same closed form in delta
+
+
+def test_score_cover_hand_example():
+    # scores 0.1 0.4 0.2 0.2 0.1 (total 1): sorted 0.4 (1), 0.2 (2), 0.2 (3),
+    # 0.1 (0), 0.1 (4); cumulative 0.4 0.6 0.8 0.9 1.0
+    sc = np.array([0.1, 0.4, 0.2, 0.2, 0.1])
+    for p, k in ((0.05, 1), (0.39, 1), (0.5, 2), (0.7, 3), (0.85, 4), (0.95, 5)):
+        assert E.score_cover(sc, p) == k, p
+    # with k = 4 the tie at 0.1 goes to the lower index
+    assert E.topk_lower(sc, E.score_cover(sc, 0.85)).tolist() == [0, 1, 2, 3]
+    # "at least": reaching the threshold exactly is enough (binary-exact values)
+    sc = np.array([0.25, 0.25, 0.5])
+    assert E.score_cover(sc, 0.5) == 1 and E.score_cover(sc, 0.75) == 2
+
+
+def test_score_cover_brute_force_subsets():
+    # the budget is the smallest size of ANY subset reaching p of the total mass
+    import itertools
+    rng = np.random.default_rng(5)
+    checked = 0
+    for _ in range(60):
+        n = int(rng.integers(1, 9))
+        sc = rng.random(n) ** 3
+        p = float(rng.uniform(0.02, 0.98))
+        theta = p * sc.sum()
+        best = [max(math.fsum(sc[list(c)]) for c in itertools.combinations(range(n), r)) for r in range(1, n + 1)]
+        if min(abs(x - theta) for x in best) < 1e-9:     # too close to call in floating point
+            continue
+        want = 1 + min(r for r in range(n) if best[r] >= theta)
+        assert E.score_cover(sc, p) == want, (sc, p)
+        checked += 1
+    assert checked > 40
+
+
+def test_score_cover_invariants():
+    rng = np.random.default_rng(6)
+    sc = rng.exponential(size=3000) ** 4
+    srt = np.sort(sc)[::-1]
+    last = 0
+    for p in np.linspace(0.01, 0.99, 50):
+        k = E.score_cover(sc, p)
+        assert srt[:k].sum() >= p * sc.sum() * (1 - 1e-12)
+        assert k == 1 or srt[:k - 1].sum() < p * sc.sum()
+        assert k >= last
+        last = k
+
+
+def test_estimate_topp_cap_padding_and_fixed_k():
+    rng = np.random.default_rng(7)
+    B, Hq, Hkv, N, d, L = 1, 4, 2, 256, 8, 16
+    q = 2 * rng.standard_normal((B, Hq, N, d))
+    k = rng.standard_normal((B, Hkv, N, d))
+    vi, si, vc, sc_, vs, ss = E.estimate_topp(q, k, L, 0.6, 0.8, 40, 60, 0.35)
+    for h in range(Hq):
+        kv = min(E.score_cover(vs[0, h], 0.6), 40)
+        ks = min(E.score_cover(ss[0, h], 0.8), 60)
+        assert (vc[0, h], sc_[0, h]) == (kv, ks)
+        assert vi[0, h, :kv].tolist() == E.topk_lower(vs[0, h], kv).tolist()
+        assert si[0, h, :ks].tolist() == E.topk_lower(ss[0, h], ks).tolist()
+        assert (vi[0, h, kv:] == -1).all() and (si[0, h, ks:] == -1).all()
+    # a cap below the budget gives exactly the fixed-k estimate
+    vi2, si2, vc2, sc2, _, _ = E.estimate_topp(q, k, L, 0.99, 0.99, 3, 5, 0.35)
+    vi3, si3, _, _ = E.estimate(q, k, L, 3, 5, 0.35)
+    assert (vc2 == 3).all() and (sc2 == 5).all()
+    np.testing.assert_array_equal(vi2, vi3)
+    np.testing.assert_array_equal(si2, si3)

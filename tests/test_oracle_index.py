@@ -126,3 +126,20 @@ def test_layouts_owner_counts():
     # zigzag worker 0 holds the first and the last chunk
     assert I.local_blocks(0, 16, 2, "zigzag").tolist() == [0, 1, 2, 3, 12, 13, 14, 15]
     assert I.local_blocks(1, 16, 4, "striped").tolist() == [1, 5, 9, 13]
+
+
+def test_unused_slots_are_dropped():
+    # top-p lists are padded with -1 to the caller's capacity
+    rng = np.random.default_rng(11)
+    N = 1024
+    v = np.sort(rng.choice(N, 20, replace=False)).astype(np.int32)
+    s = np.sort(rng.choice(N, 30, replace=False)).astype(np.int32)
+    vp = np.concatenate([v, np.full(7, -1, np.int32)])
+    sp = np.concatenate([s, np.full(5, -1, np.int32)])
+    assert I.diag_set(sp, N // B64).tolist() == I.diag_set(s, N // B64).tolist()
+    for W, layout in ((1, "striped"), (4, "striped"), (2, "zigzag")):
+        for t in range(W):
+            a = I.Index(v[None, None], s[None, None], N, W, 1 % W, t, layout).csr()
+            b = I.Index(vp[None, None], sp[None, None], N, W, 1 % W, t, layout).csr()
+            for key in a:
+                np.testing.assert_array_equal(a[key], b[key], err_msg=key)
