@@ -153,6 +153,30 @@ MSPARSE_API msparse_status msparse_estimate(const msparse_dims* dims, const void
                                 int32_t k_v, int32_t k_s, int32_t* v_idx, int32_t* s_idx, float* v_score,
                                 float* s_score, void* workspace, size_t workspace_bytes, void* stream);
 
+/* Pattern estimation with the online top-p budget (score_cover of Algorithm 1,
+ * Section 4.1 (i)).  The scores are those of msparse_estimate.  For each list
+ * the budget is the smallest k whose k largest scores (ties to the lower index)
+ * sum to at least p times the list's total mass (L for both lists: every
+ * observed softmax row sums to 1), capped at kmax; then argtopk with that k.
+ * Masses are summed exactly in fixed point (score * 2^40, truncated), so the
+ * budget does not depend on the order of the additions.
+ *   p_v, p_s      fractions in (0, 1) (the paper prints no value)
+ *   kmax_v/_s     capacities, 1 <= kmax <= N
+ *   v_idx         int32 [B, Hq, kmax_v]: the v_cnt[b, h] selected positions
+ *                 ascending, then -1 in every unused slot; s_idx alike
+ *   v_cnt, s_cnt  int32 [B, Hq] (device): the budgets after the cap
+ * The padded lists go to msparse_index_count / msparse_build_index unchanged,
+ * with k_v = kmax_v and k_s = kmax_s: negative entries are ignored there.
+ * Errors as msparse_estimate, plus MSPARSE_ERR_INVALID for p outside (0, 1)
+ * or NULL budget outputs.  The workspace is msparse_estimate's. */
+MSPARSE_API size_t msparse_estimate_topp_workspace(const msparse_dims* dims, int32_t last_q, int32_t kmax_v,
+                                                   int32_t kmax_s);
+MSPARSE_API msparse_status msparse_estimate_topp(const msparse_dims* dims, const void* q, const void* k,
+                                                 int32_t last_q, double p_v, double p_s, int32_t kmax_v,
+                                                 int32_t kmax_s, int32_t* v_idx, int32_t* s_idx, int32_t* v_cnt,
+                                                 int32_t* s_cnt, float* v_score, float* s_score, void* workspace,
+                                                 size_t workspace_bytes, void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* Index construction (Section 4.1 (ii); convert_index of Algorithms 1, 2).
  * v_idx [B, Hq, k_v] and s_idx [B, Hq, k_s] are in global token coordinates:
@@ -161,7 +185,8 @@ MSPARSE_API msparse_status msparse_estimate(const msparse_dims* dims, const void
  * (D); query block i gets the key blocks i - x for x in D, x <= i, and the
  * verticals v <= 64 i + 63 whose block-diagonal i - v/64 is not in D.  With a
  * ring descriptor, the lists are restricted to the step's KV shard and written
- * in local coordinates.  Duplicate entries in v_idx or s_idx count once.
+ * in local coordinates.  Duplicate entries in v_idx or s_idx count once;
+ * negative entries (the unused slots of a top-p list) are ignored.
  *
  * msparse_index_count returns the exact element counts the build will write
  * (it waits for the GPU).  msparse_build_index writes them asynchronously,

@@ -55,6 +55,9 @@ _SIGS = {
     "msparse_last_error": (ctypes.c_char_p, []),
     "msparse_estimate_workspace": (c_sz, [_P(Dims), c_i32, c_i32, c_i32]),
     "msparse_estimate": (c_i32, [_P(Dims), c_vp, c_vp, c_i32, c_i32, c_i32, c_vp, c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]),
+    "msparse_estimate_topp_workspace": (c_sz, [_P(Dims), c_i32, c_i32, c_i32]),
+    "msparse_estimate_topp": (c_i32, [_P(Dims), c_vp, c_vp, c_i32, ctypes.c_double, ctypes.c_double, c_i32, c_i32,
+                                      c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]),
     "msparse_index_workspace": (c_sz, [_P(Dims), c_i32, c_i32, _P(Ring)]),
     "msparse_index_count": (c_i32, [_P(Dims), c_vp, c_i32, c_vp, c_i32, _P(Ring), _P(c_i64), _P(c_i64), _P(c_i64),
                                     c_vp, c_sz, c_vp]),
@@ -136,6 +139,24 @@ def estimate(dims: Dims, q, k, last_q, k_v, k_s, v_idx=None, s_idx=None, v_score
     _check(lib().msparse_estimate(ctypes.byref(dims), _p(q), _p(k), last_q, k_v, k_s, _p(v_idx), _p(s_idx),
                                   _p(v_score), _p(s_score), _p(workspace), workspace.numel(), _stream(stream)))
     return v_idx, s_idx
+
+
+def estimate_topp(dims: Dims, q, k, last_q, p_v, p_s, kmax_v, kmax_s, v_score=None, s_score=None, workspace=None,
+                  stream=None):
+    """msparse_estimate_topp: returns (v_idx [B, Hq, kmax_v], s_idx [B, Hq, kmax_s], v_cnt, s_cnt [B, Hq]), int32;
+    unused slots of the index lists hold -1."""
+    BH = (dims.batch, dims.heads_q)
+    v_idx = torch.empty(BH + (kmax_v,), dtype=torch.int32, device=q.device)
+    s_idx = torch.empty(BH + (kmax_s,), dtype=torch.int32, device=q.device)
+    v_cnt = torch.empty(BH, dtype=torch.int32, device=q.device)
+    s_cnt = torch.empty(BH, dtype=torch.int32, device=q.device)
+    if workspace is None:
+        workspace = _workspace(lib().msparse_estimate_topp_workspace(ctypes.byref(dims), last_q, kmax_v, kmax_s),
+                               q.device)
+    _check(lib().msparse_estimate_topp(ctypes.byref(dims), _p(q), _p(k), last_q, float(p_v), float(p_s), kmax_v,
+                                       kmax_s, _p(v_idx), _p(s_idx), _p(v_cnt), _p(s_cnt), _p(v_score), _p(s_score),
+                                       _p(workspace), workspace.numel(), _stream(stream)))
+    return v_idx, s_idx, v_cnt, s_cnt
 
 
 # ------------------------------------------------------------------ index

@@ -468,9 +468,10 @@ size_t msparse_estimate_workspace(const msparse_dims* dims, int32_t last_q, int3
     return 2 * scores + est_workspace_bytes(dims->batch, dims->heads_q, dims->seq_q, last_q);
 }
 
-msparse_status msparse_estimate(const msparse_dims* dims, const void* q, const void* k, int32_t last_q, int32_t k_v,
-                                int32_t k_s, int32_t* v_idx, int32_t* s_idx, float* v_score, float* s_score, void* ws,
-                                size_t ws_bytes, void* stream) {
+static msparse_status estimate_impl(const msparse_dims* dims, const void* q, const void* k, int32_t last_q, int32_t k_v,
+                                    int32_t k_s, double p_v, double p_s, int32_t* v_idx, int32_t* s_idx, int32_t* v_cnt,
+                                    int32_t* s_cnt, float* v_score, float* s_score, void* ws, size_t ws_bytes,
+                                    void* stream) {
     msparse_status st = check_dims(dims, true);
     if (st) return st;
     const int32_t N = dims->seq_q;
@@ -493,6 +494,10 @@ msparse_status msparse_estimate(const msparse_dims* dims, const void* q, const v
     a.L = last_q;
     a.k_v = k_v;
     a.k_s = k_s;
+    a.p_v = p_v;
+    a.p_s = p_s;
+    a.v_cnt = v_cnt;
+    a.s_cnt = s_cnt;
     a.scale = resolve_scale(dims);
     a.v_idx = v_idx;
     a.s_idx = s_idx;
@@ -503,6 +508,28 @@ msparse_status msparse_estimate(const msparse_dims* dims, const void* q, const v
     est_carve(a, base + 2 * scores);
     hipStream_t s = static_cast<hipStream_t>(stream);
     return check_hip(launch_estimate(a, s), s, "estimate");
+}
+
+msparse_status msparse_estimate(const msparse_dims* dims, const void* q, const void* k, int32_t last_q, int32_t k_v,
+                                int32_t k_s, int32_t* v_idx, int32_t* s_idx, float* v_score, float* s_score, void* ws,
+                                size_t ws_bytes, void* stream) {
+    return estimate_impl(dims, q, k, last_q, k_v, k_s, 0.0, 0.0, v_idx, s_idx, nullptr, nullptr, v_score, s_score, ws,
+                         ws_bytes, stream);
+}
+
+size_t msparse_estimate_topp_workspace(const msparse_dims* dims, int32_t last_q, int32_t kmax_v, int32_t kmax_s) {
+    return msparse_estimate_workspace(dims, last_q, kmax_v, kmax_s);
+}
+
+msparse_status msparse_estimate_topp(const msparse_dims* dims, const void* q, const void* k, int32_t last_q, double p_v,
+                                     double p_s, int32_t kmax_v, int32_t kmax_s, int32_t* v_idx, int32_t* s_idx,
+                                     int32_t* v_cnt, int32_t* s_cnt, float* v_score, float* s_score, void* ws,
+                                     size_t ws_bytes, void* stream) {
+    if (!(p_v > 0.0 && p_v < 1.0) || !(p_s > 0.0 && p_s < 1.0))
+        return fail(MSPARSE_ERR_INVALID, "top-p fractions p_v=%g p_s=%g outside (0, 1)", p_v, p_s);
+    if (!v_cnt || !s_cnt) return fail(MSPARSE_ERR_INVALID, "budget output pointer is NULL");
+    return estimate_impl(dims, q, k, last_q, kmax_v, kmax_s, p_v, p_s, v_idx, s_idx, v_cnt, s_cnt, v_score, s_score,
+                         ws, ws_bytes, stream);
 }
 
 }  // extern "C"

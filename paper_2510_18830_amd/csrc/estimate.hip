@@ -18,6 +18,11 @@
 //   topk     radix select of the k-th largest fp32 bit pattern (scores are
 //            >= 0, so bit patterns order like values) and an ordered
 //            compaction: all entries above it, then the lowest-index ties.
+//            With the top-p budget (score_cover of Algorithm 1) a radix select
+//            on mass comes first: the same 8-bit digits, each bin carrying
+//            its count and its summed mass, finds the value t at which the
+//            descending cumulative mass reaches p of the list's total, and k
+//            follows from the count and mass above t.
 // The last 64 query rows form the last 64-row block exactly (N % 64 == 0), so
 // tile j (keys 64 j .. 64 j + 63) holds offsets delta = 64 (nb - 1 - j) + r - c
 // for in-block row r and key c.
@@ -276,66 +281,212 @@ __device__ __forceinline__ void hist_add(uint32_t* wh, uint32_t bin, bool on) {
     }
     if (pending) atomicAdd(&wh[bin], 1u);
 }
+// Masses in fixed point: a score x (0 <= x <= L <= 64) counts floor(x 2^40), so
+// every sum of masses is an exact integer (below 2^47) whatever the order of
+// the additions, and the budget is deterministic.
+__device__ __forceinline__ uint64_t mass_fx(uint32_t bits) {
+    return uint64_t(double(__uint_as_float(bits)) * 1099511627776.0);
+}
+
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+    return v;
+}
+
+// hist_add with a mass: the lanes of one ballot group add their summed mass.
+__device__ __forceinline__ void hist_add_mass(uint32_t* wh, uint64_t* wm, uint32_t bin, uint64_t mass, bool on) {
+    const int lane = threadIdx.x & 63;
+    bool pending = on;
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+        const uint64_t pm = __ballot(pending);
+        if (pm == 0) return;
+        const int first = __builtin_ctzll(pm);
+        const uint32_t lb = uint32_t(__shfl(int(bin), first));
+        const bool same = pending && bin == lb;
+        const uint64_t sm = __ballot(same);
+        const uint64_t ms = wave_sum_u64(same ? mass : 0ull);
+        if (lane == first) {
+            atomicAdd(&wh[lb], uint32_t(__popcll(sm)));
+            atomicAdd(reinterpret_cast<unsigned long long*>(&wm[lb]), (unsigned long long)ms);
+        }
+        pending = pending && !same;
+    }
+    if (pending) {
+        atomicAdd(&wh[bin], 1u);
+        atomicAdd(reinterpret_cast<unsigned long long*>(&wm[bin]), (unsigned long long)mass);
+    }
+}
+
+struct TopkLds {
+    uint32_t whist[kTopkWaves * kHistStride];
+    uint64_t wmass[kTopkWaves * 256];
+    uint32_t hist[256];
+    uint64_t hmass[256];
+    uint64_t wsum[kTopkWaves];
+    uint32_t s_prefix, s_krem, s_k, s_above;
+    uint64_t s_rem;
+    int64_t wgt[kTopkWaves], weq[kTopkWaves];
+};
+
 __global__ void __launch_bounds__(kTopkThreads) est_topk_kernel(EstArgs a) {
-    __shared__ uint32_t whist[kTopkWaves * kHistStride];
-    __shared__ uint32_t hist[256];
-    __shared__ uint32_t s_prefix, s_krem;
-    __shared__ int64_t wgt[kTopkWaves], weq[kTopkWaves];
+    __shared__ TopkLds sm;
     const int BH = a.B * a.Hq;
     const bool is_v = blockIdx.x < BH;
     const int bh = is_v ? blockIdx.x : blockIdx.x - BH;
-    const int k = is_v ? a.k_v : a.k_s;
+    const int cap = is_v ? a.k_v : a.k_s;
+    const double p = is_v ? a.p_v : a.p_s;
     const uint32_t* sc = reinterpret_cast<const uint32_t*>((is_v ? a.v_score : a.s_score) + int64_t(bh) * a.N);
-    int32_t* out = (is_v ? a.v_idx : a.s_idx) + int64_t(bh) * k;
+    int32_t* out = (is_v ? a.v_idx : a.s_idx) + int64_t(bh) * cap;
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int N = a.N;
     const int n4 = N / 4;
     const u32x4* sc4 = reinterpret_cast<const u32x4*>(sc);
 
-    uint32_t prefix = 0, mask = 0, krem = uint32_t(k);
-    for (int shift = 24; shift >= 0; shift -= 8) {
-        for (int i = tid; i < kTopkWaves * kHistStride; i += kTopkThreads) whist[i] = 0;
-        __syncthreads();
-        uint32_t* wh = whist + wv * kHistStride;
-        for (int i0 = tid; i0 < n4; i0 += 4 * kTopkThreads) {
-            u32x4 x[4];
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const int i = i0 + u * kTopkThreads;
-                x[u] = i < n4 ? sc4[i] : u32x4{~0u, ~0u, ~0u, ~0u};
-            }
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const bool in = i0 + u * kTopkThreads < n4;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) hist_add(wh, (x[u][e] >> shift) & 255u, in && (x[u][e] & mask) == prefix);
-            }
+    uint32_t k = uint32_t(cap);
+    uint32_t prefix = 0, krem = 0;
+    bool selected = false;
+    if (p > 0.0) {
+        // ---- total mass and the threshold theta = ceil(p T)
+        uint64_t t = 0;
+        for (int i = tid; i < n4; i += kTopkThreads) {
+            const u32x4 x = sc4[i];
+            t += mass_fx(x[0]) + mass_fx(x[1]) + mass_fx(x[2]) + mass_fx(x[3]);
         }
+        t = wave_sum_u64(t);
+        if (lane == 0) sm.wsum[wv] = t;
         __syncthreads();
-        for (int bb = tid; bb < 256; bb += kTopkThreads) {
-            uint32_t t = 0;
-            for (int w = 0; w < kTopkWaves; ++w) t += whist[w * kHistStride + bb];
-            hist[bb] = t;
-        }
-        __syncthreads();
-        if (tid == 0) {
-            uint32_t run = 0;
-            int bsel = 0;
-            for (int bb = 255; bb >= 0; --bb) {
-                if (run + hist[bb] >= krem) {
-                    bsel = bb;
-                    break;
+        uint64_t total = 0;
+        for (int w = 0; w < kTopkWaves; ++w) total += sm.wsum[w];
+        uint64_t rem = uint64_t(ceil(p * double(total)));
+        uint32_t above = 0;   // count of scores above the current prefix
+        if (total > 0) {
+            uint32_t mask = 0;
+            for (int shift = 24; shift >= 0; shift -= 8) {
+                for (int i = tid; i < kTopkWaves * kHistStride; i += kTopkThreads) sm.whist[i] = 0;
+                for (int i = tid; i < kTopkWaves * 256; i += kTopkThreads) sm.wmass[i] = 0;
+                __syncthreads();
+                uint32_t* wh = sm.whist + wv * kHistStride;
+                uint64_t* wm = sm.wmass + wv * 256;
+                for (int i0 = tid; i0 < n4; i0 += 4 * kTopkThreads) {
+                    u32x4 x[4];
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        const int i = i0 + u * kTopkThreads;
+                        x[u] = i < n4 ? sc4[i] : u32x4{0u, 0u, 0u, 0u};
+                    }
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        const bool in = i0 + u * kTopkThreads < n4;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            hist_add_mass(wh, wm, (x[u][e] >> shift) & 255u, mass_fx(x[u][e]),
+                                          in && (x[u][e] & mask) == prefix);
+                    }
                 }
-                run += hist[bb];
+                __syncthreads();
+                for (int bb = tid; bb < 256; bb += kTopkThreads) {
+                    uint32_t c = 0;
+                    uint64_t m = 0;
+                    for (int w = 0; w < kTopkWaves; ++w) {
+                        c += sm.whist[w * kHistStride + bb];
+                        m += sm.wmass[w * 256 + bb];
+                    }
+                    sm.hist[bb] = c;
+                    sm.hmass[bb] = m;
+                }
+                __syncthreads();
+                if (tid == 0) {
+                    // the prefix group holds at least rem (> 0): some bin is taken
+                    uint64_t run = 0;
+                    uint32_t runc = 0;
+                    int bsel = 0;
+                    for (int bb = 255; bb >= 0; --bb) {
+                        if (run + sm.hmass[bb] >= rem) {
+                            bsel = bb;
+                            break;
+                        }
+                        run += sm.hmass[bb];
+                        runc += sm.hist[bb];
+                    }
+                    sm.s_prefix = prefix | (uint32_t(bsel) << shift);
+                    sm.s_rem = rem - run;
+                    sm.s_above = above + runc;
+                    if (shift == 0) {
+                        // t = the prefix; every score equal to t adds mass_fx(t)
+                        const uint64_t qt = mass_fx(sm.s_prefix);
+                        const uint64_t ties = qt ? (sm.s_rem + qt - 1) / qt : uint64_t(sm.hist[bsel]);
+                        sm.s_k = uint32_t(min<uint64_t>(uint64_t(above + runc) + min<uint64_t>(ties, sm.hist[bsel]),
+                                                        uint64_t(N)));
+                    }
+                }
+                __syncthreads();
+                prefix = sm.s_prefix;
+                rem = sm.s_rem;
+                above = sm.s_above;
+                mask |= 255u << shift;
+                __syncthreads();
             }
-            s_prefix = prefix | (uint32_t(bsel) << shift);
-            s_krem = krem - run;
+            k = sm.s_k;
+        } else {
+            k = 1;   // no mass at all: one entry reaches p of it
         }
-        __syncthreads();
-        prefix = s_prefix;
-        krem = s_krem;
-        mask |= 255u << shift;
-        __syncthreads();
+        if (k <= uint32_t(cap)) {
+            krem = k - above;
+            selected = total > 0;
+        } else {
+            k = uint32_t(cap);
+        }
+    }
+    if (!selected) {
+        prefix = 0;
+        uint32_t mask = 0;
+        krem = k;
+        for (int shift = 24; shift >= 0; shift -= 8) {
+            for (int i = tid; i < kTopkWaves * kHistStride; i += kTopkThreads) sm.whist[i] = 0;
+            __syncthreads();
+            uint32_t* wh = sm.whist + wv * kHistStride;
+            for (int i0 = tid; i0 < n4; i0 += 4 * kTopkThreads) {
+                u32x4 x[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int i = i0 + u * kTopkThreads;
+                    x[u] = i < n4 ? sc4[i] : u32x4{~0u, ~0u, ~0u, ~0u};
+                }
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const bool in = i0 + u * kTopkThreads < n4;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) hist_add(wh, (x[u][e] >> shift) & 255u, in && (x[u][e] & mask) == prefix);
+                }
+            }
+            __syncthreads();
+            for (int bb = tid; bb < 256; bb += kTopkThreads) {
+                uint32_t t = 0;
+                for (int w = 0; w < kTopkWaves; ++w) t += sm.whist[w * kHistStride + bb];
+                sm.hist[bb] = t;
+            }
+            __syncthreads();
+            if (tid == 0) {
+                uint32_t run = 0;
+                int bsel = 0;
+                for (int bb = 255; bb >= 0; --bb) {
+                    if (run + sm.hist[bb] >= krem) {
+                        bsel = bb;
+                        break;
+                    }
+                    run += sm.hist[bb];
+                }
+                sm.s_prefix = prefix | (uint32_t(bsel) << shift);
+                sm.s_krem = krem - run;
+            }
+            __syncthreads();
+            prefix = sm.s_prefix;
+            krem = sm.s_krem;
+            mask |= 255u << shift;
+            __syncthreads();
+        }
     }
     // prefix = bit pattern of the k-th largest; take all above it and the
     // first krem equal ones, in index order.  Wave wv owns the contiguous
@@ -352,14 +503,14 @@ __global__ void __launch_bounds__(kTopkThreads) est_topk_kernel(EstArgs a) {
         eq += __popcll(__ballot(i < hi && x == prefix));
     }
     if (lane == 0) {
-        wgt[wv] = gt;
-        weq[wv] = eq;
+        sm.wgt[wv] = gt;
+        sm.weq[wv] = eq;
     }
     __syncthreads();
     int64_t off = 0, eq_before = 0;
     for (int w = 0; w < wv; ++w) {
-        off += wgt[w] + min<int64_t>(weq[w], max<int64_t>(0, int64_t(krem) - eq_before));
-        eq_before += weq[w];
+        off += sm.wgt[w] + min<int64_t>(sm.weq[w], max<int64_t>(0, int64_t(krem) - eq_before));
+        eq_before += sm.weq[w];
     }
     for (int i0 = lo; i0 < hi; i0 += 64) {
         const int i = i0 + lane;
@@ -371,6 +522,10 @@ __global__ void __launch_bounds__(kTopkThreads) est_topk_kernel(EstArgs a) {
         if (take) out[off + __popcll(mt & below)] = i;
         off += __popcll(mt);
         eq_before += __popcll(me);
+    }
+    if (p > 0.0) {
+        for (int i = int(k) + tid; i < cap; i += kTopkThreads) out[i] = -1;
+        if (tid == 0) (is_v ? a.v_cnt : a.s_cnt)[bh] = int32_t(k);
     }
 }
 

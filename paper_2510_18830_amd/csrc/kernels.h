@@ -154,8 +154,13 @@ struct EstArgs {
     float scale;
     float* v_score;     // [B*Hq, N]
     float* s_score;     // [B*Hq, N]
-    int32_t* v_idx;
-    int32_t* s_idx;
+    int32_t* v_idx;     // [B*Hq, k_v]
+    int32_t* s_idx;     // [B*Hq, k_s]
+    // top-p budget (p_v > 0): k_v / k_s are the caps, the budgets go to
+    // v_cnt / s_cnt [B*Hq] and the unused slots of v_idx / s_idx are set to -1
+    double p_v, p_s;
+    int32_t* v_cnt;
+    int32_t* s_cnt;
     // workspace (est_carve)
     float* part_max;    // [B*Hq, nchunk, 64]
     float* part_sum;    // [B*Hq, nchunk, 64]

@@ -93,3 +93,33 @@ def assert_topk_match(got, ref, score, k, rel=TOPK_REL):
     bad = diff[np.abs(score[diff] - t_k) > rel * abs(t_k)]
     assert bad.size == 0, f"{bad.size} index differences outside the tie band (t_k={t_k:.6e})"
     assert len(np.unique(got)) == k and np.all(np.diff(got) > 0)
+
+
+TOPP_MASS_REL = 1e-4
+
+
+def budget_fixed_point(score32, p: float) -> int:
+    """score_cover (Algorithm 1) taken in the kernel's precision, so that the GPU's
+    budget can be checked exactly on its own scores: every fp32 score x counts
+    floor(x 2^40) (exact integers, summed in any order), the threshold is
+    ceil(p T) rounded in fp64, and k is the first count of the descending list
+    whose cumulative mass reaches it."""
+    x = np.asarray(score32, dtype=np.float32).astype(np.float64)
+    q = np.floor(x * 2.0 ** 40).astype(np.int64)
+    theta = math.ceil(p * float(int(q.sum())))
+    order = np.lexsort((np.arange(x.size), -x))
+    c = np.cumsum(q[order])
+    return int(np.searchsorted(c, theta, side="left")) + 1
+
+
+def assert_budget_near(cnt: int, score, p: float, kmax: int, rel=TOPP_MASS_REL):
+    """The budget against the oracle's fp64 scores: the mass of the cnt largest
+    reaches p of the total and that of the cnt - 1 largest stays below it, both
+    within `rel` of the threshold (a cap at kmax only needs the second)."""
+    srt = np.sort(np.asarray(score, dtype=np.float64))[::-1]
+    c = np.cumsum(srt)
+    theta = p * c[-1]
+    assert 1 <= cnt <= kmax
+    if cnt < kmax:
+        assert c[cnt - 1] >= theta * (1 - rel), f"mass {c[cnt - 1]:.6e} below p of the total {theta:.6e}"
+    assert cnt == 1 or c[cnt - 2] < theta * (1 + rel), f"cnt {cnt} larger than needed"

@@ -80,3 +80,20 @@ def test_index_overflow_flag(gpu):
     ms.build_index(dims, tv, ts, ok)
     torch.cuda.synchronize()
     assert int(ok["overflow"].item()) == 0
+
+
+@pytest.mark.parametrize("W,r,t,layout", [(1, 0, 0, "striped"), (4, 1, 2, "striped"), (2, 1, 1, "zigzag")])
+def test_index_from_padded_topp_lists(gpu, W, r, t, layout):
+    # top-p lists: per-head counts, -1 in the unused slots
+    rng = np.random.default_rng(40 + W + r + t)
+    B, Hq, Ng, k_v, k_s = 1, 3, 8192, 120, 900
+    v, s = _indices(rng, B, Hq, Ng, k_v, k_s)
+    for h in range(Hq):
+        v[0, h, int(rng.integers(1, k_v)):] = -1
+        s[0, h, int(rng.integers(1, k_s)):] = -1
+    ref = OI.Index(v, s, Ng, world=W, rank=r, step=t, layout=layout).csr()
+    dims = ms.make_dims(B, Ng // W, Hq, 1, 128)
+    idx = ms.make_index(dims, torch.from_numpy(v).to(gpu), torch.from_numpy(s).to(gpu), ms.make_ring(W, r, t, layout))
+    torch.cuda.synchronize()
+    _compare(gpu_csr(idx), ref)
+    assert int(idx["overflow"].item()) == 0

@@ -84,3 +84,24 @@ def test_workspace_queries_are_positive():
     assert L.msparse_estimate_workspace(ctypes.byref(d), 64, 2048, 8192) >= 2 * 32 * 131072 * 4
     assert L.msparse_attn_bwd_workspace(ctypes.byref(d), 32 * 2048) >= 32 * 131072 * 4
     assert L.msparse_index_workspace(ctypes.byref(d), 2048, 8192, ctypes.byref(ms.Ring(8, 0, 3, 1))) > 0
+
+
+def test_topp_validation_before_launch():
+    L = ms.lib()
+    d = ms.make_dims(1, 4096, 4, 2, 128)
+    fake = ctypes.c_void_p(16)
+    iv = ctypes.c_void_p(32)
+
+    def call(p_v, p_s, kv=10, ks=10, cnt=iv, ws=1 << 30):
+        return L.msparse_estimate_topp(ctypes.byref(d), fake, fake, 64, p_v, p_s, kv, ks, iv, iv, cnt, cnt, None,
+                                       None, fake, ws, None)
+
+    for p in (0.0, 1.0, -0.5, 1.5, float("nan")):
+        _bad(-1, call, p, 0.5)
+        _bad(-1, call, 0.5, p)
+    _bad(-1, lambda: call(0.5, 0.5, cnt=None))
+    _bad(-1, lambda: call(0.5, 0.5, kv=0))
+    _bad(-1, lambda: call(0.5, 0.5, ks=4097))
+    _bad(-4, lambda: call(0.5, 0.5, ws=8))
+    assert L.msparse_estimate_topp_workspace(ctypes.byref(d), 64, 100, 100) == \
+        L.msparse_estimate_workspace(ctypes.byref(d), 64, 100, 100)
