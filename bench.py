@@ -247,6 +247,97 @@ def ring_leg(x, v_idx, s_idx, wl, world: int, rank: int, steps: int):
     }
 
 
+def prefill_leg(ms, torch, wl, x, steps: int, warmup: int) -> dict:
+    """Forward-only sparse prefill (inference): estimate -> index -> forward per
+    layer, inputs resident in HBM, stage times from HIP events on the stream."""
+    dev = x["q"].device
+    q, k, v = x["q"], x["k"], x["v"]
+    B, Hq, N, d = wl.batch, wl.heads_q, wl.seq, wl.head_dim
+    dims = ms.make_dims(B, N, Hq, wl.heads_kv, d)
+    est_ws = ms._workspace(ms.lib().msparse_estimate_workspace(ms.ctypes.byref(dims), wl.last_q, wl.k_v, wl.k_s), dev)
+    idx_ws = ms._workspace(ms.index_workspace_bytes(dims, wl.k_v, wl.k_s), dev)
+    fwd_ws = ms._workspace(ms.attn_fwd_workspace_bytes(dims), dev)
+    v_idx = torch.empty((B, Hq, wl.k_v), dtype=torch.int32, device=dev)
+    s_idx = torch.empty((B, Hq, wl.k_s), dtype=torch.int32, device=dev)
+    out = torch.empty_like(q)
+    lse = torch.empty(q.shape[:-1], dtype=torch.float32, device=dev)
+    ev = {s_: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for s_ in ("estimate", "index", "fwd")}
+    acc = {s_: 0.0 for s_ in ev}
+    state = {}
+
+    def step(timed):
+        def mark(stage, i):
+            if timed:
+                ev[stage][i].record()
+        mark("estimate", 0)
+        ms.estimate(dims, q, k, wl.last_q, wl.k_v, wl.k_s, v_idx, s_idx, workspace=est_ws)
+        mark("estimate", 1)
+        mark("index", 0)
+        blk, col, vcol = ms.index_count(dims, v_idx, s_idx, workspace=idx_ws)
+        if state.get("caps", (0, 0, 0))[0] < blk or state["caps"][1] < col or state["caps"][2] < vcol:
+            state["caps"] = (int(blk * 1.05) + 64, int(col * 1.05) + 64, vcol)
+            state["idx"] = ms.alloc_index(dims, *state["caps"], dev)
+        ms.build_index(dims, v_idx, s_idx, state["idx"], workspace=idx_ws)
+        mark("index", 1)
+        mark("fwd", 0)
+        ms.attn_fwd(dims, q, k, v, state["idx"], out=out, lse=lse, workspace=fwd_ws)
+        mark("fwd", 1)
+        state["nnz"] = (blk, col)
+        if timed:
+            torch.cuda.synchronize()
+            for s_, (a, b) in ev.items():
+                acc[s_] += a.elapsed_time(b)
+
+    for _ in range(warmup):
+        step(False)
+    torch.cuda.synchronize()
+    for _ in range(steps):
+        step(True)
+    stage = {s_: acc[s_] / steps for s_ in acc}
+    T, C = state["nnz"]
+    fwd_flops = 4.0 * d * (4096.0 * T + 64.0 * C)
+    nb = N // 64
+    total = sum(stage.values())
+    del state
+    torch.cuda.empty_cache()
+    return {"ms_per_layer": round(total, 3), "stage_ms": {s_: round(t, 3) for s_, t in stage.items()},
+            "fwd_tflops_kernel": round(fwd_flops / (stage["fwd"] * 1e-3) / 1e12, 2),
+            "fwd_tflops_layer": round(fwd_flops / (total * 1e-3) / 1e12, 2),
+            "tokens_per_s": round(B * N / (total * 1e-3)),
+            "counted_tiles": int(T), "counted_col_pairs": int(C),
+            "tile_density_causal": round(T / (B * Hq * nb * (nb + 1) / 2.0), 4),
+            "shape": {"seq_len": N, "heads_q": Hq, "heads_kv": wl.heads_kv, "head_dim": d, "k_v": wl.k_v,
+                      "k_s": wl.k_s}}
+
+
+def topp_leg(ms, torch, wl, x, ps, reps: int = 3) -> dict:
+    """Estimation with the online top-p budget (score_cover): time per call and
+    the budgets it picks, per fraction p (caps = N, so nothing is capped)."""
+    dev = x["q"].device
+    B, Hq, N, d = wl.batch, wl.heads_q, wl.seq, wl.head_dim
+    dims = ms.make_dims(B, N, Hq, wl.heads_kv, d)
+    ws = ms._workspace(ms.lib().msparse_estimate_topp_workspace(ms.ctypes.byref(dims), wl.last_q, N, N), dev)
+    out = {}
+    for p in ps:
+        ms.estimate_topp(dims, x["q"], x["k"], wl.last_q, p, p, N, N, workspace=ws)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            vi, si, vc, sc = ms.estimate_topp(dims, x["q"], x["k"], wl.last_q, p, p, N, N, workspace=ws)
+        b.record()
+        torch.cuda.synchronize()
+        vc = vc.float()
+        sc = sc.float()
+        out[str(p)] = {"estimate_ms": round(a.elapsed_time(b) / reps, 3),
+                       "k_v_min_mean_max": [int(vc.min()), round(float(vc.mean()), 1), int(vc.max())],
+                       "k_s_min_mean_max": [int(sc.min()), round(float(sc.mean()), 1), int(sc.max())]}
+        del vi, si
+    torch.cuda.empty_cache()
+    return out
+
+
 def torch_index(rows):
     import torch
     return torch.from_numpy(rows)
@@ -262,6 +353,9 @@ def main():
     ap.add_argument("--cpu-rows", type=int, default=1024)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--ring", type=int, default=1, help="also time worker 0's share of the 8-worker ring (512K)")
+    ap.add_argument("--prefill", default="layer_128k,layer_512k,prefill_1m",
+                    help="workloads timed as forward-only sparse prefill ('' to skip)")
+    ap.add_argument("--topp", default="0.5,0.9", help="top-p fractions timed on the main workload ('' to skip)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (HBM counter calibration) and exit")
     args = ap.parse_args()
@@ -426,6 +520,20 @@ def main():
         si_t = torch.from_numpy(main_r["s_idx"]).to(dev)
         line["detail"]["ring_512k_w8"] = ring_leg(main_r["x"], vi_t, si_t, rw, rw.world, 0, max(1, args.steps // 2))
         torch.cuda.empty_cache()
+    if args.topp:
+        print("[bench] top-p estimation", file=sys.stderr, flush=True)
+        line["detail"][f"{wl.name}_topp"] = topp_leg(ms, torch, wl, main_r["x"],
+                                                     [float(p) for p in args.topp.split(",")])
+    if args.prefill:
+        line["detail"]["prefill"] = {}
+        for pname in args.prefill.split(","):
+            pwl = WORKLOADS[pname]
+            print(f"[bench] prefill {pname}", file=sys.stderr, flush=True)
+            px = main_r["x"] if pname == wl.name else make_inputs(pwl, dev, with_do=False)
+            line["detail"]["prefill"][pname] = prefill_leg(ms, torch, pwl, px, args.steps, args.warmup)
+            if px is not main_r["x"]:
+                del px
+            torch.cuda.empty_cache()
     if not args.no_cpu:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline(wl, main_r["x"], main_r["v_idx"], main_r["s_idx"], args.cpu_rows)

@@ -72,6 +72,8 @@ WORKLOADS = {
     "ring_512k_w8": Workload("ring_512k_w8", 1, 28, 4, 524288, 128, 64, 4096, 16384, 64, True, 5,
                              world=8, layout="striped"),
     "layer_512k": Workload("layer_512k", 1, 28, 4, 524288, 128, 64, 4096, 16384, 64, True, 5),
+    # forward-only sparse prefill (inference) at 1M tokens, the 512K layer's heads and budgets
+    "prefill_1m": Workload("prefill_1m", 1, 28, 4, 1048576, 128, 64, 4096, 16384, 64, True, 6),
 }
 
 

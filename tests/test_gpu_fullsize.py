@@ -86,3 +86,48 @@ def test_fullsize_sampled_rows_and_invariants(gpu, name):
         assert ((s_dv - want).abs() <= 1e-4 * dv64.abs().sum(0) + 1e-3).all(), f"sum dV kv{g}"
     del x, out, out32, dq, dk, dv
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("name", ["prefill_1m"])
+def test_prefill_forward_sampled_rows(gpu, name):
+    """Forward-only sparse prefill at 1M tokens: estimate sets from the oracle on
+    two heads, GPU index and forward over every head, sampled rows checked."""
+    wl = WORKLOADS[name]
+    print(f"prefill {name}", flush=True)
+    B, Hq, Hkv, N, d = wl.batch, wl.heads_q, wl.heads_kv, wl.seq, wl.head_dim
+    G = Hq // Hkv
+    scale = 1 / math.sqrt(d)
+    x = make_inputs(wl, gpu, with_do=False)
+    heads = [3, Hq - 2]
+    sets = {}
+    for h in heads:
+        vs, ss = OE.vs_scores(to_f64(x["q"][0, h, N - wl.last_q:].cpu()), to_f64(x["k"][0, h // G].cpu()), scale)
+        sets[h] = (OE.topk_lower(vs, wl.k_v), OE.topk_lower(ss, wl.k_s))
+        del vs, ss
+    vi = np.stack([sets[heads[h % 2]][0] for h in range(Hq)])[None].astype(np.int32)
+    si = np.stack([sets[heads[h % 2]][1] for h in range(Hq)])[None].astype(np.int32)
+    print("oracle sets ready", flush=True)
+    dims = ms.make_dims(B, N, Hq, Hkv, d)
+    idx = ms.make_index(dims, torch.from_numpy(vi).to(gpu), torch.from_numpy(si).to(gpu))
+    out, lse = ms.attn_fwd(dims, x["q"], x["k"], x["v"], idx)
+    torch.cuda.synchronize()
+    print("gpu done", flush=True)
+    nb = N // 64
+    blocks = np.unique(np.concatenate([[0, nb - 1], np.linspace(1, nb - 2, 9).astype(np.int64)]))
+    rows = np.unique(np.concatenate([blocks * 64 + 5, blocks * 64 + 63]))
+    sel = torch.from_numpy(rows).to(gpu)
+    for h in heads:
+        ref = OI.Index(vi[:, h:h + 1], si[:, h:h + 1], N)
+        q = to_f64(x["q"][:, h:h + 1, sel].cpu())
+        k = to_f64(x["k"][:, h // G:h // G + 1].cpu())
+        v = to_f64(x["v"][:, h // G:h // G + 1].cpu())
+
+        class Rows:
+            def mask_rows(self, bh, rr):
+                return ref.mask_rows(0, rows[np.asarray(rr)])
+
+        ro, rl = OA.layer_fwd(q, k, v, Rows(), scale)
+        assert_close(f"out h{h}", out[:, h:h + 1, sel].float().cpu().numpy(), ro)
+        assert_lse_close(lse[:, h:h + 1, sel].cpu().numpy(), rl)
+    del x, out, lse
+    torch.cuda.empty_cache()
