@@ -26,6 +26,13 @@ Each worker keeps its own blocks in ascending global order (its local order).
 At ring step t, worker r holds the KV shard of worker s = (r - t) mod W; the
 step's lists are the whole-sequence lists restricted to the keys of shard s, in
 local coordinates (convert_index of Algorithms 1 and 2).
+
+Hierarchical order (Section 4.3, Algorithm 2): the W = nodes x inner workers
+run an outer ring over nodes and, inside each outer step, an inner ring over
+the node's cards; ring_schedule replays the loops' buffer passing to find which
+shard each worker holds at each step.  ring_work and imbalance_degrees give the
+worker x shard workload in tile-equivalents and the imbalance degrees of
+Section 5's workload balance analysis.
 """
 import numpy as np
 
@@ -54,6 +61,43 @@ def owner(g: int, nb: int, W: int, layout: str) -> int:
 
 def local_blocks(w: int, nb: int, W: int, layout: str) -> np.ndarray:
     return np.array([g for g in range(nb) if owner(g, nb, W, layout) == w], dtype=np.int64)
+
+
+def ring_schedule(W: int, inner: int = 0) -> np.ndarray:
+    """S[r, t] = the worker whose KV shard worker r holds at step t.
+
+    inner = 0 (or 1, or W) is the flat ring: every step each worker passes its
+    current KV buffer to worker r + 1.  Otherwise the W workers sit on
+    W / inner nodes of `inner` cards (worker r = node * inner + card), and the
+    loops of Algorithm 2 are replayed: at the start of each outer step a
+    worker posts its current buffer to the same card of the next node; the
+    inner loop computes `inner` steps, passing buffers to the next card of the
+    same node between them; at the end of the outer step the buffer posted by
+    the previous node's card replaces the current one.
+    """
+    if inner in (0, 1, W):
+        inner, nodes = W, 1
+        flat = True
+    else:
+        assert W % inner == 0
+        nodes = W // inner
+        flat = False
+    buf = list(range(W))                     # shard id in each worker's KV buffer
+    S = np.zeros((W, W), dtype=np.int64)
+    step = 0
+    for i in range(nodes):
+        posted = list(buf)                   # the outer send takes the buffer as it is now
+        for j in range(inner):
+            for r in range(W):
+                S[r, step] = buf[r]
+            step += 1
+            if j < inner - 1:                # inner pass: receive from the previous card of the node
+                buf = [buf[(r // inner) * inner + (r % inner - 1) % inner] for r in range(W)]
+        if i < nodes - 1:                    # outer pass: receive what the previous node posted
+            buf = [posted[(r - inner) % W] for r in range(W)]
+    if flat:
+        assert all(S[r, t] == (r - t) % W for r in range(W) for t in range(W))
+    return S
 
 
 def head_lists(v_idx, s_idx, N: int):
@@ -87,7 +131,7 @@ class Index:
     """
 
     def __init__(self, v_idx, s_idx, N: int, world: int = 1, rank: int = 0, step: int = 0,
-                 layout: str = "striped"):
+                 layout: str = "striped", inner: int = 0):
         v_idx = np.asarray(v_idx)
         s_idx = np.asarray(s_idx)
         BH = v_idx.shape[0] * v_idx.shape[1]
@@ -95,7 +139,7 @@ class Index:
         s2 = s_idx.reshape(BH, -1)
         nb = N // BLOCK
         W = world
-        shard = (rank - step) % W
+        shard = int(ring_schedule(W, inner)[rank, step]) if W > 1 else 0
         qg = local_blocks(rank, nb, W, layout) if W > 1 else np.arange(nb)
         kg = local_blocks(shard, nb, W, layout) if W > 1 else np.arange(nb)
         kloc = {int(g): j for j, g in enumerate(kg)}
@@ -186,6 +230,41 @@ class Index:
         """Tile-equivalents per head: selected tiles + columns / 64."""
         return np.array([sum(len(x) for x in self.blocks[bh]) + sum(len(x) for x in self.cols[bh]) / BLOCK
                          for bh in range(self.BH)])
+
+
+def ring_work(v_idx, s_idx, N: int, W: int, layout: str):
+    """Selected tiles and column entries of query worker r against KV shard s,
+    summed over heads: (tiles[W, W], cols[W, W]), int64.  Worker r computes the
+    query blocks it owns; a tile (i, j) or a column c of query block i falls to
+    shard owner(j) or owner(c // 64)."""
+    v_idx = np.asarray(v_idx)
+    s_idx = np.asarray(s_idx)
+    BH = v_idx.shape[0] * v_idx.shape[1]
+    v2, s2 = v_idx.reshape(BH, -1), s_idx.reshape(BH, -1)
+    nb = N // BLOCK
+    own = np.array([owner(g, nb, W, layout) for g in range(nb)], dtype=np.int64)
+    tiles = np.zeros((W, W), dtype=np.int64)
+    cols = np.zeros((W, W), dtype=np.int64)
+    for bh in range(BH):
+        _, blocks, cl = head_lists(v2[bh], s2[bh], N)
+        for i in range(nb):
+            np.add.at(tiles[own[i]], own[blocks[i]], 1)
+            np.add.at(cols[own[i]], own[cl[i] // BLOCK], 1)
+    return tiles, cols
+
+
+def imbalance_degrees(work, schedule) -> tuple:
+    """Imbalance degrees (max / mean) of a worker x shard workload under a step
+    schedule S[r, t] (Section 5, workload balance analysis): the worker level
+    averages, over steps, max / mean over workers of the step's work; the step
+    level averages, over workers, max / mean over that worker's steps."""
+    w = np.asarray(work, dtype=np.float64)
+    S = np.asarray(schedule)
+    W = w.shape[0]
+    per_step = np.array([[w[r, S[r, t]] for t in range(W)] for r in range(W)])   # [worker, step]
+    worker_level = np.mean([per_step[:, t].max() / per_step[:, t].mean() for t in range(W)])
+    step_level = np.mean([per_step[r].max() / per_step[r].mean() for r in range(W)])
+    return float(worker_level), float(step_level)
 
 
 def imbalance(work) -> float:

@@ -143,3 +143,71 @@ def test_unused_slots_are_dropped():
             b = I.Index(vp[None, None], sp[None, None], N, W, 1 % W, t, layout).csr()
             for key in a:
                 np.testing.assert_array_equal(a[key], b[key], err_msg=key)
+
+
+# ---- hierarchical step order (Section 4.3, Algorithm 2) and workload matrix
+
+@pytest.mark.parametrize("W,inner", [(2, 0), (4, 2), (8, 4), (8, 2), (12, 3), (12, 4), (6, 6), (6, 1)])
+def test_ring_schedule_properties(W, inner):
+    S = I.ring_schedule(W, inner)
+    ar = np.arange(W)
+    for r in range(W):
+        assert sorted(S[r].tolist()) == ar.tolist()           # every shard once per worker
+        assert S[r, 0] == r                                  # step 0: own KV
+    for t in range(W):
+        assert sorted(S[:, t].tolist()) == ar.tolist()       # each shard held once per step
+    w = W if inner in (0, 1, W) else inner
+    nodes = W // w
+    for r in range(W):
+        n, c = divmod(r, w)
+        for t in range(W):
+            i, j = divmod(t, w)
+            # the inner loop only circulates one node's shards, one card back per step
+            assert S[r, t] == ((n - i) % nodes) * w + (c - j) % w, (r, t)
+
+
+def test_ring_schedule_flat_limits():
+    for W in (3, 4, 8):
+        flat = np.array([[(r - t) % W for t in range(W)] for r in range(W)])
+        for inner in (0, 1, W):
+            np.testing.assert_array_equal(I.ring_schedule(W, inner), flat)
+
+
+@pytest.mark.parametrize("W,layout,inner", [(2, "striped", 0), (4, "striped", 0), (4, "striped", 2),
+                                            (2, "zigzag", 0), (4, "zigzag", 2)])
+def test_ring_work_matches_ring_indices(W, layout, inner):
+    rng = np.random.default_rng(60 + W)
+    N = 2048
+    v = rng.integers(0, N, (1, 2, 40)).astype(np.int32)
+    s = np.concatenate([np.tile(np.arange(70), (1, 2, 1)), rng.integers(0, N, (1, 2, 30))], -1).astype(np.int32)
+    tiles, cols = I.ring_work(v, s, N, W, layout)
+    S = I.ring_schedule(W, inner)
+    for r in range(W):
+        for t in range(W):
+            c = I.Index(v, s, N, W, r, t, layout, inner=inner).csr()
+            assert c["blk_ptr"][-1] == tiles[r, S[r, t]] and c["col_ptr"][-1] == cols[r, S[r, t]], (r, t)
+    whole = I.Index(v, s, N).csr()
+    assert tiles.sum() == whole["blk_ptr"][-1] and cols.sum() == whole["col_ptr"][-1]
+
+
+def test_ring_work_dense_causal_brute_force():
+    N, W = 1024, 4
+    nb = N // B64
+    v = np.zeros((1, 1, 1), np.int32)
+    s = np.arange(N, dtype=np.int32)[None, None]         # every offset: the full causal grid, no columns
+    for layout in ("striped", "zigzag"):
+        tiles, cols = I.ring_work(v, s, N, W, layout)
+        want = np.zeros((W, W), np.int64)
+        for i in range(nb):
+            for j in range(i + 1):
+                want[I.owner(i, nb, W, layout), I.owner(j, nb, W, layout)] += 1
+        np.testing.assert_array_equal(tiles, want)
+        assert cols.sum() == 0
+
+
+def test_imbalance_degrees_hand_example():
+    work = np.array([[3.0, 1.0], [2.0, 2.0]])
+    # flat ring: worker 0 sees shards 0, 1 (3, 1); worker 1 sees 1, 0 (2, 2)
+    wl, sl = I.imbalance_degrees(work, I.ring_schedule(2))
+    assert abs(wl - (3 / 2.5 + 2 / 1.5) / 2) < 1e-15
+    assert abs(sl - (3 / 2 + 1.0) / 2) < 1e-15
