@@ -338,6 +338,42 @@ def topp_leg(ms, torch, wl, x, ps, reps: int = 3) -> dict:
     return out
 
 
+def balance_leg(ms, torch, wl, v_idx, s_idx, worlds, inner: int = 8) -> dict:
+    """Striped vs zigzag ring balance from the index (Section 4.2; Section 5's
+    workload balance analysis): per world size W, the worker x shard workload in
+    tile-equivalents (tiles + columns / 64, msparse_ring_work) and its imbalance
+    degrees max / mean under the flat ring and the hierarchical order with
+    `inner` cards per node: worker level = mean over steps of max / mean over
+    workers, step level = mean over workers of max / mean over steps."""
+    import numpy as np
+    dims = ms.make_dims(wl.batch, wl.seq, wl.heads_q, wl.heads_kv, wl.head_dim)
+    ws = ms._workspace(ms.index_workspace_bytes(dims, v_idx.shape[-1], s_idx.shape[-1]), v_idx.device)
+
+    def degrees(work, W, inn):
+        sched = np.array([[ms.ring_shard(W, inn, r, t) for t in range(W)] for r in range(W)])
+        per = work[np.arange(W)[:, None], sched]            # [worker, step]
+        return (float(np.mean(per.max(0) / per.mean(0))), float(np.mean(per.max(1) / per.mean(1))))
+
+    out = {}
+    for layout in ("striped", "zigzag"):
+        for W in worlds:
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            tiles, cols = ms.ring_work(dims, v_idx, s_idx, W, layout, workspace=ws)
+            b.record()
+            torch.cuda.synchronize()
+            work = tiles.cpu().numpy().astype(np.float64) + cols.cpu().numpy() / 64.0
+            fw, fs = degrees(work, W, 0)
+            ent = {"ms": round(a.elapsed_time(b), 3), "worker_level_flat": round(fw, 4), "step_level": round(fs, 4),
+                   "worker0_steps_flat": [round(float(work[0, ms.ring_shard(W, 0, 0, t)])) for t in range(min(W, 8))]}
+            if W % inner == 0 and W > inner:
+                hw, hs = degrees(work, W, inner)
+                ent["worker_level_hierarchical"] = round(hw, 4)
+                assert abs(hs - fs) < 1e-9       # a step order permutes each worker's row
+            out[f"{layout}_w{W}"] = ent
+    return out
+
+
 def torch_index(rows):
     import torch
     return torch.from_numpy(rows)
@@ -356,6 +392,7 @@ def main():
     ap.add_argument("--prefill", default="layer_128k,layer_512k,prefill_1m",
                     help="workloads timed as forward-only sparse prefill ('' to skip)")
     ap.add_argument("--topp", default="0.5,0.9", help="top-p fractions timed on the main workload ('' to skip)")
+    ap.add_argument("--balance", default="8,32,128", help="ring sizes of the striped / zigzag balance sweep ('' to skip)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (HBM counter calibration) and exit")
     args = ap.parse_args()
@@ -520,6 +557,11 @@ def main():
         si_t = torch.from_numpy(main_r["s_idx"]).to(dev)
         line["detail"]["ring_512k_w8"] = ring_leg(main_r["x"], vi_t, si_t, rw, rw.world, 0, max(1, args.steps // 2))
         torch.cuda.empty_cache()
+    if args.balance:
+        print("[bench] ring balance sweep", file=sys.stderr, flush=True)
+        line["detail"][f"{wl.name}_ring_balance"] = balance_leg(
+            ms, torch, wl, torch.from_numpy(main_r["v_idx"]).to(dev), torch.from_numpy(main_r["s_idx"]).to(dev),
+            [int(w) for w in args.balance.split(",")])
     if args.topp:
         print("[bench] top-p estimation", file=sys.stderr, flush=True)
         line["detail"][f"{wl.name}_topp"] = topp_leg(ms, torch, wl, main_r["x"],

@@ -77,13 +77,21 @@ enum { MSPARSE_LAYOUT_STRIPED = 0, MSPARSE_LAYOUT_ZIGZAG = 1 };
  *   STRIPED: worker g mod world;
  *   ZIGZAG:  worker c if c < world else 2 world - 1 - c, c = g / (nb / (2 world)).
  * A worker keeps its blocks in ascending global order.  At step t worker
- * `rank` holds the KV shard of worker (rank - t) mod world.  Passing NULL
+ * `rank` holds the KV shard of worker (rank - t) mod world (the flat ring).
+ * With inner > 1 dividing world (and below it), the steps follow the
+ * hierarchical order of Section 4.3 / Algorithm 2 instead: the world / inner
+ * nodes of `inner` cards (rank = node * inner + card) run an outer ring over
+ * nodes and, within each outer step, an inner ring over the node's cards, so
+ * at step t = i * inner + j worker rank holds the shard of worker
+ *   ((node - i) mod (world / inner)) * inner + (card - j) mod inner
+ * (msparse_ring_shard).  inner = 0, 1 or world is the flat ring.  Passing NULL
  * instead of a descriptor means the whole sequence (world = 1). */
 typedef struct {
     int32_t world;
     int32_t rank;
     int32_t step;
     int32_t layout;
+    int32_t inner; /* cards per node for the hierarchical order; 0 = flat ring */
 } msparse_ring;
 
 /* The sparse index of one call (whole sequence or one ring step).  All arrays
@@ -128,6 +136,12 @@ typedef struct {
     int32_t* overflow;
     int32_t world;
 } msparse_index;
+
+/* The worker whose KV shard `rank` holds at ring step `step` (host only, no
+ * GPU work), for the flat (inner = 0, 1, world) or hierarchical order above;
+ * -1 when the arguments are outside 0 <= rank, step < world or inner does not
+ * divide world. */
+MSPARSE_API int32_t msparse_ring_shard(int32_t world, int32_t inner, int32_t rank, int32_t step);
 
 /* Human-readable name of a status code (static storage). */
 MSPARSE_API const char* msparse_strerror(msparse_status status);
@@ -202,6 +216,23 @@ MSPARSE_API msparse_status msparse_build_index(const msparse_dims* dims, const i
                                    const int32_t* s_idx, int32_t k_s, const msparse_ring* ring,
                                    const msparse_index* index, void* workspace, size_t workspace_bytes,
                                    void* stream);
+
+/* Ring workload matrix (Section 4.2; the workload balance analysis of Section 5).
+ * For a ring of `world` workers with the given layout over the whole sequence
+ * (dims: seq_q = seq_k = N, the global length), counts, summed over all heads,
+ * the selected tiles and the column entries of worker r's query blocks whose
+ * keys lie in worker s's shard:
+ *   tiles, cols  int64 [world * world] (device), entry r * world + s, overwritten.
+ * Any step order (flat or hierarchical, msparse_ring_shard) is a permutation of
+ * each row; work in tile-equivalents is tiles + cols / 64.  Integer counts,
+ * identical to the sizes msparse_index_count reports per ring step.
+ * Requires 1 <= world <= 4096 and N / 64 divisible by world (striped) or by
+ * 2 world (zigzag); otherwise as msparse_index_count.  The workspace is that
+ * of msparse_index_workspace for (dims, k_v, k_s, NULL). */
+MSPARSE_API msparse_status msparse_ring_work(const msparse_dims* dims, const int32_t* v_idx, int32_t k_v,
+                                             const int32_t* s_idx, int32_t k_s, int32_t world, int32_t layout,
+                                             int64_t* tiles, int64_t* cols, void* workspace,
+                                             size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* Sparse attention forward (block_bar_sparse_attention_forward, Algorithm 2).

@@ -31,7 +31,7 @@ class Dims(ctypes.Structure):
 
 
 class Ring(ctypes.Structure):
-    _fields_ = [("world", c_i32), ("rank", c_i32), ("step", c_i32), ("layout", c_i32)]
+    _fields_ = [("world", c_i32), ("rank", c_i32), ("step", c_i32), ("layout", c_i32), ("inner", c_i32)]
 
 
 class IndexStruct(ctypes.Structure):
@@ -56,6 +56,8 @@ _SIGS = {
     "msparse_estimate_workspace": (c_sz, [_P(Dims), c_i32, c_i32, c_i32]),
     "msparse_estimate": (c_i32, [_P(Dims), c_vp, c_vp, c_i32, c_i32, c_i32, c_vp, c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]),
     "msparse_estimate_topp_workspace": (c_sz, [_P(Dims), c_i32, c_i32, c_i32]),
+    "msparse_ring_shard": (c_i32, [c_i32, c_i32, c_i32, c_i32]),
+    "msparse_ring_work": (c_i32, [_P(Dims), c_vp, c_i32, c_vp, c_i32, c_i32, c_i32, c_vp, c_vp, c_vp, c_sz, c_vp]),
     "msparse_estimate_topp": (c_i32, [_P(Dims), c_vp, c_vp, c_i32, ctypes.c_double, ctypes.c_double, c_i32, c_i32,
                                       c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]),
     "msparse_index_workspace": (c_sz, [_P(Dims), c_i32, c_i32, _P(Ring)]),
@@ -113,10 +115,29 @@ def make_dims(batch, seq_q, heads_q, heads_kv, head_dim, seq_k=None, scale=0.0) 
     return Dims(batch, seq_q, seq_q if seq_k is None else seq_k, heads_q, heads_kv, head_dim, 64, 1, scale)
 
 
-def make_ring(world=1, rank=0, step=0, layout="striped"):
+def make_ring(world=1, rank=0, step=0, layout="striped", inner=0):
+    """A ring step descriptor; inner > 1 selects the hierarchical step order (cards per node)."""
     if world == 1 and rank == 0 and step == 0:
         return None
-    return Ring(world, rank, step, _LAYOUTS[layout] if isinstance(layout, str) else layout)
+    return Ring(world, rank, step, _LAYOUTS[layout] if isinstance(layout, str) else layout, inner)
+
+
+def ring_shard(world, inner, rank, step) -> int:
+    """msparse_ring_shard: the worker whose KV shard `rank` holds at `step` (-1 if invalid)."""
+    return int(lib().msparse_ring_shard(world, inner, rank, step))
+
+
+def ring_work(dims, v_idx, s_idx, world, layout="striped", workspace=None, stream=None):
+    """msparse_ring_work: (tiles, cols) int64 [world, world] on the device, query worker x KV shard."""
+    k_v, k_s = v_idx.shape[-1], s_idx.shape[-1]
+    if workspace is None:
+        workspace = _workspace(index_workspace_bytes(dims, k_v, k_s), v_idx.device)
+    tiles = torch.empty((world, world), dtype=torch.int64, device=v_idx.device)
+    cols = torch.empty_like(tiles)
+    _check(lib().msparse_ring_work(ctypes.byref(dims), _p(v_idx), k_v, _p(s_idx), k_s, world,
+                                   _LAYOUTS[layout] if isinstance(layout, str) else layout, _p(tiles), _p(cols),
+                                   _p(workspace), workspace.numel(), _stream(stream)))
+    return tiles, cols
 
 
 def _ring_ptr(ring):

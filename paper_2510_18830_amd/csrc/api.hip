@@ -85,6 +85,18 @@ struct RingInfo {
     int32_t world = 1, rank = 0, step = 0, layout = MSPARSE_LAYOUT_STRIPED, shard = 0;
 };
 
+// Shard held by `rank` at `step`: flat ring, or the hierarchical order of
+// Algorithm 2 (outer ring over nodes of `inner` cards, inner ring per node).
+int32_t ring_shard(int32_t world, int32_t inner, int32_t rank, int32_t step) {
+    if (world < 1 || rank < 0 || rank >= world || step < 0 || step >= world) return -1;
+    if (inner < 0 || (inner > 0 && world % inner != 0)) return -1;
+    if (inner <= 1 || inner == world) return ((rank - step) % world + world) % world;
+    const int32_t nodes = world / inner;
+    const int32_t node = rank / inner, card = rank % inner;
+    const int32_t i = step / inner, j = step % inner;
+    return ((node - i) % nodes + nodes) % nodes * inner + ((card - j) % inner + inner) % inner;
+}
+
 msparse_status check_ring(const msparse_dims* d, const msparse_ring* r, RingInfo* out) {
     RingInfo ri;
     if (r) {
@@ -92,11 +104,13 @@ msparse_status check_ring(const msparse_dims* d, const msparse_ring* r, RingInfo
             return fail(MSPARSE_ERR_INVALID, "ring world %d rank %d step %d", r->world, r->rank, r->step);
         if (r->layout != MSPARSE_LAYOUT_STRIPED && r->layout != MSPARSE_LAYOUT_ZIGZAG)
             return fail(MSPARSE_ERR_INVALID, "ring layout %d", r->layout);
+        if (r->inner < 0 || (r->inner > 0 && r->world % r->inner != 0))
+            return fail(MSPARSE_ERR_INVALID, "ring inner %d does not divide world %d", r->inner, r->world);
         ri.world = r->world;
         ri.rank = r->rank;
         ri.step = r->step;
         ri.layout = r->layout;
-        ri.shard = ((r->rank - r->step) % r->world + r->world) % r->world;
+        ri.shard = ring_shard(r->world, r->inner, r->rank, r->step);
         if (r->layout == MSPARSE_LAYOUT_ZIGZAG && (d->seq_q / kBlock) % 2 != 0)
             return fail(MSPARSE_ERR_UNSUPPORTED, "zigzag shards need an even number of 64-token blocks");
     }
@@ -203,6 +217,10 @@ const char* msparse_strerror(msparse_status s) {
 }
 
 const char* msparse_last_error(void) { return g_last_error.c_str(); }
+
+int32_t msparse_ring_shard(int32_t world, int32_t inner, int32_t rank, int32_t step) {
+    return ring_shard(world, inner, rank, step);
+}
 
 // ------------------------------------------------------------------ index
 size_t msparse_index_workspace(const msparse_dims* dims, int32_t k_v, int32_t k_s, const msparse_ring* ring) {
@@ -457,6 +475,32 @@ msparse_status msparse_attn_bwd(const msparse_dims* dims, const void* q, const v
     a.dq_accumulate = dq_accumulate;
     hipStream_t s = static_cast<hipStream_t>(stream);
     return check_hip(launch_attn_bwd(a, s), s, "attn bwd");
+}
+
+// ------------------------------------------------------------------ ring workload
+msparse_status msparse_ring_work(const msparse_dims* dims, const int32_t* v_idx, int32_t k_v, const int32_t* s_idx,
+                                 int32_t k_s, int32_t world, int32_t layout, int64_t* tiles, int64_t* cols, void* ws,
+                                 size_t ws_bytes, void* stream) {
+    RingInfo ri;
+    msparse_status st = check_index_inputs(dims, v_idx, k_v, s_idx, k_s, nullptr, &ri);
+    if (st) return st;
+    if (!tiles || !cols) return fail(MSPARSE_ERR_INVALID, "workload outputs are NULL");
+    if (world < 1 || world > kMaxRingWorld) return fail(MSPARSE_ERR_INVALID, "world %d outside [1, %d]", world, kMaxRingWorld);
+    if (layout != MSPARSE_LAYOUT_STRIPED && layout != MSPARSE_LAYOUT_ZIGZAG)
+        return fail(MSPARSE_ERR_INVALID, "ring layout %d", layout);
+    const int32_t nb = dims->seq_q / kBlock;
+    const int32_t unit = layout == MSPARSE_LAYOUT_ZIGZAG ? 2 * world : world;
+    if (nb % unit != 0)
+        return fail(MSPARSE_ERR_UNSUPPORTED, "%d blocks do not split into %d equal %s shards", nb, world,
+                    layout == MSPARSE_LAYOUT_ZIGZAG ? "zigzag" : "striped");
+    IndexPlan p = plan_index(dims, k_v, k_s, ri, ws, true);
+    if (!ws || ws_bytes < p.bytes)
+        return fail(MSPARSE_ERR_WORKSPACE, "index workspace %zu < %zu bytes", ws_bytes, p.bytes);
+    p.a.v_idx = v_idx;
+    p.a.s_idx = s_idx;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if ((st = check_hip(launch_index_prep(p.a, s), s, "index prep"))) return st;
+    return check_hip(launch_ring_work(p.a, world, layout, tiles, cols, s), s, "ring work");
 }
 
 // ------------------------------------------------------------------ estimation

@@ -13,6 +13,9 @@
 //   count one wavefront per (head, query block) and per (head, key block);
 //   scan  exclusive prefix sums of the counts (one workgroup per array);
 //   fill  the count pass again, writing entries in order via wave ballots.
+// The ring workload matrix (msparse_ring_work) reuses prep and counts, per
+// (head, worker, chunk of the worker's query blocks), the tiles and columns
+// that fall into each worker's KV shard.
 #include "common.h"
 #include "kernels.h"
 #include "trace.h"
@@ -310,7 +313,104 @@ __global__ void __launch_bounds__(1024) index_scan_kernel(IndexArgs a) {
     }
 }
 
+// ---------------------------------------------------------------- ring workload
+constexpr int kWorkThreads = 256;
+constexpr int kWorkChunk = 64;   // query blocks per workgroup
+
+// Adds 1 to bin `bin` for every lane with `on`: lanes sharing the first pending
+// lane's bin are counted with a ballot (zigzag shards are runs of neighbouring
+// blocks, so most lanes share a bin), up to four rounds, then single adds.
+__device__ __forceinline__ void bin_add(uint32_t* h, int32_t bin, bool on) {
+    bool pending = on;
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+        const uint64_t pm = __ballot(pending);
+        if (pm == 0) return;
+        const int first = __builtin_ctzll(pm);
+        const int32_t lb = __shfl(bin, first);
+        const bool same = pending && bin == lb;
+        const uint64_t sm = __ballot(same);
+        if (lane_id() == first) atomicAdd(&h[lb], uint32_t(__popcll(sm)));
+        pending = pending && !same;
+    }
+    if (pending) atomicAdd(&h[bin], 1u);
+}
+
+__global__ void __launch_bounds__(256) ring_work_zero_kernel(int64_t* tiles, int64_t* cols, int64_t n) {
+    for (int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x; i < n; i += int64_t(gridDim.x) * 256) {
+        tiles[i] = 0;
+        cols[i] = 0;
+    }
+}
+
+__global__ void __launch_bounds__(kWorkThreads) ring_work_kernel(IndexArgs a, int32_t W, int32_t layout,
+                                                                 int64_t* tiles, int64_t* cols) {
+    __shared__ uint32_t ht[kMaxRingWorld], hc[kMaxRingWorld];
+    const int tid = threadIdx.x, lane = lane_id(), wave = tid >> 6;
+    const Layout L{W, a.nb, layout};
+    const int per = a.nb / W;                        // query blocks per worker
+    const int nchunk = (per + kWorkChunk - 1) / kWorkChunk;
+    int item = blockIdx.x;
+    const int chunk = item % nchunk;
+    item /= nchunk;
+    const int r = item % W;
+    const int bh = item / W;
+    for (int i = tid; i < W; i += kWorkThreads) {
+        ht[i] = 0;
+        hc[i] = 0;
+    }
+    __syncthreads();
+    const int32_t* dl = a.dlist + int64_t(bh) * a.nb;
+    const int dc = a.dcnt[bh];
+    const uint32_t* db = a.dbits + int64_t(bh) * a.dwords;
+    const int32_t* vl = a.vlist + int64_t(bh) * a.k_v;
+    const int vc = a.vcnt[bh];
+    const int l1 = min(per, (chunk + 1) * kWorkChunk);
+    for (int l = chunk * kWorkChunk + wave; l < l1; l += kWorkThreads / 64) {
+        const int32_t i = L.global(r, l);
+        // tiles (i, i - x), x in D, x <= i
+        for (int c0 = 0; c0 < dc; c0 += 64) {
+            const int j = c0 + lane;
+            const int32_t x = j < dc ? dl[j] : 0;
+            const bool on = j < dc && x <= i;
+            bin_add(ht, on ? L.owner(i - x) : 0, on);
+        }
+        // columns v <= 64 i + 63 whose block-diagonal is not in D
+        const int32_t limit = i * kBlock + kBlock - 1;
+        for (int c0 = 0; c0 < vc; c0 += 64) {
+            if (vl[c0] > limit) break;   // ascending list
+            const int j = c0 + lane;
+            const int32_t v = j < vc ? vl[j] : 0;
+            const bool on = j < vc && v <= limit && !dbit(db, i - v / kBlock);
+            bin_add(hc, on ? L.owner(v / kBlock) : 0, on);
+        }
+    }
+    __syncthreads();
+    for (int sh = tid; sh < W; sh += kWorkThreads) {
+        if (ht[sh]) atomicAdd(reinterpret_cast<unsigned long long*>(tiles + int64_t(r) * W + sh), (unsigned long long)ht[sh]);
+        if (hc[sh]) atomicAdd(reinterpret_cast<unsigned long long*>(cols + int64_t(r) * W + sh), (unsigned long long)hc[sh]);
+    }
+}
+
 }  // namespace
+
+hipError_t launch_ring_work(const IndexArgs& a, int32_t world, int32_t layout, int64_t* tiles, int64_t* cols,
+                            hipStream_t s) {
+    const int64_t n = int64_t(world) * world;
+    {
+        TraceScope _t("ring_work_zero", s);
+        hipLaunchKernelGGL(ring_work_zero_kernel, dim3(unsigned(std::min<int64_t>((n + 255) / 256, 4096))), dim3(256),
+                           0, s, tiles, cols, n);
+    }
+    const int per = a.nb / world;
+    const int64_t grid = int64_t(a.BH) * world * ((per + kWorkChunk - 1) / kWorkChunk);
+    {
+        TraceScope _t("ring_work", s);
+        hipLaunchKernelGGL(ring_work_kernel, dim3(unsigned(grid)), dim3(kWorkThreads), 0, s, a, world, layout, tiles,
+                           cols);
+    }
+    return hipGetLastError();
+}
 
 hipError_t launch_index_prep(const IndexArgs& a, hipStream_t s) {
     const size_t shmem = size_t(a.dwords) * sizeof(uint32_t);

@@ -48,6 +48,10 @@ struct IndexArgs {
     int32_t* overflow;
 };
 hipError_t launch_index_prep(const IndexArgs& a, hipStream_t s);
+// worker x shard tiles / columns of a ring of `world` workers (prep first)
+constexpr int32_t kMaxRingWorld = 4096;
+hipError_t launch_ring_work(const IndexArgs& a, int32_t world, int32_t layout, int64_t* tiles, int64_t* cols,
+                            hipStream_t s);
 hipError_t launch_index_count(const IndexArgs& a, hipStream_t s);
 hipError_t launch_index_scan(const IndexArgs& a, hipStream_t s);
 hipError_t launch_index_fill(const IndexArgs& a, hipStream_t s);

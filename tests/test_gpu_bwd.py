@@ -76,8 +76,8 @@ def test_bwd_empty_rows_and_dense_budget(gpu):
         assert_close(n, g, r)
 
 
-@pytest.mark.parametrize("layout", ["striped", "zigzag"])
-def test_bwd_ring_worker_share(gpu, layout):
+@pytest.mark.parametrize("layout,inner", [("striped", 0), ("zigzag", 0), ("striped", 2), ("zigzag", 2)])
+def test_bwd_ring_worker_share(gpu, layout, inner):
     """Worker r's steps: dQ of its rows summed over steps; each step's dK / dV of
     the step's shard equals the whole-sequence gradient restricted to worker r's
     query rows (dO zero elsewhere) and to the shard's keys."""
@@ -107,9 +107,10 @@ def test_bwd_ring_worker_share(gpu, layout):
     l_acc = torch.empty(q_loc.shape[:-1], dtype=torch.float32, device=dev)
     out = torch.empty_like(q_loc)
     shards = []
+    sched = OI.ring_schedule(W, inner)      # inner > 0: hierarchical order (Algorithm 2)
     for t in range(W):
-        ring = ms.make_ring(W, r, t, layout)
-        kg = OI.local_blocks((r - t) % W, nb, W, layout)
+        ring = ms.make_ring(W, r, t, layout, inner)
+        kg = OI.local_blocks(int(sched[r, t]), nb, W, layout)
         krows = (kg[:, None] * 64 + np.arange(64)[None]).reshape(-1)
         ks = torch.from_numpy(krows)
         k_loc = x["k"][:, :, ks].contiguous().to(dev)

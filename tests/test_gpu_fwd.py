@@ -75,9 +75,12 @@ def test_fwd_dense_budget(gpu):
     assert_lse_close(gl, rl)
 
 
-# (striped, 2, 4480): 35 local blocks per shard, so the pair kernels see a lone block
-@pytest.mark.parametrize("layout,W,seq", [("striped", 4, 8192), ("zigzag", 4, 8192), ("striped", 2, 4480)])
-def test_fwd_ring_steps_merge(gpu, layout, W, seq):
+# (striped, 2, 4480): 35 local blocks per shard, so the pair kernels see a lone block;
+# inner > 0: the hierarchical step order of Algorithm 2 (inner cards per node)
+@pytest.mark.parametrize("layout,W,seq,inner", [("striped", 4, 8192, 0), ("zigzag", 4, 8192, 0),
+                                                ("striped", 2, 4480, 0), ("striped", 8, 8192, 4),
+                                                ("zigzag", 4, 8192, 2)])
+def test_fwd_ring_steps_merge(gpu, layout, W, seq, inner):
     wl = SMALL["gqa_8k_b2"].resized(batch=1, seq=seq)
     x = make_inputs(wl, "cpu", with_do=False)
     f = inputs_f64(x)
@@ -95,9 +98,10 @@ def test_fwd_ring_steps_merge(gpu, layout, W, seq):
     l_acc = torch.empty(q_loc.shape[:-1], dtype=torch.float32, device=gpu)
     out = torch.empty_like(q_loc)
     tv, ts = torch.from_numpy(vi).to(gpu), torch.from_numpy(si).to(gpu)
+    sched = OI.ring_schedule(W, inner)
     for t in range(W):
-        ring = ms.make_ring(W, r, t, layout)
-        shard = (r - t) % W
+        ring = ms.make_ring(W, r, t, layout, inner)
+        shard = int(sched[r, t])
         kg = OI.local_blocks(shard, nb, W, layout)
         krows = torch.from_numpy((kg[:, None] * 64 + np.arange(64)[None]).reshape(-1))
         k_loc = x["k"][:, :, krows].contiguous().to(gpu)

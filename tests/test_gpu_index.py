@@ -97,3 +97,48 @@ def test_index_from_padded_topp_lists(gpu, W, r, t, layout):
     torch.cuda.synchronize()
     _compare(gpu_csr(idx), ref)
     assert int(idx["overflow"].item()) == 0
+
+
+@pytest.mark.parametrize("W,inner,layout", [(8, 4, "striped"), (8, 2, "zigzag"), (6, 3, "striped")])
+def test_index_hierarchical_steps_bit_exact(gpu, W, inner, layout):
+    rng = np.random.default_rng(90 + W + inner)
+    B, Hq, Ng = 1, 2, 64 * 2 * W * 8
+    v, s = _indices(rng, B, Hq, Ng, 150, 900)
+    dims = ms.make_dims(B, Ng // W, Hq, 1, 128)
+    tv, ts = torch.from_numpy(v).to(gpu), torch.from_numpy(s).to(gpu)
+    for r in (0, W - 1):
+        for t in range(W):
+            ref = OI.Index(v, s, Ng, world=W, rank=r, step=t, layout=layout, inner=inner).csr()
+            idx = ms.make_index(dims, tv, ts, ms.make_ring(W, r, t, layout, inner))
+            torch.cuda.synchronize()
+            _compare(gpu_csr(idx), ref)
+
+
+@pytest.mark.parametrize("W,layout", [(1, "striped"), (2, "zigzag"), (4, "striped"), (8, "striped"), (8, "zigzag"),
+                                      (16, "striped")])
+def test_ring_work_bit_exact(gpu, W, layout):
+    rng = np.random.default_rng(120 + W)
+    B, Hq, Ng = 2, 3, 64 * 2 * 16 * 4
+    v, s = _indices(rng, B, Hq, Ng, 200, 700)
+    for h in range(Hq):                       # a padded (top-p) head as well
+        v[0, h, 150 + 10 * h:] = -1
+    rt, rc = OI.ring_work(v, s, Ng, W, layout)
+    dims = ms.make_dims(B, Ng, Hq, 1, 128)
+    gt, gc = ms.ring_work(dims, torch.from_numpy(v).to(gpu), torch.from_numpy(s).to(gpu), W, layout)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(gt.cpu().numpy(), rt)
+    np.testing.assert_array_equal(gc.cpu().numpy(), rc)
+
+
+def test_ring_work_full_size_two_heads(gpu):
+    # the 512K shape: 8192 blocks, W = 128 (64 blocks per worker), a diagonal band plus scattered slashes
+    rng = np.random.default_rng(7)
+    Ng = 524288
+    v, s = _indices(rng, 1, 2, Ng, 4096, 16384)
+    for W, layout in ((128, "striped"), (32, "zigzag")):
+        rt, rc = OI.ring_work(v, s, Ng, W, layout)
+        gt, gc = ms.ring_work(ms.make_dims(1, Ng, 2, 1, 128), torch.from_numpy(v).to(gpu),
+                              torch.from_numpy(s).to(gpu), W, layout)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(gt.cpu().numpy(), rt)
+        np.testing.assert_array_equal(gc.cpu().numpy(), rc)

@@ -105,3 +105,33 @@ def test_topp_validation_before_launch():
     _bad(-4, lambda: call(0.5, 0.5, ws=8))
     assert L.msparse_estimate_topp_workspace(ctypes.byref(d), 64, 100, 100) == \
         L.msparse_estimate_workspace(ctypes.byref(d), 64, 100, 100)
+
+
+def test_ring_shard_matches_oracle_schedule():
+    from oracle import index as OI
+    for W, inner in ((1, 0), (2, 0), (4, 2), (8, 4), (8, 2), (12, 3), (16, 16), (6, 1)):
+        S = OI.ring_schedule(W, inner)
+        for r in range(W):
+            for t in range(W):
+                assert ms.ring_shard(W, inner, r, t) == S[r, t], (W, inner, r, t)
+    assert ms.ring_shard(8, 3, 0, 0) == -1 and ms.ring_shard(8, 4, 8, 0) == -1 and ms.ring_shard(8, 4, 0, -1) == -1
+
+
+def test_ring_validation_before_launch():
+    L = ms.lib()
+    d = ms.make_dims(1, 8192, 2, 1, 128)
+    fake = ctypes.c_void_p(16)
+    iv = ctypes.c_void_p(32)
+    # hierarchical inner must divide world
+    r = ms.Ring(8, 1, 0, 0, 3)
+    _bad(-1, L.msparse_index_count, ctypes.byref(d), iv, 10, iv, 10, ctypes.byref(r), ctypes.byref(ctypes.c_int64()),
+         ctypes.byref(ctypes.c_int64()), ctypes.byref(ctypes.c_int64()), fake, 1 << 30, None)
+
+    def work(world, layout, tiles=iv, ws=1 << 30):
+        return L.msparse_ring_work(ctypes.byref(d), iv, 10, iv, 10, world, layout, tiles, iv, fake, ws, None)
+    _bad(-1, lambda: work(0, 0))
+    _bad(-1, lambda: work(8, 5))
+    _bad(-1, lambda: work(8, 0, tiles=None))
+    _bad(-2, lambda: work(3, 0))         # 128 blocks do not split into 3 shards
+    _bad(-2, lambda: work(128, 1))       # zigzag needs 2 * 128 chunks
+    _bad(-4, lambda: work(8, 0, ws=8))
