@@ -111,6 +111,9 @@ __global__ void __launch_bounds__(256) bwd_rowprep_kernel(AttnArgs a) {
 // S^T = K Q^T, dP^T = V dO^T (K, V rows from LDS, Q and dO rows in VGPRs),
 // dQ^T += K^T dZ^T (K^T read transposed from the same K tile).
 constexpr int kDqThreads = 256;
+#ifndef MS_DQ_WAVES
+#define MS_DQ_WAVES 2   // waves per SIMD: 2 = key halves in turn, 1 = phase schedule
+#endif
 
 template <int D>
 struct DqRows {
@@ -134,6 +137,62 @@ __device__ __forceinline__ void dq_tile(const uint16_t* kt, const uint16_t* vt, 
         sacc[c] = f32x16{};
         pacc[c] = f32x16{};
     }
+#if MS_DQ_WAVES == 2
+    // Two waves per SIMD (the other wave's MFMAs overlap this wave's softmax
+    // terms), so the key halves c run one after the other and only one half's
+    // S^T / dP^T accumulators are live: S^T, dP^T of keys 32 c .. 32 c + 31,
+    // the dZ terms, then that half's dQ k-steps.  Each S / dP k-step's operands
+    // are read one step ahead into a second register set.
+    u32x4 fk[2], fv[2], ak[1][2];
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+        f32x16 sa = f32x16{}, pa = f32x16{};
+        auto read_sd = [&](int set, int s) {
+            fk[set] = dma_read16<D, kDualPad>(kt, 32 * c + l32, h + 2 * s);
+            fv[set] = dma_read16<D, kDualPad>(vt, 32 * c + l32, h + 2 * s);
+        };
+        auto read_tr = [&](int set, int i) {
+#pragma unroll
+            for (int j = 0; j < 2; ++j) ak[set][j] = dma_read_tr<D, kDualPad>(kt, 16 * (2 * c + j), 32 * i, lane);
+        };
+        read_sd(0, 0);
+#pragma unroll
+        for (int k = 0; k < KD; ++k) {
+            const int set = k & 1;
+            if (k + 1 < KD) read_sd(set ^ 1, k + 1);
+            else read_tr(0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+            sa = mfma32h(fk[set], st.q[k], sa);
+            pa = mfma32h(fv[set], st.g[k], pa);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        // s dZ^T = P o (s dP^T - s Delta), P = exp2(c2 z - lse2)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const float p = fast_exp2(__builtin_fmaf(sa[r], c2, -st.lse2));
+            sa[r] = p * __builtin_fmaf(pa[r], isv, -st.dlt);
+        }
+        if (lims) {
+            keep_branch();
+#pragma unroll
+            for (int q4 = 0; q4 < 4; ++q4) {
+                const i32x4 l4 = *reinterpret_cast<const i32x4*>(lims + 32 * c + 8 * q4 + 4 * h);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (qrow < l4[e]) sa[4 * q4 + e] = 0.f;
+            }
+        }
+        u32x4 zb[2];
+        zb[0] = pack8_f16<0>(sa);
+        zb[1] = pack8_f16<8>(sa);
+#pragma unroll
+        for (int i = 0; i < ND; ++i) {
+            if (i > 0) read_tr(0, i);
+#pragma unroll
+            for (int j = 0; j < 2; ++j) st.acc[i] = mfma32h(ak[0][j], zb[j], st.acc[i]);
+        }
+    }
+#else
     // Same phase schedule as kv_tile, over the two key halves c:
     //   A  S^T, dP^T of keys 32 c .. for c = 0
     //   B  S^T, dP^T of c = 1, interleaved with c = 0's dZ terms
@@ -244,10 +303,11 @@ __device__ __forceinline__ void dq_tile(const uint16_t* kt, const uint16_t* vt, 
         mfma_q(set, i);
         __builtin_amdgcn_sched_barrier(0);
     }
+#endif
 }
 
 template <int D>
-__global__ void __launch_bounds__(kDqThreads) __attribute__((amdgpu_waves_per_eu(1, 1))) bwd_dq_kernel(AttnArgs a) {
+__global__ void __launch_bounds__(kDqThreads) __attribute__((amdgpu_waves_per_eu(MS_DQ_WAVES, MS_DQ_WAVES))) bwd_dq_kernel(AttnArgs a) {
     constexpr int KD = DqRows<D>::KD, ND = DqRows<D>::ND;
     constexpr int TE = DmaTile<D, kDualPad>::kElems;
     __shared__ uint16_t k0s[TE], v0s[TE], k1s[TE], v1s[TE];
