@@ -349,6 +349,23 @@ __global__ void __launch_bounds__(kDqThreads) __attribute__((amdgpu_waves_per_eu
     const int64_t item0 = int64_t(bh) * a.nqb + qb0;
     const int64_t e00 = ldc(a.blk_ptr, item0), e01 = ldc(a.blk_ptr, item0 + 1);
     const int64_t e11 = has1 ? ldc(a.blk_ptr, item0 + 2) : e01;
+#if MS_WALK_DESC
+    // walked from the diagonal down (as in the forward: the group's shared
+    // band first)
+    int64_t p0 = e01 - 1, p1 = e11 - 1;
+    auto next = [&](int32_t& kb, bool& in0, bool& in1, bool& diag) {
+        if (p0 < e00 && p1 < e01) return false;
+        const int32_t k0 = p0 >= e00 ? ldc(a.blk_idx, p0) : -1;
+        const int32_t k1 = p1 >= e01 ? ldc(a.blk_idx, p1) : -1;
+        kb = max(k0, k1);
+        in0 = k0 == kb;
+        in1 = k1 == kb;
+        p0 -= in0;
+        p1 -= in1;
+        diag = ldc(a.k_blk_global, kb) == qg;
+        return true;
+    };
+#else
     int64_t p0 = e00, p1 = e01;
     // the diagonal test is made here, one tile ahead (no scalar load pending
     // inside a tile)
@@ -364,6 +381,7 @@ __global__ void __launch_bounds__(kDqThreads) __attribute__((amdgpu_waves_per_eu
         diag = ldc(a.k_blk_global, kb) == qg;
         return true;
     };
+#endif
     auto load = [&](uint16_t* kt, uint16_t* vt, auto rows) {
         dma_rows<D, kDualPad, 4>(kt, kp, rows, w, lane);
         dma_rows<D, kDualPad, 4>(vt, vp, rows, w, lane);
