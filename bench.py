@@ -382,7 +382,7 @@ def torch_index(rows):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="layer_512k")
     ap.add_argument("--also", default="layer_128k", help="second workload timed the same way ('' to skip)")
@@ -442,6 +442,7 @@ def main():
         ev = {s: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
               for s in ("estimate", "index", "fwd", "bwd")}
         acc = {s: 0.0 for s in ev}
+        per_step = []
         state = {}
 
         def step(timed):
@@ -469,8 +470,12 @@ def main():
             state["vcol"] = vcol
             if timed:
                 torch.cuda.synchronize()
+                tot = 0.0
                 for s, (a, b) in ev.items():
-                    acc[s] += a.elapsed_time(b)
+                    t = a.elapsed_time(b)
+                    acc[s] += t
+                    tot += t
+                per_step.append(tot)
 
         print(f"[bench] {name}: warmup {args.warmup}", file=sys.stderr, flush=True)
         for _ in range(args.warmup):
@@ -500,6 +505,7 @@ def main():
         nb = N // 64
         results[name] = dict(
             wl=wl, ms_per_step=ms_step, wall_ms_per_step=wall, stage_ms=step_ms, kernels=per_kernel,
+            median_ms_per_step=float(np.median(per_step)),
             fwd_flops=fwd_flops, T=T, C=C, vcol=state["vcol"],
             density=T / (B * Hq * nb * (nb + 1) / 2.0),
             v_idx=v_idx.cpu().numpy(), s_idx=s_idx.cpu().numpy(), x=x if name == args.workload else None)
@@ -520,8 +526,11 @@ def main():
     traffic = hbm_traffic(wl.name, f"{dom}_kernel<{wl.head_dim}>")
     for r in results.values():
         r["est_idx"] = estimation_and_index_report(r)
+    # achievable dense fp16 MFMA rate on this GPU (probe kernel, no memory traffic)
+    peak_meas = max(ms.mfma_peak_tflops(w) for w in (2, 4))
     roofline = {"bound": "mfma", "kernel": dom, "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                "peak_measured": round(peak_meas, 1), "frac_of_measured": round(achieved / peak_meas, 4),
                 "traffic": None if traffic is None else round(traffic), "traffic_unit": "HBM bytes per launch"}
     line = {
         "metric": "sparse attn fwd+bwd TFLOP/s on computed blocks + ms/layer at 128K and 512K",
@@ -541,7 +550,9 @@ def main():
                    "k_s": wl.k_s, "parallelism": "single GPU"},
         "roofline": roofline,
         "detail": {
-            n: {"ms_per_layer": round(r["ms_per_step"], 3), "stage_ms": {s: round(t, 3) for s, t in r["stage_ms"].items()},
+            n: {"ms_per_layer": round(r["ms_per_step"], 3), "median_ms_per_layer": round(r["median_ms_per_step"], 3),
+                "wall_ms_per_layer": round(r["wall_ms_per_step"], 3),
+                "stage_ms": {s: round(t, 3) for s, t in r["stage_ms"].items()},
                 "fwd_tflops_kernel": round(r["fwd_flops"] / (r["stage_ms"]["fwd"] * 1e-3) / 1e12, 2),
                 "bwd_tflops_kernel": round(2.5 * r["fwd_flops"] / (r["stage_ms"]["bwd"] * 1e-3) / 1e12, 2),
                 "fwd_bwd_tflops_step": round(3.5 * r["fwd_flops"] / (r["ms_per_step"] * 1e-3) / 1e12, 2),

@@ -16,7 +16,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD_DIR = os.path.join(HERE, "_build")
 LIB_PATH = os.path.join(HERE, "libmsparse.so")
-SOURCES = ["api.hip", "index.hip", "attn_fwd.hip", "attn_bwd.hip", "convert.hip", "estimate.hip", "trace.hip"]
+SOURCES = ["api.hip", "index.hip", "attn_fwd.hip", "attn_bwd.hip", "convert.hip", "estimate.hip", "trace.hip", "peak.hip"]
 ARCH = "gfx950"
 
 

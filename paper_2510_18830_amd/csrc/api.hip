@@ -155,6 +155,11 @@ IndexPlan plan_index(const msparse_dims* d, int32_t k_v, int32_t k_s, const Ring
     a.cnt_col = c.take<int64_t>(size_t(a.BH) * a.nqb);
     a.cnt_kblk = c.take<int64_t>(size_t(a.BH) * a.nkb);
     a.cnt_vcol = c.take<int64_t>(a.BH);
+    {
+        const int64_t nmax = std::max<int64_t>(int64_t(a.BH) * std::max(a.nqb, a.nkb), a.BH);
+        a.scan_stride = (nmax + kScanEntriesPerBlock - 1) / kScanEntriesPerBlock;
+        a.scan_sums = c.take<int64_t>(size_t(4 * a.scan_stride));
+    }
     if (own_ptrs) {
         a.blk_ptr = c.take<int64_t>(size_t(a.BH) * a.nqb + 1);
         a.col_ptr = c.take<int64_t>(size_t(a.BH) * a.nqb + 1);
@@ -182,6 +187,10 @@ msparse_status check_index_inputs(const msparse_dims* d, const int32_t* v_idx, i
     if (k_v < 1 || k_v > ng || k_s < 1 || k_s > ng)
         return fail(MSPARSE_ERR_INVALID, "budgets k_v=%d k_s=%d outside [1, %lld]", k_v, k_s, (long long)ng);
     if (d->seq_q == 0) return fail(MSPARSE_ERR_INVALID, "empty sequence");
+    const int64_t items = int64_t(d->batch) * d->heads_q * std::max(d->seq_q, d->seq_k) / kBlock;
+    if (items > int64_t(kScanEntriesPerBlock) * kScanEntriesPerBlock)
+        return fail(MSPARSE_ERR_UNSUPPORTED, "%lld (head, block) items exceed the index scan's %d^2",
+                    (long long)items, kScanEntriesPerBlock);
     return MSPARSE_OK;
 }
 

@@ -271,45 +271,133 @@ __global__ void __launch_bounds__(64 * kItemWaves) index_items_kernel(IndexArgs 
     }
 }
 
-// dst[0] = 0, dst[i + 1] = cnt[0] + ... + cnt[i]; one workgroup per array.
-__global__ void __launch_bounds__(1024) index_scan_kernel(IndexArgs a) {
-    __shared__ int64_t tmp[17];
-    const int64_t* cnt;
-    int64_t* dst;
-    int64_t n;
-    switch (blockIdx.x) {
+// dst[0] = 0, dst[i + 1] = cnt[0] + ... + cnt[i] for the four count arrays
+// (gridDim.y selects the array): per-block sums of kScanBlock entries, one
+// workgroup scans the block sums (kept in the workspace), then every block
+// scans its own entries from its offset.  Loads are coalesced and the sums are
+// integers, so the result does not depend on the grid.
+constexpr int kScanThreads = 256;
+constexpr int kScanPer = 16;
+constexpr int kScanBlock = kScanThreads * kScanPer;   // 4096 entries per block
+static_assert(kScanBlock == kScanEntriesPerBlock, "scan geometry");
+
+__device__ __forceinline__ void scan_array(const IndexArgs& a, int which, const int64_t*& cnt, int64_t*& dst,
+                                           int64_t& n) {
+    switch (which) {
         case 0: cnt = a.cnt_blk; dst = a.blk_ptr; n = int64_t(a.BH) * a.nqb; break;
         case 1: cnt = a.cnt_col; dst = a.col_ptr; n = int64_t(a.BH) * a.nqb; break;
         case 2: cnt = a.cnt_kblk; dst = a.kblk_ptr; n = int64_t(a.BH) * a.nkb; break;
         default: cnt = a.cnt_vcol; dst = a.vcol_ptr; n = a.BH; break;
     }
-    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-    const int64_t per = (n + 1023) / 1024;
-    const int64_t i0 = tid * per, i1 = min(n, i0 + per);
-    int64_t s = 0;
-    for (int64_t i = i0; i < i1; ++i) s += cnt[i];
-    int64_t x = s;
+}
+
+// exclusive scan of one value per thread over the workgroup; returns the total in *total
+__device__ int64_t block_scan64(int64_t v, int64_t* tmp, int64_t* total) {
+    const int lane = lane_id(), wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    int64_t x = v;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
-        int64_t y = __shfl_up(x, o);
+        const int64_t y = __shfl_up(x, o);
         if (lane >= o) x += y;
     }
     if (lane == 63) tmp[wid] = x;
     __syncthreads();
-    if (tid == 0) {
+    if (threadIdx.x == 0) {
         int64_t run = 0;
-        for (int w = 0; w < 16; ++w) {
-            int64_t t = tmp[w];
+        for (int w = 0; w < nw; ++w) {
+            const int64_t t = tmp[w];
             tmp[w] = run;
             run += t;
         }
+        tmp[16] = run;
     }
     __syncthreads();
-    int64_t run = tmp[wid] + x - s;
-    if (tid == 0) dst[0] = 0;
-    for (int64_t i = i0; i < i1; ++i) {
-        run += cnt[i];
-        dst[i + 1] = run;
+    const int64_t res = tmp[wid] + x - v;
+    *total = tmp[16];
+    __syncthreads();
+    return res;
+}
+
+__global__ void __launch_bounds__(kScanThreads) index_scan_sums_kernel(IndexArgs a) {
+    __shared__ int64_t tmp[17];
+    const int64_t* cnt;
+    int64_t* dst;
+    int64_t n;
+    scan_array(a, blockIdx.y, cnt, dst, n);
+    const int64_t base = int64_t(blockIdx.x) * kScanBlock;
+    if (base >= n) return;
+    int64_t s = 0;
+#pragma unroll
+    for (int j = 0; j < kScanPer; ++j) {
+        const int64_t i = base + j * kScanThreads + threadIdx.x;
+        if (i < n) s += cnt[i];
+    }
+    int64_t total = 0;
+    block_scan64(s, tmp, &total);
+    if (threadIdx.x == 0) a.scan_sums[int64_t(blockIdx.y) * a.scan_stride + blockIdx.x] = total;
+}
+
+// one workgroup per array: exclusive scan of the block sums (at most kScanThreads * kScanPer blocks)
+__global__ void __launch_bounds__(kScanThreads) index_scan_top_kernel(IndexArgs a) {
+    __shared__ int64_t tmp[17];
+    const int64_t* cnt;
+    int64_t* dst;
+    int64_t n;
+    scan_array(a, blockIdx.x, cnt, dst, n);
+    const int nblk = int((n + kScanBlock - 1) / kScanBlock);
+    int64_t* sums = a.scan_sums + int64_t(blockIdx.x) * a.scan_stride;
+    // thread t owns sums [t * kScanPer, (t + 1) * kScanPer)
+    int64_t v[kScanPer];
+    int64_t s = 0;
+#pragma unroll
+    for (int j = 0; j < kScanPer; ++j) {
+        const int i = threadIdx.x * kScanPer + j;
+        v[j] = i < nblk ? sums[i] : 0;
+        s += v[j];
+    }
+    int64_t total = 0;
+    int64_t run = block_scan64(s, tmp, &total);
+#pragma unroll
+    for (int j = 0; j < kScanPer; ++j) {
+        const int i = threadIdx.x * kScanPer + j;
+        if (i < nblk) sums[i] = run;
+        run += v[j];
+    }
+    if (threadIdx.x == 0) dst[0] = 0;
+}
+
+__global__ void __launch_bounds__(kScanThreads) index_scan_fill_kernel(IndexArgs a) {
+    __shared__ int64_t tmp[17];
+    __shared__ int64_t vals[kScanBlock];
+    const int64_t* cnt;
+    int64_t* dst;
+    int64_t n;
+    scan_array(a, blockIdx.y, cnt, dst, n);
+    const int64_t base = int64_t(blockIdx.x) * kScanBlock;
+    if (base >= n) return;
+    // coalesced load into LDS, then thread t scans entries [t * kScanPer, (t + 1) * kScanPer)
+#pragma unroll
+    for (int j = 0; j < kScanPer; ++j) {
+        const int k = j * kScanThreads + threadIdx.x;
+        vals[k] = base + k < n ? cnt[base + k] : 0;
+    }
+    __syncthreads();
+    int64_t s = 0;
+#pragma unroll
+    for (int j = 0; j < kScanPer; ++j) s += vals[threadIdx.x * kScanPer + j];
+    int64_t total = 0;
+    int64_t run = block_scan64(s, tmp, &total) + a.scan_sums[int64_t(blockIdx.y) * a.scan_stride + blockIdx.x];
+#pragma unroll
+    for (int j = 0; j < kScanPer; ++j) {
+        const int k = threadIdx.x * kScanPer + j;
+        run += vals[k];
+        vals[k] = run;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kScanPer; ++j) {
+        const int k = j * kScanThreads + threadIdx.x;
+        if (base + k < n) dst[base + k + 1] = vals[k];
     }
 }
 
@@ -426,7 +514,11 @@ hipError_t launch_index_count(const IndexArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_index_scan(const IndexArgs& a, hipStream_t s) {
-    { TraceScope _t("index_scan", s); hipLaunchKernelGGL(index_scan_kernel, dim3(4), dim3(1024), 0, s, a); }
+    const int64_t nmax = std::max<int64_t>(int64_t(a.BH) * std::max(a.nqb, a.nkb), a.BH);
+    const unsigned nblk = unsigned((nmax + kScanBlock - 1) / kScanBlock);
+    { TraceScope _t("index_scan", s); hipLaunchKernelGGL(index_scan_sums_kernel, dim3(nblk, 4), dim3(kScanThreads), 0, s, a); }
+    { TraceScope _t("index_scan", s); hipLaunchKernelGGL(index_scan_top_kernel, dim3(4), dim3(kScanThreads), 0, s, a); }
+    { TraceScope _t("index_scan", s); hipLaunchKernelGGL(index_scan_fill_kernel, dim3(nblk, 4), dim3(kScanThreads), 0, s, a); }
     return hipGetLastError();
 }
 

@@ -29,6 +29,8 @@ struct IndexArgs {
     int64_t* cnt_col;      // [BH*nqb]
     int64_t* cnt_kblk;     // [BH*nkb]
     int64_t* cnt_vcol;     // [BH]
+    int64_t* scan_sums;    // [4, scan_stride] per-block sums of the scan
+    int64_t scan_stride;
     // scanned offsets (n + 1 entries each)
     int64_t* blk_ptr;
     int64_t* col_ptr;
@@ -48,6 +50,9 @@ struct IndexArgs {
     int32_t* overflow;
 };
 hipError_t launch_index_prep(const IndexArgs& a, hipStream_t s);
+// the prefix scans of the index counts: blocks of kScanEntriesPerBlock entries,
+// at most kScanEntriesPerBlock blocks per array
+constexpr int kScanEntriesPerBlock = 4096;
 // worker x shard tiles / columns of a ring of `world` workers (prep first)
 constexpr int32_t kMaxRingWorld = 4096;
 hipError_t launch_ring_work(const IndexArgs& a, int32_t world, int32_t layout, int64_t* tiles, int64_t* cols,
