@@ -40,8 +40,19 @@ constexpr int kChunkTiles = 16;   // 1024 keys per workgroup
 constexpr float kLog2e = 1.4426950408889634f;
 
 struct EstLayout {
-    size_t part_max, part_sum, row_lse, diag_part, bytes;
+    size_t part_max, part_sum, row_lse, diag_part, sel_cnt, sel_mass, sel_gt, sel_eq, sel_state, bytes;
 };
+
+constexpr int kSliceLen = 16384;   // scores per selection slice
+struct SelState {
+    uint32_t prefix, mask;   // decided high bits of the selected threshold
+    uint32_t krem;           // count select: entries still to take from the prefix group
+    uint32_t above;          // entries strictly above the prefix group
+    uint64_t rem;            // mass select: mass still to reach (2^-40 units)
+    uint32_t k;              // the budget (entries written)
+    uint32_t mode;           // kModeMass, kModeCount or kModeDone
+};
+constexpr uint32_t kModeMass = 1, kModeCount = 2, kModeDone = 3;
 
 size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
@@ -58,6 +69,17 @@ EstLayout est_layout(int64_t BH, int32_t N) {
     off = align256(off + size_t(BH) * kBlock * 4);
     L.diag_part = off;
     off = align256(off + size_t(BH) * nb * 128 * 4);
+    const int64_t NL = 2 * BH, ns = (N + kSliceLen - 1) / kSliceLen;
+    L.sel_cnt = off;
+    off = align256(off + size_t(NL) * ns * 256 * 4);
+    L.sel_mass = off;
+    off = align256(off + size_t(NL) * ns * 256 * 8);
+    L.sel_gt = off;
+    off = align256(off + size_t(NL) * ns * 8);
+    L.sel_eq = off;
+    off = align256(off + size_t(NL) * ns * 8);
+    L.sel_state = off;
+    off = align256(off + size_t(NL) * sizeof(SelState));
     L.bytes = off;
     return L;
 }
@@ -249,17 +271,25 @@ __global__ void __launch_bounds__(256) est_diag_kernel(EstArgs a) {
     a.s_score[i] = s;
 }
 
-// ---------------------------------------------------------------- top-k
-constexpr int kTopkThreads = 1024;
-
-
-// Histograms are private per wave (16 copies, stride 257 words so the copies
-// sit on different banks): scores of one list share few exponents, and one
-// shared histogram would serialise nearly every atomic on the same bins.
-// Scores are read 4 at a time (16-byte loads, N % 64 == 0), several loads in
-// flight per thread.
+// ---------------------------------------------------------------- top-k / top-p
+// Selection over the 2 B Hq score lists (vertical lists first), each cut into
+// slices of kSliceLen scores: per digit (8 bits, high first) a histogram pass
+// over every (list, slice) writes per-slice bin counts (and masses), and a
+// select pass per list sums them in slice order and narrows the prefix.  With
+// a top-p fraction, four mass digits find the threshold score t at which the
+// descending cumulative mass reaches p of the total; then four count digits
+// (skipped by lists already decided) find the k-th largest for fixed budgets
+// or for capped ones.  Two compaction passes write all entries above the
+// threshold and the lowest-index ties, in index order.  Scores are >= 0, so
+// fp32 bit patterns order like values.
+constexpr int kSelThreads = 256;
+constexpr int kSelWaves = kSelThreads / 64;
+// Histograms are private per wave (stride 257 words, so the copies sit on
+// different banks): the scores of a list share few exponents, and one shared
+// histogram would serialise nearly every atomic on the same bins.  Scores are
+// read 4 at a time (16-byte loads, N % 64 == 0), several loads in flight per
+// thread.
 constexpr int kHistStride = 257;
-constexpr int kTopkWaves = kTopkThreads / 64;
 
 // Adds 1 to bin `bin` of the wave's histogram for every lane with `on`.  The
 // lanes sharing the first pending lane's bin are counted with a ballot and
@@ -319,214 +349,282 @@ __device__ __forceinline__ void hist_add_mass(uint32_t* wh, uint64_t* wm, uint32
     }
 }
 
-struct TopkLds {
-    uint32_t whist[kTopkWaves * kHistStride];
-    uint64_t wmass[kTopkWaves * 256];
-    uint32_t hist[256];
-    uint64_t hmass[256];
-    uint64_t wsum[kTopkWaves];
-    uint32_t s_prefix, s_krem, s_k, s_above;
-    uint64_t s_rem;
-    int64_t wgt[kTopkWaves], weq[kTopkWaves];
-};
+__device__ __forceinline__ SelState* sel_state(const EstArgs& a) { return reinterpret_cast<SelState*>(a.sel_state); }
 
-__global__ void __launch_bounds__(kTopkThreads) est_topk_kernel(EstArgs a) {
-    __shared__ TopkLds sm;
+__global__ void __launch_bounds__(256) sel_init_kernel(EstArgs a) {
+    const int NL = 2 * a.B * a.Hq;
+    const int l = blockIdx.x * 256 + threadIdx.x;
+    if (l >= NL) return;
+    const bool is_v = l < a.B * a.Hq;
+    SelState st{};
+    st.mode = (is_v ? a.p_v : a.p_s) > 0.0 ? kModeMass : kModeCount;
+    st.krem = uint32_t(is_v ? a.k_v : a.k_s);
+    st.k = st.krem;
+    sel_state(a)[l] = st;
+}
+
+// one (list, slice) per workgroup: histogram of digit `shift` over the scores
+// that match the list's prefix
+template <bool MASS>
+__global__ void __launch_bounds__(kSelThreads) sel_hist_kernel(EstArgs a, int shift) {
+    __shared__ uint32_t whist[kSelWaves * kHistStride];
+    __shared__ uint64_t wmass[MASS ? kSelWaves * 256 : 1];
+    const int list = blockIdx.x / a.nslice, slice = blockIdx.x % a.nslice;
+    const SelState st = sel_state(a)[list];
+    if (st.mode != (MASS ? kModeMass : kModeCount)) return;
     const int BH = a.B * a.Hq;
-    const bool is_v = blockIdx.x < BH;
-    const int bh = is_v ? blockIdx.x : blockIdx.x - BH;
-    const int cap = is_v ? a.k_v : a.k_s;
-    const double p = is_v ? a.p_v : a.p_s;
-    const uint32_t* sc = reinterpret_cast<const uint32_t*>((is_v ? a.v_score : a.s_score) + int64_t(bh) * a.N);
-    int32_t* out = (is_v ? a.v_idx : a.s_idx) + int64_t(bh) * cap;
-    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-    const int N = a.N;
-    const int n4 = N / 4;
+    const float* sc = (list < BH ? a.v_score + int64_t(list) * a.N : a.s_score + int64_t(list - BH) * a.N);
     const u32x4* sc4 = reinterpret_cast<const u32x4*>(sc);
-
-    uint32_t k = uint32_t(cap);
-    uint32_t prefix = 0, krem = 0;
-    bool selected = false;
-    if (p > 0.0) {
-        // ---- total mass and the threshold theta = ceil(p T)
-        uint64_t t = 0;
-        for (int i = tid; i < n4; i += kTopkThreads) {
-            const u32x4 x = sc4[i];
-            t += mass_fx(x[0]) + mass_fx(x[1]) + mass_fx(x[2]) + mass_fx(x[3]);
+    const int tid = threadIdx.x, wv = tid >> 6;
+    for (int i = tid; i < kSelWaves * kHistStride; i += kSelThreads) whist[i] = 0;
+    if (MASS)
+        for (int i = tid; i < kSelWaves * 256; i += kSelThreads) wmass[i] = 0;
+    __syncthreads();
+    uint32_t* wh = whist + wv * kHistStride;
+    const int lo4 = slice * (kSliceLen / 4), hi4 = min(a.N / 4, lo4 + kSliceLen / 4);
+    for (int i0 = lo4 + tid; i0 < hi4; i0 += 4 * kSelThreads) {
+        u32x4 x[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int i = i0 + u * kSelThreads;
+            x[u] = i < hi4 ? sc4[i] : u32x4{0u, 0u, 0u, 0u};
         }
-        t = wave_sum_u64(t);
-        if (lane == 0) sm.wsum[wv] = t;
-        __syncthreads();
-        uint64_t total = 0;
-        for (int w = 0; w < kTopkWaves; ++w) total += sm.wsum[w];
-        uint64_t rem = uint64_t(ceil(p * double(total)));
-        uint32_t above = 0;   // count of scores above the current prefix
-        if (total > 0) {
-            uint32_t mask = 0;
-            for (int shift = 24; shift >= 0; shift -= 8) {
-                for (int i = tid; i < kTopkWaves * kHistStride; i += kTopkThreads) sm.whist[i] = 0;
-                for (int i = tid; i < kTopkWaves * 256; i += kTopkThreads) sm.wmass[i] = 0;
-                __syncthreads();
-                uint32_t* wh = sm.whist + wv * kHistStride;
-                uint64_t* wm = sm.wmass + wv * 256;
-                for (int i0 = tid; i0 < n4; i0 += 4 * kTopkThreads) {
-                    u32x4 x[4];
 #pragma unroll
-                    for (int u = 0; u < 4; ++u) {
-                        const int i = i0 + u * kTopkThreads;
-                        x[u] = i < n4 ? sc4[i] : u32x4{0u, 0u, 0u, 0u};
-                    }
+        for (int u = 0; u < 4; ++u) {
+            const bool in = i0 + u * kSelThreads < hi4;
 #pragma unroll
-                    for (int u = 0; u < 4; ++u) {
-                        const bool in = i0 + u * kTopkThreads < n4;
-#pragma unroll
-                        for (int e = 0; e < 4; ++e)
-                            hist_add_mass(wh, wm, (x[u][e] >> shift) & 255u, mass_fx(x[u][e]),
-                                          in && (x[u][e] & mask) == prefix);
-                    }
-                }
-                __syncthreads();
-                for (int bb = tid; bb < 256; bb += kTopkThreads) {
-                    uint32_t c = 0;
-                    uint64_t m = 0;
-                    for (int w = 0; w < kTopkWaves; ++w) {
-                        c += sm.whist[w * kHistStride + bb];
-                        m += sm.wmass[w * 256 + bb];
-                    }
-                    sm.hist[bb] = c;
-                    sm.hmass[bb] = m;
-                }
-                __syncthreads();
-                if (tid == 0) {
-                    // the prefix group holds at least rem (> 0): some bin is taken
-                    uint64_t run = 0;
-                    uint32_t runc = 0;
-                    int bsel = 0;
-                    for (int bb = 255; bb >= 0; --bb) {
-                        if (run + sm.hmass[bb] >= rem) {
-                            bsel = bb;
-                            break;
-                        }
-                        run += sm.hmass[bb];
-                        runc += sm.hist[bb];
-                    }
-                    sm.s_prefix = prefix | (uint32_t(bsel) << shift);
-                    sm.s_rem = rem - run;
-                    sm.s_above = above + runc;
-                    if (shift == 0) {
-                        // t = the prefix; every score equal to t adds mass_fx(t)
-                        const uint64_t qt = mass_fx(sm.s_prefix);
-                        const uint64_t ties = qt ? (sm.s_rem + qt - 1) / qt : uint64_t(sm.hist[bsel]);
-                        sm.s_k = uint32_t(min<uint64_t>(uint64_t(above + runc) + min<uint64_t>(ties, sm.hist[bsel]),
-                                                        uint64_t(N)));
-                    }
-                }
-                __syncthreads();
-                prefix = sm.s_prefix;
-                rem = sm.s_rem;
-                above = sm.s_above;
-                mask |= 255u << shift;
-                __syncthreads();
+            for (int e = 0; e < 4; ++e) {
+                const bool on = in && (x[u][e] & st.mask) == st.prefix;
+                const uint32_t bin = (x[u][e] >> shift) & 255u;
+                if (MASS) hist_add_mass(wh, wmass + wv * 256, bin, mass_fx(x[u][e]), on);
+                else hist_add(wh, bin, on);
             }
-            k = sm.s_k;
-        } else {
-            k = 1;   // no mass at all: one entry reaches p of it
         }
-        if (k <= uint32_t(cap)) {
-            krem = k - above;
-            selected = total > 0;
-        } else {
-            k = uint32_t(cap);
-        }
-    }
-    if (!selected) {
-        prefix = 0;
-        uint32_t mask = 0;
-        krem = k;
-        for (int shift = 24; shift >= 0; shift -= 8) {
-            for (int i = tid; i < kTopkWaves * kHistStride; i += kTopkThreads) sm.whist[i] = 0;
-            __syncthreads();
-            uint32_t* wh = sm.whist + wv * kHistStride;
-            for (int i0 = tid; i0 < n4; i0 += 4 * kTopkThreads) {
-                u32x4 x[4];
-#pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    const int i = i0 + u * kTopkThreads;
-                    x[u] = i < n4 ? sc4[i] : u32x4{~0u, ~0u, ~0u, ~0u};
-                }
-#pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    const bool in = i0 + u * kTopkThreads < n4;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) hist_add(wh, (x[u][e] >> shift) & 255u, in && (x[u][e] & mask) == prefix);
-                }
-            }
-            __syncthreads();
-            for (int bb = tid; bb < 256; bb += kTopkThreads) {
-                uint32_t t = 0;
-                for (int w = 0; w < kTopkWaves; ++w) t += sm.whist[w * kHistStride + bb];
-                sm.hist[bb] = t;
-            }
-            __syncthreads();
-            if (tid == 0) {
-                uint32_t run = 0;
-                int bsel = 0;
-                for (int bb = 255; bb >= 0; --bb) {
-                    if (run + sm.hist[bb] >= krem) {
-                        bsel = bb;
-                        break;
-                    }
-                    run += sm.hist[bb];
-                }
-                sm.s_prefix = prefix | (uint32_t(bsel) << shift);
-                sm.s_krem = krem - run;
-            }
-            __syncthreads();
-            prefix = sm.s_prefix;
-            krem = sm.s_krem;
-            mask |= 255u << shift;
-            __syncthreads();
-        }
-    }
-    // prefix = bit pattern of the k-th largest; take all above it and the
-    // first krem equal ones, in index order.  Wave wv owns the contiguous
-    // slice [wv C, (wv + 1) C) and reads it 64 scores at a time (coalesced);
-    // ballots give the counts and ranks, one scan over the waves the offsets.
-    const int C = ((N + kTopkWaves * 64 - 1) / (kTopkWaves * 64)) * 64;
-    const int lo = wv * C, hi = min(N, lo + C);
-    const uint64_t below = (1ull << lane) - 1ull;
-    int64_t gt = 0, eq = 0;
-    for (int i0 = lo; i0 < hi; i0 += 64) {
-        const int i = i0 + lane;
-        const uint32_t x = i < hi ? sc[i] : 0u;
-        gt += __popcll(__ballot(i < hi && x > prefix));
-        eq += __popcll(__ballot(i < hi && x == prefix));
-    }
-    if (lane == 0) {
-        sm.wgt[wv] = gt;
-        sm.weq[wv] = eq;
     }
     __syncthreads();
-    int64_t off = 0, eq_before = 0;
-    for (int w = 0; w < wv; ++w) {
-        off += sm.wgt[w] + min<int64_t>(sm.weq[w], max<int64_t>(0, int64_t(krem) - eq_before));
-        eq_before += sm.weq[w];
+    const int64_t o = (int64_t(list) * a.nslice + slice) * 256;
+    for (int b = tid; b < 256; b += kSelThreads) {
+        uint32_t c = 0;
+        uint64_t m = 0;
+#pragma unroll
+        for (int w = 0; w < kSelWaves; ++w) {
+            c += whist[w * kHistStride + b];
+            if (MASS) m += wmass[w * 256 + b];
+        }
+        a.sel_cnt[o + b] = c;
+        if (MASS) a.sel_mass[o + b] = m;
     }
-    for (int i0 = lo; i0 < hi; i0 += 64) {
+}
+
+// one list per workgroup: sum the slices' bins (fixed order) and narrow the prefix
+template <bool MASS>
+__global__ void __launch_bounds__(256) sel_pick_kernel(EstArgs a, int shift) {
+    __shared__ uint32_t hc[256];
+    __shared__ uint64_t hm[MASS ? 256 : 1];
+    const int list = blockIdx.x;
+    SelState* stp = sel_state(a) + list;
+    const SelState st0 = *stp;
+    if (st0.mode != (MASS ? kModeMass : kModeCount)) return;
+    const int b = threadIdx.x;
+    uint32_t c = 0;
+    uint64_t m = 0;
+    for (int sl = 0; sl < a.nslice; ++sl) {
+        const int64_t o = (int64_t(list) * a.nslice + sl) * 256 + b;
+        c += a.sel_cnt[o];
+        if (MASS) m += a.sel_mass[o];
+    }
+    hc[b] = c;
+    if (MASS) hm[b] = m;
+    __syncthreads();
+    if (b != 0) return;
+    SelState st = st0;
+    const int BH = a.B * a.Hq;
+    const bool is_v = list < BH;
+    const uint32_t cap = uint32_t(is_v ? a.k_v : a.k_s);
+    if (MASS) {
+        if (shift == 24) {
+            // every score matches the empty prefix: the bins hold the total mass
+            uint64_t total = 0;
+            for (int bb = 0; bb < 256; ++bb) total += hm[bb];
+            if (total == 0) {   // no mass at all: one entry reaches p of it
+                st.mode = kModeCount;
+                st.krem = 1;
+                st.k = 1;
+                *stp = st;
+                return;
+            }
+            st.rem = uint64_t(ceil((is_v ? a.p_v : a.p_s) * double(total)));
+        }
+        // the prefix group holds at least rem (> 0) of mass, so some bin is taken
+        uint64_t run = 0;
+        uint32_t runc = 0;
+        int bsel = 0;
+        for (int bb = 255; bb >= 0; --bb) {
+            if (run + hm[bb] >= st.rem) {
+                bsel = bb;
+                break;
+            }
+            run += hm[bb];
+            runc += hc[bb];
+        }
+        st.prefix |= uint32_t(bsel) << shift;
+        st.mask |= 255u << shift;
+        st.rem -= run;
+        st.above += runc;
+        if (shift == 0) {
+            // t = prefix; every score equal to t adds mass_fx(t)
+            const uint64_t qt = mass_fx(st.prefix);
+            const uint64_t ties = qt ? (st.rem + qt - 1) / qt : uint64_t(hc[bsel]);
+            const uint64_t k = uint64_t(st.above) + min<uint64_t>(ties, hc[bsel]);
+            if (k <= cap) {
+                st.k = uint32_t(k);
+                st.krem = uint32_t(k) - st.above;
+                st.mode = kModeDone;
+            } else {   // capped: the count select finds the cap-th largest
+                st.k = cap;
+                st.krem = cap;
+                st.prefix = 0;
+                st.mask = 0;
+                st.above = 0;
+                st.mode = kModeCount;
+            }
+        }
+    } else {
+        uint32_t run = 0;
+        int bsel = 0;
+        for (int bb = 255; bb >= 0; --bb) {
+            if (run + hc[bb] >= st.krem) {
+                bsel = bb;
+                break;
+            }
+            run += hc[bb];
+        }
+        st.prefix |= uint32_t(bsel) << shift;
+        st.mask |= 255u << shift;
+        st.krem -= run;
+        st.above += run;
+        if (shift == 0) st.mode = kModeDone;
+    }
+    *stp = st;
+}
+
+// per (list, slice): entries above the threshold and ties with it
+__global__ void __launch_bounds__(kSelThreads) sel_count_kernel(EstArgs a) {
+    __shared__ int64_t wgt[kSelWaves], weq[kSelWaves];
+    const int list = blockIdx.x / a.nslice, slice = blockIdx.x % a.nslice;
+    const SelState st = sel_state(a)[list];
+    const int BH = a.B * a.Hq;
+    const uint32_t* sc = reinterpret_cast<const uint32_t*>(list < BH ? a.v_score + int64_t(list) * a.N
+                                                                      : a.s_score + int64_t(list - BH) * a.N);
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int lo = slice * kSliceLen, hi = min(a.N, lo + kSliceLen);
+    int64_t gt = 0, eq = 0;
+    for (int i0 = lo + wv * 64; i0 < hi; i0 += kSelThreads) {
         const int i = i0 + lane;
         const uint32_t x = i < hi ? sc[i] : 0u;
-        const bool e = i < hi && x == prefix;
+        gt += __popcll(__ballot(i < hi && x > st.prefix));
+        eq += __popcll(__ballot(i < hi && x == st.prefix));
+    }
+    if (lane == 0) {
+        wgt[wv] = gt;
+        weq[wv] = eq;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        int64_t g = 0, e = 0;
+        for (int w = 0; w < kSelWaves; ++w) {
+            g += wgt[w];
+            e += weq[w];
+        }
+        a.sel_gt[int64_t(list) * a.nslice + slice] = g;
+        a.sel_eq[int64_t(list) * a.nslice + slice] = e;
+    }
+}
+
+// per (list, slice): write the slice's selected indices at its offset, in
+// index order (wave-contiguous sub-slices, ballots for the ranks)
+__global__ void __launch_bounds__(kSelThreads) sel_write_kernel(EstArgs a) {
+    __shared__ int64_t wgt[kSelWaves], weq[kSelWaves];
+    const int list = blockIdx.x / a.nslice, slice = blockIdx.x % a.nslice;
+    const SelState st = sel_state(a)[list];
+    const int BH = a.B * a.Hq;
+    const bool is_v = list < BH;
+    const int cap = is_v ? a.k_v : a.k_s;
+    const uint32_t* sc = reinterpret_cast<const uint32_t*>(is_v ? a.v_score + int64_t(list) * a.N
+                                                                : a.s_score + int64_t(list - BH) * a.N);
+    int32_t* out = (is_v ? a.v_idx + int64_t(list) * cap : a.s_idx + int64_t(list - BH) * cap);
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    // slices before this one: entries taken and ties seen
+    int64_t off = 0, eq_before = 0;
+    for (int sl = 0; sl < slice; ++sl) {
+        off += a.sel_gt[int64_t(list) * a.nslice + sl];
+        eq_before += a.sel_eq[int64_t(list) * a.nslice + sl];
+    }
+    off += min<int64_t>(eq_before, st.krem);
+    // this slice: wave wv owns [lo + wv C, lo + (wv + 1) C)
+    const int lo = slice * kSliceLen, hi = min(a.N, lo + kSliceLen);
+    const int C = ((hi - lo + kSelWaves * 64 - 1) / (kSelWaves * 64)) * 64;
+    const int wlo = lo + wv * C, whi = min(hi, wlo + C);
+    const uint64_t below = (1ull << lane) - 1ull;
+    int64_t gt = 0, eq = 0;
+    for (int i0 = wlo; i0 < whi; i0 += 64) {
+        const int i = i0 + lane;
+        const uint32_t x = i < whi ? sc[i] : 0u;
+        gt += __popcll(__ballot(i < whi && x > st.prefix));
+        eq += __popcll(__ballot(i < whi && x == st.prefix));
+    }
+    if (lane == 0) {
+        wgt[wv] = gt;
+        weq[wv] = eq;
+    }
+    __syncthreads();
+    for (int w = 0; w < wv; ++w) {
+        off += wgt[w] + min<int64_t>(weq[w], max<int64_t>(0, int64_t(st.krem) - eq_before));
+        eq_before += weq[w];
+    }
+    for (int i0 = wlo; i0 < whi; i0 += 64) {
+        const int i = i0 + lane;
+        const uint32_t x = i < whi ? sc[i] : 0u;
+        const bool e = i < whi && x == st.prefix;
         const uint64_t me = __ballot(e);
-        const bool take = (i < hi && x > prefix) || (e && eq_before + __popcll(me & below) < int64_t(krem));
+        const bool take = (i < whi && x > st.prefix) || (e && eq_before + __popcll(me & below) < int64_t(st.krem));
         const uint64_t mt = __ballot(take);
         if (take) out[off + __popcll(mt & below)] = i;
         off += __popcll(mt);
         eq_before += __popcll(me);
     }
-    if (p > 0.0) {
-        for (int i = int(k) + tid; i < cap; i += kTopkThreads) out[i] = -1;
-        if (tid == 0) (is_v ? a.v_cnt : a.s_cnt)[bh] = int32_t(k);
+}
+
+// top-p lists: the budget and -1 in the unused slots
+__global__ void __launch_bounds__(256) sel_finish_kernel(EstArgs a) {
+    const int list = blockIdx.x;
+    const SelState st = sel_state(a)[list];
+    const int BH = a.B * a.Hq;
+    const bool is_v = list < BH;
+    const int cap = is_v ? a.k_v : a.k_s;
+    int32_t* out = (is_v ? a.v_idx + int64_t(list) * cap : a.s_idx + int64_t(list - BH) * cap);
+    for (int i = int(st.k) + threadIdx.x; i < cap; i += 256) out[i] = -1;
+    if (threadIdx.x == 0) (is_v ? a.v_cnt + list : a.s_cnt + (list - BH))[0] = int32_t(st.k);
+}
+
+hipError_t launch_select(const EstArgs& a, hipStream_t s) {
+    const int NL = 2 * a.B * a.Hq;
+    const unsigned grid = unsigned(NL * a.nslice);
+    const bool topp = a.p_v > 0.0;
+    { TraceScope _t("est_topk", s); hipLaunchKernelGGL(sel_init_kernel, dim3((NL + 255) / 256), dim3(256), 0, s, a); }
+    if (topp)
+        for (int shift = 24; shift >= 0; shift -= 8) {
+            { TraceScope _t("est_topk", s); hipLaunchKernelGGL(sel_hist_kernel<true>, dim3(grid), dim3(kSelThreads), 0, s, a, shift); }
+            { TraceScope _t("est_topk", s); hipLaunchKernelGGL(sel_pick_kernel<true>, dim3(NL), dim3(256), 0, s, a, shift); }
+        }
+    for (int shift = 24; shift >= 0; shift -= 8) {
+        { TraceScope _t("est_topk", s); hipLaunchKernelGGL(sel_hist_kernel<false>, dim3(grid), dim3(kSelThreads), 0, s, a, shift); }
+        { TraceScope _t("est_topk", s); hipLaunchKernelGGL(sel_pick_kernel<false>, dim3(NL), dim3(256), 0, s, a, shift); }
     }
+    { TraceScope _t("est_topk", s); hipLaunchKernelGGL(sel_count_kernel, dim3(grid), dim3(kSelThreads), 0, s, a); }
+    { TraceScope _t("est_topk", s); hipLaunchKernelGGL(sel_write_kernel, dim3(grid), dim3(kSelThreads), 0, s, a); }
+    if (topp) { TraceScope _t("est_topk", s); hipLaunchKernelGGL(sel_finish_kernel, dim3(NL), dim3(256), 0, s, a); }
+    return hipGetLastError();
 }
 
 template <int D>
@@ -537,8 +635,8 @@ hipError_t launch_d(const EstArgs& a, hipStream_t s) {
     { TraceScope _t("est_pass2", s); hipLaunchKernelGGL(est_pass2_kernel<D>, dim3(BH * a.nchunk), dim3(kThreads), 0, s, a); }
     const int64_t n = int64_t(BH) * a.N;
     { TraceScope _t("est_diag", s); hipLaunchKernelGGL(est_diag_kernel, dim3(unsigned((n + 255) / 256)), dim3(256), 0, s, a); }
-    { TraceScope _t("est_topk", s); hipLaunchKernelGGL(est_topk_kernel, dim3(2 * BH), dim3(kTopkThreads), 0, s, a); }
-    return hipGetLastError();
+    if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+    return launch_select(a, s);
 }
 
 }  // namespace
@@ -555,6 +653,12 @@ void est_carve(EstArgs& a, char* base) {
     a.part_sum = reinterpret_cast<float*>(base + L.part_sum);
     a.row_lse = reinterpret_cast<float*>(base + L.row_lse);
     a.diag_part = reinterpret_cast<float*>(base + L.diag_part);
+    a.nslice = (a.N + kSliceLen - 1) / kSliceLen;
+    a.sel_cnt = reinterpret_cast<uint32_t*>(base + L.sel_cnt);
+    a.sel_mass = reinterpret_cast<uint64_t*>(base + L.sel_mass);
+    a.sel_gt = reinterpret_cast<int64_t*>(base + L.sel_gt);
+    a.sel_eq = reinterpret_cast<int64_t*>(base + L.sel_eq);
+    a.sel_state = base + L.sel_state;
 }
 
 hipError_t launch_estimate(const EstArgs& a, hipStream_t s) {

@@ -176,6 +176,14 @@ struct EstArgs {
     float* row_lse;     // [B*Hq, 64] (log2 domain)
     float* diag_part;   // [B*Hq, N/64, 128]
     int32_t nchunk;
+    // selection (top-k / top-p) over 2 B Hq lists of N scores cut into nslice
+    // slices: per-slice histograms and compaction counts, per-list state
+    int32_t nslice;
+    uint32_t* sel_cnt;  // [2 BH, nslice, 256]
+    uint64_t* sel_mass; // [2 BH, nslice, 256]
+    int64_t* sel_gt;    // [2 BH, nslice]
+    int64_t* sel_eq;    // [2 BH, nslice]
+    void* sel_state;    // [2 BH] selection state
 };
 size_t est_workspace_bytes(int32_t B, int32_t Hq, int32_t N, int32_t L);
 void est_carve(EstArgs& a, char* base);
