@@ -111,6 +111,9 @@ __global__ void __launch_bounds__(256) bwd_rowprep_kernel(AttnArgs a) {
 // S^T = K Q^T, dP^T = V dO^T (K, V rows from LDS, Q and dO rows in VGPRs),
 // dQ^T += K^T dZ^T (K^T read transposed from the same K tile).
 constexpr int kDqThreads = 256;
+#ifndef MS_KV_AHEAD
+#define MS_KV_AHEAD 1   // dK/dV operand groups read this many groups ahead
+#endif
 #ifndef MS_DQ_WAVES
 #define MS_DQ_WAVES 2   // waves per SIMD: 2 = key halves in turn, 1 = phase schedule
 #endif
@@ -386,25 +389,34 @@ __global__ void __launch_bounds__(kDqThreads) __attribute__((amdgpu_waves_per_eu
         dma_rows<D, kDualPad, 4>(kt, kp, rows, w, lane);
         dma_rows<D, kDualPad, 4>(vt, vp, rows, w, lane);
     };
-    int32_t kb = 0;
-    bool in0 = false, in1 = false, diag = false;
+    // the walk runs one tile ahead of the loads (as in the forward): no scalar
+    // load is outstanding inside a tile
+    int32_t kb = 0, kbn = 0;
+    bool in0 = false, in1 = false, diag = false, in0n = false, in1n = false, diagn = false;
     bool have = next(kb, in0, in1, diag);
     if (have) load(k0s, v0s, ContiguousRows{int64_t(kb) * 64});
+    bool haven = have && next(kbn, in0n, in1n, diagn);
     wait_vmem();
     __syncthreads();
     auto step = [&](const uint16_t* ck, const uint16_t* cv, uint16_t* nk, uint16_t* nv) {
-        int32_t kb2 = 0;
-        bool in0n = false, in1n = false, diagn = false;
-        const bool more = next(kb2, in0n, in1n, diagn);
-        if (more) load(nk, nv, ContiguousRows{int64_t(kb2) * 64});
+        if (haven) load(nk, nv, ContiguousRows{int64_t(kbn) * 64});
         if (half == 0 ? in0 : in1) dq_tile<D>(ck, cv, diag ? dlims : nullptr, st, qrow, lane, c2, isv);
+        __builtin_amdgcn_sched_barrier(0);
+        int32_t kb2 = 0;
+        bool in02 = false, in12 = false, diag2 = false;
+        const bool more2 = haven && next(kb2, in02, in12, diag2);
         wait_vmem();
         __syncthreads();
-        kb = kb2;
+        kb = kbn;
         in0 = in0n;
         in1 = in1n;
         diag = diagn;
-        have = more;
+        have = haven;
+        kbn = kb2;
+        in0n = in02;
+        in1n = in12;
+        diagn = diag2;
+        haven = more2;
     };
     while (have) {
         step(k0s, v0s, k1s, v1s);
@@ -506,15 +518,22 @@ __device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, co
     // scheduling fences separate the groups (the default schedule waits for
     // every read right before its MFMA and runs the phases back to back).
     // Rows of acc element r: 32 rb + 8 (r/4) + 4 h + r%4; column = this lane's key.
-    u32x4 fq[2][2], fg[2][2];   // [set][k-step of group]
-    auto read_sd = [&](int set, int rb, int s0) {
+    // Operand groups are read kAhead groups before their MFMAs, into rings of
+    // kAhead + 1 register sets (S / dP operands and transposed dV / dK
+    // operands); the first transposed groups are read during the last S / dP
+    // groups.
+    constexpr int kAhead = MS_KV_AHEAD < KD / 2 ? MS_KV_AHEAD : KD / 2, kSets = kAhead + 1;
+    u32x4 fq[kSets][2], fg[kSets][2];   // [set][k-step of group]
+    auto read_sd = [&](int n) {          // S / dP group n: half n / NG, k-steps 2 (n % NG) + {0, 1}
+        const int set = n % kSets, rb = n / (KD / 2), s0 = 2 * (n % (KD / 2));
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
             fq[set][j] = dma_read16<D, kDualPad>(t + T::kQ16, 32 * rb + l32, h + 2 * (s0 + j));
             fg[set][j] = dma_read16<D, kDualPad>(t + T::kG16, 32 * rb + l32, h + 2 * (s0 + j));
         }
     };
-    auto mfma_sd = [&](int set, int rb, int s0) {
+    auto mfma_sd = [&](int n) {
+        const int set = n % kSets, rb = n / (KD / 2), s0 = 2 * (n % (KD / 2));
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
             sacc[rb] = mfma32h(fq[set][j], kreg[s0 + j], sacc[rb]);
@@ -547,8 +566,9 @@ __device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, co
         }
     };
     // transposed A operands of dV (s dO)^T and dK Q^T for one 32-wide d block
-    u32x4 av[2][2], ak[2][2];   // [set][j]
-    auto read_tr = [&](int set, int rb, int i) {
+    u32x4 av[kSets][2], ak[kSets][2];   // [set][j]
+    auto read_tr = [&](int m) {            // dV / dK group m: half m / ND, d block m % ND
+        const int set = m % kSets, rb = m / ND, i = m % ND;
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
             av[set][j] = dma_read_tr<D, kDualPad>(t + T::kG16, 16 * (2 * rb + j), 32 * i, lane);
@@ -562,7 +582,8 @@ __device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, co
         zb[0] = pack8_f16<0>(pacc[rb]);
         zb[1] = pack8_f16<8>(pacc[rb]);
     };
-    auto mfma_kv = [&](int set, int i) {
+    auto mfma_kv = [&](int m) {
+        const int set = m % kSets, i = m % ND;
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
             dv[i] = mfma32h(av[set][j], pb[j], dv[i]);
@@ -571,24 +592,29 @@ __device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, co
     };
     static_assert(KD == 2 * ND, "four S/dP groups and four dV/dK groups per half");
     constexpr int NG = KD / 2;   // groups per half (4 for d = 128)
+    constexpr int NSD = 2 * NG, NTR = 2 * ND;
+    static_assert(kAhead >= 1 && kAhead <= NG && kAhead <= ND, "read distance");
+    // reads issued at S / dP group n: group n + kAhead, or the first transposed groups
+    auto ahead_sd = [&](int n) {
+        if (n + kAhead < NSD) read_sd(n + kAhead);
+        else read_tr(n + kAhead - NSD);
+    };
+#pragma unroll
+    for (int n = 0; n < kAhead; ++n) read_sd(n);
     // ---- A
-    read_sd(0, 0, 0);
 #pragma unroll
     for (int g = 0; g < NG; ++g) {
-        const int set = g & 1;
-        if (g + 1 < NG) read_sd(set ^ 1, 0, 2 * (g + 1));
-        else read_sd(set ^ 1, 1, 0);
+        ahead_sd(g);
         __builtin_amdgcn_sched_barrier(0);
-        mfma_sd(set, 0, 2 * g);
+        mfma_sd(g);
         __builtin_amdgcn_sched_barrier(0);
     }
     // ---- B
 #pragma unroll
     for (int g = 0; g < NG; ++g) {
-        const int set = (NG + g) & 1;
-        if (g + 1 < NG) read_sd(set ^ 1, 1, 2 * (g + 1));
+        ahead_sd(NG + g);
         __builtin_amdgcn_sched_barrier(0);
-        mfma_sd(set, 1, 2 * g);
+        mfma_sd(NG + g);
         if (g < 4) soft(0, g);
         __builtin_amdgcn_sched_barrier(0);
     }
@@ -597,14 +623,11 @@ __device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, co
     mask(0);
     pack(0);
     // ---- C
-    read_tr(0, 0, 0);
 #pragma unroll
     for (int i = 0; i < ND; ++i) {
-        const int set = i & 1;
-        if (i + 1 < ND) read_tr(set ^ 1, 0, i + 1);
-        else read_tr(set ^ 1, 1, 0);
+        if (i + kAhead < NTR) read_tr(i + kAhead);
         __builtin_amdgcn_sched_barrier(0);
-        mfma_kv(set, i);
+        mfma_kv(i);
         if (i < 4) soft(1, i);
         __builtin_amdgcn_sched_barrier(0);
     }
@@ -615,10 +638,9 @@ __device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, co
     // ---- D
 #pragma unroll
     for (int i = 0; i < ND; ++i) {
-        const int set = (ND + i) & 1;
-        if (i + 1 < ND) read_tr(set ^ 1, 1, i + 1);
+        if (ND + i + kAhead < NTR) read_tr(ND + i + kAhead);
         __builtin_amdgcn_sched_barrier(0);
-        mfma_kv(set, i);
+        mfma_kv(ND + i);
         __builtin_amdgcn_sched_barrier(0);
     }
 }
@@ -700,26 +722,36 @@ __global__ void __launch_bounds__(kKvThreads) __attribute__((amdgpu_waves_per_eu
         diag = ldc(a.q_blk_global, qb) == kg;
         return true;
     };
-    int bh = 0, qb = 0;
-    bool in0 = false, in1 = false, diag = false;
+    // the walk runs one tile ahead of the loads (as in the forward): no scalar
+    // load is outstanding inside a tile
+    int bh = 0, qb = 0, bhn = 0, qbn = 0;
+    bool in0 = false, in1 = false, diag = false, in0n = false, in1n = false, diagn = false;
     bool have = next(bh, qb, in0, in1, diag);
     if (have) kv_load_query_tile<D, 4>(t0s, a, bh, qb, w, lane);
+    bool haven = have && next(bhn, qbn, in0n, in1n, diagn);
     wait_vmem();
     __syncthreads();
     auto step = [&](const uint16_t* ct, uint16_t* nt) {
-        int bh2 = 0, qb2 = 0;
-        bool in0n = false, in1n = false, diagn = false;
-        const bool more = next(bh2, qb2, in0n, in1n, diagn);
-        if (more) kv_load_query_tile<D, 4>(nt, a, bh2, qb2, w, lane);
+        if (haven) kv_load_query_tile<D, 4>(nt, a, bhn, qbn, w, lane);
         if (half == 0 ? in0 : in1) kv_tile<D>(ct, kreg, vreg, diag ? dlims : nullptr, key, c2, isv, lane, dv, dk);
+        __builtin_amdgcn_sched_barrier(0);
+        int bh2 = 0, qb2 = 0;
+        bool in02 = false, in12 = false, diag2 = false;
+        const bool more2 = haven && next(bh2, qb2, in02, in12, diag2);
         wait_vmem();
         __syncthreads();
-        bh = bh2;
-        qb = qb2;
+        bh = bhn;
+        qb = qbn;
         in0 = in0n;
         in1 = in1n;
         diag = diagn;
-        have = more;
+        have = haven;
+        bhn = bh2;
+        qbn = qb2;
+        in0n = in02;
+        in1n = in12;
+        diagn = diag2;
+        haven = more2;
     };
     while (have) {
         step(t0s, t1s);

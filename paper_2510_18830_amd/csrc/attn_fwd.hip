@@ -290,33 +290,43 @@ attn_fwd_kernel(AttnArgs a) {
     };
 #endif
     if (tid < 64) dlims[tid] = tid;   // causal diagonal: key k visible to rows >= k
-    int32_t kb = 0, kg = 0;
-    uint32_t sel = 0;
+    // The walk runs one tile ahead of the loads: the list entries of tile t + 2
+    // are read (scalar loads) after tile t's compute, so they arrive during the
+    // end-of-tile wait, and no scalar load is outstanding inside a tile (it
+    // would make the LDS operand waits drain completely).
+    int32_t kb = 0, kg = 0, kbn = 0, kgn = 0;
+    uint32_t sel = 0, seln = 0;
     bool have = next(kb, sel, kg);
     if (have) {
         const ContiguousRows rows{int64_t(kb) * 64};
         dma_rows<D, kRowPad, NW>(k0s, kp, rows, w, lane);
         dma_rows<D, kTrPad, NW>(v0s, vp, rows, w, lane);
     }
+    bool haven = have && next(kbn, seln, kgn);
     wait_vmem();
     __syncthreads();
     // one tile: compute from (ck, cv) while the next tile lands in (nk, nv)
     auto step = [&](const uint16_t* ck, const uint16_t* cv, uint16_t* nk, uint16_t* nv) {
-        int32_t kb2 = 0, kg2 = 0;
-        uint32_t sel2 = 0;
-        const bool more = next(kb2, sel2, kg2);
-        if (more) {
-            const ContiguousRows rows{int64_t(kb2) * 64};
+        if (haven) {
+            const ContiguousRows rows{int64_t(kbn) * 64};
             dma_rows<D, kRowPad, NW>(nk, kp, rows, w, lane);
             dma_rows<D, kTrPad, NW>(nv, vp, rows, w, lane);
         }
         if ((sel >> blk) & 1u) fwd_tile<D>(ck, cv, kg == qg ? dlims : nullptr, st, qrow, lane, c2);
+        __builtin_amdgcn_sched_barrier(0);
+        int32_t kb2 = 0, kg2 = 0;
+        uint32_t sel2 = 0;
+        const bool more2 = haven && next(kb2, sel2, kg2);
         wait_vmem();
         __syncthreads();
-        kb = kb2;
-        kg = kg2;
-        sel = sel2;
-        have = more;
+        kb = kbn;
+        kg = kgn;
+        sel = seln;
+        have = haven;
+        kbn = kb2;
+        kgn = kg2;
+        seln = sel2;
+        haven = more2;
     };
     while (have) {
         step(k0s, v0s, k1s, v1s);
