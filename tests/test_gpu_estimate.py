@@ -203,3 +203,9 @@ def test_estimate_topp_full_size_sampled_heads(gpu, name, heads):
     _check_topp(got, (np.array(rv)[None], np.array(rs)[None]), p_v, p_s, wl.k_v, wl.k_s, heads=heads)
     del x
     torch.cuda.empty_cache()
+
+
+def test_mfma_peak_probe_runs(gpu):
+    # the measurement kernel beside the attention path: a plausible dense fp16 rate
+    t = ms.mfma_peak_tflops(2, 2000)
+    assert 300.0 < t < 3000.0, t

@@ -135,3 +135,10 @@ def test_ring_validation_before_launch():
     _bad(-2, lambda: work(3, 0))         # 128 blocks do not split into 3 shards
     _bad(-2, lambda: work(128, 1))       # zigzag needs 2 * 128 chunks
     _bad(-4, lambda: work(8, 0, ws=8))
+
+
+def test_peak_probe_validation():
+    L = ms.lib()
+    fake = ctypes.c_void_p(16)
+    for w, it, out in ((0, 10, fake), (9, 10, fake), (2, 0, fake), (2, 10, None)):
+        assert L.msparse_mfma_peak_probe(w, it, out, None) == -1
