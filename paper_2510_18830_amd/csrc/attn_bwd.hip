@@ -280,7 +280,6 @@ __device__ __forceinline__ void dq_tile(const uint16_t* kt, const uint16_t* vt, 
 #pragma unroll
     for (int q4 = NG; q4 < 4; ++q4) soft(0, q4);   // d = 64: two groups per half
     mask(0);
-    pack(0);
     // ---- C
     constexpr int S0 = (2 * NG) & 1;   // register set holding c = 0's first dQ operands
 #pragma unroll
@@ -296,7 +295,6 @@ __device__ __forceinline__ void dq_tile(const uint16_t* kt, const uint16_t* vt, 
 #pragma unroll
     for (int q4 = ND; q4 < 4; ++q4) soft(1, q4);
     mask(1);
-    pack(1);
     // ---- D
 #pragma unroll
     for (int i = 0; i < ND; ++i) {
@@ -540,19 +538,30 @@ __device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, co
             pacc[rb] = mfma32h(fg[set][j], vreg[s0 + j], pacc[rb]);
         }
     };
+    // P and s dZ of half rb as the fp16 B operands of dV / dK (pb, zb: element
+    // r of the accumulator goes to half r % 2 of word (r % 8) / 2 of operand
+    // r / 8), written straight from the softmax terms, so the accumulators are
+    // never written back
+    u32x4 pb[2][2], zb[2][2];   // [rb][j]
     // softmax terms of rows 32 rb + 8 q4 + 4 h + 0..3
     auto soft = [&](int rb, int q4) {
         const int row0 = 32 * rb + 8 * q4 + 4 * h;
         const f32x4 l4 = *reinterpret_cast<const f32x4*>(lse2 + row0);
         const f32x4 d4 = *reinterpret_cast<const f32x4*>(dlt + row0);
+        float pv[4], zv[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const int r = 4 * q4 + e;
-            const float p = fast_exp2(__builtin_fmaf(sacc[rb][r], c2, -l4[e]));
-            sacc[rb][r] = p;
-            pacc[rb][r] = p * __builtin_fmaf(pacc[rb][r], isv, -d4[e]);
+            pv[e] = fast_exp2(__builtin_fmaf(sacc[rb][r], c2, -l4[e]));
+            zv[e] = pv[e] * __builtin_fmaf(pacc[rb][r], isv, -d4[e]);
         }
+        const int j = q4 >> 1, w0 = 2 * (q4 & 1);
+        pb[rb][j][w0] = pack_f16x2(pv[0], pv[1]);
+        pb[rb][j][w0 + 1] = pack_f16x2(pv[2], pv[3]);
+        zb[rb][j][w0] = pack_f16x2(zv[0], zv[1]);
+        zb[rb][j][w0 + 1] = pack_f16x2(zv[2], zv[3]);
     };
+    // masked entries (rare diagonal tiles): clear their fp16 halves
     auto mask = [&](int rb) {
         if (lims) {
             keep_branch();
@@ -560,8 +569,9 @@ __device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, co
 #pragma unroll
             for (int r = 0; r < 16; ++r)
                 if (8 * (r >> 2) + (r & 3) < lim) {
-                    sacc[rb][r] = 0.f;
-                    pacc[rb][r] = 0.f;
+                    const uint32_t keep = (r & 1) ? 0x0000FFFFu : 0xFFFF0000u;
+                    pb[rb][r >> 3][(r & 7) >> 1] &= keep;
+                    zb[rb][r >> 3][(r & 7) >> 1] &= keep;
                 }
         }
     };
@@ -575,19 +585,12 @@ __device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, co
             ak[set][j] = dma_read_tr<D, kDualPad>(t + T::kQ16, 16 * (2 * rb + j), 32 * i, lane);
         }
     };
-    u32x4 pb[2], zb[2];
-    auto pack = [&](int rb) {
-        pb[0] = pack8_f16<0>(sacc[rb]);
-        pb[1] = pack8_f16<8>(sacc[rb]);
-        zb[0] = pack8_f16<0>(pacc[rb]);
-        zb[1] = pack8_f16<8>(pacc[rb]);
-    };
     auto mfma_kv = [&](int m) {
-        const int set = m % kSets, i = m % ND;
+        const int set = m % kSets, rb = m / ND, i = m % ND;
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
-            dv[i] = mfma32h(av[set][j], pb[j], dv[i]);
-            dk[i] = mfma32h(ak[set][j], zb[j], dk[i]);
+            dv[i] = mfma32h(av[set][j], pb[rb][j], dv[i]);
+            dk[i] = mfma32h(ak[set][j], zb[rb][j], dk[i]);
         }
     };
     static_assert(KD == 2 * ND, "four S/dP groups and four dV/dK groups per half");
@@ -621,7 +624,6 @@ __device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, co
 #pragma unroll
     for (int q4 = NG; q4 < 4; ++q4) soft(0, q4);   // d = 64: two groups per half
     mask(0);
-    pack(0);
     // ---- C
 #pragma unroll
     for (int i = 0; i < ND; ++i) {
@@ -634,7 +636,6 @@ __device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, co
 #pragma unroll
     for (int q4 = ND; q4 < 4; ++q4) soft(1, q4);
     mask(1);
-    pack(1);
     // ---- D
 #pragma unroll
     for (int i = 0; i < ND; ++i) {
