@@ -114,9 +114,6 @@ constexpr int kDqThreads = 256;
 #ifndef MS_KV_AHEAD
 #define MS_KV_AHEAD 1   // dK/dV operand groups read this many groups ahead
 #endif
-#ifndef MS_DQ_WAVES
-#define MS_DQ_WAVES 2   // waves per SIMD: 2 = key halves in turn, 1 = phase schedule
-#endif
 
 template <int D>
 struct DqRows {
@@ -134,19 +131,12 @@ __device__ __forceinline__ void dq_tile(const uint16_t* kt, const uint16_t* vt, 
                                         int qrow, int lane, float c2, float isv) {
     constexpr int KD = DqRows<D>::KD, ND = DqRows<D>::ND;
     const int h = lane >> 5, l32 = lane & 31;
-    f32x16 sacc[2], pacc[2];
-#pragma unroll
-    for (int c = 0; c < 2; ++c) {
-        sacc[c] = f32x16{};
-        pacc[c] = f32x16{};
-    }
-#if MS_DQ_WAVES == 2
     // Two waves per SIMD (the other wave's MFMAs overlap this wave's softmax
     // terms), so the key halves c run one after the other and only one half's
     // S^T / dP^T accumulators are live: S^T, dP^T of keys 32 c .. 32 c + 31,
     // the dZ terms, then that half's dQ k-steps.  Each S / dP k-step's operands
     // are read one step ahead into a second register set.
-    u32x4 fk[2], fv[2], ak[1][2];
+    u32x4 fk[2], fv[2], ak[2];
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
         f32x16 sa = f32x16{}, pa = f32x16{};
@@ -154,16 +144,16 @@ __device__ __forceinline__ void dq_tile(const uint16_t* kt, const uint16_t* vt, 
             fk[set] = dma_read16<D, kDualPad>(kt, 32 * c + l32, h + 2 * s);
             fv[set] = dma_read16<D, kDualPad>(vt, 32 * c + l32, h + 2 * s);
         };
-        auto read_tr = [&](int set, int i) {
+        auto read_tr = [&](int i) {
 #pragma unroll
-            for (int j = 0; j < 2; ++j) ak[set][j] = dma_read_tr<D, kDualPad>(kt, 16 * (2 * c + j), 32 * i, lane);
+            for (int j = 0; j < 2; ++j) ak[j] = dma_read_tr<D, kDualPad>(kt, 16 * (2 * c + j), 32 * i, lane);
         };
         read_sd(0, 0);
 #pragma unroll
         for (int k = 0; k < KD; ++k) {
             const int set = k & 1;
             if (k + 1 < KD) read_sd(set ^ 1, k + 1);
-            else read_tr(0, 0);
+            else read_tr(0);
             __builtin_amdgcn_sched_barrier(0);
             sa = mfma32h(fk[set], st.q[k], sa);
             pa = mfma32h(fv[set], st.g[k], pa);
@@ -190,125 +180,16 @@ __device__ __forceinline__ void dq_tile(const uint16_t* kt, const uint16_t* vt, 
         zb[1] = pack8_f16<8>(sa);
 #pragma unroll
         for (int i = 0; i < ND; ++i) {
-            if (i > 0) read_tr(0, i);
+            if (i > 0) read_tr(i);
 #pragma unroll
-            for (int j = 0; j < 2; ++j) st.acc[i] = mfma32h(ak[0][j], zb[j], st.acc[i]);
+            for (int j = 0; j < 2; ++j) st.acc[i] = mfma32h(ak[j], zb[j], st.acc[i]);
         }
     }
-#else
-    // Same phase schedule as kv_tile, over the two key halves c:
-    //   A  S^T, dP^T of keys 32 c .. for c = 0
-    //   B  S^T, dP^T of c = 1, interleaved with c = 0's dZ terms
-    //   C  dQ k-steps of c = 0, interleaved with c = 1's dZ terms
-    //   D  dQ k-steps of c = 1
-    // with operands read one group ahead into two register sets.
-    u32x4 fk[2][2], fv[2][2];   // [set][k-step of group]
-    auto read_sd = [&](int set, int c, int s0) {
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            fk[set][j] = dma_read16<D, kDualPad>(kt, 32 * c + l32, h + 2 * (s0 + j));
-            fv[set][j] = dma_read16<D, kDualPad>(vt, 32 * c + l32, h + 2 * (s0 + j));
-        }
-    };
-    auto mfma_sd = [&](int set, int c, int s0) {
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            sacc[c] = mfma32h(fk[set][j], st.q[s0 + j], sacc[c]);
-            pacc[c] = mfma32h(fv[set][j], st.g[s0 + j], pacc[c]);
-        }
-    };
-    // s dZ^T = P o (s dP^T - s Delta), P = exp2(c2 z - lse2), for accumulator
-    // elements 4 q4 .. 4 q4 + 3 (keys 32 c + 8 q4 + 4 h + 0..3)
-    auto soft = [&](int c, int q4) {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const int r = 4 * q4 + e;
-            const float p = fast_exp2(__builtin_fmaf(sacc[c][r], c2, -st.lse2));
-            sacc[c][r] = p * __builtin_fmaf(pacc[c][r], isv, -st.dlt);
-        }
-    };
-    auto mask = [&](int c) {
-        if (lims) {
-            keep_branch();
-#pragma unroll
-            for (int q4 = 0; q4 < 4; ++q4) {
-                const i32x4 l4 = *reinterpret_cast<const i32x4*>(lims + 32 * c + 8 * q4 + 4 * h);
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    if (qrow < l4[e]) sacc[c][4 * q4 + e] = 0.f;
-            }
-        }
-    };
-    u32x4 zb[2];
-    auto pack = [&](int c) {
-        zb[0] = pack8_f16<0>(sacc[c]);
-        zb[1] = pack8_f16<8>(sacc[c]);
-    };
-    // dQ += (s dZ) K for key half c, d block i: K^T read transposed
-    u32x4 ak[2][2];   // [set][j]
-    auto read_tr = [&](int set, int c, int i) {
-#pragma unroll
-        for (int j = 0; j < 2; ++j) ak[set][j] = dma_read_tr<D, kDualPad>(kt, 16 * (2 * c + j), 32 * i, lane);
-    };
-    auto mfma_q = [&](int set, int i) {
-#pragma unroll
-        for (int j = 0; j < 2; ++j) st.acc[i] = mfma32h(ak[set][j], zb[j], st.acc[i]);
-    };
-    constexpr int NG = KD / 2;
-    // ---- A
-    read_sd(0, 0, 0);
-#pragma unroll
-    for (int g = 0; g < NG; ++g) {
-        const int set = g & 1;
-        if (g + 1 < NG) read_sd(set ^ 1, 0, 2 * (g + 1));
-        else read_sd(set ^ 1, 1, 0);
-        __builtin_amdgcn_sched_barrier(0);
-        mfma_sd(set, 0, 2 * g);
-        __builtin_amdgcn_sched_barrier(0);
-    }
-    // ---- B
-#pragma unroll
-    for (int g = 0; g < NG; ++g) {
-        const int set = (NG + g) & 1;
-        if (g + 1 < NG) read_sd(set ^ 1, 1, 2 * (g + 1));
-        else read_tr(set ^ 1, 0, 0);
-        __builtin_amdgcn_sched_barrier(0);
-        mfma_sd(set, 1, 2 * g);
-        if (g < 4) soft(0, g);
-        __builtin_amdgcn_sched_barrier(0);
-    }
-#pragma unroll
-    for (int q4 = NG; q4 < 4; ++q4) soft(0, q4);   // d = 64: two groups per half
-    mask(0);
-    // ---- C
-    constexpr int S0 = (2 * NG) & 1;   // register set holding c = 0's first dQ operands
-#pragma unroll
-    for (int i = 0; i < ND; ++i) {
-        const int set = (S0 + i) & 1;
-        if (i + 1 < ND) read_tr(set ^ 1, 0, i + 1);
-        else read_tr(set ^ 1, 1, 0);
-        __builtin_amdgcn_sched_barrier(0);
-        mfma_q(set, i);
-        if (i < 4) soft(1, i);
-        __builtin_amdgcn_sched_barrier(0);
-    }
-#pragma unroll
-    for (int q4 = ND; q4 < 4; ++q4) soft(1, q4);
-    mask(1);
-    // ---- D
-#pragma unroll
-    for (int i = 0; i < ND; ++i) {
-        const int set = (S0 + ND + i) & 1;
-        if (i + 1 < ND) read_tr(set ^ 1, 1, i + 1);
-        __builtin_amdgcn_sched_barrier(0);
-        mfma_q(set, i);
-        __builtin_amdgcn_sched_barrier(0);
-    }
-#endif
+
 }
 
 template <int D>
-__global__ void __launch_bounds__(kDqThreads) __attribute__((amdgpu_waves_per_eu(MS_DQ_WAVES, MS_DQ_WAVES))) bwd_dq_kernel(AttnArgs a) {
+__global__ void __launch_bounds__(kDqThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) bwd_dq_kernel(AttnArgs a) {
     constexpr int KD = DqRows<D>::KD, ND = DqRows<D>::ND;
     constexpr int TE = DmaTile<D, kDualPad>::kElems;
     __shared__ uint16_t k0s[TE], v0s[TE], k1s[TE], v1s[TE];
@@ -350,7 +231,6 @@ __global__ void __launch_bounds__(kDqThreads) __attribute__((amdgpu_waves_per_eu
     const int64_t item0 = int64_t(bh) * a.nqb + qb0;
     const int64_t e00 = ldc(a.blk_ptr, item0), e01 = ldc(a.blk_ptr, item0 + 1);
     const int64_t e11 = has1 ? ldc(a.blk_ptr, item0 + 2) : e01;
-#if MS_WALK_DESC
     // walked from the diagonal down (as in the forward: the group's shared
     // band first)
     int64_t p0 = e01 - 1, p1 = e11 - 1;
@@ -366,23 +246,6 @@ __global__ void __launch_bounds__(kDqThreads) __attribute__((amdgpu_waves_per_eu
         diag = ldc(a.k_blk_global, kb) == qg;
         return true;
     };
-#else
-    int64_t p0 = e00, p1 = e01;
-    // the diagonal test is made here, one tile ahead (no scalar load pending
-    // inside a tile)
-    auto next = [&](int32_t& kb, bool& in0, bool& in1, bool& diag) {
-        if (p0 >= e01 && p1 >= e11) return false;
-        const int32_t k0 = p0 < e01 ? ldc(a.blk_idx, p0) : INT32_MAX;
-        const int32_t k1 = p1 < e11 ? ldc(a.blk_idx, p1) : INT32_MAX;
-        kb = min(k0, k1);
-        in0 = k0 == kb;
-        in1 = k1 == kb;
-        p0 += in0;
-        p1 += in1;
-        diag = ldc(a.k_blk_global, kb) == qg;
-        return true;
-    };
-#endif
     auto load = [&](uint16_t* kt, uint16_t* vt, auto rows) {
         dma_rows<D, kDualPad, 4>(kt, kp, rows, w, lane);
         dma_rows<D, kDualPad, 4>(vt, vp, rows, w, lane);

@@ -33,9 +33,6 @@ namespace {
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kSlack = 8.f;   // log2 units
-#ifndef MS_FWD_DOT2
-#define MS_FWD_DOT2 0
-#endif
 
 // Online-softmax state of one wave: 32 query rows, O^T accumulator.
 template <int D>
@@ -116,27 +113,6 @@ __device__ __forceinline__ void fwd_tile(const uint16_t* kt, const uint16_t* vt,
         st.m = m_new;
     }
     const float m_use = st.m == -INFINITY ? 0.f : st.m;
-#if MS_FWD_DOT2
-#pragma unroll
-    for (int c = 0; c < 2; ++c)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) sacc[c][r] = fast_exp2(__builtin_fmaf(sacc[c][r], c2, -m_use));
-    // ---- O^T += V^T P^T (A = V^T read transposed from the fp16 V rows)
-    u32x4 pb[4];
-    pb[0] = pack8_f16<0>(sacc[0]);
-    pb[1] = pack8_f16<8>(sacc[0]);
-    pb[2] = pack8_f16<0>(sacc[1]);
-    pb[3] = pack8_f16<8>(sacc[1]);
-    // row sum of the fp16 P that the PV product uses: 2 terms per dot2
-    typedef _Float16 h2 __attribute__((ext_vector_type(2)));
-    const h2 one2 = {(_Float16)1.f, (_Float16)1.f};
-    float rs = 0.f;
-#pragma unroll
-    for (int g = 0; g < 4; ++g)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) rs = __builtin_amdgcn_fdot2(__builtin_bit_cast(h2, pb[g][e]), one2, rs, false);
-    st.l += rs + __shfl_xor(rs, 32);
-#else
     float rs = 0.f;
 #pragma unroll
     for (int c = 0; c < 2; ++c)
@@ -153,7 +129,6 @@ __device__ __forceinline__ void fwd_tile(const uint16_t* kt, const uint16_t* vt,
     pb[1] = pack8_f16<8>(sacc[0]);
     pb[2] = pack8_f16<0>(sacc[1]);
     pb[3] = pack8_f16<8>(sacc[1]);
-#endif
     // V^T operands in groups of one d block (4 operands) into two register sets
     u32x4 av[2][4];
     auto read_tr = [&](int set, int i) {
@@ -230,7 +205,6 @@ attn_fwd_kernel(AttnArgs a) {
     // ---- block tiles: the union of the NB ascending block lists, software
     // pipelined (the loads of the next tile are in flight during this tile)
     const int64_t item0 = int64_t(bh) * a.nqb + qb0;
-#if MS_WALK_DESC
     // Lists are walked from their last (nearest the diagonal) tile down: the
     // band of block-diagonals that a KV group's heads share comes first, so
     // the group's workgroups read the same K / V tiles at about the same time
@@ -260,35 +234,6 @@ attn_fwd_kernel(AttnArgs a) {
         kg = ldc(a.k_blk_global, kb);
         return true;
     };
-#else
-    int64_t p[NB], e[NB];
-#pragma unroll
-    for (int j = 0; j < NB; ++j) {
-        p[j] = j < nblk ? ldc(a.blk_ptr, item0 + j) : 0;
-        e[j] = j < nblk ? ldc(a.blk_ptr, item0 + j + 1) : 0;
-    }
-    // next key tile of the union: kb, the blocks that selected it (bit j), and
-    // its global key block (for the diagonal tests; read one tile ahead)
-    auto next = [&](int32_t& kb, uint32_t& sel, int32_t& kg) {
-        int32_t k[NB];
-        kb = INT32_MAX;
-#pragma unroll
-        for (int j = 0; j < NB; ++j) {
-            k[j] = p[j] < e[j] ? ldc(a.blk_idx, p[j]) : INT32_MAX;
-            kb = min(kb, k[j]);
-        }
-        if (kb == INT32_MAX) return false;
-        sel = 0;
-#pragma unroll
-        for (int j = 0; j < NB; ++j)
-            if (k[j] == kb) {
-                sel |= 1u << j;
-                ++p[j];
-            }
-        kg = ldc(a.k_blk_global, kb);
-        return true;
-    };
-#endif
     if (tid < 64) dlims[tid] = tid;   // causal diagonal: key k visible to rows >= k
     // The walk runs one tile ahead of the loads: the list entries of tile t + 2
     // are read (scalar loads) after tile t's compute, so they arrive during the

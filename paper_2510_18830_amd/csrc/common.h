@@ -54,26 +54,6 @@ __device__ __forceinline__ T ldc(const T* p, int64_t i) {
 // it a branch instead of turning its body into unconditional selects.
 __device__ __forceinline__ void keep_branch() { asm volatile(""); }
 
-// Scheduling hint for a run of N MFMAs each fed by one LDS read: issue
-// kLdsAhead reads first, then alternate MFMA / read, so that kLdsAhead reads
-// are in flight while the MFMAs issue (the default schedule waits for each
-// read right before its MFMA).
-#ifndef MS_LDS_AHEAD
-#define MS_LDS_AHEAD 4
-#endif
-constexpr int kLdsAhead = MS_LDS_AHEAD;
-template <int N>
-__device__ __forceinline__ void sched_reads_ahead() {
-    constexpr int kMfma = 0x008, kDsRead = 0x100;
-    __builtin_amdgcn_sched_group_barrier(kDsRead, kLdsAhead, 0);
-#pragma unroll
-    for (int i = 0; i < N - kLdsAhead; ++i) {
-        __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(kDsRead, 1, 0);
-    }
-    __builtin_amdgcn_sched_group_barrier(kMfma, kLdsAhead, 0);
-}
-
 // ---------------------------------------------------------------- MFMA
 // D(32x32) += A(32x16) * B(16x32), bf16 inputs, fp32 accumulate.
 // Lane l supplies A[l%32][8*(l/32) .. +8] and B[8*(l/32) .. +8][l%32];

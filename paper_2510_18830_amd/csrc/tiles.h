@@ -148,9 +148,6 @@ __device__ __forceinline__ u32x4 dma_read_tr(const uint16_t* x, int k0, int m0, 
     return o;
 }
 
-#ifndef MS_WALK_DESC
-#define MS_WALK_DESC 1   // walk block lists from the diagonal down (0: ascending)
-#endif
 #ifndef MS_XCHUNK
 #define MS_XCHUNK 64   // logical items per XCD run
 #endif
