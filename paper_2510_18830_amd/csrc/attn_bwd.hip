@@ -861,13 +861,23 @@ __global__ void __launch_bounds__(128) bwd_colmerge_kernel(AttnArgs a) {
             const int i0 = a.col_item[ch], i1 = a.col_item[ch + 1];
             const int64_t row = int64_t(bk) * a.Nk + a.vcol_idx[e];
             for (int j = threadIdx.x; j < a.d; j += blockDim.x) {
-                float sk = 0.f, sv = 0.f;
-                for (int it = i0; it < i1; ++it) {
-                    sk += a.dk_col[(int64_t(it) * 64 + key) * a.d + j];
-                    sv += a.dv_col[(int64_t(it) * 64 + key) * a.d + j];
+                // four independent partial sums (eight loads in flight), combined
+                // in a fixed order
+                float sk[4] = {0.f, 0.f, 0.f, 0.f}, sv[4] = {0.f, 0.f, 0.f, 0.f};
+                int it = i0;
+                for (; it + 4 <= i1; it += 4) {
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        sk[u] += a.dk_col[(int64_t(it + u) * 64 + key) * a.d + j];
+                        sv[u] += a.dv_col[(int64_t(it + u) * 64 + key) * a.d + j];
+                    }
                 }
-                a.dk[row * a.d + j] += sk;
-                a.dv[row * a.d + j] += sv;
+                for (; it < i1; ++it) {
+                    sk[0] += a.dk_col[(int64_t(it) * 64 + key) * a.d + j];
+                    sv[0] += a.dv_col[(int64_t(it) * 64 + key) * a.d + j];
+                }
+                a.dk[row * a.d + j] += (sk[0] + sk[1]) + (sk[2] + sk[3]);
+                a.dv[row * a.d + j] += (sv[0] + sv[1]) + (sv[2] + sv[3]);
             }
         }
     }
