@@ -214,7 +214,7 @@ def ring_leg(x, v_idx, s_idx, wl, world: int, rank: int, steps: int):
             if timed:
                 ev[t][2].record()
             ms.attn_bwd(dims, q_loc, k_s, v_s, out, do_loc, l_acc, idx, dq, dk, dv, dq_accumulate=(t > 0),
-                        out_f32=o_acc, workspace=bws)
+                        out_f32=o_acc, workspace=bws, reuse_qrows=(t > 0))
             if timed:
                 ev[t][3].record()
 

@@ -272,16 +272,27 @@ MSPARSE_API msparse_status msparse_merge_out_lse(const msparse_dims* dims, const
  * are the forward's final (merged) results; out_f32 (may be NULL) is the same
  * output unrounded and is used for Delta when given (recommended: Delta from
  * a bf16-rounded O moves large gradients by about 2^-9 of their size).
- * dq, dk, dv are fp32 and overwritten, except that dq_accumulate = 1 adds into
- * dq (ring steps after the first).
+ * dq, dk, dv are fp32 and overwritten, with two flags:
+ *   MSPARSE_BWD_ACCUMULATE_DQ  add into dq instead (ring steps after the first);
+ *   MSPARSE_BWD_REUSE_QROWS    the workspace still holds the query-side data of
+ *                              the previous msparse_attn_bwd call, made with the
+ *                              same dims, q, out, out_f32, dout and lse and the
+ *                              same workspace (the previous ring step of the
+ *                              same worker; only k, v and the index differ):
+ *                              Delta, the lse rows and the fp16 copies of q and
+ *                              dO are not recomputed.  Results are undefined if
+ *                              that does not hold.
+ * Other flag bits are MSPARSE_ERR_INVALID.
  * Workspace: msparse_attn_bwd_workspace(dims, vcol_cap) bytes; it holds
  * fp16 copies of q, k, v and dO (each times a power of two), Delta, lse, and
- * the column pass's work list and per-item partials. */
+ * the column pass's work list and per-item partials (the query-side part sits
+ * first and does not depend on vcol_cap). */
+enum { MSPARSE_BWD_ACCUMULATE_DQ = 1, MSPARSE_BWD_REUSE_QROWS = 2 };
 MSPARSE_API size_t msparse_attn_bwd_workspace(const msparse_dims* dims, int64_t vcol_cap);
 MSPARSE_API msparse_status msparse_attn_bwd(const msparse_dims* dims, const void* q, const void* k, const void* v,
                                 const void* out, const float* out_f32, const void* dout, const float* lse,
                                 const msparse_index* index, float* dq, float* dk, float* dv,
-                                int32_t dq_accumulate, void* workspace, size_t workspace_bytes, void* stream);
+                                int32_t flags, void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* Kernel-level tracing for measurement.  While enabled, every kernel the

@@ -283,8 +283,9 @@ def attn_bwd_workspace_bytes(dims, vcol_cap):
 
 
 def attn_bwd(dims, q, k, v, out, dout, lse, index: SparseIndex, dq=None, dk=None, dv=None, dq_accumulate=False,
-             out_f32=None, workspace=None, stream=None):
-    """msparse_attn_bwd: returns (dq, dk, dv) fp32."""
+             out_f32=None, workspace=None, stream=None, reuse_qrows=False):
+    """msparse_attn_bwd: returns (dq, dk, dv) fp32.  reuse_qrows: the workspace still holds the query-side
+    data of the previous call of the same ring worker (MSPARSE_BWD_REUSE_QROWS)."""
     f32 = torch.float32
     dq = torch.empty(q.shape, dtype=f32, device=q.device) if dq is None else dq
     dk = torch.empty(k.shape, dtype=f32, device=q.device) if dk is None else dk
@@ -292,7 +293,8 @@ def attn_bwd(dims, q, k, v, out, dout, lse, index: SparseIndex, dq=None, dk=None
     if workspace is None:
         workspace = _workspace(attn_bwd_workspace_bytes(dims, index.struct.vcol_cap), q.device)
     _check(lib().msparse_attn_bwd(ctypes.byref(dims), _p(q), _p(k), _p(v), _p(out), _p(out_f32), _p(dout), _p(lse),
-                                  ctypes.byref(index.struct), _p(dq), _p(dk), _p(dv), int(bool(dq_accumulate)),
+                                  ctypes.byref(index.struct), _p(dq), _p(dk), _p(dv),
+                                  int(bool(dq_accumulate)) | (2 if reuse_qrows else 0),
                                   _p(workspace), workspace.numel(), _stream(stream)))
     return dq, dk, dv
 

@@ -457,13 +457,15 @@ size_t msparse_attn_bwd_workspace(const msparse_dims* dims, int64_t vcol_cap) {
 
 msparse_status msparse_attn_bwd(const msparse_dims* dims, const void* q, const void* k, const void* v,
                                 const void* out, const float* out_f32, const void* dout, const float* lse,
-                                const msparse_index* index, float* dq, float* dk, float* dv, int32_t dq_accumulate,
+                                const msparse_index* index, float* dq, float* dk, float* dv, int32_t flags,
                                 void* ws, size_t ws_bytes, void* stream) {
     msparse_status st = check_dims(dims, false);
     if (st) return st;
     if (!q || !k || !v || !out || !dout || !lse || !dq || !dk || !dv)
         return fail(MSPARSE_ERR_INVALID, "tensor pointer is NULL");
     if ((st = check_index_struct(dims, index, true))) return st;
+    if (flags & ~(MSPARSE_BWD_ACCUMULATE_DQ | MSPARSE_BWD_REUSE_QROWS))
+        return fail(MSPARSE_ERR_INVALID, "backward flags 0x%x", unsigned(flags));
     const size_t need = msparse_attn_bwd_workspace(dims, index->vcol_cap);
     if (!ws || ws_bytes < need) return fail(MSPARSE_ERR_WORKSPACE, "bwd workspace %zu < %zu bytes", ws_bytes, need);
     if (dims->seq_q == 0 && dims->seq_k == 0) return MSPARSE_OK;
@@ -481,7 +483,8 @@ msparse_status msparse_attn_bwd(const msparse_dims* dims, const void* q, const v
     a.dq = dq;
     a.dk = dk;
     a.dv = dv;
-    a.dq_accumulate = dq_accumulate;
+    a.dq_accumulate = (flags & MSPARSE_BWD_ACCUMULATE_DQ) != 0;
+    a.reuse_qrows = (flags & MSPARSE_BWD_REUSE_QROWS) != 0;
     hipStream_t s = static_cast<hipStream_t>(stream);
     return check_hip(launch_attn_bwd(a, s), s, "attn bwd");
 }

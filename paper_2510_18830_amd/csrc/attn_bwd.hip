@@ -38,8 +38,10 @@ constexpr int kThreads = 128;
 constexpr float kLog2e = 1.4426950408889634f;
 
 // ------------------------------------------------------------------ Delta
+// max-word reset: all four, or only those of K and V when the Q-side data is reused
 __global__ void bwd_init_kernel(AttnArgs a) {
-    if (threadIdx.x < 4) (threadIdx.x == 0 ? a.dmax : a.qkvmax + threadIdx.x - 1)[0] = 0u;
+    const int i = threadIdx.x;
+    if (i < 4 && (!a.reuse_qrows || i >= 2)) (i == 0 ? a.dmax : a.qkvmax + i - 1)[0] = 0u;
 }
 
 constexpr int kDeltaBlocks = 2048;
@@ -887,7 +889,10 @@ template <int D>
 hipError_t launch_bwd_d(const AttnArgs& a, hipStream_t s) {
     const int64_t rows = int64_t(a.B) * a.Hq * a.Nq;
     { TraceScope _t("bwd_init", s); hipLaunchKernelGGL(bwd_init_kernel, dim3(1), dim3(64), 0, s, a); }
-    if (rows > 0) {
+    // Q-side data (Delta, lse rows, max |dO|, max |Q|, the Q and dO copies) is
+    // the same for every ring step of a worker: a later step may reuse it
+    const bool qside = !a.reuse_qrows;
+    if (qside && rows > 0) {
         TraceScope _t("bwd_delta", s);
         const int64_t groups = (rows + 15) / 16;
         hipLaunchKernelGGL(bwd_delta_kernel, dim3(unsigned(groups < kDeltaBlocks ? groups : int64_t(kDeltaBlocks))),
@@ -895,7 +900,7 @@ hipError_t launch_bwd_d(const AttnArgs& a, hipStream_t s) {
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    if (rows > 0) {
+    if (qside && rows > 0) {
         TraceScope _t("bwd_rowprep", s);
         const int64_t want = (rows + 255) / 256;
         hipLaunchKernelGGL(bwd_rowprep_kernel, dim3(unsigned(want < kDeltaBlocks ? want : int64_t(kDeltaBlocks))),
@@ -904,13 +909,13 @@ hipError_t launch_bwd_d(const AttnArgs& a, hipStream_t s) {
     // scaled fp16 copies: Q, K, V to max in [2^14, 2^15), dO to [8, 16)
     const int64_t nkv = int64_t(a.B) * a.Hkv * a.Nk * a.d;
     const int64_t nq = int64_t(a.B) * a.Hq * a.Nq * a.d;
-    if ((e = launch_absmax(a.q, nq, a.qkvmax, s)) != hipSuccess) return e;
+    if (qside && (e = launch_absmax(a.q, nq, a.qkvmax, s)) != hipSuccess) return e;
     if ((e = launch_absmax(a.k, nkv, a.qkvmax + 1, s)) != hipSuccess) return e;
     if ((e = launch_absmax(a.v, nkv, a.qkvmax + 2, s)) != hipSuccess) return e;
-    if ((e = launch_to_f16(a.q, a.q16, nq, a.qkvmax, kOperandExp, s)) != hipSuccess) return e;
+    if (qside && (e = launch_to_f16(a.q, a.q16, nq, a.qkvmax, kOperandExp, s)) != hipSuccess) return e;
     if ((e = launch_to_f16(a.k, a.k16, nkv, a.qkvmax + 1, kOperandExp, s)) != hipSuccess) return e;
     if ((e = launch_to_f16(a.v, a.v16, nkv, a.qkvmax + 2, kOperandExp, s)) != hipSuccess) return e;
-    if ((e = launch_to_f16(a.dout, a.g16, nq, a.dmax, 4, s)) != hipSuccess) return e;
+    if (qside && (e = launch_to_f16(a.dout, a.g16, nq, a.dmax, 4, s)) != hipSuccess) return e;
     const int64_t qgrid = int64_t(a.B) * a.Hq * ((a.nqb + 1) / 2);
     if (qgrid > 0) { TraceScope _t("bwd_dq", s); hipLaunchKernelGGL(bwd_dq_kernel<D>, dim3(unsigned(qgrid)), dim3(kDqThreads), 0, s, a); }
     if ((e = hipGetLastError()) != hipSuccess) return e;

@@ -97,6 +97,7 @@ struct AttnArgs {
     int64_t col_budget;    // items the span is chosen for
     int64_t col_slots;     // item capacity (grid of the column kernel)
     int32_t dq_accumulate;
+    int32_t reuse_qrows;   // the workspace already holds the Q-side data (a later ring step)
     int32_t B, Hq, Hkv, Nq, Nk, d;
     int32_t nqb, nkb;
     float scale;

@@ -76,8 +76,9 @@ def test_bwd_empty_rows_and_dense_budget(gpu):
         assert_close(n, g, r)
 
 
-@pytest.mark.parametrize("layout,inner", [("striped", 0), ("zigzag", 0), ("striped", 2), ("zigzag", 2)])
-def test_bwd_ring_worker_share(gpu, layout, inner):
+@pytest.mark.parametrize("layout,inner,reuse", [("striped", 0, False), ("zigzag", 0, False), ("striped", 2, False),
+                                                ("zigzag", 2, True), ("striped", 0, True)])
+def test_bwd_ring_worker_share(gpu, layout, inner, reuse):
     """Worker r's steps: dQ of its rows summed over steps; each step's dK / dV of
     the step's shard equals the whole-sequence gradient restricted to worker r's
     query rows (dO zero elsewhere) and to the shard's keys."""
@@ -121,9 +122,11 @@ def test_bwd_ring_worker_share(gpu, layout, inner):
         _, pl = ms.attn_fwd(dims, q_loc, k_loc, v_loc, idx, out_f32=po, bf16_out=False)
         ms.merge_out_lse(dims, po, pl, o_acc, l_acc, out if t == W - 1 else None, first=(t == 0))
     dq = torch.empty(q_loc.shape, dtype=torch.float32, device=dev)
+    # reuse: one workspace for the worker's steps; later steps keep its query-side data
+    bws = ms._workspace(max(ms.attn_bwd_workspace_bytes(dims, s[3].struct.vcol_cap) for s in shards), dev)
     for t, (krows, k_loc, v_loc, idx) in enumerate(shards):
         _, dk, dv = ms.attn_bwd(dims, q_loc, k_loc, v_loc, out, do_loc, l_acc, idx, dq=dq, dq_accumulate=(t > 0),
-                                out_f32=o_acc)
+                                out_f32=o_acc, workspace=bws, reuse_qrows=reuse and t > 0)
         torch.cuda.synchronize()
         assert_close(f"dk step {t}", dk.cpu().numpy(), rk[:, :, krows])
         assert_close(f"dv step {t}", dv.cpu().numpy(), rv[:, :, krows])

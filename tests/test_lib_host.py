@@ -142,3 +142,18 @@ def test_peak_probe_validation():
     fake = ctypes.c_void_p(16)
     for w, it, out in ((0, 10, fake), (9, 10, fake), (2, 0, fake), (2, 10, None)):
         assert L.msparse_mfma_peak_probe(w, it, out, None) == -1
+
+
+def test_bwd_flags_validation():
+    L = ms.lib()
+    d = ms.make_dims(1, 4096, 4, 2, 128)
+    fake = ctypes.c_void_p(16)
+    idx = ms.IndexStruct()
+    for f in ("blk_ptr", "blk_idx", "col_ptr", "col_idx", "kblk_ptr", "kblk_idx", "vcol_ptr", "vcol_idx", "diag_bits",
+              "q_blk_global", "k_blk_global"):
+        setattr(idx, f, 64)
+    idx.blk_cap = idx.col_cap = idx.vcol_cap = 1
+    idx.world = 1
+    st = L.msparse_attn_bwd(ctypes.byref(d), fake, fake, fake, fake, None, fake, fake, ctypes.byref(idx), fake, fake,
+                            fake, 4, fake, 1 << 40, None)
+    assert st == -1, ms.lib().msparse_last_error()
