@@ -58,28 +58,40 @@ __device__ __forceinline__ void stage_rows(uint16_t* lds, const uint16_t* __rest
 // instruction writes 64 lanes x 16 bytes contiguously (the lanes free to
 // gather any rows), i.e. RPI = 1024 / (2 D) whole rows.  Instruction g of a
 // tile carries rows g, g + NG, g + 2 NG, ... (NG = 64 / RPI groups) and the
-// groups lie 1024 + P bytes apart:
-//   byte offset of (row r, chunk c) = (r % NG) (1024 + P) + (r / NG) 2 D + 16 c.
-// Every operand read is then a per-lane base plus immediate offsets.  P = 16
-// spreads the 16 rows of a row-wise operand read over distinct banks; P = 64
-// does the same for the 4 rows x 32 bytes of each 16-lane group of a
-// transposing read (and for two such groups served together).
+// groups start at goff(g):
+//   byte offset of (row r, chunk c) = goff(r % NG) + (r / NG) 2 D + 16 c.
+// Every operand read is then a per-lane base plus immediate offsets.  The LDS
+// serves 256 bytes (64 banks x 4 bytes) per cycle: 16 lanes of a row-wise
+// 16-byte read, or 32 lanes of a transposing 8-byte read.  With uniform
+// spacing goff(g) = g (1024 + P), P = 16 puts the 16 rows of a row-wise
+// operand read in distinct banks and P = 64 the 4 rows x 64 bytes of a
+// transposing read; no uniform P serves both, hence the placement of the
+// tiles read both ways.
 template <int D, int P>
 struct DmaTile {
     static constexpr int kRowBytes = 2 * D;
     static constexpr int kRowsPerInst = 1024 / kRowBytes;   // 4 (D = 128) or 8 (D = 64)
     static constexpr int kGroups = 64 / kRowsPerInst;       // 16 or 8
-    static constexpr int kGroupBytes = 1024 + P;
-    static constexpr int kBytes = kGroups * kGroupBytes;
+    // byte offset of group g: uniform pad P, or (P < 0, tiles read both ways,
+    // D = 128) groups placed so that, modulo the 256 bytes one LDS cycle
+    // serves, the 16 groups start at distinct multiples of 16 (a row-wise
+    // read: 16 lanes, one 16-byte chunk per group) and each quad of groups
+    // 4j .. 4j + 3 starts 64 bytes apart (a transposing read: 32 lanes, 64
+    // contiguous bytes of each of four groups of one quad); P < 0 at D = 64
+    // is a uniform 48-byte pad
+    __host__ __device__ static constexpr int goff(int g) {
+        return P >= 0 ? g * (1024 + P)
+                      : (D == 128 ? 1024 * g + 272 * (g >> 2) + 64 * (g & 3) : g * (1024 + 48));
+    }
+    static constexpr int kBytes = goff(kGroups - 1) + 1024 + (P >= 0 ? P : (D == 128 ? 0 : 48));
     static constexpr int kElems = kBytes / 2;
     __device__ static constexpr int off(int r, int c) {      // element offset of chunk c of row r
-        return ((r % kGroups) * kGroupBytes + (r / kGroups) * kRowBytes + 16 * c) / 2;
+        return (goff(r % kGroups) + (r / kGroups) * kRowBytes + 16 * c) / 2;
     }
 };
 constexpr int kRowPad = 16;   // tiles read row-wise
 constexpr int kTrPad = 64;    // tiles read through transposing loads
-constexpr int kDualPad = 48;  // tiles read both ways (48 g mod 256 is distinct for
-                              // g = 0..15, and 4 groups x 64 bytes do not overlap)
+constexpr int kDualPad = -1;  // tiles read both ways (group placement above)
 
 typedef __attribute__((address_space(3))) void* lds_void_ptr;
 
@@ -114,7 +126,7 @@ __device__ __forceinline__ void dma_rows(uint16_t* tile, const uint16_t* __restr
         if (T::kGroups % NW != 0 && g >= T::kGroups) break;
         const int r = g + T::kGroups * (lane / NC);
         const int c = lane % NC;
-        dma16(src + rows(r) * D + c * 8, lds_addr(tile + g * (T::kGroupBytes / 2)));
+        dma16(src + rows(r) * D + c * 8, lds_addr(tile + T::goff(g) / 2));
     }
 }
 
