@@ -131,3 +131,97 @@ def test_prefill_forward_sampled_rows(gpu, name):
         assert_lse_close(lse[:, h:h + 1, sel].cpu().numpy(), rl)
     del x, out, lse
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("name,rank", [("ring_512k_w8", 5)])
+def test_ring_share_fullsize_sampled_rows(gpu, name, rank):
+    """One worker's share of the striped ring at full size (Section 4.2,
+    Algorithm 2): its query shard against all W KV shards as sequential steps,
+    forward partials merged by log-sum-exp, backward per step with dQ summed
+    over the steps and later steps reusing the worker's query-side data.  The
+    sampled global rows of the worker are checked against the oracle on the
+    whole sequence (a row's out, lse and dQ do not depend on the partition);
+    dK and dV are checked through invariants of the whole share: summed over
+    the steps and keys, dK is 0 and dV equals the sum of dO over the worker's
+    rows of the group's heads."""
+    wl = WORKLOADS[name]
+    print(f"ring share {name} rank {rank}", flush=True)
+    B, Hq, Hkv, N, d, W = wl.batch, wl.heads_q, wl.heads_kv, wl.seq, wl.head_dim, wl.world
+    G = Hq // Hkv
+    scale = 1 / math.sqrt(d)
+    x = make_inputs(wl, gpu)
+    heads = [1, Hq - 1]
+    sets = {}
+    for h in heads:
+        vs, ss = OE.vs_scores(to_f64(x["q"][0, h, N - wl.last_q:].cpu()), to_f64(x["k"][0, h // G].cpu()), scale)
+        sets[h] = (OE.topk_lower(vs, wl.k_v), OE.topk_lower(ss, wl.k_s))
+        del vs, ss
+    vi = np.stack([sets[heads[h % 2]][0] for h in range(Hq)])[None].astype(np.int32)
+    si = np.stack([sets[heads[h % 2]][1] for h in range(Hq)])[None].astype(np.int32)
+    print("oracle sets ready", flush=True)
+
+    T = N // W
+    dims = ms.make_dims(B, T, Hq, Hkv, d)
+    tv, ts = torch.from_numpy(vi).to(gpu), torch.from_numpy(si).to(gpu)
+    lane = torch.arange(64, device=gpu)
+    shards = []
+    for t in range(W):
+        idx = ms.make_index(dims, tv, ts, ms.make_ring(W, rank, t, wl.layout))
+        kr = (idx["k_blk_global"].long()[:, None] * 64 + lane[None]).reshape(-1)
+        shards.append((x["k"][:, :, kr].contiguous(), x["v"][:, :, kr].contiguous(), idx))
+    qblk = shards[0][2]["q_blk_global"].long()
+    assert np.array_equal(qblk.cpu().numpy(), OI.local_blocks(rank, N // 64, W, wl.layout))
+    rr = (qblk[:, None] * 64 + lane[None]).reshape(-1)
+    q_loc = x["q"][:, :, rr].contiguous()
+    do_loc = x["do"][:, :, rr].contiguous()
+    o_acc = torch.empty(q_loc.shape, dtype=torch.float32, device=gpu)
+    l_acc = torch.empty(q_loc.shape[:-1], dtype=torch.float32, device=gpu)
+    part = torch.empty_like(o_acc)
+    lse_p = torch.empty_like(l_acc)
+    out = torch.empty_like(q_loc)
+    for t, (k_s, v_s, idx) in enumerate(shards):
+        ms.attn_fwd(dims, q_loc, k_s, v_s, idx, lse=lse_p, out_f32=part, bf16_out=False)
+        ms.merge_out_lse(dims, part, lse_p, o_acc, l_acc, out if t == W - 1 else None, first=(t == 0))
+    dq = torch.empty(q_loc.shape, dtype=torch.float32, device=gpu)
+    bws = ms._workspace(max(ms.attn_bwd_workspace_bytes(dims, s[2].struct.vcol_cap) for s in shards), gpu)
+    sum_dk = torch.zeros(Hkv, d, dtype=torch.float64, device=gpu)
+    sum_dv = torch.zeros_like(sum_dk)
+    abs_dk = torch.zeros_like(sum_dk)
+    abs_dv = torch.zeros_like(sum_dk)
+    for t, (k_s, v_s, idx) in enumerate(shards):
+        _, dk, dv = ms.attn_bwd(dims, q_loc, k_s, v_s, out, do_loc, l_acc, idx, dq=dq, dq_accumulate=(t > 0),
+                                out_f32=o_acc, workspace=bws, reuse_qrows=(t > 0))
+        sum_dk += dk[0].double().sum(1)
+        sum_dv += dv[0].double().sum(1)
+        abs_dk += dk[0].double().abs().sum(1)
+        abs_dv += dv[0].double().abs().sum(1)
+    torch.cuda.synchronize()
+    print("gpu done", flush=True)
+
+    nl = T // 64
+    lblocks = np.unique(np.concatenate([[0, 1, nl - 1], np.linspace(2, nl - 2, 9).astype(np.int64)]))
+    lrows = np.unique(np.concatenate([lblocks * 64 + 3, lblocks * 64 + 63]))
+    grows = rr.cpu().numpy()[lrows]
+    sel = torch.from_numpy(lrows).to(gpu)
+    for h in heads:
+        ref = OI.Index(vi[:, h:h + 1], si[:, h:h + 1], N)
+        q = to_f64(q_loc[:, h:h + 1, sel].cpu())
+        do = to_f64(do_loc[:, h:h + 1, sel].cpu())
+        k = to_f64(x["k"][:, h // G:h // G + 1].cpu())
+        v = to_f64(x["v"][:, h // G:h // G + 1].cpu())
+
+        class Rows:      # the oracle's mask rows for the sampled global rows, in sample order
+            def mask_rows(self, bh, r):
+                return ref.mask_rows(0, grows[np.asarray(r)])
+
+        ro, rl = OA.layer_fwd(q, k, v, Rows(), scale)
+        rq = OA.layer_dq(q, k, v, do, Rows(), scale, np.arange(len(grows)))
+        assert_close(f"out h{h}", out[:, h:h + 1, sel].float().cpu().numpy(), ro)
+        assert_close(f"out32 h{h}", o_acc[:, h:h + 1, sel].cpu().numpy(), ro)
+        assert_lse_close(l_acc[:, h:h + 1, sel].cpu().numpy(), rl)
+        assert_close(f"dq h{h}", dq[:, h:h + 1, sel].cpu().numpy(), rq)
+    want_dv = do_loc[0].double().sum(1).reshape(Hkv, G, d).sum(1)
+    assert ((sum_dk).abs() <= 1e-4 * abs_dk + 1e-3).all(), "sum dK over the share"
+    assert ((sum_dv - want_dv).abs() <= 1e-4 * abs_dv + 1e-3).all(), "sum dV over the share"
+    del x, shards, q_loc, do_loc, out, o_acc, dq
+    torch.cuda.empty_cache()
