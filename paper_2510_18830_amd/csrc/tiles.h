@@ -161,18 +161,24 @@ __device__ __forceinline__ u32x4 dma_read_tr(const uint16_t* x, int k0, int m0, 
 }
 
 #ifndef MS_XCHUNK
-#define MS_XCHUNK 64   // logical items per XCD run
+#define MS_XCHUNK 64   // longest run of logical items per XCD
 #endif
 // Workgroup ids are dispatched round-robin over the 8 XCDs, each with its own
 // L2.  xcd_chunk maps id t to a logical index so that each XCD receives runs
-// of C consecutive logical items (the tail past the last full round of 8 runs
-// keeps its identity mapping); a bijection on [0, total).
+// of C consecutive logical items, C = MS_XCHUNK halved until every XCD gets
+// at least 16 runs (a small grid would otherwise give each XCD one
+// contiguous stretch of the sequence, and the causal work falls along it),
+// with the XCD order reversed every other round (each XCD gets early and late
+// runs alike).  The tail past the last full round keeps its identity mapping;
+// a bijection on [0, total).
 __device__ __forceinline__ int64_t xcd_chunk(int64_t t, int64_t total) {
-    constexpr int64_t C = MS_XCHUNK;
+    int64_t C = MS_XCHUNK;
+    while (C > 1 && total < 8 * 16 * C) C >>= 1;
     const int64_t full = total / (8 * C) * (8 * C);
     if (t >= full) return t;
-    const int64_t n = t >> 3, x = t & 7;
-    return (n / C) * 8 * C + x * C + (n % C);
+    const int64_t n = t >> 3, k = n / C;
+    const int64_t x = (k & 1) ? 7 - (t & 7) : (t & 7);
+    return k * 8 * C + x * C + (n % C);
 }
 
 // (head, query block) of workgroup t in a B*Hq*nqb grid: KV-group-major
