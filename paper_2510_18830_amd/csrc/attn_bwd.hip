@@ -838,49 +838,69 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1
 // Adds the column partials of key block kb into dK / dV: one workgroup per
 // (b, KV head, key block); query heads in order, then each chunk's items in
 // order.
-__global__ void __launch_bounds__(128) bwd_colmerge_kernel(AttnArgs a) {
+// One workgroup per (KV head, 64-key block): for each query head of the group
+// in order, the head's vertical entries inside the block (distinct keys, so
+// distinct rows) are merged one per wave; the heads follow one another, so
+// every row receives its heads' sums in a fixed order.
+constexpr int kMergeThreads = 512;
+__global__ void __launch_bounds__(kMergeThreads) bwd_colmerge_kernel(AttnArgs a) {
+    __shared__ int64_t span_lo[kMergeThreads], span_hi[kMergeThreads];
     const int BK = a.B * a.Hkv;
     const int bk = int(blockIdx.x % BK);
     const int kb = int(blockIdx.x / BK);
     const int b = bk / a.Hkv, hk = bk % a.Hkv;
     const int G = a.Hq / a.Hkv;
     const int lo = kb * 64, hi = lo + 64;
-    for (int g = 0; g < G; ++g) {
-        const int bh = b * a.Hq + hk * G + g;
-        const int64_t v0 = a.vcol_ptr[bh], v1 = min(a.vcol_ptr[bh + 1], a.vcol_cap);
-        if (v0 >= v1) continue;
-        // first entry >= lo
-        int64_t L = v0, R = v1;
+    const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    constexpr int NW = kMergeThreads / 64;
+    // first entry >= v of an ascending list [L, R)
+    auto lower = [&](int64_t L, int64_t R, int32_t v) {
         while (L < R) {
             const int64_t m = (L + R) >> 1;
-            if (a.vcol_idx[m] < lo) L = m + 1; else R = m;
+            if (a.vcol_idx[m] < v) L = m + 1; else R = m;
         }
-        const int32_t c0 = a.col_choff[bh];
-        for (int64_t e = L; e < v1 && a.vcol_idx[e] < hi; ++e) {
-            if (a.vcol_idx[e] < lo) continue;
-            const int64_t ch = c0 + (e - v0) / 64;
-            const int key = int((e - v0) % 64);
-            const int i0 = a.col_item[ch], i1 = a.col_item[ch + 1];
-            const int64_t row = int64_t(bk) * a.Nk + a.vcol_idx[e];
-            for (int j = threadIdx.x; j < a.d; j += blockDim.x) {
-                // four independent partial sums (eight loads in flight), combined
-                // in a fixed order
-                float sk[4] = {0.f, 0.f, 0.f, 0.f}, sv[4] = {0.f, 0.f, 0.f, 0.f};
-                int it = i0;
-                for (; it + 4 <= i1; it += 4) {
+        return L;
+    };
+    for (int gb = 0; gb < G; gb += kMergeThreads) {
+        const int ng = min(kMergeThreads, G - gb);
+        if (int(threadIdx.x) < ng) {   // one thread per head: the head's entries in this block
+            const int bh = b * a.Hq + hk * G + gb + threadIdx.x;
+            const int64_t v0 = a.vcol_ptr[bh], v1 = min(a.vcol_ptr[bh + 1], a.vcol_cap);
+            const int64_t L = v0 < v1 ? lower(v0, v1, lo) : v1;
+            span_lo[threadIdx.x] = L;
+            span_hi[threadIdx.x] = L < v1 ? lower(L, v1, hi) : L;
+        }
+        __syncthreads();
+        for (int gi = 0; gi < ng; ++gi) {
+            const int bh = b * a.Hq + hk * G + gb + gi;
+            const int64_t v0 = a.vcol_ptr[bh];
+            const int32_t c0 = a.col_choff[bh];
+            for (int64_t e = span_lo[gi] + w; e < span_hi[gi]; e += NW) {
+                const int64_t ch = c0 + (e - v0) / 64;
+                const int key = int((e - v0) % 64);
+                const int i0 = a.col_item[ch], i1 = a.col_item[ch + 1];
+                const int64_t row = int64_t(bk) * a.Nk + a.vcol_idx[e];
+                for (int j = lane; j < a.d; j += 64) {
+                    // four independent partial sums (eight loads in flight),
+                    // combined in a fixed order
+                    float sk[4] = {0.f, 0.f, 0.f, 0.f}, sv[4] = {0.f, 0.f, 0.f, 0.f};
+                    int it = i0;
+                    for (; it + 4 <= i1; it += 4) {
 #pragma unroll
-                    for (int u = 0; u < 4; ++u) {
-                        sk[u] += a.dk_col[(int64_t(it + u) * 64 + key) * a.d + j];
-                        sv[u] += a.dv_col[(int64_t(it + u) * 64 + key) * a.d + j];
+                        for (int u = 0; u < 4; ++u) {
+                            sk[u] += a.dk_col[(int64_t(it + u) * 64 + key) * a.d + j];
+                            sv[u] += a.dv_col[(int64_t(it + u) * 64 + key) * a.d + j];
+                        }
                     }
+                    for (; it < i1; ++it) {
+                        sk[0] += a.dk_col[(int64_t(it) * 64 + key) * a.d + j];
+                        sv[0] += a.dv_col[(int64_t(it) * 64 + key) * a.d + j];
+                    }
+                    a.dk[row * a.d + j] += (sk[0] + sk[1]) + (sk[2] + sk[3]);
+                    a.dv[row * a.d + j] += (sv[0] + sv[1]) + (sv[2] + sv[3]);
                 }
-                for (; it < i1; ++it) {
-                    sk[0] += a.dk_col[(int64_t(it) * 64 + key) * a.d + j];
-                    sv[0] += a.dv_col[(int64_t(it) * 64 + key) * a.d + j];
-                }
-                a.dk[row * a.d + j] += (sk[0] + sk[1]) + (sk[2] + sk[3]);
-                a.dv[row * a.d + j] += (sv[0] + sv[1]) + (sv[2] + sv[3]);
             }
+            __syncthreads();   // the next head may add to the same rows
         }
     }
 }
@@ -930,7 +950,7 @@ hipError_t launch_bwd_d(const AttnArgs& a, hipStream_t s) {
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const int64_t kgrid = int64_t(a.B) * a.Hkv * a.nkb;
-    if (kgrid > 0) { TraceScope _t("bwd_colmerge", s); hipLaunchKernelGGL(bwd_colmerge_kernel, dim3(unsigned(kgrid)), dim3(128), 0, s, a); }
+    if (kgrid > 0) { TraceScope _t("bwd_colmerge", s); hipLaunchKernelGGL(bwd_colmerge_kernel, dim3(unsigned(kgrid)), dim3(kMergeThreads), 0, s, a); }
     return hipGetLastError();
 }
 
