@@ -193,9 +193,8 @@ def ring_leg(x, v_idx, s_idx, wl, world: int, rank: int, steps: int):
     do_loc = x["do"][:, :, rr].contiguous()
     o_acc = torch.empty(q_loc.shape, dtype=torch.float32, device=dev)
     l_acc = torch.empty(q_loc.shape[:-1], dtype=torch.float32, device=dev)
-    part = torch.empty_like(o_acc)
-    lse_p = torch.empty_like(l_acc)
     out = torch.empty_like(q_loc)
+    fws = ms._workspace(ms.attn_fwd_workspace_bytes(dims), dev)
     dq = torch.empty(q_loc.shape, dtype=torch.float32, device=dev)
     dk = torch.empty(shards[0][0].shape, dtype=torch.float32, device=dev)
     dv = torch.empty_like(dk)
@@ -206,8 +205,8 @@ def ring_leg(x, v_idx, s_idx, wl, world: int, rank: int, steps: int):
         for t, (k_s, v_s, idx) in enumerate(shards):
             if timed:
                 ev[t][0].record()
-            ms.attn_fwd(dims, q_loc, k_s, v_s, idx, lse=lse_p, out_f32=part, bf16_out=False)
-            ms.merge_out_lse(dims, part, lse_p, o_acc, l_acc, out if t == world - 1 else None, first=(t == 0))
+            ms.attn_fwd_merge(dims, q_loc, k_s, v_s, idx, o_acc, l_acc, out if t == world - 1 else None,
+                              first=(t == 0), workspace=fws)
             if timed:
                 ev[t][1].record()
         for t, (k_s, v_s, idx) in enumerate(shards):

@@ -252,6 +252,19 @@ MSPARSE_API msparse_status msparse_attn_fwd(const msparse_dims* dims, const void
                                 const msparse_index* index, void* out, float* lse, float* out_f32,
                                 void* workspace, size_t workspace_bytes, void* stream);
 
+/* One ring step's forward merged straight into the running result: the
+ * forward above (same arguments up to index), then the merge of
+ * msparse_merge_out_lse below, without storing the step's partial.
+ *   o_acc fp32 [B, Hq, Nq, d], lse_acc fp32 [B, Hq, Nq]: the running (O, lse);
+ *   read and updated unless `first`, which writes the step's own result
+ *   out_bf16 bf16 [B, Hq, Nq, d] or NULL: also stores the merged O as bf16
+ *   (pass it on the last step).
+ * Each query row is merged by the workgroup that computes it.  Workspace:
+ * msparse_attn_fwd_workspace(dims) bytes.  Errors as msparse_attn_fwd. */
+MSPARSE_API msparse_status msparse_attn_fwd_merge(const msparse_dims* dims, const void* q, const void* k, const void* v,
+                                      const msparse_index* index, float* o_acc, float* lse_acc, void* out_bf16,
+                                      int32_t first, void* workspace, size_t workspace_bytes, void* stream);
+
 /* Log-sum-exp merge of one ring step's partial result into a running one
  * (merge_out_and_lse, Algorithm 2): lse = logaddexp(lse_acc, lse_part),
  * o_acc = exp(lse_acc - lse) o_acc + exp(lse_part - lse) o_part.

@@ -67,6 +67,8 @@ _SIGS = {
     "msparse_build_index": (c_i32, [_P(Dims), c_vp, c_i32, c_vp, c_i32, _P(Ring), _P(IndexStruct), c_vp, c_sz, c_vp]),
     "msparse_attn_fwd_workspace": (c_sz, [_P(Dims)]),
     "msparse_attn_fwd": (c_i32, [_P(Dims), c_vp, c_vp, c_vp, _P(IndexStruct), c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]),
+    "msparse_attn_fwd_merge": (c_i32, [_P(Dims), c_vp, c_vp, c_vp, _P(IndexStruct), c_vp, c_vp, c_vp, c_i32, c_vp,
+                                       c_sz, c_vp]),
     "msparse_merge_out_lse": (c_i32, [_P(Dims), c_vp, c_vp, c_vp, c_vp, c_vp, c_i32, c_vp]),
     "msparse_attn_bwd_workspace": (c_sz, [_P(Dims), c_i64]),
     "msparse_attn_bwd": (c_i32, [_P(Dims), c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, _P(IndexStruct), c_vp, c_vp,
@@ -271,6 +273,16 @@ def attn_fwd(dims, q, k, v, index: SparseIndex, out=None, lse=None, out_f32=None
     _check(lib().msparse_attn_fwd(ctypes.byref(dims), _p(q), _p(k), _p(v), ctypes.byref(index.struct), _p(out),
                                   _p(lse), _p(out_f32), _p(workspace), workspace.numel(), _stream(stream)))
     return out, lse
+
+
+def attn_fwd_merge(dims, q, k, v, index: SparseIndex, o_acc, lse_acc, out_bf16=None, first=False, workspace=None,
+                   stream=None):
+    """msparse_attn_fwd_merge: one ring step's forward merged into the running (o_acc, lse_acc)."""
+    if workspace is None:
+        workspace = _workspace(attn_fwd_workspace_bytes(dims), q.device)
+    _check(lib().msparse_attn_fwd_merge(ctypes.byref(dims), _p(q), _p(k), _p(v), ctypes.byref(index.struct),
+                                        _p(o_acc), _p(lse_acc), _p(out_bf16), int(bool(first)), _p(workspace),
+                                        workspace.numel(), _stream(stream)))
 
 
 def merge_out_lse(dims, o_part, lse_part, o_acc, lse_acc, out_bf16=None, first=False, stream=None):

@@ -386,6 +386,31 @@ msparse_status msparse_attn_fwd(const msparse_dims* dims, const void* q, const v
     return check_hip(launch_attn_fwd(a, s), s, "attn fwd");
 }
 
+msparse_status msparse_attn_fwd_merge(const msparse_dims* dims, const void* q, const void* k, const void* v,
+                                      const msparse_index* index, float* o_acc, float* lse_acc, void* out_bf16,
+                                      int32_t first, void* ws, size_t ws_bytes, void* stream) {
+    msparse_status st = check_dims(dims, false);
+    if (st) return st;
+    if (!q || !k || !v || !o_acc || !lse_acc) return fail(MSPARSE_ERR_INVALID, "tensor pointer is NULL");
+    if ((st = check_index_struct(dims, index, false))) return st;
+    const size_t need = msparse_attn_fwd_workspace(dims);
+    if (need && (!ws || ws_bytes < need))
+        return fail(MSPARSE_ERR_WORKSPACE, "fwd workspace %zu < %zu bytes", ws_bytes, need);
+    if (dims->seq_q == 0) return MSPARSE_OK;
+    AttnArgs a{};
+    fill_attn(dims, index, &a);
+    a.q = static_cast<const uint16_t*>(q);
+    a.k = static_cast<const uint16_t*>(k);
+    a.v = static_cast<const uint16_t*>(v);
+    a.out = static_cast<uint16_t*>(out_bf16);
+    a.out_f32 = o_acc;
+    a.lse = lse_acc;
+    a.merge_acc = first ? 0 : 1;
+    carve_fwd(dims, static_cast<char*>(ws), &a);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    return check_hip(launch_attn_fwd(a, s), s, "attn fwd merge");
+}
+
 msparse_status msparse_merge_out_lse(const msparse_dims* dims, const float* o_part, const float* lse_part, float* o_acc,
                                      float* lse_acc, void* out_bf16, int32_t first, void* stream) {
     msparse_status st = check_dims(dims, false);

@@ -302,10 +302,29 @@ attn_fwd_kernel(AttnArgs a) {
     if (!live) return;
 
     // ---- epilogue: normalise (V carried the factor sv), store bf16 out and
-    // natural-log lse
+    // natural-log lse; with merge_acc, merge into the running (out_f32, lse)
+    // instead (the log-sum-exp merge of ring-step partials, same arithmetic as
+    // merge_kernel)
     const bool empty = !(st.l > 0.f);
     const float inv = empty ? 0.f : 1.f / (st.l * operand_scale(a.qkvmax + 2));
-    const int64_t orow = (int64_t(bh) * a.Nq + int64_t(qb) * 64 + qrow) * D;
+    const int64_t lrow = int64_t(bh) * a.Nq + int64_t(qb) * 64 + qrow;
+    const int64_t orow = lrow * D;
+    const float lp = empty ? -INFINITY : (st.m + fast_log2(st.l)) * kLn2;
+    float lnew = lp, wa = 0.f, wp = 1.f, ws = 1.f;
+    bool zero = false;
+    if (a.merge_acc) {
+        const float la = a.lse[lrow];
+        const float mx = fmaxf(la, lp);
+        if (mx == -INFINITY) {
+            lnew = -INFINITY;
+            zero = true;
+        } else {
+            wa = expf(la - mx);
+            wp = expf(lp - mx);
+            ws = wa + wp;
+            lnew = mx + logf(ws);
+        }
+    }
 #pragma unroll
     for (int i = 0; i < ND; ++i)
 #pragma unroll
@@ -315,18 +334,23 @@ attn_fwd_kernel(AttnArgs a) {
             o4.y = st.o[i][4 * g + 1] * inv;
             o4.z = st.o[i][4 * g + 2] * inv;
             o4.w = st.o[i][4 * g + 3] * inv;
+            float* of = a.out_f32 ? a.out_f32 + orow + 32 * i + 8 * g + 4 * h : nullptr;
+            if (a.merge_acc) {
+                const f32x4 acc = *reinterpret_cast<const f32x4*>(of);
+                o4.x = zero ? 0.f : (wa * acc.x + wp * o4.x) / ws;
+                o4.y = zero ? 0.f : (wa * acc.y + wp * o4.y) / ws;
+                o4.z = zero ? 0.f : (wa * acc.z + wp * o4.z) / ws;
+                o4.w = zero ? 0.f : (wa * acc.w + wp * o4.w) / ws;
+            }
             if (a.out) {
                 u32x2 pk;
                 pk.x = pack_bf16x2(o4.x, o4.y);
                 pk.y = pack_bf16x2(o4.z, o4.w);
                 *reinterpret_cast<u32x2*>(a.out + orow + 32 * i + 8 * g + 4 * h) = pk;
             }
-            if (a.out_f32) *reinterpret_cast<f32x4*>(a.out_f32 + orow + 32 * i + 8 * g + 4 * h) = o4;
+            if (of) *reinterpret_cast<f32x4*>(of) = o4;
         }
-    if (h == 0) {
-        float* lp = a.lse + int64_t(bh) * a.Nq + int64_t(qb) * 64 + qrow;
-        *lp = empty ? -INFINITY : (st.m + fast_log2(st.l)) * kLn2;
-    }
+    if (h == 0) a.lse[lrow] = lnew;
 }
 
 __global__ void fwd_prep_kernel(AttnArgs a) {

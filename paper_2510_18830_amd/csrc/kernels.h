@@ -98,6 +98,7 @@ struct AttnArgs {
     int64_t col_slots;     // item capacity (grid of the column kernel)
     int32_t dq_accumulate;
     int32_t reuse_qrows;   // the workspace already holds the Q-side data (a later ring step)
+    int32_t merge_acc;     // fwd: out_f32 / lse hold a running (o, lse) that the result is merged into
     int32_t B, Hq, Hkv, Nq, Nk, d;
     int32_t nqb, nkb;
     float scale;

@@ -137,7 +137,8 @@ def test_prefill_forward_sampled_rows(gpu, name):
 def test_ring_share_fullsize_sampled_rows(gpu, name, rank):
     """One worker's share of the striped ring at full size (Section 4.2,
     Algorithm 2): its query shard against all W KV shards as sequential steps,
-    forward partials merged by log-sum-exp, backward per step with dQ summed
+    forward steps merged by log-sum-exp as they finish (the fused entry
+    point), backward per step with dQ summed
     over the steps and later steps reusing the worker's query-side data.  The
     sampled global rows of the worker are checked against the oracle on the
     whole sequence (a row's out, lse and dQ do not depend on the partition);
@@ -176,12 +177,9 @@ def test_ring_share_fullsize_sampled_rows(gpu, name, rank):
     do_loc = x["do"][:, :, rr].contiguous()
     o_acc = torch.empty(q_loc.shape, dtype=torch.float32, device=gpu)
     l_acc = torch.empty(q_loc.shape[:-1], dtype=torch.float32, device=gpu)
-    part = torch.empty_like(o_acc)
-    lse_p = torch.empty_like(l_acc)
     out = torch.empty_like(q_loc)
-    for t, (k_s, v_s, idx) in enumerate(shards):
-        ms.attn_fwd(dims, q_loc, k_s, v_s, idx, lse=lse_p, out_f32=part, bf16_out=False)
-        ms.merge_out_lse(dims, part, lse_p, o_acc, l_acc, out if t == W - 1 else None, first=(t == 0))
+    for t, (k_s, v_s, idx) in enumerate(shards):   # forward steps merged as they finish
+        ms.attn_fwd_merge(dims, q_loc, k_s, v_s, idx, o_acc, l_acc, out if t == W - 1 else None, first=(t == 0))
     dq = torch.empty(q_loc.shape, dtype=torch.float32, device=gpu)
     bws = ms._workspace(max(ms.attn_bwd_workspace_bytes(dims, s[2].struct.vcol_cap) for s in shards), gpu)
     sum_dk = torch.zeros(Hkv, d, dtype=torch.float64, device=gpu)

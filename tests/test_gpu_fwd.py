@@ -97,6 +97,10 @@ def test_fwd_ring_steps_merge(gpu, layout, W, seq, inner):
     o_acc = torch.empty(q_loc.shape, dtype=torch.float32, device=gpu)
     l_acc = torch.empty(q_loc.shape[:-1], dtype=torch.float32, device=gpu)
     out = torch.empty_like(q_loc)
+    # the same steps through the fused forward + merge
+    f_acc = torch.empty_like(o_acc)
+    fl_acc = torch.empty_like(l_acc)
+    f_out = torch.empty_like(q_loc)
     tv, ts = torch.from_numpy(vi).to(gpu), torch.from_numpy(si).to(gpu)
     sched = OI.ring_schedule(W, inner)
     for t in range(W):
@@ -110,7 +114,15 @@ def test_fwd_ring_steps_merge(gpu, layout, W, seq, inner):
         po = torch.empty(q_loc.shape, dtype=torch.float32, device=q_loc.device)
         _, pl = ms.attn_fwd(dims, q_loc, k_loc, v_loc, idx, out_f32=po, bf16_out=False)
         ms.merge_out_lse(dims, po, pl, o_acc, l_acc, out if t == W - 1 else None, first=(t == 0))
+        ms.attn_fwd_merge(dims, q_loc, k_loc, v_loc, idx, f_acc, fl_acc, f_out if t == W - 1 else None,
+                          first=(t == 0))
     torch.cuda.synchronize()
     assert_close("ring out", out.float().cpu().numpy(), ref_o)
     assert_close("ring out fp32", o_acc.cpu().numpy(), ref_o)
     assert_lse_close(l_acc.cpu().numpy(), ref_l)
+    assert_close("fused ring out", f_out.float().cpu().numpy(), ref_o)
+    assert_close("fused ring out fp32", f_acc.cpu().numpy(), ref_o)
+    assert_lse_close(fl_acc.cpu().numpy(), ref_l)
+    # same arithmetic as the separate merge, up to the compiler's fma contraction
+    assert torch.allclose(f_acc, o_acc, rtol=1e-5, atol=1e-6)
+    assert torch.allclose(fl_acc, l_acc, rtol=1e-6, atol=1e-6)

@@ -66,6 +66,15 @@ def test_validation_before_launch():
          ctypes.byref(ctypes.c_int64()), ctypes.byref(ctypes.c_int64()), fake, 1 << 30, None)
     # a null index
     _bad(-1, L.msparse_attn_fwd, ctypes.byref(d), fake, fake, fake, None, fake, fake, None, fake, 1 << 40, None)
+    # fused forward + merge: a null index, a null accumulator, a bad head_dim
+    _bad(-1, L.msparse_attn_fwd_merge, ctypes.byref(d), fake, fake, fake, None, fake, fake, None, 0, fake, 1 << 40,
+         None)
+    _bad(-1, L.msparse_attn_fwd_merge, ctypes.byref(d), fake, fake, fake, None, None, fake, None, 1, fake, 1 << 40,
+         None)
+    dd = ms.make_dims(1, 4096, 4, 2, 128)
+    dd.head_dim = 96
+    _bad(-2, L.msparse_attn_fwd_merge, ctypes.byref(dd), fake, fake, fake, None, fake, fake, None, 0, fake, 1 << 40,
+         None)
 
 
 def test_index_capacity_needs_overflow_flag_or_bound():
