@@ -155,3 +155,31 @@ def test_bwd_independent_head_indices(gpu):
     gq, gk, gv = _gpu_fwd_bwd(gpu, wl, vi, si, x)
     for n, g, r in (("dq", gq, rq), ("dk", gk, rk), ("dv", gv, rv)):
         assert_close(n, g, r)
+
+
+# degenerate sizes: one block (every tile is the causal diagonal), two blocks,
+# unit budgets and a one-row estimation window, both head dims
+@pytest.mark.parametrize("seq,head_dim,k_v,k_s,last_q", [(64, 128, 1, 1, 64), (64, 64, 1, 64, 16),
+                                                          (128, 128, 1, 1, 1), (128, 64, 3, 2, 1)])
+def test_fwd_bwd_minimal_sizes(gpu, seq, head_dim, k_v, k_s, last_q):
+    wl = WORKLOADS["tiny_4k"].resized(seq=seq, heads_q=2, heads_kv=1, head_dim=head_dim, k_v=k_v, k_s=k_s,
+                                      last_q=last_q, n_vert=0)
+    print(f"minimal {wl}", flush=True)
+    x = make_inputs(wl, "cpu")
+    f = inputs_f64(x)
+    vi, si, _, _ = oracle_indices(f, wl)
+    scale = 1 / math.sqrt(wl.head_dim)
+    ref = OI.Index(vi, si, wl.seq)
+    ro, rl = OA.layer_fwd(f["q"], f["k"], f["v"], ref, scale)
+    rq, rk, rv = OA.layer_bwd(f["q"], f["k"], f["v"], f["do"], ref, scale)
+    dims = ms.make_dims(wl.batch, wl.seq, wl.heads_q, wl.heads_kv, wl.head_dim)
+    idx = ms.make_index(dims, torch.from_numpy(vi).to(gpu), torch.from_numpy(si).to(gpu))
+    q, k, v, do = (x[n].to(gpu) for n in ("q", "k", "v", "do"))
+    of = torch.empty(q.shape, dtype=torch.float32, device=gpu)
+    out, lse = ms.attn_fwd(dims, q, k, v, idx, out_f32=of)
+    dq, dk, dv = ms.attn_bwd(dims, q, k, v, out, do, lse, idx, out_f32=of)
+    torch.cuda.synchronize()
+    assert_close("out", of.cpu().numpy(), ro)
+    assert_close("dq", dq.cpu().numpy(), rq)
+    assert_close("dk", dk.cpu().numpy(), rk)
+    assert_close("dv", dv.cpu().numpy(), rv)
