@@ -161,7 +161,7 @@ __device__ __forceinline__ u32x4 dma_read_tr(const uint16_t* x, int k0, int m0, 
 }
 
 #ifndef MS_XCHUNK
-#define MS_XCHUNK 64   // longest run of logical items per XCD
+#define MS_XCHUNK 8    // longest run of logical items per XCD
 #endif
 // Workgroup ids are dispatched round-robin over the 8 XCDs, each with its own
 // L2.  xcd_chunk maps id t to a logical index so that each XCD receives runs
