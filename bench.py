@@ -75,12 +75,8 @@ def estimation_and_index_report(r) -> dict:
                  + B * Hq * (wl.k_v + wl.k_s) * 4)
     est_flops = 2 * 2.0 * L * B * Hq * N * d
     t_est = r["stage_ms"]["estimate"] * 1e-3
-    measured = None
-    names = [f"est_pass1_kernel<{d}>", f"est_pass2_kernel<{d}>", "est_combine_kernel", "est_diag_kernel",
-             "est_topk_kernel"]
-    vals = [hbm_traffic(wl.name, n) for n in names]
-    if all(v is not None for v in vals):
-        measured = round(sum(vals))
+    measured = hbm_traffic(wl.name, "estimation_total")   # every estimation launch of one step
+    measured = None if measured is None else round(measured)
     nqb = N // 64
     idx_bytes = (B * Hq * (wl.k_v + wl.k_s) * 4                       # read the selected indices
                  + 4 * (2 * r["T"] + r["C"] + r["vcol"])             # block, transposed, column, vertical entries
