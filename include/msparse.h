@@ -252,9 +252,12 @@ MSPARSE_API msparse_status msparse_attn_fwd(const msparse_dims* dims, const void
                                 const msparse_index* index, void* out, float* lse, float* out_f32,
                                 void* workspace, size_t workspace_bytes, void* stream);
 
-/* One ring step's forward merged straight into the running result: the
- * forward above (same arguments up to index), then the merge of
- * msparse_merge_out_lse below, without storing the step's partial.
+/* One ring step's forward merged straight into the running result
+ * (block_bar_sparse_attention_forward followed by merge_out_and_lse,
+ * Algorithm 2): the forward above (same arguments up to index), then the
+ * merge of msparse_merge_out_lse below, without storing the step's partial.
+ * A row that neither the running result nor this step has seen stays at
+ * O = 0, lse = -inf.
  *   o_acc fp32 [B, Hq, Nq, d], lse_acc fp32 [B, Hq, Nq]: the running (O, lse);
  *   read and updated unless `first`, which writes the step's own result
  *   out_bf16 bf16 [B, Hq, Nq, d] or NULL: also stores the merged O as bf16
