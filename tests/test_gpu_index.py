@@ -142,3 +142,42 @@ def test_ring_work_full_size_two_heads(gpu):
         torch.cuda.synchronize()
         np.testing.assert_array_equal(gt.cpu().numpy(), rt)
         np.testing.assert_array_equal(gc.cpu().numpy(), rc)
+
+
+def _head_rows(c, key_ptr, key_idx, first, n):
+    """Rows first .. first + n of a CSR pair, rebased to start at 0."""
+    ptr = c[key_ptr][first:first + n + 1].astype(np.int64)
+    return ptr - ptr[0], c[key_idx][int(ptr[0]):int(ptr[-1])]
+
+
+# The 512K layer's shape (28 query / 4 KV heads, k_v 4096, k_s 16384) in the
+# launch configuration of the benchmark: the GPU builds every head's index, the
+# oracle rebuilds two sampled heads (whole sequence) or one (a ring step), and
+# their rows must match bit for bit.
+@pytest.mark.parametrize("W,r,t,heads", [(1, 0, 0, [0, 27]), (8, 5, 3, [13])])
+def test_index_full_size_sampled_heads(gpu, W, r, t, heads):
+    B, Hq, Hkv, Ng, k_v, k_s = 1, 28, 4, 524288, 4096, 16384
+    rng = np.random.default_rng(2024 + W)
+    v, s = _indices(rng, B, Hq, Ng, k_v, k_s)
+    print(f"full-size index W={W} r={r} t={t}", flush=True)
+    dims = ms.make_dims(B, Ng // W, Hq, Hkv, 128)
+    idx = ms.make_index(dims, torch.from_numpy(v).to(gpu), torch.from_numpy(s).to(gpu),
+                        ms.make_ring(W, r, t, "striped"))
+    torch.cuda.synchronize()
+    assert int(idx["overflow"].item()) == 0
+    got = gpu_csr(idx)
+    nqb = nkb = Ng // W // 64
+    for h in heads:
+        ref = OI.Index(v[:, h:h + 1], s[:, h:h + 1], Ng, world=W, rank=r, step=t, layout="striped").csr()
+        for kp, ki, n in (("blk_ptr", "blk_idx", nqb), ("col_ptr", "col_idx", nqb), ("kblk_ptr", "kblk_idx", nkb),
+                          ("vcol_ptr", "vcol_idx", 1)):
+            gp, gi = _head_rows(got, kp, ki, h * n, n)
+            assert np.array_equal(gp, ref[kp].astype(np.int64)), (h, kp)
+            assert np.array_equal(gi.astype(np.int64), ref[ki].astype(np.int64)), (h, ki)
+        words = ref["diag_bits"].size
+        assert np.array_equal(got["diag_bits"][h * words:(h + 1) * words], ref["diag_bits"].view(np.uint32)), h
+        assert np.array_equal(got["q_blk_global"], ref["q_blk_global"])
+        assert np.array_equal(got["k_blk_global"], ref["k_blk_global"])
+        print(f"head {h} matches", flush=True)
+    del idx, got
+    torch.cuda.empty_cache()
