@@ -6,7 +6,9 @@ full shape.  The index comes from the oracle's estimator on two sampled heads
 The oracle then checks, on the sampled heads, sampled query rows spread over
 the sequence (out, lse and dQ need only the row itself), and the invariants
 that hold at any size: sum over keys of dK is 0 and sum over keys of dV equals
-the sum of dO over the group's query rows.
+the sum of dO over the group's query rows.  dK and dV of the last 128 keys of
+two KV heads are checked element by element: only the last 128 query rows see
+them, so the oracle's gradients over those rows are theirs in full.
 """
 import math
 
@@ -84,6 +86,25 @@ def test_fullsize_sampled_rows_and_invariants(gpu, name):
             want += x["do"][0, h].double().sum(0)
         s_dv = dv64.sum(0)
         assert ((s_dv - want).abs() <= 1e-4 * dv64.abs().sum(0) + 1e-3).all(), f"sum dV kv{g}"
+    # element-wise dK / dV of the last 128 keys of two KV heads: only the last
+    # 128 query rows (causal) of the group's heads see them, so the oracle's
+    # gradients over those rows alone are the full gradients of these keys
+    tail = np.arange(N - 128, N)
+    tsel = torch.from_numpy(tail).to(gpu)
+    for g in sorted({0, Hkv - 1}):
+        k = to_f64(x["k"][:, g:g + 1].cpu())[0, 0]
+        v = to_f64(x["v"][:, g:g + 1].cpu())[0, 0]
+        rk = np.zeros((128, d))
+        rv = np.zeros((128, d))
+        for h in range(g * G, (g + 1) * G):
+            ref = OI.Index(vi[:, h:h + 1], si[:, h:h + 1], N)
+            M = ref.mask_rows(0, tail)
+            _, gk, gv = OA.head_bwd(to_f64(x["q"][0, h, tsel].cpu()), k, v, to_f64(x["do"][0, h, tsel].cpu()), M,
+                                    scale)
+            rk += gk[N - 128:]
+            rv += gv[N - 128:]
+        assert_close(f"dk tail kv{g}", dk[0, g, N - 128:].cpu().numpy(), rk)
+        assert_close(f"dv tail kv{g}", dv[0, g, N - 128:].cpu().numpy(), rv)
     del x, out, out32, dq, dk, dv
     torch.cuda.empty_cache()
 
