@@ -31,12 +31,13 @@ PEAK_HBM_GBS = 8000.0
 
 
 def kernel_source_hash() -> str:
-    """sha256 over the kernel library sources (csrc and the C header)."""
+    """sha256 over the kernel library sources (csrc: the kernels and their
+    launchers; the public header holds declarations and documentation only)."""
     import hashlib
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2510_18830_amd", "csrc")
     files = sorted(f for f in os.listdir(csrc) if f.endswith((".hip", ".h")))
-    for f in files + ["../../include/msparse.h"]:
+    for f in files:
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(f.encode() + b"\0" + fh.read())
     return h.hexdigest()
