@@ -522,11 +522,15 @@ def main():
     traffic = hbm_traffic(wl.name, f"{dom}_kernel<{wl.head_dim}>")
     for r in results.values():
         r["est_idx"] = estimation_and_index_report(r)
-    # achievable dense fp16 MFMA rate on this GPU (probe kernel, no memory traffic)
+    # achievable dense fp16 MFMA rate on this GPU (probe kernel, no memory traffic): constant
+    # operands, and random operands (real data's switching; the power limit then lowers the clock)
     peak_meas = max(ms.mfma_peak_tflops(w) for w in (2, 4))
+    peak_rand = max(ms.mfma_peak_tflops(w, random=True) for w in (2, 4))
     roofline = {"bound": "mfma", "kernel": dom, "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                 "peak_measured": round(peak_meas, 1), "frac_of_measured": round(achieved / peak_meas, 4),
+                "peak_measured_random_operands": round(peak_rand, 1),
+                "frac_of_measured_random_operands": round(achieved / peak_rand, 4),
                 "traffic": None if traffic is None else round(traffic), "traffic_unit": "HBM bytes per launch"}
     line = {
         "metric": "sparse attn fwd+bwd TFLOP/s on computed blocks + ms/layer at 128K and 512K",

@@ -330,10 +330,14 @@ MSPARSE_API int32_t msparse_trace_read(msparse_trace_entry* out, int32_t cap);
  * launch of (CUs x waves_per_simd) workgroups of 256 threads on `stream`,
  * each wave running `iters` rounds of four independent 32x32x16 fp16 MFMA
  * chains (4 x 32768 FLOPs per round) with no memory traffic in the loop; the
- * caller times it with HIP events.  `out` (device) receives one float per
- * thread: CUs x waves_per_simd x 256 floats.  MSPARSE_ERR_INVALID for
- * waves_per_simd outside [1, 8], iters < 1 or a NULL out. */
-MSPARSE_API int32_t msparse_mfma_peak_probe(int32_t waves_per_simd, int32_t iters, float* out, void* stream);
+ * caller times it with HIP events.  random_operands = 0: one constant operand
+ * pair; otherwise eight pairs of random fp16 values cycled from MFMA to MFMA
+ * (the power, and so the clock, of the matrix cores depends on the operand
+ * data).  `out` (device) receives one float per thread: CUs x waves_per_simd
+ * x 256 floats.  MSPARSE_ERR_INVALID for waves_per_simd outside [1, 8],
+ * iters < 1 or not a multiple of 8, or a NULL out. */
+MSPARSE_API int32_t msparse_mfma_peak_probe(int32_t waves_per_simd, int32_t iters, int32_t random_operands, float* out,
+                                void* stream);
 
 #ifdef __cplusplus
 }

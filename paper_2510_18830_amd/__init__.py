@@ -57,7 +57,7 @@ _SIGS = {
     "msparse_estimate": (c_i32, [_P(Dims), c_vp, c_vp, c_i32, c_i32, c_i32, c_vp, c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]),
     "msparse_estimate_topp_workspace": (c_sz, [_P(Dims), c_i32, c_i32, c_i32]),
     "msparse_ring_shard": (c_i32, [c_i32, c_i32, c_i32, c_i32]),
-    "msparse_mfma_peak_probe": (c_i32, [c_i32, c_i32, c_vp, c_vp]),
+    "msparse_mfma_peak_probe": (c_i32, [c_i32, c_i32, c_i32, c_vp, c_vp]),
     "msparse_ring_work": (c_i32, [_P(Dims), c_vp, c_i32, c_vp, c_i32, c_i32, c_i32, c_vp, c_vp, c_vp, c_sz, c_vp]),
     "msparse_estimate_topp": (c_i32, [_P(Dims), c_vp, c_vp, c_i32, ctypes.c_double, ctypes.c_double, c_i32, c_i32,
                                       c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]),
@@ -316,15 +316,17 @@ def default_scale(head_dim: int) -> float:
 
 
 # ------------------------------------------------------------------ tracing
-def mfma_peak_tflops(waves_per_simd: int = 4, iters: int = 20000, device=None) -> float:
-    """Achievable dense fp16 MFMA rate in TFLOP/s (msparse_mfma_peak_probe, timed with HIP events)."""
+def mfma_peak_tflops(waves_per_simd: int = 4, iters: int = 20000, device=None, random: bool = False) -> float:
+    """Achievable dense fp16 MFMA rate in TFLOP/s (msparse_mfma_peak_probe, timed with HIP events);
+    random=True cycles random operands (real data's switching) instead of one constant pair."""
     device = device or torch.device("cuda", torch.cuda.current_device())
     cus = torch.cuda.get_device_properties(device).multi_processor_count
     out = torch.empty(cus * waves_per_simd * 256, dtype=torch.float32, device=device)
-    _check(lib().msparse_mfma_peak_probe(waves_per_simd, 100, _p(out), _stream(None)))
+    iters = (iters + 7) // 8 * 8
+    _check(lib().msparse_mfma_peak_probe(waves_per_simd, 104, int(random), _p(out), _stream(None)))
     a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     a.record()
-    _check(lib().msparse_mfma_peak_probe(waves_per_simd, iters, _p(out), _stream(None)))
+    _check(lib().msparse_mfma_peak_probe(waves_per_simd, iters, int(random), _p(out), _stream(None)))
     b.record()
     torch.cuda.synchronize()
     flops = cus * waves_per_simd * 4 * iters * 4 * 32768.0

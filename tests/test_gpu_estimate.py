@@ -209,3 +209,5 @@ def test_mfma_peak_probe_runs(gpu):
     # the measurement kernel beside the attention path: a plausible dense fp16 rate
     t = ms.mfma_peak_tflops(2, 2000)
     assert 300.0 < t < 3000.0, t
+    r = ms.mfma_peak_tflops(2, 2000, random=True)
+    assert 300.0 < r < 3000.0, r

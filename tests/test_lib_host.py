@@ -149,8 +149,9 @@ def test_ring_validation_before_launch():
 def test_peak_probe_validation():
     L = ms.lib()
     fake = ctypes.c_void_p(16)
-    for w, it, out in ((0, 10, fake), (9, 10, fake), (2, 0, fake), (2, 10, None)):
-        assert L.msparse_mfma_peak_probe(w, it, out, None) == -1
+    for w, it, out in ((0, 16, fake), (9, 16, fake), (2, 0, fake), (2, 12, fake), (2, 16, None)):
+        for rnd in (0, 1):
+            assert L.msparse_mfma_peak_probe(w, it, rnd, out, None) == -1
 
 
 def test_bwd_flags_validation():
