@@ -309,11 +309,7 @@ msparse_status msparse_build_index(const msparse_dims* dims, const int32_t* v_id
     a.k_blk_global = index->k_blk_global;
     a.overflow = index->overflow;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    if (a.overflow) {
-        hipError_t e = hipMemsetAsync(a.overflow, 0, sizeof(int32_t), s);
-        if (e != hipSuccess) return fail(MSPARSE_ERR_HIP, "overflow reset: %s", hipGetErrorString(e));
-    }
-    if ((st = check_hip(launch_index_prep(a, s), s, "index prep"))) return st;
+    if ((st = check_hip(launch_index_prep(a, s), s, "index prep"))) return st;   // also clears the overflow flag
     if ((st = check_hip(launch_index_count(a, s), s, "index count"))) return st;
     if ((st = check_hip(launch_index_scan(a, s), s, "index scan"))) return st;
     return check_hip(launch_index_fill(a, s), s, "index fill");

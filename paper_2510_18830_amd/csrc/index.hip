@@ -66,6 +66,9 @@ __global__ void __launch_bounds__(kPrepThreads) index_prep_kernel(IndexArgs a) {
     const Layout L{a.world, a.nb, a.layout};
     const int64_t Ng = int64_t(a.nb) * kBlock;
 
+    // the overflow flag starts at 0 for this build (a kernel store, not a memset,
+    // so that the call can be captured in a graph); the fill pass may set it
+    if (bh == 0 && tid == 0 && a.overflow) *a.overflow = 0;
     // ---- verticals: bitmap (dedupes and sorts), then ordered compaction
     uint32_t* vb = a.vbits + int64_t(bh) * a.vwords;
     for (int w = tid; w < a.vwords; w += kPrepThreads) vb[w] = 0u;

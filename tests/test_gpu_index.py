@@ -181,3 +181,39 @@ def test_index_full_size_sampled_heads(gpu, W, r, t, heads):
         print(f"head {h} matches", flush=True)
     del idx, got
     torch.cuda.empty_cache()
+
+
+def test_index_build_graph_replay(gpu):
+    """msparse_build_index captured in a HIP graph and replayed three times on
+    new index lists (eager copies and synchronisations between the replays):
+    every replay equals an eager build of the same lists."""
+    B, Hq, Hkv, Ng, k_v, k_s = 1, 2, 1, 8192, 97, 700
+    dims = ms.make_dims(B, Ng, Hq, Hkv, 128)
+    rng = np.random.default_rng(404)
+    sets = [_indices(rng, B, Hq, Ng, k_v, k_s) for _ in range(3)]
+    ws = ms._workspace(ms.index_workspace_bytes(dims, k_v, k_s), gpu)
+    caps = [ms.index_count(dims, torch.from_numpy(v).to(gpu), torch.from_numpy(s).to(gpu), workspace=ws)
+            for v, s in sets]
+    cap = [max(c[i] for c in caps) for i in range(3)]
+    refs = []
+    for v, s in sets:
+        e = ms.alloc_index(dims, *cap, gpu)
+        ms.build_index(dims, torch.from_numpy(v).to(gpu), torch.from_numpy(s).to(gpu), e, workspace=ws)
+        torch.cuda.synchronize()
+        refs.append(gpu_csr(e))
+    vbuf = torch.from_numpy(sets[0][0]).to(gpu)
+    sbuf = torch.from_numpy(sets[0][1]).to(gpu)
+    idx = ms.alloc_index(dims, *cap, gpu)
+    stream = torch.cuda.Stream()
+    graph = torch.cuda.CUDAGraph()
+    torch.cuda.synchronize()
+    with torch.cuda.graph(graph, stream=stream):
+        ms.build_index(dims, vbuf, sbuf, idx, workspace=ws, stream=stream)
+    for (v, s), ref in zip(sets, refs):
+        vbuf.copy_(torch.from_numpy(v).to(gpu))
+        sbuf.copy_(torch.from_numpy(s).to(gpu))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        _compare(gpu_csr(idx), ref)
+        assert int(idx["overflow"].item()) == 0
