@@ -183,3 +183,52 @@ def test_fwd_bwd_minimal_sizes(gpu, seq, head_dim, k_v, k_s, last_q):
     assert_close("dq", dq.cpu().numpy(), rq)
     assert_close("dk", dk.cpu().numpy(), rk)
     assert_close("dv", dv.cpu().numpy(), rv)
+
+
+def test_fwd_bwd_graph_replay(gpu):
+    """msparse_attn_fwd and msparse_attn_bwd captured in one HIP graph and
+    replayed on three input sets (eager copies and synchronisations between
+    the replays): every replay equals the eager calls bit for bit (the kernels
+    are deterministic)."""
+    wl = SMALL["gqa_4k_d128"].resized(seq=2048)
+    dims = ms.make_dims(wl.batch, wl.seq, wl.heads_q, wl.heads_kv, wl.head_dim)
+    xs = [make_inputs(wl.resized(seed=wl.seed + i), "cpu") for i in range(3)]
+    f = inputs_f64(xs[0])
+    vi, si, _, _ = oracle_indices(f, wl)
+    idx = ms.make_index(dims, torch.from_numpy(vi).to(gpu), torch.from_numpy(si).to(gpu))
+    fws = ms._workspace(ms.attn_fwd_workspace_bytes(dims), gpu)
+    bws = ms._workspace(ms.attn_bwd_workspace_bytes(dims, idx.struct.vcol_cap), gpu)
+    bufs = {n: xs[0][n].to(gpu) for n in ("q", "k", "v", "do")}
+    out = torch.empty_like(bufs["q"])
+    lse = torch.empty(bufs["q"].shape[:-1], dtype=torch.float32, device=gpu)
+    of = torch.empty(bufs["q"].shape, dtype=torch.float32, device=gpu)
+    dq = torch.empty(bufs["q"].shape, dtype=torch.float32, device=gpu)
+    dk = torch.empty(bufs["k"].shape, dtype=torch.float32, device=gpu)
+    dv = torch.empty(bufs["v"].shape, dtype=torch.float32, device=gpu)
+
+    def step(stream=None):
+        ms.attn_fwd(dims, bufs["q"], bufs["k"], bufs["v"], idx, out=out, lse=lse, out_f32=of, workspace=fws,
+                    stream=stream)
+        ms.attn_bwd(dims, bufs["q"], bufs["k"], bufs["v"], out, bufs["do"], lse, idx, dq, dk, dv, out_f32=of,
+                    workspace=bws, stream=stream)
+
+    refs = []
+    for x in xs:
+        for n in bufs:
+            bufs[n].copy_(x[n].to(gpu))
+        step()
+        torch.cuda.synchronize()
+        refs.append([t.clone() for t in (out, lse, dq, dk, dv)])
+    stream = torch.cuda.Stream()
+    graph = torch.cuda.CUDAGraph()
+    torch.cuda.synchronize()
+    with torch.cuda.graph(graph, stream=stream):
+        step(stream)
+    for x, ref in zip(xs, refs):
+        for n in bufs:
+            bufs[n].copy_(x[n].to(gpu))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for name, got, want in zip(("out", "lse", "dq", "dk", "dv"), (out, lse, dq, dk, dv), ref):
+            assert torch.equal(got, want), name
