@@ -211,3 +211,45 @@ def test_mfma_peak_probe_runs(gpu):
     assert 300.0 < t < 3000.0, t
     r = ms.mfma_peak_tflops(2, 2000, random=True)
     assert 300.0 < r < 3000.0, r
+
+
+def test_estimate_graph_replay(gpu):
+    """msparse_estimate captured in a HIP graph and replayed on three input sets
+    (eager copies and synchronisations between the replays): every replay
+    equals the eager call bit for bit."""
+    wl = SMALL["gqa_8k"]
+    dims = ms.make_dims(wl.batch, wl.seq, wl.heads_q, wl.heads_kv, wl.head_dim)
+    xs = [make_inputs(wl.resized(seed=wl.seed + i), "cpu", with_do=False) for i in range(3)]
+    q = xs[0]["q"].to(gpu)
+    k = xs[0]["k"].to(gpu)
+    shape = (wl.batch, wl.heads_q)
+    vi = torch.empty(shape + (wl.k_v,), dtype=torch.int32, device=gpu)
+    si = torch.empty(shape + (wl.k_s,), dtype=torch.int32, device=gpu)
+    vs = torch.empty(shape + (wl.seq,), dtype=torch.float32, device=gpu)
+    ss = torch.empty_like(vs)
+    ws = ms._workspace(ms.lib().msparse_estimate_workspace(ms.ctypes.byref(dims), wl.last_q, wl.k_v, wl.k_s), gpu)
+
+    def run(stream=None):
+        ms.estimate(dims, q, k, wl.last_q, wl.k_v, wl.k_s, vi, si, v_score=vs, s_score=ss, workspace=ws,
+                    stream=stream)
+
+    refs = []
+    for x in xs:
+        q.copy_(x["q"].to(gpu))
+        k.copy_(x["k"].to(gpu))
+        run()
+        torch.cuda.synchronize()
+        refs.append([t.clone() for t in (vi, si, vs, ss)])
+    stream = torch.cuda.Stream()
+    graph = torch.cuda.CUDAGraph()
+    torch.cuda.synchronize()
+    with torch.cuda.graph(graph, stream=stream):
+        run(stream)
+    for x, ref in zip(xs, refs):
+        q.copy_(x["q"].to(gpu))
+        k.copy_(x["k"].to(gpu))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for name, got, want in zip(("v_idx", "s_idx", "v_score", "s_score"), (vi, si, vs, ss), ref):
+            assert torch.equal(got, want), name
