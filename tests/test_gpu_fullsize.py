@@ -244,3 +244,26 @@ def test_ring_share_fullsize_sampled_rows(gpu, name, rank):
     assert ((sum_dv - want_dv).abs() <= 1e-4 * abs_dv + 1e-3).all(), "sum dV over the share"
     del x, shards, q_loc, do_loc, out, o_acc, dq
     torch.cuda.empty_cache()
+
+
+def test_layer_512k_deterministic(gpu):
+    """The whole step at 512K (estimate, index, forward, backward) run twice on
+    the same inputs gives bit-identical results: every reduction has a fixed
+    order (no atomics on floating point)."""
+    wl = WORKLOADS["layer_512k"]
+    x = make_inputs(wl, gpu)
+    dims = ms.make_dims(wl.batch, wl.seq, wl.heads_q, wl.heads_kv, wl.head_dim)
+    runs = []
+    for _ in range(2):
+        vi, si = ms.estimate(dims, x["q"], x["k"], wl.last_q, wl.k_v, wl.k_s)
+        idx = ms.make_index(dims, vi, si)
+        of = torch.empty(x["q"].shape, dtype=torch.float32, device=gpu)
+        out, lse = ms.attn_fwd(dims, x["q"], x["k"], x["v"], idx, out_f32=of)
+        dq, dk, dv = ms.attn_bwd(dims, x["q"], x["k"], x["v"], out, x["do"], lse, idx, out_f32=of)
+        torch.cuda.synchronize()
+        runs.append({"v_idx": vi, "s_idx": si, "blk_ptr": idx["blk_ptr"], "col_ptr": idx["col_ptr"], "out": of,
+                     "lse": lse, "dq": dq, "dk": dk, "dv": dv})
+    for name in runs[0]:
+        assert torch.equal(runs[0][name], runs[1][name]), name
+    del x, runs
+    torch.cuda.empty_cache()
