@@ -167,3 +167,15 @@ def test_bwd_flags_validation():
     st = L.msparse_attn_bwd(ctypes.byref(d), fake, fake, fake, fake, None, fake, fake, ctypes.byref(idx), fake, fake,
                             fake, 4, fake, 1 << 40, None)
     assert st == -1, ms.lib().msparse_last_error()
+
+
+def test_header_compiles_as_c_and_cpp():
+    """include/msparse.h is a plain C header (C99 and C++)."""
+    import shutil
+    import subprocess
+    hdr = os.path.join(os.path.dirname(__file__), "..", "include", "msparse.h")
+    for cc, lang, std in (("gcc", "c", "-std=c99"), ("g++", "c++", "-std=c++17")):
+        if shutil.which(cc) is None:
+            pytest.skip(f"{cc} not installed")
+        r = subprocess.run([cc, "-fsyntax-only", "-Wall", "-Werror", "-x", lang, std, hdr], capture_output=True, text=True)
+        assert r.returncode == 0, r.stderr
