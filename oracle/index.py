@@ -226,11 +226,6 @@ class Index:
             M[r] = sel & (kpos <= npos)
         return M
 
-    def work(self) -> np.ndarray:
-        """Tile-equivalents per head: selected tiles + columns / 64."""
-        return np.array([sum(len(x) for x in self.blocks[bh]) + sum(len(x) for x in self.cols[bh]) / BLOCK
-                         for bh in range(self.BH)])
-
 
 def ring_work(v_idx, s_idx, N: int, W: int, layout: str):
     """Selected tiles and column entries of query worker r against KV shard s,
@@ -265,9 +260,3 @@ def imbalance_degrees(work, schedule) -> tuple:
     worker_level = np.mean([per_step[:, t].max() / per_step[:, t].mean() for t in range(W)])
     step_level = np.mean([per_step[r].max() / per_step[r].mean() for r in range(W)])
     return float(worker_level), float(step_level)
-
-
-def imbalance(work) -> float:
-    """Imbalance degree max / mean (Section 5.4, Workload Balance Analysis)."""
-    w = np.asarray(work, dtype=np.float64)
-    return float(w.max() / w.mean())

@@ -162,3 +162,81 @@ def test_merge_with_empty_partial():
     mo, ml = A.merge(o, l, np.zeros((3, 4)), np.full(3, -np.inf))
     np.testing.assert_array_equal(ml, l)
     np.testing.assert_allclose(mo, o, atol=0)
+
+
+# ---- layer_dq: dQ of sampled rows only (Eq. attention_backward restricted to
+# those rows; a row's dQ needs only that row's probabilities and gradients)
+def test_layer_dq_equals_full_backward_rows():
+    q, k, v, do, idx = _case(21, B=2, Hq=4, Hkv=2, N=256, d=8, nv=7, ns=6)
+    scale = 0.35
+    dq_full = A.layer_bwd(q, k, v, do, idx, scale)[0]
+    rows = np.array([255, 3, 64, 63, 130, 0, 191, 64])     # unsorted, with a repeat
+    dq = A.layer_dq(q[:, :, rows], k, v, do[:, :, rows], _RowsOf(idx, rows), scale, np.arange(len(rows)))
+    np.testing.assert_allclose(dq, dq_full[:, :, rows], rtol=0, atol=1e-12)
+
+
+class _RowsOf:
+    """An index whose mask row r is row rows[r] of `idx` (the sampled-row form
+    the full-size tests hand to the oracle)."""
+
+    def __init__(self, idx, rows):
+        self.idx, self.rows = idx, np.asarray(rows)
+
+    def mask_rows(self, bh, rr):
+        return self.idx.mask_rows(bh, self.rows[np.asarray(rr)])
+
+
+def test_layer_dq_brute_force_loops():
+    # dQ_n = scale sum_m P[n,m] (dO_n . v_m - dO_n . O_n) k_m over the executed
+    # keys, written as plain loops; Delta is taken as dO . O here (the oracle
+    # uses the row sum of dA o A: the two agree only if the code is right)
+    q, k, v, do, idx = _case(22, B=1, Hq=2, Hkv=1, N=128, d=4, nv=3, ns=4)
+    scale = 0.6
+    rows = np.array([0, 1, 17, 63, 64, 100, 127])
+    dq = A.layer_dq(q, k, v, do, idx, scale, rows)
+    for h in range(2):
+        M = idx.mask_rows(h, np.arange(128))
+        for r, n in enumerate(rows.tolist()):
+            ms = [m for m in range(128) if M[n, m]]
+            z = [scale * sum(q[0, h, n, t] * k[0, 0, m, t] for t in range(4)) for m in ms]
+            mx = max(z)
+            w = [math.exp(zz - mx) for zz in z]
+            s = sum(w)
+            p = [wi / s for wi in w]
+            o = [sum(pi * v[0, 0, m, t] for pi, m in zip(p, ms)) for t in range(4)]
+            delta = sum(do[0, h, n, t] * o[t] for t in range(4))
+            for t in range(4):
+                want = scale * sum(pi * (sum(do[0, h, n, u] * v[0, 0, m, u] for u in range(4)) - delta)
+                                   * k[0, 0, m, t] for pi, m in zip(p, ms))
+                assert abs(dq[0, h, r, t] - want) < 1e-12, (h, n, t, dq[0, h, r, t], want)
+
+
+def test_layer_dq_finite_differences():
+    # d/dq_n of sum over the sampled rows of O o dO, one row's forward at a time
+    q, k, v, do, idx = _case(23, B=1, Hq=2, Hkv=1, N=128, d=4, nv=3, ns=5)
+    scale = 0.8
+    rows = np.array([5, 70, 127])
+    dq = A.layer_dq(q, k, v, do, idx, scale, rows)
+
+    def loss(q_):
+        return float((A.layer_fwd(q_, k, v, idx, scale, rows=rows)[0] * do[:, :, rows]).sum())
+
+    eps = 1e-6
+    for h in range(2):
+        for r, n in enumerate(rows.tolist()):
+            for t in range(4):
+                qp, qm = q.copy(), q.copy()
+                qp[0, h, n, t] += eps
+                qm[0, h, n, t] -= eps
+                fd = (loss(qp) - loss(qm)) / (2 * eps)
+                assert abs(fd - dq[0, h, r, t]) <= 1e-6 * max(1.0, abs(fd)), (h, n, t, fd, dq[0, h, r, t])
+
+
+def test_layer_dq_empty_row_is_zero():
+    N, d = 128, 4
+    rng = np.random.default_rng(24)
+    q, k, v, do = (rng.standard_normal((1, 1, N, d)) for _ in range(4))
+    idx = I.Index(np.array([[[100]]]), np.array([[[70]]]), N)   # block 0 sees nothing
+    dq = A.layer_dq(q, k, v, do, idx, 0.5, np.array([0, 40, 63, 64, 127]))
+    assert np.all(dq[0, 0, :3] == 0)
+    assert np.abs(dq[0, 0, 3:]).max() > 0
