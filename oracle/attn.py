@@ -57,6 +57,13 @@ def head_bwd(q, k, v, do, mask, scale):
     return dq, dk, dv
 
 
+def seen_keys(mask):
+    """Keys that some row of the mask sees.  A masked entry has weight exactly
+    0 (additive -inf before the softmax), so leaving out keys that no row of a
+    chunk sees changes no sum; it only skips work."""
+    return np.flatnonzero(mask.any(axis=0))
+
+
 def layer_fwd(q, k, v, index, scale, rows=None):
     """q [B, Hq, Nq, d], k/v [B, Hkv, Nk, d] fp64 -> out [B, Hq, R, d], lse [B, Hq, R].
 
@@ -73,7 +80,8 @@ def layer_fwd(q, k, v, index, scale, rows=None):
             for c0 in range(0, len(rows), ROW_CHUNK):
                 rr = rows[c0:c0 + ROW_CHUNK]
                 M = index.mask_rows(bh, rr)
-                o, l = head_fwd(q[b, h, rr], k[b, h // G], v[b, h // G], M, scale)
+                sk = seen_keys(M)
+                o, l = head_fwd(q[b, h, rr], k[b, h // G][sk], v[b, h // G][sk], M[:, sk], scale)
                 out[b, h, c0:c0 + len(rr)] = o
                 lse[b, h, c0:c0 + len(rr)] = l
     return out, lse
@@ -88,7 +96,9 @@ def layer_dq(q, k, v, do, index, scale, rows):
     for b in range(B):
         for h in range(Hq):
             M = index.mask_rows(b * Hq + h, rows)
-            dq[b, h] = head_bwd(q[b, h, rows], k[b, h // G], v[b, h // G], do[b, h, rows], M, scale)[0]
+            sk = seen_keys(M)
+            dq[b, h] = head_bwd(q[b, h, rows], k[b, h // G][sk], v[b, h // G][sk], do[b, h, rows], M[:, sk],
+                                scale)[0]
     return dq
 
 
@@ -105,10 +115,12 @@ def layer_bwd(q, k, v, do, index, scale):
             for c0 in range(0, Nq, ROW_CHUNK):
                 rr = np.arange(c0, min(Nq, c0 + ROW_CHUNK))
                 M = index.mask_rows(b * Hq + h, rr)
-                gq, gk, gv = head_bwd(q[b, h, rr], k[b, h // G], v[b, h // G], do[b, h, rr], M, scale)
+                sk = seen_keys(M)
+                gq, gk, gv = head_bwd(q[b, h, rr], k[b, h // G][sk], v[b, h // G][sk], do[b, h, rr], M[:, sk],
+                                      scale)
                 dq[b, h, rr] = gq
-                dk[b, h // G] += gk
-                dv[b, h // G] += gv
+                dk[b, h // G, sk] += gk
+                dv[b, h // G, sk] += gv
     return dq, dk, dv
 
 

@@ -216,13 +216,16 @@ class Index:
         koff = np.arange(nk)
         kpos = self.k_blk_global[koff // BLOCK].astype(np.int64) * BLOCK + koff % BLOCK
         M = np.zeros((len(rows), nk), dtype=bool)
+        sel, sel_qi = None, -1
         for r, n in enumerate(rows.tolist()):
             qi = n // BLOCK
             npos = int(self.q_blk_global[qi]) * BLOCK + n % BLOCK
-            sel = np.zeros(nk, dtype=bool)
-            for j in self.blocks[bh][qi].tolist():
-                sel[j * BLOCK:(j + 1) * BLOCK] = True
-            sel[self.cols[bh][qi]] = True
+            if qi != sel_qi:           # the keys selected for query block qi (shared by its rows)
+                sel = np.zeros(nk, dtype=bool)
+                for j in self.blocks[bh][qi].tolist():
+                    sel[j * BLOCK:(j + 1) * BLOCK] = True
+                sel[self.cols[bh][qi]] = True
+                sel_qi = qi
             M[r] = sel & (kpos <= npos)
         return M
 
