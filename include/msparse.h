@@ -112,8 +112,17 @@ typedef struct {
  *                                  nb = global blocks
  *   q_blk_global int32 [nqb], k_blk_global int32 [nkb]: global block numbers
  *   overflow int32 [1] (may be NULL): set to 1 by msparse_build_index when a
- *                                  capacity was too small (what does not fit
- *                                  is dropped, nothing is written out of bounds)
+ *                                  capacity was too small, else 0.  The build
+ *                                  then writes nothing out of bounds, but the
+ *                                  lists are incomplete (an entry range that
+ *                                  crosses a capacity is left unwritten), so
+ *                                  the attention calls read this flag first and,
+ *                                  when it is set, return from every kernel
+ *                                  without reading the lists or writing any
+ *                                  output: out, lse, out_f32, o_acc, lse_acc,
+ *                                  dq, dk and dv keep their previous contents.
+ *                                  Check the flag (or size the index with
+ *                                  msparse_index_count) before using them.
  *   world    host-side: ring workers the index was built for (1 for a whole
  *            sequence), so nb = world * seq_q / 64
  * blk_cap, col_cap, vcol_cap are host-side element capacities of blk_idx (and
@@ -204,9 +213,13 @@ MSPARSE_API msparse_status msparse_estimate_topp(const msparse_dims* dims, const
  *
  * msparse_index_count returns the exact element counts the build will write
  * (it waits for the GPU).  msparse_build_index writes them asynchronously,
- * never past blk_cap / col_cap / vcol_cap; when a capacity is too small it sets
- * *overflow and the host-visible caps check returns MSPARSE_ERR_CAPACITY only
- * when a cap is below the trivial lower bound (use msparse_index_count). */
+ * never past blk_cap / col_cap / vcol_cap.  With an overflow flag, a capacity
+ * that turns out too small sets *overflow on the GPU (see msparse_index: the
+ * attention calls then leave their outputs untouched).  Without one, every
+ * capacity must cover the worst case for the budgets (B Hq nqb min(nkb,
+ * 2 k_s, nb) block entries, B Hq nqb min(k_v, seq_k) column entries, B Hq
+ * min(k_v, seq_k) vertical entries), else MSPARSE_ERR_CAPACITY before any
+ * launch.  The exact sizes come from msparse_index_count. */
 MSPARSE_API size_t msparse_index_workspace(const msparse_dims* dims, int32_t k_v, int32_t k_s, const msparse_ring* ring);
 MSPARSE_API msparse_status msparse_index_count(const msparse_dims* dims, const int32_t* v_idx, int32_t k_v,
                                    const int32_t* s_idx, int32_t k_s, const msparse_ring* ring,
@@ -295,14 +308,19 @@ MSPARSE_API msparse_status msparse_merge_out_lse(const msparse_dims* dims, const
  *                              same dims, q, out, out_f32, dout and lse and the
  *                              same workspace (the previous ring step of the
  *                              same worker; only k, v and the index differ):
- *                              Delta, the lse rows and the fp16 copies of q and
- *                              dO are not recomputed.  Results are undefined if
+ *                              Delta, max |dO| and the fp16 copies of q and dO
+ *                              are not recomputed.  Results are undefined if
  *                              that does not hold.
  * Other flag bits are MSPARSE_ERR_INVALID.
+ * Range: the fp16 operands are scaled by powers of two chosen per call from
+ * max |q|, |k|, |v| and |dO| (dZ by t with t head_dim max|v| in
+ * [2^9, 2^10)), so no input scale makes them overflow, and inputs multiplied
+ * by powers of two (within the bf16 range) give exactly the correspondingly
+ * scaled results; every finite bf16 input is accepted.
  * Workspace: msparse_attn_bwd_workspace(dims, vcol_cap) bytes; it holds
- * fp16 copies of q, k, v and dO (each times a power of two), Delta, lse, and
- * the column pass's work list and per-item partials (the query-side part sits
- * first and does not depend on vcol_cap). */
+ * fp16 copies of q, k, v and dO (each times a power of two), Delta, the scaled
+ * row values, and the column pass's work list and per-item partials (its size
+ * grows with vcol_cap). */
 enum { MSPARSE_BWD_ACCUMULATE_DQ = 1, MSPARSE_BWD_REUSE_QROWS = 2 };
 MSPARSE_API size_t msparse_attn_bwd_workspace(const msparse_dims* dims, int64_t vcol_cap);
 MSPARSE_API msparse_status msparse_attn_bwd(const msparse_dims* dims, const void* q, const void* k, const void* v,

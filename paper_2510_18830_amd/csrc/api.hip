@@ -338,6 +338,7 @@ static msparse_status fill_attn(const msparse_dims* d, const msparse_index* x, A
     a->dwords = (d->seq_q / kBlock * x->world + 31) / 32;
     a->q_blk_global = x->q_blk_global;
     a->k_blk_global = x->k_blk_global;
+    a->overflow = x->overflow;
     return MSPARSE_OK;
 }
 
@@ -426,7 +427,7 @@ msparse_status msparse_merge_out_lse(const msparse_dims* dims, const float* o_pa
     return check_hip(launch_merge(m, s), s, "merge out/lse");
 }
 
-// Backward workspace: scaled fp16 copies of K, V, Q and dO, Delta, lse2, the
+// Backward workspace: scaled fp16 copies of K, V, Q and dO, Delta, s Delta, lse2, the
 // max words, the column work list and the per-item column partials.
 static size_t carve_bwd(const msparse_dims* d, int64_t vcol_cap, char* base, AttnArgs* a) {
     const int64_t bh = int64_t(d->batch) * d->heads_q;
@@ -436,6 +437,7 @@ static size_t carve_bwd(const msparse_dims* d, int64_t vcol_cap, char* base, Att
     uint16_t* v16 = c.take<uint16_t>(size_t(d->batch) * d->heads_kv * d->seq_k * d->head_dim);
     uint16_t* q16 = c.take<uint16_t>(size_t(bh) * d->seq_q * d->head_dim);
     uint16_t* g16 = c.take<uint16_t>(size_t(bh) * d->seq_q * d->head_dim);
+    float* draw = c.take<float>(size_t(bh) * d->seq_q);
     float* delta = c.take<float>(size_t(bh) * d->seq_q);
     float* lse2 = c.take<float>(size_t(bh) * d->seq_q);
     uint32_t* dmax = c.take<uint32_t>(4);   // max |dO|, |Q|, |K|, |V|
@@ -452,6 +454,7 @@ static size_t carve_bwd(const msparse_dims* d, int64_t vcol_cap, char* base, Att
         a->v16 = v16;
         a->q16 = q16;
         a->g16 = g16;
+        a->draw = draw;
         a->delta = delta;
         a->lse2 = lse2;
         a->dmax = dmax;

@@ -7,6 +7,7 @@
 // value; the only atomic is an order-free max):
 //   init/delta  Delta_n = dO_n . O_n (from the fp32 forward output when given)
 //               and max |dO| over the tensor
+//   rowprep     per call: lse2 = lse log2(e) and t s Delta per row
 //   dq          query-major over the forward's block + column lists; per tile
 //               S^T = K Q^T, dP^T = V dO^T, dQ^T += K^T dZ^T        (3 GEMMs)
 //   dkdv        key-major over 64-key blocks: for every query head of the KV
@@ -22,9 +23,11 @@
 //   merge       adds the column partials into dK / dV, heads and items in order.
 // The second GEMM of each pair takes fp16 operands (P or dZ, and Q^T, K^T or
 // dO^T converted while staging): 3 more significand bits than bf16 at the same
-// MFMA rate.  dO is multiplied by a power of two s so that max |s dO| = 16,
-// which keeps s dP, s Delta and s dZ inside the fp16 range whatever the scale
-// of the incoming gradient; results are divided by s.
+// MFMA rate.  Two powers of two keep the fp16 operands in range whatever the
+// scales of dO and V: dO is multiplied by s (max |s dO| in [8, 16)), and dZ
+// by t with t d max|V| in [2^9, 2^10) (dz_scale), so that |t s dZ| < 2^15.
+// Results are divided by s (dV) or s t (dQ, dK), so inputs scaled by powers
+// of two give exactly the rescaled results.
 #include "common.h"
 #include "kernels.h"
 #include "trace.h"
@@ -79,7 +82,7 @@ __global__ void __launch_bounds__(256) bwd_delta_kernel(AttnArgs a) {
         }
 #pragma unroll
         for (int off = 8; off >= 1; off >>= 1) acc += __shfl_xor(acc, off);
-        if (row < rows && sub == 0) a.delta[row] = acc;
+        if (row < rows && sub == 0) a.draw[row] = acc;
     }
     mx = wave_max(mx);
     if ((threadIdx.x & 63) == 0) wmax[threadIdx.x >> 6] = mx;
@@ -92,15 +95,16 @@ __global__ void __launch_bounds__(256) bwd_delta_kernel(AttnArgs a) {
 
 __device__ __forceinline__ float dout_scale(const uint32_t* dmax) { return pow2_scale(dmax); }
 
-// Per-row values the tiles read: lse2 = lse log2(e) (+inf for a row without
-// keys, so its P is 0) and s Delta in place of Delta.
+// Per-row values the tiles read, made on every call (the dZ scale t depends
+// on this call's V): lse2 = lse log2(e) (+inf for a row without keys, so its
+// P is 0) and t s Delta.
 __global__ void __launch_bounds__(256) bwd_rowprep_kernel(AttnArgs a) {
     const int64_t rows = int64_t(a.B) * a.Hq * a.Nq;
-    const float sc = dout_scale(a.dmax);
+    const float ts = dout_scale(a.dmax) * dz_scale(a.qkvmax + 2, a.d);
     for (int64_t n = int64_t(blockIdx.x) * 256 + threadIdx.x; n < rows; n += int64_t(gridDim.x) * 256) {
         const float l = a.lse[n];
         a.lse2[n] = l == -INFINITY ? INFINITY : l * kLog2e;
-        a.delta[n] *= sc;
+        a.delta[n] = ts * a.draw[n];
     }
 }
 
@@ -127,7 +131,7 @@ struct DqRows {
 
 // lims (LDS, or NULL for a tile without masking): key k visible to in-block
 // query row r iff r >= lims[k]; a rare uniform branch (see fwd_tile).
-// c2 = scale log2(e) / (sq sk); isv = 1 / sv (turns the dP^T accumulator into s dP^T)
+// c2 = scale log2(e) / (sq sk); isv = t / sv (turns the dP^T accumulator into t s dP^T)
 template <int D>
 __device__ __forceinline__ void dq_tile(const uint16_t* kt, const uint16_t* vt, const int32_t* lims, DqRows<D>& st,
                                         int qrow, int lane, float c2, float isv) {
@@ -161,7 +165,7 @@ __device__ __forceinline__ void dq_tile(const uint16_t* kt, const uint16_t* vt, 
             pa = mfma32h(fv[set], st.g[k], pa);
             __builtin_amdgcn_sched_barrier(0);
         }
-        // s dZ^T = P o (s dP^T - s Delta), P = exp2(c2 z - lse2)
+        // t s dZ^T = P o (t s dP^T - t s Delta), P = exp2(c2 z - lse2)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             const float p = fast_exp2(__builtin_fmaf(sa[r], c2, -st.lse2));
@@ -196,6 +200,7 @@ __global__ void __launch_bounds__(kDqThreads) __attribute__((amdgpu_waves_per_eu
     constexpr int TE = DmaTile<D, kDualPad>::kElems;
     __shared__ uint16_t k0s[TE], v0s[TE], k1s[TE], v1s[TE];
     __shared__ int32_t kidx[64], lims[64], dlims[64];
+    if (index_overflowed(a.overflow)) return;   // incomplete lists: outputs are left untouched
     const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, l32 = lane & 31;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6), half = w >> 1;
     const int npair = (a.nqb + 1) >> 1;
@@ -210,6 +215,7 @@ __global__ void __launch_bounds__(kDqThreads) __attribute__((amdgpu_waves_per_eu
     const int qrow = 32 * (w & 1) + l32;
     const int64_t grow = int64_t(bh) * a.Nq + int64_t(qb) * 64 + qrow;
     const int32_t qg = ldc(a.q_blk_global, qb);
+    const float pt = dz_scale(a.qkvmax + 2, D);   // the tiles give t s dZ
 
     const int64_t kvoff = (int64_t(b) * a.Hkv + hk) * int64_t(a.Nk) * D;
     const uint16_t* __restrict__ kp = a.k16 + kvoff;
@@ -221,7 +227,7 @@ __global__ void __launch_bounds__(kDqThreads) __attribute__((amdgpu_waves_per_eu
         st.g[s] = *reinterpret_cast<const u32x4*>(a.g16 + grow * D + 16 * s + 8 * h);
     }
     const float sq = operand_scale(a.qkvmax), sk = operand_scale(a.qkvmax + 1);
-    const float isv = 1.f / operand_scale(a.qkvmax + 2);
+    const float isv = dz_scale(a.qkvmax + 2, D) / operand_scale(a.qkvmax + 2);   // t / sv
     const float c2 = a.scale * kLog2e / (sq * sk);
     st.lse2 = a.lse2[grow];
     const float sc = dout_scale(a.dmax);
@@ -308,7 +314,7 @@ __global__ void __launch_bounds__(kDqThreads) __attribute__((amdgpu_waves_per_eu
     }
     if (!live) return;
     float* dq = a.dq + grow * D;
-    const float fin = a.scale / (sc * sk);
+    const float fin = a.scale / (sc * pt * sk);
 #pragma unroll
     for (int i = 0; i < ND; ++i)
 #pragma unroll
@@ -353,11 +359,16 @@ __device__ __forceinline__ void kv_load_query_tile(uint16_t* t, const AttnArgs& 
 
 // One 64-row query tile against this wave's 32 keys (`key` = this lane's key
 // inside the 64-key block; kreg, vreg its scaled fp16 K and V rows).  c2 =
-// scale log2(e) / (sq sk); isv = 1 / sv turns the dP accumulator into s dP.  lims (LDS, or NULL for a tile without masking):
+// scale log2(e) / (sq sk); isv = t / sv turns the dP accumulator into t s dP.  lims (LDS, or NULL for a tile without masking):
 // the key is visible to in-block query row r iff r >= lims[key] (64: not
 // visible); a rare uniform branch whose limit comes from LDS, so nothing of
 // it is hoisted into the loop.
-template <int D>
+// SPLIT: P and t s dZ enter the dV / dK products as two fp16 parts each
+// (x = hi + lo, hi = fp16(x), lo = fp16(x - hi); about 22 significand bits):
+// the column pass carries most of a vertical key's rows (hundreds of
+// thousands at long lengths), where one fp16 rounding of every term would add
+// up to errors near the parity bar; it costs two more MFMAs per group there.
+template <int D, bool SPLIT = false>
 __device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, const u32x4* vreg, const int32_t* lims,
                                         int key, float c2, float isv, int lane, f32x16* dv, f32x16* dk) {
     using T = KvTile<D>;
@@ -408,6 +419,7 @@ __device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, co
     // r / 8), written straight from the softmax terms, so the accumulators are
     // never written back
     u32x4 pb[2][2], zb[2][2];   // [rb][j]
+    u32x4 pl[SPLIT ? 2 : 1][2], zl[SPLIT ? 2 : 1][2];   // low parts (SPLIT)
     // softmax terms of rows 32 rb + 8 q4 + 4 h + 0..3
     auto soft = [&](int rb, int q4) {
         const int row0 = 32 * rb + 8 * q4 + 4 * h;
@@ -425,6 +437,19 @@ __device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, co
         pb[rb][j][w0 + 1] = pack_f16x2(pv[2], pv[3]);
         zb[rb][j][w0] = pack_f16x2(zv[0], zv[1]);
         zb[rb][j][w0 + 1] = pack_f16x2(zv[2], zv[3]);
+        if constexpr (SPLIT) {
+            float plo[4], zlo[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                plo[e] = pv[e] - float(_Float16(pv[e]));
+                zlo[e] = zv[e] - float(_Float16(zv[e]));
+            }
+            const int r2 = SPLIT ? rb : 0;
+            pl[r2][j][w0] = pack_f16x2(plo[0], plo[1]);
+            pl[r2][j][w0 + 1] = pack_f16x2(plo[2], plo[3]);
+            zl[r2][j][w0] = pack_f16x2(zlo[0], zlo[1]);
+            zl[r2][j][w0 + 1] = pack_f16x2(zlo[2], zlo[3]);
+        }
     };
     // masked entries (rare diagonal tiles): clear their fp16 halves
     auto mask = [&](int rb) {
@@ -437,6 +462,10 @@ __device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, co
                     const uint32_t keep = (r & 1) ? 0x0000FFFFu : 0xFFFF0000u;
                     pb[rb][r >> 3][(r & 7) >> 1] &= keep;
                     zb[rb][r >> 3][(r & 7) >> 1] &= keep;
+                    if constexpr (SPLIT) {
+                        pl[SPLIT ? rb : 0][r >> 3][(r & 7) >> 1] &= keep;
+                        zl[SPLIT ? rb : 0][r >> 3][(r & 7) >> 1] &= keep;
+                    }
                 }
         }
     };
@@ -456,6 +485,10 @@ __device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, co
         for (int j = 0; j < 2; ++j) {
             dv[i] = mfma32h(av[set][j], pb[rb][j], dv[i]);
             dk[i] = mfma32h(ak[set][j], zb[rb][j], dk[i]);
+            if constexpr (SPLIT) {
+                dv[i] = mfma32h(av[set][j], pl[SPLIT ? rb : 0][j], dv[i]);
+                dk[i] = mfma32h(ak[set][j], zl[SPLIT ? rb : 0][j], dk[i]);
+            }
         }
     };
     static_assert(KD == 2 * ND, "four S/dP groups and four dV/dK groups per half");
@@ -524,6 +557,7 @@ __global__ void __launch_bounds__(kKvThreads) __attribute__((amdgpu_waves_per_eu
     constexpr int KD = D / 16, ND = D / 32;
     __shared__ __attribute__((aligned(16))) uint16_t t0s[KvTile<D>::kElems], t1s[KvTile<D>::kElems];
     __shared__ int32_t dlims[64];
+    if (index_overflowed(a.overflow)) return;   // incomplete lists: outputs are left untouched
     const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, l32 = lane & 31;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6), half = w >> 1;
     if (tid < 64) dlims[tid] = tid;   // causal diagonal: key k visible to rows >= k
@@ -554,7 +588,7 @@ __global__ void __launch_bounds__(kKvThreads) __attribute__((amdgpu_waves_per_eu
         dk[i] = f32x16{};
     }
     const float sq = operand_scale(a.qkvmax), sk = operand_scale(a.qkvmax + 1);
-    const float isv = 1.f / operand_scale(a.qkvmax + 2);
+    const float isv = dz_scale(a.qkvmax + 2, D) / operand_scale(a.qkvmax + 2);   // t / sv
     const float c2 = a.scale * kLog2e / (sq * sk);
     const float sc = dout_scale(a.dmax);
     const int32_t kg = ldc(a.k_blk_global, kb);
@@ -627,7 +661,8 @@ __global__ void __launch_bounds__(kKvThreads) __attribute__((amdgpu_waves_per_eu
     if (!live) return;
     float* dkp = a.dk + krow * D;
     float* dvp = a.dv + krow * D;
-    const float fk = a.scale / (sc * sq), fv = 1.f / sc;
+    const float pt = dz_scale(a.qkvmax + 2, D);   // the tiles give s dV and t s dK
+    const float fk = a.scale / (sc * pt * sq), fv = 1.f / sc;
 #pragma unroll
     for (int i = 0; i < ND; ++i)
 #pragma unroll
@@ -687,6 +722,7 @@ __device__ int plan_scan(int v, int* tmp, int* total) {
 __global__ void __launch_bounds__(kPlanThreads) bwd_colplan_kernel(AttnArgs a) {
     __shared__ int tmp[17];
     __shared__ long long part[kPlanThreads / 64];
+    if (index_overflowed(a.overflow)) return;   // the column kernels return as well
     const int tid = threadIdx.x;
     const int BH = a.B * a.Hq;
     // chunks per head (entries past the capacity are ignored)
@@ -758,6 +794,7 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1
     constexpr int KD = D / 16, ND = D / 32;
     __shared__ __attribute__((aligned(16))) uint16_t ts[KvTile<D>::kElems];
     __shared__ int32_t clims[64];
+    if (index_overflowed(a.overflow)) return;   // no work list was planned
     const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, l32 = lane & 31;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int nc = a.col_choff[a.B * a.Hq];
@@ -795,7 +832,7 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1
         dk[i] = f32x16{};
     }
     const float sq = operand_scale(a.qkvmax), sk = operand_scale(a.qkvmax + 1);
-    const float isv = 1.f / operand_scale(a.qkvmax + 2);
+    const float isv = dz_scale(a.qkvmax + 2, D) / operand_scale(a.qkvmax + 2);   // t / sv
     const float c2 = a.scale * kLog2e / (sq * sk);
     const float sc = dout_scale(a.dmax);
     const uint32_t* db = a.diag_bits + int64_t(bh) * a.dwords;
@@ -809,14 +846,15 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1
         kv_load_query_tile<D, 2>(ts, a, bh, qb, w, lane);
         wait_vmem();
         __syncthreads();
-        kv_tile<D>(ts, kreg, vreg, clims, key, c2, isv, lane, dv, dk);
+        kv_tile<D, true>(ts, kreg, vreg, clims, key, c2, isv, lane, dv, dk);
         __syncthreads();
     }
     if (!valid) return;
     const int64_t slot = int64_t(item) * 64 + key;
     float* dkp = a.dk_col + slot * D;
     float* dvp = a.dv_col + slot * D;
-    const float fk = a.scale / (sc * sq), fv = 1.f / sc;
+    const float pt = dz_scale(a.qkvmax + 2, D);   // the tiles give s dV and t s dK
+    const float fk = a.scale / (sc * pt * sq), fv = 1.f / sc;
 #pragma unroll
     for (int i = 0; i < ND; ++i)
 #pragma unroll
@@ -845,6 +883,7 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1
 constexpr int kMergeThreads = 512;
 __global__ void __launch_bounds__(kMergeThreads) bwd_colmerge_kernel(AttnArgs a) {
     __shared__ int64_t span_lo[kMergeThreads], span_hi[kMergeThreads];
+    if (index_overflowed(a.overflow)) return;   // no work list was planned
     const int BK = a.B * a.Hkv;
     const int bk = int(blockIdx.x % BK);
     const int kb = int(blockIdx.x / BK);
@@ -920,18 +959,20 @@ hipError_t launch_bwd_d(const AttnArgs& a, hipStream_t s) {
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    if (qside && rows > 0) {
-        TraceScope _t("bwd_rowprep", s);
-        const int64_t want = (rows + 255) / 256;
-        hipLaunchKernelGGL(bwd_rowprep_kernel, dim3(unsigned(want < kDeltaBlocks ? want : int64_t(kDeltaBlocks))),
-                           dim3(256), 0, s, a);
-    }
     // scaled fp16 copies: Q, K, V to max in [2^14, 2^15), dO to [8, 16)
     const int64_t nkv = int64_t(a.B) * a.Hkv * a.Nk * a.d;
     const int64_t nq = int64_t(a.B) * a.Hq * a.Nq * a.d;
     if (qside && (e = launch_absmax(a.q, nq, a.qkvmax, s)) != hipSuccess) return e;
     if ((e = launch_absmax(a.k, nkv, a.qkvmax + 1, s)) != hipSuccess) return e;
     if ((e = launch_absmax(a.v, nkv, a.qkvmax + 2, s)) != hipSuccess) return e;
+    // row values after max |V| (the probability scale t)
+    if (rows > 0) {
+        TraceScope _t("bwd_rowprep", s);
+        const int64_t want = (rows + 255) / 256;
+        hipLaunchKernelGGL(bwd_rowprep_kernel, dim3(unsigned(want < kDeltaBlocks ? want : int64_t(kDeltaBlocks))),
+                           dim3(256), 0, s, a);
+    }
+    if ((e = hipGetLastError()) != hipSuccess) return e;
     if (qside && (e = launch_to_f16(a.q, a.q16, nq, a.qkvmax, kOperandExp, s)) != hipSuccess) return e;
     if ((e = launch_to_f16(a.k, a.k16, nkv, a.qkvmax + 1, kOperandExp, s)) != hipSuccess) return e;
     if ((e = launch_to_f16(a.v, a.v16, nkv, a.qkvmax + 2, kOperandExp, s)) != hipSuccess) return e;

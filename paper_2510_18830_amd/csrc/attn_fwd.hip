@@ -113,22 +113,23 @@ __device__ __forceinline__ void fwd_tile(const uint16_t* kt, const uint16_t* vt,
         st.m = m_new;
     }
     const float m_use = st.m == -INFINITY ? 0.f : st.m;
-    float rs = 0.f;
 #pragma unroll
     for (int c = 0; c < 2; ++c)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const float p = fast_exp2(__builtin_fmaf(sacc[c][r], c2, -m_use));
-            sacc[c][r] = p;
-            rs += p;
-        }
-    st.l += rs + __shfl_xor(rs, 32);
+        for (int r = 0; r < 16; ++r) sacc[c][r] = fast_exp2(__builtin_fmaf(sacc[c][r], c2, -m_use));
     // ---- O^T += V^T P^T (A = V^T read transposed from the fp16 V rows)
     u32x4 pb[4];
     pb[0] = pack8_f16<0>(sacc[0]);
     pb[1] = pack8_f16<8>(sacc[0]);
     pb[2] = pack8_f16<0>(sacc[1]);
     pb[3] = pack8_f16<8>(sacc[1]);
+    // The normaliser sums the fp16 weights the product uses, so O is an exact
+    // convex combination of V rows with those weights: its rounding error then
+    // shrinks with the weight outside the largest one, and Delta = dO . O of
+    // the backward stays consistent with its own probabilities even for
+    // nearly one-hot rows (which would otherwise amplify the 2^-12 rounding
+    // of P by 1 / (1 - max P)).
+    st.l += row_sum_f16(pb);
     // V^T operands in groups of one d block (4 operands) into two register sets
     u32x4 av[2][4];
     auto read_tr = [&](int set, int i) {
@@ -168,6 +169,7 @@ attn_fwd_kernel(AttnArgs a) {
     constexpr int KE = DmaTile<D, kRowPad>::kElems, VE = DmaTile<D, kTrPad>::kElems;
     __shared__ uint16_t k0s[KE], v0s[VE], k1s[KE], v1s[VE];
     __shared__ int32_t kidx[64], lims[64], dlims[64];
+    if (index_overflowed(a.overflow)) return;   // incomplete lists: outputs are left untouched
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;

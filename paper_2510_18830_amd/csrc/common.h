@@ -50,6 +50,10 @@ __device__ __forceinline__ T ldc(const T* p, int64_t i) {
     return ((const __attribute__((address_space(4))) T*)(p))[i];
 }
 
+// True when the index build that produced the lists ran out of capacity
+// (flag may be NULL): the lists are then incomplete and are not walked.
+__device__ __forceinline__ bool index_overflowed(const int32_t* flag) { return flag && ldc(flag, 0) != 0; }
+
 // Marks a rarely taken branch as having a side effect, so the compiler keeps
 // it a branch instead of turning its body into unconditional selects.
 __device__ __forceinline__ void keep_branch() { asm volatile(""); }
@@ -99,6 +103,20 @@ __device__ __forceinline__ float pow2_scale_to(const uint32_t* maxbits) {
 }
 // dO: max |s dO| in [8, 16), so s dP, s Delta and s dZ stay inside fp16
 __device__ __forceinline__ float pow2_scale(const uint32_t* maxbits) { return pow2_scale_to<4>(maxbits); }
+// dZ scale of the backward: the power of two t with t d max|V| in
+// [2^9, 2^10).  The fp16 operand t s dZ then satisfies |t s dZ| = t P
+// |s dP - s Delta| <= t 2 max|s dO| d max|V| < 2^15 (P <= 1, max|s dO| < 16,
+// and |dP|, |Delta| <= max|dO| d max|V|, O being a convex combination of V
+// rows): inside the fp16 range whatever the scale of V, and the same fp16
+// values for V times any power of two (t = 1 for unit-normal V at d = 128).
+// vmaxbits: max |V| as fp32 bits; 1 when it is 0 or not finite.
+__device__ __forceinline__ float dz_scale(const uint32_t* vmaxbits, int d) {
+    const float mx = __uint_as_float(*vmaxbits) * float(d);
+    if (!(mx > 0.f) || !isfinite(mx)) return 1.f;
+    int e;
+    frexpf(mx, &e);           // mx in [2^(e-1), 2^e)
+    return ldexpf(1.f, max(-100, min(100, 10 - e)));
+}
 // fp16 copies of Q, K, V: max in [2^14, 2^15) (exact conversion of every bf16
 // value down to 2^-29 of the max; products stay far inside fp32)
 constexpr int kOperandExp = 15;

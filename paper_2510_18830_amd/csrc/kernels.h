@@ -78,7 +78,8 @@ struct AttnArgs {
     uint32_t* dmax;        // bwd workspace: max |dO| as fp32 bits
     uint32_t* qkvmax;      // workspace: max |Q|, |K|, |V| as fp32 bits (the fwd uses [2])
     float* lse;            // fwd output / bwd input
-    float* delta;          // bwd workspace [B,Hq,Nq]: Delta, then s * Delta after row prep
+    float* draw;           // bwd workspace [B,Hq,Nq]: Delta = dO . O (query-side, reusable)
+    float* delta;          // bwd workspace [B,Hq,Nq]: t * s * Delta, t = dz_scale() (per call, row prep)
     float* lse2;           // bwd workspace [B,Hq,Nq]: lse * log2(e) (+inf for a row without keys)
     float* dq;
     float* dk;
@@ -114,6 +115,9 @@ struct AttnArgs {
     int32_t dwords;
     const int32_t* q_blk_global;
     const int32_t* k_blk_global;
+    // set by an index build that ran out of capacity (may be NULL): every
+    // kernel that walks the lists then returns before reading them
+    const int32_t* overflow;
 };
 hipError_t launch_attn_fwd(const AttnArgs& a, hipStream_t s);
 // *maxbits = max(*maxbits, max |src|) as fp32 bits, n bf16 elements (n a

@@ -207,4 +207,25 @@ __device__ __forceinline__ u32x4 pack8_f16(const f32x16& acc) {
     return r;
 }
 
+// Sum over a row of the fp16 weights in four packed B operands (32 values per
+// lane) plus the partner lane l ^ 32 (the other half of the row's keys), in
+// fp32: one v_dot2 per pair, two chains.
+__device__ __forceinline__ float row_sum_f16(const u32x4* pb) {
+    typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+    const h2 one = {(_Float16)1.f, (_Float16)1.f};
+    float a = 0.f, b = 0.f;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+        // elements copied out first: a bit cast of an ext_vector element
+        // expression reads element 0 under this compiler
+        const uint32_t w0 = pb[g].x, w1 = pb[g].y, w2 = pb[g].z, w3 = pb[g].w;
+        a = __builtin_amdgcn_fdot2(__builtin_bit_cast(h2, w0), one, a, false);
+        b = __builtin_amdgcn_fdot2(__builtin_bit_cast(h2, w1), one, b, false);
+        a = __builtin_amdgcn_fdot2(__builtin_bit_cast(h2, w2), one, a, false);
+        b = __builtin_amdgcn_fdot2(__builtin_bit_cast(h2, w3), one, b, false);
+    }
+    const float s = a + b;
+    return s + __shfl_xor(s, 32);
+}
+
 }  // namespace msparse

@@ -123,3 +123,45 @@ def assert_budget_near(cnt: int, score, p: float, kmax: int, rel=TOPP_MASS_REL):
     if cnt < kmax:
         assert c[cnt - 1] >= theta * (1 - rel), f"mass {c[cnt - 1]:.6e} below p of the total {theta:.6e}"
     assert cnt == 1 or c[cnt - 2] < theta * (1 + rel), f"cnt {cnt} larger than needed"
+
+
+def assert_close_rows(name, got, ref, max_abs=MAX_ABS, mean_abs=MEAN_ABS):
+    """The parity bars per row, in units of max(1, RMS of that row of the
+    reference): a row built from inputs scaled far from unity (an outlier value
+    row of size 2^10, say) carries rounding errors proportional to its own
+    size, so the absolute bars apply relative to each row's magnitude."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    assert got.shape == ref.shape, (name, got.shape, ref.shape)
+    unit = np.maximum(1.0, np.sqrt(np.mean(ref ** 2, axis=-1, keepdims=True)))
+    err = np.abs(got - ref) / unit
+    assert np.isfinite(err).all(), f"{name}: non-finite difference"
+    assert err.max() <= max_abs and err.mean() <= mean_abs, \
+        f"{name}: row-scaled max-abs {err.max():.3e} mean-abs {err.mean():.3e}"
+
+
+def _head_reference(job):
+    """Full oracle forward and backward of one query head (a process-pool worker)."""
+    q, k, v, do, vi, si, N, scale, threads = job
+    from threadpoolctl import threadpool_limits
+    from oracle import attn as OA_
+    with threadpool_limits(threads):
+        idx = OI.Index(vi, si, N)
+        o, lse = OA_.layer_fwd(q, k, v, idx, scale)
+        dq, dk, dv = OA_.layer_bwd(q, k, v, do, idx, scale)
+    return o[0, 0], lse[0, 0], dq[0, 0], dk[0, 0], dv[0, 0]
+
+
+def oracle_heads(f: dict, vi, si, heads, scale, workers=8, threads=2):
+    """The oracle's out, lse, dQ and the per-head dK, dV contributions of the
+    given query heads (batch 0), one head per worker process (spawned, so no
+    GPU state is inherited): {h: (out, lse, dq, dk_h, dv_h)}."""
+    import multiprocessing as mp
+    q, k = f["q"], f["k"]
+    G = q.shape[1] // k.shape[1]
+    N = q.shape[2]
+    jobs = [(q[:1, [h]], k[:1, [h // G]], f["v"][:1, [h // G]], f["do"][:1, [h]], vi[:1, [h]], si[:1, [h]], N,
+             scale, threads) for h in heads]
+    with mp.get_context("spawn").Pool(min(workers, len(jobs))) as pool:
+        res = pool.map(_head_reference, jobs)
+    return dict(zip(heads, res))
