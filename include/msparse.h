@@ -230,6 +230,24 @@ MSPARSE_API msparse_status msparse_build_index(const msparse_dims* dims, const i
                                    const msparse_index* index, void* workspace, size_t workspace_bytes,
                                    void* stream);
 
+/* msparse_build_index without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Same arguments, results and errors as
+ * msparse_build_index, whose kernels it runs; their scratch (the
+ * msparse_index_workspace(dims, k_v, k_s, ring) bytes) lives instead in a
+ * fixed device array of 64 MiB inside the library, one per GPU, held from
+ * the library's loading on that GPU until the process ends (28 heads at 1M
+ * tokens need about 28 MB).  A larger need is MSPARSE_ERR_WORKSPACE before
+ * any launch.  The call allocates nothing; its first call on a device looks
+ * up that device's array (the calling thread's current device must be the
+ * device of `stream` and of the buffers).  Every call on one GPU shares the
+ * array: calls that overlap on a GPU (other streams, other threads) race and
+ * must be serialised by the caller.  Nothing in the array needs clearing
+ * between calls: each build writes what it reads. */
+MSPARSE_API msparse_status msparse_build_index_noalloc(const msparse_dims* dims, const int32_t* v_idx, int32_t k_v,
+                                                       const int32_t* s_idx, int32_t k_s, const msparse_ring* ring,
+                                                       const msparse_index* index, void* stream);
+
 /* Ring workload matrix (Section 4.2; the workload balance analysis of Section 5).
  * For a ring of `world` workers with the given layout over the whole sequence
  * (dims: seq_q = seq_k = N, the global length), counts, summed over all heads,

@@ -65,6 +65,7 @@ _SIGS = {
     "msparse_index_count": (c_i32, [_P(Dims), c_vp, c_i32, c_vp, c_i32, _P(Ring), _P(c_i64), _P(c_i64), _P(c_i64),
                                     c_vp, c_sz, c_vp]),
     "msparse_build_index": (c_i32, [_P(Dims), c_vp, c_i32, c_vp, c_i32, _P(Ring), _P(IndexStruct), c_vp, c_sz, c_vp]),
+    "msparse_build_index_noalloc": (c_i32, [_P(Dims), c_vp, c_i32, c_vp, c_i32, _P(Ring), _P(IndexStruct), c_vp]),
     "msparse_attn_fwd_workspace": (c_sz, [_P(Dims)]),
     "msparse_attn_fwd": (c_i32, [_P(Dims), c_vp, c_vp, c_vp, _P(IndexStruct), c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]),
     "msparse_attn_fwd_merge": (c_i32, [_P(Dims), c_vp, c_vp, c_vp, _P(IndexStruct), c_vp, c_vp, c_vp, c_i32, c_vp,
@@ -244,6 +245,14 @@ def build_index(dims, v_idx, s_idx, index: SparseIndex, ring=None, workspace=Non
         workspace = _workspace(index_workspace_bytes(dims, k_v, k_s, ring), v_idx.device)
     _check(lib().msparse_build_index(ctypes.byref(dims), _p(v_idx), k_v, _p(s_idx), k_s, _ring_ptr(ring),
                                      ctypes.byref(index.struct), _p(workspace), workspace.numel(), _stream(stream)))
+    return index
+
+
+def build_index_noalloc(dims, v_idx, s_idx, index: SparseIndex, ring=None, stream=None):
+    """msparse_build_index_noalloc: the index build with the library's fixed scratch (no workspace)."""
+    k_v, k_s = v_idx.shape[-1], s_idx.shape[-1]
+    _check(lib().msparse_build_index_noalloc(ctypes.byref(dims), _p(v_idx), k_v, _p(s_idx), k_s, _ring_ptr(ring),
+                                             ctypes.byref(index.struct), _stream(stream)))
     return index
 
 

@@ -6,6 +6,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <string>
 
 #include "common.h"
@@ -209,6 +210,43 @@ msparse_status check_index_struct(const msparse_dims* d, const msparse_index* x,
     return MSPARSE_OK;
 }
 
+// ------------------------------------------------------------------ allocation-free index build
+// Scratch of msparse_build_index_noalloc: file-scope device memory, one copy
+// per GPU, made when the code object loads on that GPU and held until the
+// process ends.  In host code `scratch` names a host-side stand-in, not a
+// device address: the address each GPU uses comes from hipGetSymbolAddress
+// (scratch_on_current_device) and is the only one passed to kernels.
+constexpr size_t kNoallocScratchBytes = size_t(64) << 20;
+constexpr int kMaxDevices = 256;
+
+}  // namespace
+
+static __device__ __align__(256) unsigned char scratch[kNoallocScratchBytes];
+
+namespace {
+
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's copy of `scratch`, looked up once per device (with
+// that device current) and kept.
+msparse_status scratch_on_current_device(void** out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(MSPARSE_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+    if (dev < 0 || dev >= kMaxDevices) return fail(MSPARSE_ERR_UNSUPPORTED, "device %d beyond %d", dev, kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return fail(MSPARSE_ERR_HIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev, hipGetErrorString(e));
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return MSPARSE_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -313,6 +351,22 @@ msparse_status msparse_build_index(const msparse_dims* dims, const int32_t* v_id
     if ((st = check_hip(launch_index_count(a, s), s, "index count"))) return st;
     if ((st = check_hip(launch_index_scan(a, s), s, "index scan"))) return st;
     return check_hip(launch_index_fill(a, s), s, "index fill");
+}
+
+msparse_status msparse_build_index_noalloc(const msparse_dims* dims, const int32_t* v_idx, int32_t k_v,
+                                           const int32_t* s_idx, int32_t k_s, const msparse_ring* ring,
+                                           const msparse_index* index, void* stream) {
+    RingInfo ri;
+    msparse_status st = check_index_inputs(dims, v_idx, k_v, s_idx, k_s, ring, &ri);
+    if (st) return st;
+    if ((st = check_index_struct(dims, index, true))) return st;
+    const size_t need = plan_index(dims, k_v, k_s, ri, nullptr, false).bytes;
+    if (need > kNoallocScratchBytes)
+        return fail(MSPARSE_ERR_WORKSPACE, "index build needs %zu bytes of scratch; the fixed scratch holds %zu",
+                    need, kNoallocScratchBytes);
+    void* ws = nullptr;
+    if ((st = scratch_on_current_device(&ws))) return st;
+    return msparse_build_index(dims, v_idx, k_v, s_idx, k_s, ring, index, ws, need, stream);
 }
 
 // ------------------------------------------------------------------ attention
