@@ -16,7 +16,9 @@ from dataclasses import dataclass
 import torch
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libmsparse.so")
+# MSPARSE_LIBRARY selects another build of the same library (the host
+# AddressSanitizer build of build.build_asan, for the host-side tests)
+LIB_PATH = os.environ.get("MSPARSE_LIBRARY") or os.path.join(HERE, "libmsparse.so")
 
 STRIPED = 0
 ZIGZAG = 1

@@ -59,5 +59,42 @@ def build(jobs: int | None = None, verbose: bool = False, out: str = LIB_PATH, d
     return out
 
 
+def asan_runtime() -> str:
+    """The compiler's AddressSanitizer runtime (to preload into the host process)."""
+    import glob
+    root = os.path.dirname(os.path.dirname(os.path.realpath(hipcc())))
+    cands = sorted(glob.glob(os.path.join(root, "lib", "clang", "*", "lib", "linux", "libclang_rt.asan-x86_64.so")))
+    cands += sorted(glob.glob("/opt/rocm/llvm/lib/clang/*/lib/linux/libclang_rt.asan-x86_64.so"))
+    if not cands:
+        raise RuntimeError("libclang_rt.asan-x86_64.so not found")
+    return cands[0]
+
+
+def build_asan(out: str | None = None) -> str:
+    """A host-AddressSanitizer build of the library: the C ABI's host code
+    (argument validation, workspace carving, launch plumbing: api.hip) is
+    instrumented for the host only (-Xarch_host), the kernels are the usual
+    gfx950 objects.  Load it with the runtime from asan_runtime() preloaded."""
+    build_dir = os.path.join(BUILD_DIR, "asan")
+    os.makedirs(build_dir, exist_ok=True)
+    out = out or os.path.join(build_dir, "libmsparse_asan.so")
+    objs = []
+    for src in SOURCES:
+        obj = os.path.join(build_dir, os.path.splitext(src)[0] + ".o")
+        extra = (["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fno-omit-frame-pointer", "-g"]
+                 if src == "api.hip" else [])
+        cmd = [hipcc(), *common_flags(), *extra, "-c", os.path.join(CSRC, src), "-o", obj]
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"hipcc failed for {src}:\n{r.stdout}\n{r.stderr}")
+        objs.append(obj)
+    cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-shared-libasan", "-Xarch_host",
+           "-fsanitize=address", *objs, "-o", out]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"asan link failed:\n{r.stdout}\n{r.stderr}")
+    return out
+
+
 if __name__ == "__main__":
     build(verbose=True)
