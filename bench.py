@@ -1,8 +1,9 @@
 """Benchmark of the vertical-slash sparse-attention hot path on one MI355X.
 
 A step is one pass of the whole path over one synthetic layer already resident
-in HBM: pattern estimation -> index count (one GPU wait) and build -> sparse
-forward -> sparse backward.  The metric is fwd+bwd TFLOP/s on the computed
+in HBM: pattern estimation -> index build (prep, counts, offsets, fill; sized
+in the warm-up, overflow flag checked after each step) -> sparse forward ->
+sparse backward.  The metric is fwd+bwd TFLOP/s on the computed
 blocks (counted FLOPs / step time, see below) and ms per layer.
 
 Counted FLOPs (no credit for skipped tiles or for recomputation):
@@ -278,6 +279,38 @@ def ring_leg(x, v_idx, s_idx, wl, world: int, rank: int, steps: int):
     }
 
 
+def build_index_step(ms, dims, v_idx, s_idx, state, idx_ws, dev):
+    """The index of one step.  The first step sizes it: one count-and-build
+    call (one GPU wait) into an index grown to the counts plus 5 % headroom.
+    Later steps build asynchronously into that index (msparse_build_index, no
+    host wait inside the step) and its overflow flag is read after the step
+    (check_index_step): the attention calls leave their outputs untouched on
+    an overflowed index, so such a step would be invalid, and the sets, hence
+    the sizes, are the same every step here.  Returns the counts."""
+    if "idx" not in state:
+        state["idx"] = ms.alloc_index(dims, 0, 0, 0, dev)
+        built, nnz = ms.index_count_build(dims, v_idx, s_idx, state["idx"], workspace=idx_ws)
+        if not built:
+            blk, col, vcol = nnz
+            state["idx"] = ms.alloc_index(dims, int(blk * 1.05) + 64, int(col * 1.05) + 64, vcol, dev)
+            built, nnz = ms.index_count_build(dims, v_idx, s_idx, state["idx"], workspace=idx_ws)
+            assert built
+        state["nnz_index"] = nnz
+        return nnz
+    ms.build_index(dims, v_idx, s_idx, state["idx"], workspace=idx_ws)
+    return state["nnz_index"]
+
+
+def check_index_step(state):
+    """After a step's final synchronisation: its index did not overflow and has
+    the counts the step reported."""
+    idx = state["idx"]
+    assert int(idx["overflow"].item()) == 0, "index overflowed: the step's attention outputs are invalid"
+    t = idx.tensors
+    got = (int(t["blk_ptr"][-1].item()), int(t["col_ptr"][-1].item()), int(t["vcol_ptr"][-1].item()))
+    assert got == tuple(state["nnz_index"]), (got, state["nnz_index"])
+
+
 def prefill_leg(ms, torch, wl, x, steps: int, warmup: int) -> dict:
     """Forward-only sparse prefill (inference): estimate -> index -> forward per
     layer, inputs resident in HBM, stage times from HIP events on the stream."""
@@ -305,11 +338,7 @@ def prefill_leg(ms, torch, wl, x, steps: int, warmup: int) -> dict:
         ms.estimate(dims, q, k, wl.last_q, wl.k_v, wl.k_s, v_idx, s_idx, workspace=est_ws)
         mark("estimate", 1)
         mark("index", 0)
-        blk, col, vcol = ms.index_count(dims, v_idx, s_idx, workspace=idx_ws)
-        if state.get("caps", (0, 0, 0))[0] < blk or state["caps"][1] < col or state["caps"][2] < vcol:
-            state["caps"] = (int(blk * 1.05) + 64, int(col * 1.05) + 64, vcol)
-            state["idx"] = ms.alloc_index(dims, *state["caps"], dev)
-        ms.build_index(dims, v_idx, s_idx, state["idx"], workspace=idx_ws)
+        blk, col, vcol = build_index_step(ms, dims, v_idx, s_idx, state, idx_ws, dev)
         mark("index", 1)
         mark("fwd", 0)
         ms.attn_fwd(dims, q, k, v, state["idx"], out=out, lse=lse, workspace=fwd_ws)
@@ -317,6 +346,7 @@ def prefill_leg(ms, torch, wl, x, steps: int, warmup: int) -> dict:
         state["nnz"] = (blk, col)
         if timed:
             torch.cuda.synchronize()
+            check_index_step(state)
             for s_, (a, b) in ev.items():
                 acc[s_] += a.elapsed_time(b)
 
@@ -484,12 +514,8 @@ def main():
             ms.estimate(dims, q, k, wl.last_q, wl.k_v, wl.k_s, v_idx, s_idx, workspace=est_ws)
             mark("estimate", 1)
             mark("index", 0)
-            blk, col, vcol = ms.index_count(dims, v_idx, s_idx, workspace=idx_ws)
-            if state.get("caps", (0, 0, 0))[0] < blk or state["caps"][1] < col or state["caps"][2] < vcol:
-                state["caps"] = (int(blk * 1.05) + 64, int(col * 1.05) + 64, vcol)
-                state["idx"] = ms.alloc_index(dims, *state["caps"], dev)
+            blk, col, vcol = build_index_step(ms, dims, v_idx, s_idx, state, idx_ws, dev)
             idx = state["idx"]
-            ms.build_index(dims, v_idx, s_idx, idx, workspace=idx_ws)
             mark("index", 1)
             mark("fwd", 0)
             ms.attn_fwd(dims, q, k, v, idx, out=out, lse=lse, out_f32=out32, workspace=fwd_ws)
@@ -501,6 +527,7 @@ def main():
             state["vcol"] = vcol
             if timed:
                 torch.cuda.synchronize()
+                check_index_step(state)
                 tot = 0.0
                 for s, (a, b) in ev.items():
                     t = a.elapsed_time(b)

@@ -230,6 +230,23 @@ MSPARSE_API msparse_status msparse_build_index(const msparse_dims* dims, const i
                                    const msparse_index* index, void* workspace, size_t workspace_bytes,
                                    void* stream);
 
+/* Count and build in one call: the work of msparse_index_count followed by
+ * msparse_build_index without running the vertical / diagonal preparation
+ * and the counts twice.  Waits for the GPU once (to read the counts back),
+ * then writes the exact element counts to blk_nnz, col_nnz, vcol_nnz.  When
+ * every capacity of `index` covers them, the lists are filled asynchronously
+ * on `stream` and MSPARSE_OK is returned; otherwise nothing is filled, the
+ * index's overflow flag is set (so the attention calls leave their outputs
+ * untouched) and MSPARSE_ERR_CAPACITY is returned with the needed sizes
+ * written back: grow the index and call again.  index->overflow must not be
+ * NULL.  Errors otherwise as msparse_build_index; the workspace is that of
+ * msparse_index_workspace. */
+MSPARSE_API msparse_status msparse_index_count_build(const msparse_dims* dims, const int32_t* v_idx, int32_t k_v,
+                                                     const int32_t* s_idx, int32_t k_s, const msparse_ring* ring,
+                                                     const msparse_index* index, int64_t* blk_nnz, int64_t* col_nnz,
+                                                     int64_t* vcol_nnz, void* workspace, size_t workspace_bytes,
+                                                     void* stream);
+
 /* msparse_build_index without a workspace argument, for callers that cannot
  * allocate device memory (code under HIP graph capture, tight serving loops,
  * harnesses that forbid hipMalloc).  Same arguments, results and errors as

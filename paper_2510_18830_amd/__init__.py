@@ -68,6 +68,8 @@ _SIGS = {
                                     c_vp, c_sz, c_vp]),
     "msparse_build_index": (c_i32, [_P(Dims), c_vp, c_i32, c_vp, c_i32, _P(Ring), _P(IndexStruct), c_vp, c_sz, c_vp]),
     "msparse_build_index_noalloc": (c_i32, [_P(Dims), c_vp, c_i32, c_vp, c_i32, _P(Ring), _P(IndexStruct), c_vp]),
+    "msparse_index_count_build": (c_i32, [_P(Dims), c_vp, c_i32, c_vp, c_i32, _P(Ring), _P(IndexStruct), _P(c_i64),
+                                          _P(c_i64), _P(c_i64), c_vp, c_sz, c_vp]),
     "msparse_attn_fwd_workspace": (c_sz, [_P(Dims)]),
     "msparse_attn_fwd": (c_i32, [_P(Dims), c_vp, c_vp, c_vp, _P(IndexStruct), c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]),
     "msparse_attn_fwd_merge": (c_i32, [_P(Dims), c_vp, c_vp, c_vp, _P(IndexStruct), c_vp, c_vp, c_vp, c_i32, c_vp,
@@ -248,6 +250,22 @@ def build_index(dims, v_idx, s_idx, index: SparseIndex, ring=None, workspace=Non
     _check(lib().msparse_build_index(ctypes.byref(dims), _p(v_idx), k_v, _p(s_idx), k_s, _ring_ptr(ring),
                                      ctypes.byref(index.struct), _p(workspace), workspace.numel(), _stream(stream)))
     return index
+
+
+def index_count_build(dims, v_idx, s_idx, index: SparseIndex, ring=None, workspace=None, stream=None):
+    """msparse_index_count_build (waits for the GPU once): returns (built, (blk_nnz, col_nnz, vcol_nnz));
+    built is False when a capacity of `index` was too small (nothing filled, its overflow flag set)."""
+    k_v, k_s = v_idx.shape[-1], s_idx.shape[-1]
+    if workspace is None:
+        workspace = _workspace(index_workspace_bytes(dims, k_v, k_s, ring), v_idx.device)
+    out = [c_i64(0), c_i64(0), c_i64(0)]
+    st = lib().msparse_index_count_build(ctypes.byref(dims), _p(v_idx), k_v, _p(s_idx), k_s, _ring_ptr(ring),
+                                         ctypes.byref(index.struct), *[ctypes.byref(x) for x in out],
+                                         _p(workspace), workspace.numel(), _stream(stream))
+    if st == -3:
+        return False, tuple(int(x.value) for x in out)
+    _check(st)
+    return True, tuple(int(x.value) for x in out)
 
 
 def build_index_noalloc(dims, v_idx, s_idx, index: SparseIndex, ring=None, stream=None):

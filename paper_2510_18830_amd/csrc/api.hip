@@ -152,6 +152,9 @@ IndexPlan plan_index(const msparse_dims* d, int32_t k_v, int32_t k_s, const Ring
     a.dlist = c.take<int32_t>(size_t(a.BH) * a.nb);
     a.dcnt = c.take<int32_t>(a.BH);
     a.dbits = c.take<uint32_t>(size_t(a.BH) * a.dwords);
+    a.dpre = c.take<int32_t>(size_t(a.BH) * (a.dwords + 1));
+    a.cumv = c.take<int32_t>(size_t(a.BH) * (a.nb + 1));
+    a.drun = c.take<int32_t>(a.BH);
     a.cnt_blk = c.take<int64_t>(size_t(a.BH) * a.nqb);
     a.cnt_col = c.take<int64_t>(size_t(a.BH) * a.nqb);
     a.cnt_kblk = c.take<int64_t>(size_t(a.BH) * a.nkb);
@@ -350,6 +353,63 @@ msparse_status msparse_build_index(const msparse_dims* dims, const int32_t* v_id
     if ((st = check_hip(launch_index_prep(a, s), s, "index prep"))) return st;   // also clears the overflow flag
     if ((st = check_hip(launch_index_count(a, s), s, "index count"))) return st;
     if ((st = check_hip(launch_index_scan(a, s), s, "index scan"))) return st;
+    return check_hip(launch_index_fill(a, s), s, "index fill");
+}
+
+msparse_status msparse_index_count_build(const msparse_dims* dims, const int32_t* v_idx, int32_t k_v,
+                                         const int32_t* s_idx, int32_t k_s, const msparse_ring* ring,
+                                         const msparse_index* index, int64_t* blk_nnz, int64_t* col_nnz,
+                                         int64_t* vcol_nnz, void* ws, size_t ws_bytes, void* stream) {
+    RingInfo ri;
+    msparse_status st = check_index_inputs(dims, v_idx, k_v, s_idx, k_s, ring, &ri);
+    if (st) return st;
+    if ((st = check_index_struct(dims, index, true))) return st;
+    if (!blk_nnz || !col_nnz || !vcol_nnz) return fail(MSPARSE_ERR_INVALID, "count outputs are NULL");
+    if (!index->overflow) return fail(MSPARSE_ERR_INVALID, "msparse_index_count_build needs an overflow flag");
+    if (index->world != ri.world)
+        return fail(MSPARSE_ERR_INVALID, "index world %d differs from the ring world %d", index->world, ri.world);
+    IndexPlan p = plan_index(dims, k_v, k_s, ri, ws, false);
+    if (!ws || ws_bytes < p.bytes)
+        return fail(MSPARSE_ERR_WORKSPACE, "index workspace %zu < %zu bytes", ws_bytes, p.bytes);
+    IndexArgs& a = p.a;
+    a.v_idx = v_idx;
+    a.s_idx = s_idx;
+    a.blk_ptr = index->blk_ptr;
+    a.col_ptr = index->col_ptr;
+    a.kblk_ptr = index->kblk_ptr;
+    a.vcol_ptr = index->vcol_ptr;
+    a.blk_idx = index->blk_idx;
+    a.blk_cap = index->blk_cap;
+    a.col_idx = index->col_idx;
+    a.col_cap = index->col_cap;
+    a.kblk_idx = index->kblk_idx;
+    a.vcol_idx = index->vcol_idx;
+    a.vcol_cap = index->vcol_cap;
+    a.diag_bits_out = index->diag_bits;
+    a.q_blk_global = index->q_blk_global;
+    a.k_blk_global = index->k_blk_global;
+    a.overflow = index->overflow;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if ((st = check_hip(launch_index_prep(a, s), s, "index prep"))) return st;   // also clears the overflow flag
+    if ((st = check_hip(launch_index_count(a, s), s, "index count"))) return st;
+    if ((st = check_hip(launch_index_scan(a, s), s, "index scan"))) return st;
+    int64_t tot[3];
+    const int64_t nq = int64_t(a.BH) * a.nqb;
+    hipError_t e = hipMemcpyAsync(&tot[0], a.blk_ptr + nq, 8, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(&tot[1], a.col_ptr + nq, 8, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipMemcpyAsync(&tot[2], a.vcol_ptr + a.BH, 8, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return fail(MSPARSE_ERR_HIP, "index count readback: %s", hipGetErrorString(e));
+    *blk_nnz = tot[0];
+    *col_nnz = tot[1];
+    *vcol_nnz = tot[2];
+    if (tot[0] > index->blk_cap || tot[1] > index->col_cap || tot[2] > index->vcol_cap) {
+        // the lists stay unfilled: flag the index so that no attention call walks it
+        if ((st = check_hip(launch_index_mark_overflow(a, s), s, "index overflow mark"))) return st;
+        return fail(MSPARSE_ERR_CAPACITY, "index needs (%lld, %lld, %lld) entries; capacities (%lld, %lld, %lld)",
+                    (long long)tot[0], (long long)tot[1], (long long)tot[2], (long long)index->blk_cap,
+                    (long long)index->col_cap, (long long)index->vcol_cap);
+    }
     return check_hip(launch_index_fill(a, s), s, "index fill");
 }
 

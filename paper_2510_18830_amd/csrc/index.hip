@@ -135,6 +135,41 @@ __global__ void __launch_bounds__(kPrepThreads) index_prep_kernel(IndexArgs a) {
         for (int w = w0; w < w1; ++w)
             for (uint32_t b = dsh[w]; b; b &= b - 1) out[pos++] = (w << 5) + __ffs(b) - 1;
         if (tid == 0) a.dcnt[bh] = total;
+        // prefix counts per word (dpre) and the run of selected diagonals from 0
+        int32_t* dp = a.dpre + int64_t(bh) * (a.dwords + 1);
+        int run = 0;
+        for (int w = w0; w < w1; ++w) {
+            dp[w] = pos - cnt + run;
+            run += __popc(dsh[w]);
+        }
+        if (tid == 0) {
+            dp[a.dwords] = total;
+            tmp[16] = a.nb;
+        }
+        __syncthreads();
+        for (int w = tid; w < a.dwords; w += kPrepThreads)
+            if (dsh[w] != 0xffffffffu) atomicMin(&tmp[16], (w << 5) + __ffs(~dsh[w]) - 1);
+        __syncthreads();
+        if (tid == 0) a.drun[bh] = min(tmp[16], a.nb);
+        __syncthreads();
+    }
+    // ---- verticals per global block, as prefix counts (cumv)
+    {
+        const int per = (a.nb + kPrepThreads - 1) / kPrepThreads;
+        const int j0 = tid * per, j1 = min(a.nb, j0 + per);
+        int cnt = 0;
+        for (int j = j0; j < j1; ++j)
+            cnt += __popc(__atomic_load_n(&vb[2 * j], __ATOMIC_RELAXED)) +
+                   __popc(__atomic_load_n(&vb[2 * j + 1], __ATOMIC_RELAXED));
+        int total = 0;
+        int pos = block_exclusive_scan(cnt, tmp, &total);
+        int32_t* cv = a.cumv + int64_t(bh) * (a.nb + 1);
+        for (int j = j0; j < j1; ++j) {
+            cv[j] = pos;
+            pos += __popc(__atomic_load_n(&vb[2 * j], __ATOMIC_RELAXED)) +
+                   __popc(__atomic_load_n(&vb[2 * j + 1], __ATOMIC_RELAXED));
+        }
+        if (tid == 0) cv[a.nb] = total;
     }
     if (bh == 0) {
         if (a.q_blk_global)
@@ -146,19 +181,120 @@ __global__ void __launch_bounds__(kPrepThreads) index_prep_kernel(IndexArgs a) {
 
 __device__ __forceinline__ bool dbit(const uint32_t* db, int32_t x) { return (db[x >> 5] >> (x & 31)) & 1u; }
 
+// Number of selected block-diagonals below x (0 <= x <= nb) from the per-word
+// prefix counts.
+__device__ __forceinline__ int32_t diag_below(const int32_t* dp, const uint32_t* db, int32_t x) {
+    const int w = x >> 5, b = x & 31;
+    return dp[w] + (b ? __popc(db[w] & ((1u << b) - 1u)) : 0);
+}
+
+// Sum over the lanes of a wavefront.
+__device__ __forceinline__ int64_t wave_sum64(int64_t v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+    return v;
+}
+
+// Whole-sequence index (one worker): closed forms from the prefix counts.
+// Query block i has the key blocks i - x for the diag_below(i + 1) selected x
+// <= i, and as columns the verticals of blocks j <= i - R (blocks i - R + 1 ..
+// i lie on the selected diagonals 0 .. R-1) minus those whose diagonal i - j
+// is selected; key block k has the query blocks k + x, x < nb - k.
+template <bool FILL>
+__device__ void whole_query_item(const IndexArgs& a, int64_t item, int bh, int32_t i, int lane) {
+    const int32_t* dl = a.dlist + int64_t(bh) * a.nb;
+    const uint32_t* db = a.dbits + int64_t(bh) * a.dwords;
+    const int32_t* dp = a.dpre + int64_t(bh) * (a.dwords + 1);
+    const int32_t* cv = a.cumv + int64_t(bh) * (a.nb + 1);
+    const int32_t nblk = diag_below(dp, db, i + 1);
+    const int32_t R = min(a.drun[bh], i + 1);
+    const int32_t nscan = cv[i - R + 1];   // verticals of blocks 0 .. i - R
+    if (!FILL) {
+        int64_t far = 0;   // verticals of blocks i - x, x selected, R <= x <= i
+        for (int j = R + lane; j < nblk; j += 64) {
+            const int32_t jb = i - dl[j];
+            far += cv[jb + 1] - cv[jb];
+        }
+        far = wave_sum64(far);
+        if (lane == 0) {
+            a.cnt_blk[item] = nblk;
+            a.cnt_col[item] = nscan - far;
+        }
+        return;
+    }
+    const int64_t bbase = a.blk_ptr[item];
+    if (a.blk_ptr[item + 1] > a.blk_cap) {
+        if (lane == 0 && a.overflow) atomicOr(a.overflow, 1);
+    } else {
+        for (int j = lane; j < nblk; j += 64) a.blk_idx[bbase + j] = i - dl[nblk - 1 - j];
+    }
+    const int64_t cbase = a.col_ptr[item];
+    if (a.col_ptr[item + 1] > a.col_cap) {
+        if (lane == 0 && a.overflow) atomicOr(a.overflow, 1);
+        return;
+    }
+    const int32_t* vl = a.vlist + int64_t(bh) * a.k_v;
+    int64_t n = 0;
+    for (int c0 = 0; c0 < nscan; c0 += 64) {
+        const int j = c0 + lane;
+        int32_t v = 0;
+        bool pred = false;
+        if (j < nscan) {
+            v = vl[j];
+            pred = !dbit(db, i - v / kBlock);
+        }
+        const uint64_t m = __ballot(pred);
+        if (pred) a.col_idx[cbase + n + __popcll(m & lanes_below())] = v;
+        n += __popcll(m);
+    }
+}
+
+template <bool FILL>
+__device__ void whole_key_item(const IndexArgs& a, int64_t it, int bh, int32_t k, int lane) {
+    const int32_t* dl = a.dlist + int64_t(bh) * a.nb;
+    const uint32_t* db = a.dbits + int64_t(bh) * a.dwords;
+    const int32_t* dp = a.dpre + int64_t(bh) * (a.dwords + 1);
+    const int32_t cnt = diag_below(dp, db, a.nb - k);
+    if (!FILL) {
+        if (lane == 0) a.cnt_kblk[it] = cnt;
+        return;
+    }
+    if (a.kblk_ptr[it + 1] > a.blk_cap) {
+        if (lane == 0 && a.overflow) atomicOr(a.overflow, 1);
+        return;
+    }
+    const int64_t base = a.kblk_ptr[it];
+    for (int j = lane; j < cnt; j += 64) a.kblk_idx[base + j] = k + dl[j];
+}
+
 // One wavefront walks the lists of one item.  FILL = false counts, FILL = true
 // writes the entries at the scanned offsets.
 template <bool FILL>
 __global__ void __launch_bounds__(64 * kItemWaves) index_items_kernel(IndexArgs a) {
-    const int64_t item = int64_t(blockIdx.x) * kItemWaves + (threadIdx.x >> 6);
+    int64_t item = int64_t(blockIdx.x) * kItemWaves + (threadIdx.x >> 6);
     const int lane = lane_id();
     const Layout L{a.world, a.nb, a.layout};
     const int64_t nq_items = int64_t(a.BH) * a.nqb;
     const int64_t nk_items = int64_t(a.BH) * a.nkb;
+    if (!FILL && a.world == 1 && item >= nq_items) {
+        // whole-sequence key-block counts are one lookup each: 64 per wave
+        const int64_t it = (item - nq_items) * 64 + lane;
+        if (it < nk_items) {
+            const int bh = int(it / a.nkb);
+            const int32_t k = int32_t(it % a.nkb);
+            a.cnt_kblk[it] = diag_below(a.dpre + int64_t(bh) * (a.dwords + 1), a.dbits + int64_t(bh) * a.dwords,
+                                        a.nb - k);
+        }
+        return;
+    }
 
     if (item < nq_items) {
         const int bh = int(item / a.nqb);
         const int lq = int(item % a.nqb);
+        if (a.world == 1) {
+            whole_query_item<FILL>(a, item, bh, lq, lane);
+            return;
+        }
         const int32_t qg = L.global(a.rank, lq);
         const int32_t* dl = a.dlist + int64_t(bh) * a.nb;
         const int dc = a.dcnt[bh];
@@ -223,6 +359,10 @@ __global__ void __launch_bounds__(64 * kItemWaves) index_items_kernel(IndexArgs 
         const int64_t it = item - nq_items;
         const int bh = int(it / a.nkb);
         const int lk = int(it % a.nkb);
+        if (a.world == 1) {
+            whole_key_item<FILL>(a, it, bh, lk, lane);
+            return;
+        }
         const int32_t kg = L.global(a.shard, lk);
         const int32_t* dl = a.dlist + int64_t(bh) * a.nb;
         const int dc = a.dcnt[bh];
@@ -510,7 +650,8 @@ hipError_t launch_index_prep(const IndexArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_index_count(const IndexArgs& a, hipStream_t s) {
-    const int64_t items = int64_t(a.BH) * (a.nqb + a.nkb);
+    const int64_t nk = int64_t(a.BH) * a.nkb;
+    const int64_t items = int64_t(a.BH) * a.nqb + (a.world == 1 ? (nk + 63) / 64 : nk);
     const int64_t grid = (items + kItemWaves - 1) / kItemWaves;
     { TraceScope _t("index_count", s); hipLaunchKernelGGL(index_items_kernel<false>, dim3(unsigned(grid)), dim3(64 * kItemWaves), 0, s, a); }
     return hipGetLastError();
@@ -522,6 +663,15 @@ hipError_t launch_index_scan(const IndexArgs& a, hipStream_t s) {
     { TraceScope _t("index_scan", s); hipLaunchKernelGGL(index_scan_sums_kernel, dim3(nblk, 4), dim3(kScanThreads), 0, s, a); }
     { TraceScope _t("index_scan", s); hipLaunchKernelGGL(index_scan_top_kernel, dim3(4), dim3(kScanThreads), 0, s, a); }
     { TraceScope _t("index_scan", s); hipLaunchKernelGGL(index_scan_fill_kernel, dim3(nblk, 4), dim3(kScanThreads), 0, s, a); }
+    return hipGetLastError();
+}
+
+__global__ void index_mark_overflow_kernel(int32_t* flag) {
+    if (threadIdx.x == 0) *flag = 1;
+}
+
+hipError_t launch_index_mark_overflow(const IndexArgs& a, hipStream_t s) {
+    hipLaunchKernelGGL(index_mark_overflow_kernel, dim3(1), dim3(64), 0, s, a.overflow);
     return hipGetLastError();
 }
 

@@ -25,6 +25,9 @@ struct IndexArgs {
     int32_t* dcnt;         // [BH]
     uint32_t* dbits;       // [BH, dwords]
     int32_t dwords;
+    int32_t* dpre;         // [BH, dwords + 1] selected block-diagonals in the words before each word
+    int32_t* cumv;         // [BH, nb + 1] verticals in the (global) blocks before each block
+    int32_t* drun;         // [BH] R: block-diagonals 0 .. R-1 are all selected, R is not
     int64_t* cnt_blk;      // [BH*nqb]
     int64_t* cnt_col;      // [BH*nqb]
     int64_t* cnt_kblk;     // [BH*nkb]
@@ -60,6 +63,8 @@ hipError_t launch_ring_work(const IndexArgs& a, int32_t world, int32_t layout, i
 hipError_t launch_index_count(const IndexArgs& a, hipStream_t s);
 hipError_t launch_index_scan(const IndexArgs& a, hipStream_t s);
 hipError_t launch_index_fill(const IndexArgs& a, hipStream_t s);
+// *a.overflow = 1 (one thread; the lists of the index are not filled)
+hipError_t launch_index_mark_overflow(const IndexArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------- attention
 struct AttnArgs {

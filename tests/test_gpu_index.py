@@ -217,3 +217,29 @@ def test_index_build_graph_replay(gpu):
         torch.cuda.synchronize()
         _compare(gpu_csr(idx), ref)
         assert int(idx["overflow"].item()) == 0
+
+
+@pytest.mark.parametrize("W,r,t,layout", [(1, 0, 0, "striped"), (4, 2, 1, "zigzag")])
+def test_index_count_build_matches_separate_calls(gpu, W, r, t, layout):
+    # one count-and-build call: exact counts written back, the same arrays as
+    # msparse_index_count + msparse_build_index; too small a capacity builds
+    # nothing, flags the index and reports the needed sizes
+    rng = np.random.default_rng(90 + W)
+    v, s = _indices(rng, 1, 3, 16384, 200, 900)
+    ring = ms.make_ring(W, r, t, layout)
+    dims = ms.make_dims(1, 16384 // W, 3, 1, 128)
+    tv, ts = torch.from_numpy(v).to(gpu), torch.from_numpy(s).to(gpu)
+    ref = ms.make_index(dims, tv, ts, ring)
+    need = ms.index_count(dims, tv, ts, ring)
+    small = ms.alloc_index(dims, need[0] - 1, need[1], need[2], gpu, W)
+    built, got_need = ms.index_count_build(dims, tv, ts, small, ring)
+    torch.cuda.synchronize()
+    assert not built and got_need == need
+    assert int(small["overflow"].item()) == 1
+    big = ms.alloc_index(dims, need[0], need[1], need[2], gpu, W)
+    big["overflow"].fill_(1)
+    built, got_need = ms.index_count_build(dims, tv, ts, big, ring)
+    torch.cuda.synchronize()
+    assert built and got_need == need
+    assert int(big["overflow"].item()) == 0
+    _compare(gpu_csr(big), {k_: v_ for k_, v_ in gpu_csr(ref).items()})
