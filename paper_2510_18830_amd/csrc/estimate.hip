@@ -37,10 +37,11 @@ namespace {
 
 constexpr int kThreads = 128;
 constexpr int kChunkTiles = 16;   // 1024 keys per workgroup
+constexpr int kMaxGroupWaves = 8;  // query heads per round of the K passes (two waves each)
 constexpr float kLog2e = 1.4426950408889634f;
 
 struct EstLayout {
-    size_t part_max, part_sum, row_lse, diag_part, sel_cnt, sel_mass, sel_gt, sel_eq, sel_state, bytes;
+    size_t part_max, part_sum, row_lse, bnd_part, sel_cnt, sel_mass, sel_gt, sel_eq, sel_state, bytes;
 };
 
 constexpr int kSliceLen = 16384;   // scores per selection slice
@@ -67,8 +68,8 @@ EstLayout est_layout(int64_t BH, int32_t N) {
     off = align256(off + size_t(BH) * nchunk * kBlock * 4);
     L.row_lse = off;
     off = align256(off + size_t(BH) * kBlock * 4);
-    L.diag_part = off;
-    off = align256(off + size_t(BH) * nb * 128 * 4);
+    L.bnd_part = off;
+    off = align256(off + size_t(BH) * nchunk * kBlock * 4);
     const int64_t NL = 2 * BH, ns = (N + kSliceLen - 1) / kSliceLen;
     L.sel_cnt = off;
     off = align256(off + size_t(NL) * ns * 256 * 4);
@@ -84,191 +85,288 @@ EstLayout est_layout(int64_t BH, int32_t N) {
     return L;
 }
 
-template <int D>
-struct Pass1Lds {
-    uint16_t k[TileLds<D>::kRowElems];
-};
+// ---------------------------------------------------------------- passes over K
+// One workgroup per (batch, KV head, chunk of kChunkTiles key tiles) and
+// 2 NH waves: waves 2 w and 2 w + 1 serve query rows 0-31 and 32-63 of the
+// query heads w, w + NH, ... of the KV group (one round per NH heads), so each
+// K tile is read from memory once per group and staged once (direct
+// global->LDS loads, double buffer) for all of its heads.  A wave holds its
+// 32 query rows as one MFMA operand (qreg); a 64-key tile is two 32-key halves.
 
-// pass 1: per-row (max, sum exp2) over one chunk of keys, log2 domain
+// (batch x KV head, chunk) of workgroup t: XCD-chunked, chunks of one KV head
+// adjacent.
+__device__ __forceinline__ void group_chunk_of(int64_t t, int BK, int nchunk, int& bk, int& chunk) {
+    const int64_t u = xcd_chunk(t, int64_t(BK) * nchunk);
+    bk = int(u / nchunk);
+    chunk = int(u % nchunk);
+}
+
 template <int D>
-__global__ void __launch_bounds__(kThreads) est_pass1_kernel(EstArgs a) {
+__device__ __forceinline__ void load_qlast(const EstArgs& a, int bh, int rb, int lane, u32x4* qreg) {
+    const int h = lane >> 5, l32 = lane & 31;
+    const uint16_t* qp = a.q + (int64_t(bh) * a.N + a.N - kBlock + 32 * rb + l32) * D;
+#pragma unroll
+    for (int s = 0; s < D / 16; ++s) qreg[s] = *reinterpret_cast<const u32x4*>(qp + 16 * s + 8 * h);
+}
+
+// pass 1: per-row (max, sum exp2) of the chunk's keys, log2 domain.
+// S^T = K Q^T puts one query row per lane (keys in the accumulator).
+template <int D, int NH>
+__global__ void __launch_bounds__(128 * NH) est_stats_kernel(EstArgs a) {
     constexpr int KD = D / 16;
-    __shared__ Pass1Lds<D> sm;
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, l32 = lane & 31;
-    const int nb = a.N / kBlock;
-    // KV-group-major order, XCD-chunked: the group's heads read each K chunk
-    // together from one L2
-    int bh, chunk;
-    query_tile_of(blockIdx.x, a.B, a.Hq, a.Hkv, a.nchunk, bh, chunk);
-    const int b = bh / a.Hq, hq = bh % a.Hq, hk = hq / (a.Hq / a.Hkv);
-    const int row = 32 * w + l32;   // in the last block
-    const uint16_t* qp = a.q + (int64_t(bh) * a.N + a.N - kBlock + row) * D;
-    const uint16_t* kp = a.k + (int64_t(b) * a.Hkv + hk) * int64_t(a.N) * D;
-    u32x4 qreg[KD];
-#pragma unroll
-    for (int s = 0; s < KD; ++s) qreg[s] = *reinterpret_cast<const u32x4*>(qp + 16 * s + 8 * h);
-    const float c2 = a.scale * kLog2e;
-    float m = -INFINITY, l = 0.f;
+    constexpr int KE = DmaTile<D, kRowPad>::kElems;
+    constexpr int NW = 2 * NH;
+    __shared__ uint16_t kt0[KE], kt1[KE];
+    const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, l32 = lane & 31;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6), rb = w & 1;
+    const int nb = a.N / kBlock, G = a.Hq / a.Hkv;
+    int bk, chunk;
+    group_chunk_of(blockIdx.x, a.B * a.Hkv, a.nchunk, bk, chunk);
+    const int b = bk / a.Hkv, g = bk % a.Hkv;
+    const uint16_t* __restrict__ kp = a.k + int64_t(bk) * a.N * D;
     const int j0 = chunk * kChunkTiles, j1 = min(nb, j0 + kChunkTiles);
-    for (int j = j0; j < j1; ++j) {
-        stage_rows<D, kThreads>(sm.k, kp, ContiguousRows{int64_t(j) * kBlock}, tid);
+    const float c2 = a.scale * kLog2e;
+    const int row = 32 * rb + l32;
+    for (int r0 = 0; r0 < G; r0 += NH) {
+        const bool act = r0 + (w >> 1) < G;
+        const int bh = b * a.Hq + g * G + (act ? r0 + (w >> 1) : 0);
+        u32x4 qreg[KD];
+        load_qlast<D>(a, bh, rb, lane, qreg);
+        float m = -INFINITY, l = 0.f;
+        dma_rows<D, kRowPad, NW>(kt0, kp, ContiguousRows{int64_t(j0) * kBlock}, w, lane);
+        wait_vmem();
         __syncthreads();
-        f32x16 acc[2];
+        for (int j = j0; j < j1; ++j) {
+            const uint16_t* cur = ((j - j0) & 1) ? kt1 : kt0;
+            if (j + 1 < j1)
+                dma_rows<D, kRowPad, NW>(((j - j0) & 1) ? kt0 : kt1, kp, ContiguousRows{int64_t(j + 1) * kBlock}, w,
+                                         lane);
+            if (act) {
+                f32x16 acc[2] = {f32x16{}, f32x16{}};
 #pragma unroll
-        for (int c = 0; c < 2; ++c) {
-            acc[c] = f32x16{};
-            const uint16_t* krow = sm.k + (32 * c + l32) * TileLds<D>::kRowStride + 8 * h;
+                for (int s = 0; s < KD; ++s)
 #pragma unroll
-            for (int s = 0; s < KD; ++s) acc[c] = mfma32(lds_read16(krow + 16 * s), qreg[s], acc[c]);
-        }
-        const bool last = j == nb - 1;
-        float mx = -INFINITY;
+                    for (int kh = 0; kh < 2; ++kh)
+                        acc[kh] = mfma32(dma_read16<D, kRowPad>(cur, 32 * kh + l32, h + 2 * s), qreg[s], acc[kh]);
+                if (j == nb - 1) {   // keys after the row are masked (causal), only in the last tile
+                    keep_branch();
 #pragma unroll
-        for (int c = 0; c < 2; ++c)
+                    for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int key = 32 * c + 8 * (r >> 2) + 4 * h + (r & 3);
-                float x = acc[c][r] * c2;
-                if (last && key > row) x = -INFINITY;
-                acc[c][r] = x;
-                mx = fmaxf(mx, x);
+                        for (int i = 0; i < 16; ++i)
+                            if (32 * kh + 8 * (i >> 2) + 4 * h + (i & 3) > row) acc[kh][i] = -INFINITY;
+                }
+                float mx = -INFINITY;
+#pragma unroll
+                for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) mx = fmaxf(mx, acc[kh][i]);
+                const float mn = fmaxf(m, mx * c2);
+                if (mn != -INFINITY) {
+                    float sum = 0.f;
+#pragma unroll
+                    for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) sum += fast_exp2(__builtin_fmaf(acc[kh][i], c2, -mn));
+                    l = (m == -INFINITY ? 0.f : l * fast_exp2(m - mn)) + sum;
+                    m = mn;
+                }
             }
-        const float mn = fmaxf(m, mx);   // finite: every row sees key 0
-        float s = 0.f;
-#pragma unroll
-        for (int c = 0; c < 2; ++c)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) s += fast_exp2(acc[c][r] - mn);
-        l = l * fast_exp2(m - mn) + s;
-        m = mn;
-        __syncthreads();
-    }
-    // combine the two lane halves (same row)
-    const float mo = __shfl_xor(m, 32), lo = __shfl_xor(l, 32);
-    const float mm = fmaxf(m, mo);
-    const float ll = (m == -INFINITY ? 0.f : l * fast_exp2(m - mm)) + (mo == -INFINITY ? 0.f : lo * fast_exp2(mo - mm));
-    if (h == 0) {
-        const int64_t o = (int64_t(bh) * a.nchunk + chunk) * kBlock + row;
-        a.part_max[o] = mm;
-        a.part_sum[o] = ll;
+            wait_vmem();
+            __syncthreads();
+        }
+        if (act) {   // the lane pair l, l ^ 32 holds one row
+            const float mo = __shfl_xor(m, 32), lo = __shfl_xor(l, 32);
+            const float mm = fmaxf(m, mo);
+            const float ll = (m == -INFINITY ? 0.f : l * fast_exp2(m - mm)) + (mo == -INFINITY ? 0.f : lo * fast_exp2(mo - mm));
+            if (h == 0) {
+                const int64_t o = (int64_t(bh) * a.nchunk + chunk) * kBlock + row;
+                a.part_max[o] = mm;
+                a.part_sum[o] = ll;
+            }
+        }
     }
 }
 
-// One workgroup per head: thread (r, j) reduces chunks j, j + 16, ... of row
-// r; the 16 partials of a row are combined in a fixed order.
-constexpr int kCombineSplit = 16;
-__global__ void __launch_bounds__(64 * kCombineSplit) est_combine_kernel(EstArgs a) {
-    __shared__ float pm_s[kCombineSplit][64], ps_s[kCombineSplit][64];
-    const int bh = blockIdx.x, r = threadIdx.x & 63, j = threadIdx.x >> 6;
+// One workgroup per (head, 16 rows): 64 threads per row combine the chunk
+// partials in a fixed order (per-thread strided runs, then a fixed tree).
+constexpr int kCombineRows = 16, kCombineSplit = 64;
+__global__ void __launch_bounds__(kCombineRows * kCombineSplit) est_combine_kernel(EstArgs a) {
+    __shared__ float pm_s[kCombineRows][kCombineSplit], ps_s[kCombineRows][kCombineSplit];
+    const int bh = blockIdx.x / (kBlock / kCombineRows);
+    const int rr = threadIdx.x / kCombineSplit, j = threadIdx.x % kCombineSplit;
+    const int r = (blockIdx.x % (kBlock / kCombineRows)) * kCombineRows + rr;
     float M = -INFINITY;
-    for (int c = j; c < a.nchunk; c += kCombineSplit) M = fmaxf(M, a.part_max[(int64_t(bh) * a.nchunk + c) * kBlock + r]);
+    for (int c = j; c < a.nchunk; c += kCombineSplit)
+        M = fmaxf(M, a.part_max[(int64_t(bh) * a.nchunk + c) * kBlock + r]);
     float S = 0.f;
     for (int c = j; c < a.nchunk; c += kCombineSplit) {
         const int64_t o = (int64_t(bh) * a.nchunk + c) * kBlock + r;
         const float pm = a.part_max[o];
         if (pm != -INFINITY) S += a.part_sum[o] * fast_exp2(pm - M);
     }
-    pm_s[j][r] = M;
-    ps_s[j][r] = S;
+    pm_s[rr][j] = M;
+    ps_s[rr][j] = S;
     __syncthreads();
     if (j == 0) {
         float MM = -INFINITY;
-        for (int t = 0; t < kCombineSplit; ++t) MM = fmaxf(MM, pm_s[t][r]);
+        for (int t = 0; t < kCombineSplit; ++t) MM = fmaxf(MM, pm_s[rr][t]);
         float SS = 0.f;
         for (int t = 0; t < kCombineSplit; ++t)
-            if (pm_s[t][r] != -INFINITY) SS += ps_s[t][r] * fast_exp2(pm_s[t][r] - MM);
+            if (pm_s[rr][t] != -INFINITY) SS += ps_s[rr][t] * fast_exp2(pm_s[rr][t] - MM);
         a.row_lse[bh * kBlock + r] = MM + fast_log2(SS);
     }
 }
 
-template <int D>
-struct Pass2Lds {
-    uint16_t k[TileLds<D>::kRowElems];
-    float p[64][65];
-    float col[2][64];
-};
+// Orders the LDS accesses of one wave around a wave-private scratch region.
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
 
-template <int D>
-__global__ void __launch_bounds__(kThreads) est_pass2_kernel(EstArgs a) {
+// pass 2: P = exp2(S - lse) per tile (S = Q K^T, one key per lane), the
+// vertical scores (column sums over the 64 rows) and the slash scores.
+// Diagonal sums: each 32x32 block (rb, kh) of P goes to the wave's LDS
+// scratch; lane e (< 63) sums the block's diagonal r - c = e - 31, which is
+// diagonal t = 32 (rb - kh) + e + 32 of the tile (t = r - c + 63 over the
+// tile's rows r and keys c).  The two waves of a head leave their column and
+// diagonal partials in LDS; after a barrier the row-0 wave adds them in a
+// fixed order and writes the scores.  The slash scores are
+//   s_score[64 D + e] = T_j[e + 63] + T_{j-1}[e - 1]   (D = nb - 1 - j)
+// since the tile j holds offsets delta = 64 (nb - 1 - j) + r - c.  The lower
+// part T_{j-1}[e - 1] of a chunk's first tile comes from the previous chunk,
+// which leaves it in bnd_part; est_bound_kernel adds it.
+template <int D, int NH>
+__global__ void __launch_bounds__(128 * NH) est_scores_kernel(EstArgs a) {
     constexpr int KD = D / 16;
-    __shared__ Pass2Lds<D> sm;
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, h = lane >> 5, l32 = lane & 31;
-    const int nb = a.N / kBlock;
-    int bh, chunk;   // order as in pass 1
-    query_tile_of(blockIdx.x, a.B, a.Hq, a.Hkv, a.nchunk, bh, chunk);
-    const int b = bh / a.Hq, hq = bh % a.Hq, hk = hq / (a.Hq / a.Hkv);
-    // A operand: this wave's 32 query rows
-    const uint16_t* qp = a.q + (int64_t(bh) * a.N + a.N - kBlock + 32 * w + l32) * D;
-    const uint16_t* kp = a.k + (int64_t(b) * a.Hkv + hk) * int64_t(a.N) * D;
-    u32x4 qreg[KD];
-#pragma unroll
-    for (int s = 0; s < KD; ++s) qreg[s] = *reinterpret_cast<const u32x4*>(qp + 16 * s + 8 * h);
-    // accumulator element r covers row 32 w + 8 (r/4) + 4 h + r%4
-    float lse2[16];
-    bool valid[16];
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-        const int row = 32 * w + 8 * (r >> 2) + 4 * h + (r & 3);
-        lse2[r] = a.row_lse[bh * kBlock + row];
-        valid[r] = row >= kBlock - a.L;
-    }
-    const float c2 = a.scale * kLog2e;
+    constexpr int KE = DmaTile<D, kRowPad>::kElems;
+    constexpr int NW = 2 * NH;
+    constexpr int SS = 33;   // scratch row stride (floats)
+    __shared__ uint16_t kt0[KE], kt1[KE];
+    __shared__ float scr[NW][32 * SS];
+    // per head: column partials [rb][64], diagonal partials A, B0, B1, C [64],
+    // the previous tile's diagonals 0..63, and the row lse of the head (log2)
+    __shared__ float colp[NH][2][kBlock], diagp[NH][4][kBlock], tprev[NH][kBlock];
+    __shared__ __attribute__((aligned(16))) float lrow[NH][kBlock];
+    const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, l32 = lane & 31;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6), rb = w & 1, hw = w >> 1;
+    const int nb = a.N / kBlock, G = a.Hq / a.Hkv;
+    int bk, chunk;
+    group_chunk_of(blockIdx.x, a.B * a.Hkv, a.nchunk, bk, chunk);
+    const int b = bk / a.Hkv, g = bk % a.Hkv;
+    const uint16_t* __restrict__ kp = a.k + int64_t(bk) * a.N * D;
     const int j0 = chunk * kChunkTiles, j1 = min(nb, j0 + kChunkTiles);
-    for (int j = j0; j < j1; ++j) {
-        stage_rows<D, kThreads>(sm.k, kp, ContiguousRows{int64_t(j) * kBlock}, tid);
+    const float c2 = a.scale * kLog2e;
+    float* sc = scr[w];
+    const int e = lane;
+    for (int r0 = 0; r0 < G; r0 += NH) {
+        const bool act = r0 + hw < G;
+        const int bh = b * a.Hq + g * G + (act ? r0 + hw : 0);
+        u32x4 qreg[KD];
+        load_qlast<D>(a, bh, rb, lane, qreg);
+        // rows before the last L contribute nothing
+        if (rb == 0) lrow[hw][lane] = lane >= kBlock - a.L ? a.row_lse[bh * kBlock + lane] : INFINITY;
+        float* vs = a.v_score + int64_t(bh) * a.N;
+        float* ss = a.s_score + int64_t(bh) * a.N;
+        dma_rows<D, kRowPad, NW>(kt0, kp, ContiguousRows{int64_t(j0) * kBlock}, w, lane);
+        wait_vmem();
         __syncthreads();
-        const bool last = j == nb - 1;
+        for (int j = j0; j < j1; ++j) {
+            const uint16_t* cur = ((j - j0) & 1) ? kt1 : kt0;
+            if (j + 1 < j1)
+                dma_rows<D, kRowPad, NW>(((j - j0) & 1) ? kt0 : kt1, kp, ContiguousRows{int64_t(j + 1) * kBlock}, w,
+                                         lane);
+            if (act) {
+                const bool last = j == nb - 1;
 #pragma unroll
-        for (int c = 0; c < 2; ++c) {
-            f32x16 acc = f32x16{};
-            const uint16_t* krow = sm.k + (32 * c + l32) * TileLds<D>::kRowStride + 8 * h;
+                for (int kh = 0; kh < 2; ++kh) {
+                    f32x16 acc = f32x16{};
 #pragma unroll
-            for (int s = 0; s < KD; ++s) acc = mfma32(qreg[s], lds_read16(krow + 16 * s), acc);
-            const int key = 32 * c + l32;
-            float cs = 0.f;
+                    for (int s = 0; s < KD; ++s)
+                        acc = mfma32(qreg[s], dma_read16<D, kRowPad>(cur, 32 * kh + l32, h + 2 * s), acc);
+                    // accumulator element i covers row 32 rb + 8 (i/4) + 4 h + i%4, key 32 kh + l32
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int row = 32 * w + 8 * (r >> 2) + 4 * h + (r & 3);
-                float p = fast_exp2(acc[r] * c2 - lse2[r]);
-                if (!valid[r] || (last && key > row)) p = 0.f;
-                sm.p[row][key] = p;
-                cs += p;
+                    for (int q4 = 0; q4 < 4; ++q4) {
+                        const f32x4 l4 = *reinterpret_cast<const f32x4*>(&lrow[hw][32 * rb + 8 * q4 + 4 * h]);
+#pragma unroll
+                        for (int e4 = 0; e4 < 4; ++e4)
+                            acc[4 * q4 + e4] = fast_exp2(__builtin_fmaf(acc[4 * q4 + e4], c2, -l4[e4]));
+                    }
+                    if (last) {   // causal mask of the last tile: key > row
+                        keep_branch();
+#pragma unroll
+                        for (int i = 0; i < 16; ++i)
+                            if (32 * kh + l32 > 32 * rb + 8 * (i >> 2) + 4 * h + (i & 3)) acc[i] = 0.f;
+                    }
+                    float cs = 0.f;
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) {
+                        cs += acc[i];
+                        sc[(8 * (i >> 2) + 4 * h + (i & 3)) * SS + l32] = acc[i];
+                    }
+                    cs += __shfl_xor(cs, 32);
+                    if (h == 0) colp[hw][rb][32 * kh + l32] = cs;
+                    wave_lds_sync();
+                    // diagonal r - c = e - 31 of the block (lanes 0..62)
+                    float d4[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 1
+                    for (int r0 = 0; r0 < 32; r0 += 8) {
+#pragma unroll
+                        for (int k = 0; k < 8; ++k) {
+                            const int c = r0 + k - e + 31;
+                            const float v = sc[(r0 + k) * SS + (c & 31)];
+                            d4[k & 3] += (c >= 0 && c < 32) ? v : 0.f;
+                        }
+                    }
+                    const float dsum = e < 63 ? (d4[0] + d4[1]) + (d4[2] + d4[3]) : 0.f;
+                    // block kind: rb < kh -> A (t = e), rb == kh -> B (t = e + 32), rb > kh -> C (t = e + 64)
+                    diagp[hw][rb < kh ? 0 : (rb > kh ? 3 : 1 + rb)][e] = dsum;
+                    wave_lds_sync();
+                }
             }
-            cs += __shfl_xor(cs, 32);
-            if (h == 0) sm.col[w][key] = cs;
-        }
-        __syncthreads();
-        if (tid < 64) a.v_score[int64_t(bh) * a.N + int64_t(j) * kBlock + tid] = sm.col[0][tid] + sm.col[1][tid];
-        if (tid < 127) {
-            // delta_local = r - c = tid - 63: a fixed 64-step walk, masked at
-            // the ends, four accumulators (the reads pipeline; neighbouring
-            // threads read neighbouring words)
-            const int dl = tid - 63;
-            float s4[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int r = 0; r < 64; ++r) {
-                const int c = r - dl;
-                const float v = sm.p[r][c & 63];
-                s4[r & 3] += (c >= 0 && c < 64) ? v : 0.f;
+            __syncthreads();
+            if (act && rb == 0) {
+                // vertical scores: rows 0-31 + rows 32-63
+                vs[int64_t(j) * kBlock + e] = colp[hw][0][e] + colp[hw][1][e];
+                // tile diagonals: tlo = T[e] (e < 64), thi = T[64 + e] (e < 63)
+                const float* dp = &diagp[hw][0][0];
+                const float tlo = dp[e] + (e >= 32 ? dp[kBlock + e - 32] + dp[2 * kBlock + e - 32] : 0.f);
+                const float thi = (e < 32 ? dp[kBlock + e + 32] + dp[2 * kBlock + e + 32] : 0.f) + dp[3 * kBlock + e];
+                sc[e] = tlo;
+                sc[kBlock + e] = thi;
+                wave_lds_sync();
+                // s_score of block-diagonal D = nb - 1 - j, offset e: T_j[e + 63] + T_{j-1}[e - 1]
+                const float up = e == 0 ? sc[63] : sc[kBlock + e - 1];
+                const float low = (e >= 1 && j > j0) ? tprev[hw][e - 1] : 0.f;
+                ss[int64_t(nb - 1 - j) * kBlock + e] = (e >= 1 && j > j0) ? up + low : up;
+                wave_lds_sync();
+                tprev[hw][e] = tlo;
+                wave_lds_sync();
             }
-            a.diag_part[(int64_t(bh) * nb + j) * 128 + tid] = (s4[0] + s4[1]) + (s4[2] + s4[3]);
+            wait_vmem();
+            __syncthreads();
         }
+        // the lower part of the chunk's last tile belongs to the next chunk's first block-diagonal
+        if (act && rb == 0 && j1 < nb)
+            a.bnd_part[(int64_t(bh) * a.nchunk + chunk) * kBlock + lane] = lane >= 1 ? tprev[hw][lane - 1] : 0.f;
         __syncthreads();
     }
 }
 
-// s_score[64 D + e] = tile(j = nb-1-D)[e + 63] + tile(j - 1)[e - 1]  (e >= 1)
-__global__ void __launch_bounds__(256) est_diag_kernel(EstArgs a) {
+// s_score of the first block-diagonal of every chunk after the first: add the
+// lower part that the previous chunk left (up + low, as inside a chunk).
+__global__ void __launch_bounds__(256) est_bound_kernel(EstArgs a) {
     const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    const int64_t per = int64_t(a.nchunk - 1) * kBlock;   // chunks 1 .. nchunk - 1
+    if (i >= int64_t(a.B) * a.Hq * per) return;
+    const int64_t bh = i / per;
+    const int c = int((i % per) / kBlock) + 1, e = int(i % kBlock);
+    if (e == 0) return;
     const int nb = a.N / kBlock;
-    if (i >= int64_t(a.B) * a.Hq * a.N) return;
-    const int64_t bh = i / a.N;
-    const int dlt = int(i % a.N);
-    const int Dg = dlt / kBlock, e = dlt % kBlock;
-    const int j = nb - 1 - Dg;
-    float s = a.diag_part[(bh * nb + j) * 128 + e + 63];
-    if (e >= 1 && j >= 1) s += a.diag_part[(bh * nb + j - 1) * 128 + e - 1];
-    a.s_score[i] = s;
+    const int j0 = c * kChunkTiles;
+    const int64_t o = int64_t(bh) * a.N + int64_t(nb - 1 - j0) * kBlock + e;
+    a.s_score[o] = a.s_score[o] + a.bnd_part[(bh * a.nchunk + c - 1) * kBlock + e];
 }
 
 // ---------------------------------------------------------------- top-k / top-p
@@ -627,15 +725,35 @@ hipError_t launch_select(const EstArgs& a, hipStream_t s) {
     return hipGetLastError();
 }
 
+template <int D, int NW>
+hipError_t launch_passes(const EstArgs& a, hipStream_t s) {
+    const int BH = a.B * a.Hq;
+    const unsigned grid = unsigned(a.B * a.Hkv * a.nchunk);
+    { TraceScope _t("est_pass1", s); hipLaunchKernelGGL((est_stats_kernel<D, NW>), dim3(grid), dim3(128 * NW), 0, s, a); }
+    { TraceScope _t("est_combine", s); hipLaunchKernelGGL(est_combine_kernel, dim3(BH * (kBlock / kCombineRows)), dim3(kCombineRows * kCombineSplit), 0, s, a); }
+    { TraceScope _t("est_pass2", s); hipLaunchKernelGGL((est_scores_kernel<D, NW>), dim3(grid), dim3(128 * NW), 0, s, a); }
+    if (a.nchunk > 1) {
+        const int64_t n = int64_t(BH) * (a.nchunk - 1) * kBlock;
+        TraceScope _t("est_bound", s);
+        hipLaunchKernelGGL(est_bound_kernel, dim3(unsigned((n + 255) / 256)), dim3(256), 0, s, a);
+    }
+    return hipGetLastError();
+}
+
 template <int D>
 hipError_t launch_d(const EstArgs& a, hipStream_t s) {
-    const int BH = a.B * a.Hq;
-    { TraceScope _t("est_pass1", s); hipLaunchKernelGGL(est_pass1_kernel<D>, dim3(BH * a.nchunk), dim3(kThreads), 0, s, a); }
-    { TraceScope _t("est_combine", s); hipLaunchKernelGGL(est_combine_kernel, dim3(BH), dim3(64 * kCombineSplit), 0, s, a); }
-    { TraceScope _t("est_pass2", s); hipLaunchKernelGGL(est_pass2_kernel<D>, dim3(BH * a.nchunk), dim3(kThreads), 0, s, a); }
-    const int64_t n = int64_t(BH) * a.N;
-    { TraceScope _t("est_diag", s); hipLaunchKernelGGL(est_diag_kernel, dim3(unsigned((n + 255) / 256)), dim3(256), 0, s, a); }
-    if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+    hipError_t e;
+    switch (std::min(a.Hq / a.Hkv, kMaxGroupWaves)) {   // two waves per query head of the KV group
+        case 1: e = launch_passes<D, 1>(a, s); break;
+        case 2: e = launch_passes<D, 2>(a, s); break;
+        case 3: e = launch_passes<D, 3>(a, s); break;
+        case 4: e = launch_passes<D, 4>(a, s); break;
+        case 5: e = launch_passes<D, 5>(a, s); break;
+        case 6: e = launch_passes<D, 6>(a, s); break;
+        case 7: e = launch_passes<D, 7>(a, s); break;
+        default: e = launch_passes<D, 8>(a, s); break;
+    }
+    if (e != hipSuccess) return e;
     return launch_select(a, s);
 }
 
@@ -652,7 +770,7 @@ void est_carve(EstArgs& a, char* base) {
     a.part_max = reinterpret_cast<float*>(base + L.part_max);
     a.part_sum = reinterpret_cast<float*>(base + L.part_sum);
     a.row_lse = reinterpret_cast<float*>(base + L.row_lse);
-    a.diag_part = reinterpret_cast<float*>(base + L.diag_part);
+    a.bnd_part = reinterpret_cast<float*>(base + L.bnd_part);
     a.nslice = (a.N + kSliceLen - 1) / kSliceLen;
     a.sel_cnt = reinterpret_cast<uint32_t*>(base + L.sel_cnt);
     a.sel_mass = reinterpret_cast<uint64_t*>(base + L.sel_mass);

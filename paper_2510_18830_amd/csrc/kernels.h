@@ -185,7 +185,7 @@ struct EstArgs {
     float* part_max;    // [B*Hq, nchunk, 64]
     float* part_sum;    // [B*Hq, nchunk, 64]
     float* row_lse;     // [B*Hq, 64] (log2 domain)
-    float* diag_part;   // [B*Hq, N/64, 128]
+    float* bnd_part;    // [B*Hq, nchunk, 64]: lower diagonal part of each chunk's last tile
     int32_t nchunk;
     // selection (top-k / top-p) over 2 B Hq lists of N scores cut into nslice
     // slices: per-slice histograms and compaction counts, per-list state
