@@ -681,6 +681,258 @@ __global__ void __launch_bounds__(kKvThreads) __attribute__((amdgpu_waves_per_eu
         }
 }
 
+// ------------------------------------------------------------------ dK / dV, two waves per SIMD
+// Row-split variant of the key-major pass (head dim 128): eight waves per
+// workgroup, wave (blk, kh, rh) holds the 32 keys 32 kh .. 32 kh + 31 of key
+// block blk of the pair and takes rows 32 rh .. 32 rh + 31 of every query
+// tile.  Each wave reads only its own query rows (row-wise and transposed), so
+// the LDS bytes per MFMA stay those of the one-wave kernel apart from V,
+// which sits in LDS (staged once per workgroup) to leave room for two waves
+// per SIMD: one wave's MFMAs then cover the other's softmax terms and LDS
+// latency.  The two row halves' partial dK / dV are added once at the end
+// (through LDS, in a fixed order).
+#ifndef MS_DKDV_ROWSPLIT
+#define MS_DKDV_ROWSPLIT 1
+#endif
+constexpr int kKvRowsThreads = 512;
+
+// Rows 32 rh .. 32 rh + 31 of query tile t against this wave's 32 keys:
+// S = Q K^T (K in registers), dP = dO V^T (V rows of the key block from LDS),
+// then dV^T += (s dO)^T P and dK^T += Q^T dZ over those rows.
+template <int D>
+__device__ __forceinline__ void kv_tile_rows(const uint16_t* t, const u32x4* kreg, const uint16_t* vt,
+                                             const int32_t* lims, int key, int rh, float c2, float isv, int lane,
+                                             f32x16* dv, f32x16* dk) {
+    using T = KvTile<D>;
+    constexpr int KD = D / 16, ND = D / 32;
+    const int h = lane >> 5, l32 = lane & 31;
+    const float* lse2 = reinterpret_cast<const float*>(t + T::kRw);
+    const float* dlt = lse2 + 64;
+    f32x16 sacc = f32x16{}, pacc = f32x16{};
+    u32x4 fq[2], fg[2], fv[2];
+    auto rd = [&](int set, int s) {
+        fq[set] = dma_read16<D, kDualPad>(t + T::kQ16, 32 * rh + l32, h + 2 * s);
+        fg[set] = dma_read16<D, kDualPad>(t + T::kG16, 32 * rh + l32, h + 2 * s);
+        fv[set] = dma_read16<D, kRowPad>(vt, key, h + 2 * s);
+    };
+    rd(0, 0);
+#pragma unroll
+    for (int s = 0; s < KD; ++s) {
+        const int set = s & 1;
+        if (s + 1 < KD) rd(set ^ 1, s + 1);
+        __builtin_amdgcn_sched_barrier(0);
+        sacc = mfma32h(fq[set], kreg[s], sacc);
+        pacc = mfma32h(fg[set], fv[set], pacc);
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    // P and t s dZ of the wave's rows as the fp16 B operands of dV / dK
+    u32x4 pb[2], zb[2];
+#pragma unroll
+    for (int q4 = 0; q4 < 4; ++q4) {
+        const int row0 = 32 * rh + 8 * q4 + 4 * h;
+        const f32x4 l4 = *reinterpret_cast<const f32x4*>(lse2 + row0);
+        const f32x4 d4 = *reinterpret_cast<const f32x4*>(dlt + row0);
+        float pv[4], zv[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int r = 4 * q4 + e;
+            pv[e] = fast_exp2(__builtin_fmaf(sacc[r], c2, -l4[e]));
+            zv[e] = pv[e] * __builtin_fmaf(pacc[r], isv, -d4[e]);
+        }
+        const int j = q4 >> 1, w0 = 2 * (q4 & 1);
+        pb[j][w0] = pack_f16x2(pv[0], pv[1]);
+        pb[j][w0 + 1] = pack_f16x2(pv[2], pv[3]);
+        zb[j][w0] = pack_f16x2(zv[0], zv[1]);
+        zb[j][w0 + 1] = pack_f16x2(zv[2], zv[3]);
+    }
+    if (lims) {   // rare diagonal tiles: row 32 rh + 8 (r/4) + 4 h + r%4 < lims[key] is masked
+        keep_branch();
+        const int lim = lims[key] - 4 * h - 32 * rh;
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+            if (8 * (r >> 2) + (r & 3) < lim) {
+                const uint32_t keep = (r & 1) ? 0x0000FFFFu : 0xFFFF0000u;
+                pb[r >> 3][(r & 7) >> 1] &= keep;
+                zb[r >> 3][(r & 7) >> 1] &= keep;
+            }
+    }
+    u32x4 av[2][2], ak[2][2];   // [set][j]: transposed dO^T / Q^T of one 32-wide d block
+    auto rt = [&](int set, int i) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            av[set][j] = dma_read_tr<D, kDualPad>(t + T::kG16, 32 * rh + 16 * j, 32 * i, lane);
+            ak[set][j] = dma_read_tr<D, kDualPad>(t + T::kQ16, 32 * rh + 16 * j, 32 * i, lane);
+        }
+    };
+    rt(0, 0);
+#pragma unroll
+    for (int i = 0; i < ND; ++i) {
+        const int set = i & 1;
+        if (i + 1 < ND) rt(set ^ 1, i + 1);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            dv[i] = mfma32h(av[set][j], pb[j], dv[i]);
+            dk[i] = mfma32h(ak[set][j], zb[j], dk[i]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+}
+
+template <int D>
+__global__ void __launch_bounds__(kKvRowsThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+bwd_dkdv_rows_kernel(AttnArgs a) {
+    constexpr int KD = D / 16, ND = D / 32;
+    constexpr int TE = KvTile<D>::kElems, VE = DmaTile<D, kRowPad>::kElems;
+    // two query-tile buffers (reused at the end for the row halves' reduction)
+    __shared__ __attribute__((aligned(16))) uint16_t tb[2 * TE];
+    __shared__ __attribute__((aligned(16))) uint16_t vsm[2 * VE];
+    __shared__ int32_t dlims[64];
+    if (index_overflowed(a.overflow)) return;   // incomplete lists: outputs are left untouched
+    const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, l32 = lane & 31;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int half = w >> 2, kh = (w >> 1) & 1, rh = w & 1;
+    if (tid < 64) dlims[tid] = tid;   // causal diagonal: key k visible to rows >= k
+    const int BK = a.B * a.Hkv;
+    const int npair = (a.nkb + 1) >> 1;
+    const int64_t u = xcd_chunk(blockIdx.x, int64_t(BK) * npair);
+    const int bk = int(u / npair);
+    const int kp = int(u % npair);
+    const int b = bk / a.Hkv, hk = bk % a.Hkv;
+    const int G = a.Hq / a.Hkv;
+    const int kb0 = 2 * kp;
+    const bool has1 = kb0 + 1 < a.nkb;
+    const int kb = kb0 + (has1 ? half : 0);
+    const bool live = half == 0 || has1;
+    const int key = 32 * kh + l32;
+    const int64_t krow = int64_t(bk) * a.Nk + int64_t(kb) * 64 + key;
+    u32x4 kreg[KD];
+#pragma unroll
+    for (int s = 0; s < KD; ++s) kreg[s] = *reinterpret_cast<const u32x4*>(a.k16 + krow * D + 16 * s + 8 * h);
+    // V rows of the pair's key blocks (a lone block stages it twice)
+    dma_rows<D, kRowPad, 8>(vsm, a.v16 + int64_t(bk) * a.Nk * D, ContiguousRows{int64_t(kb0) * 64}, w, lane);
+    dma_rows<D, kRowPad, 8>(vsm + VE, a.v16 + int64_t(bk) * a.Nk * D,
+                            ContiguousRows{int64_t(has1 ? kb0 + 1 : kb0) * 64}, w, lane);
+    const uint16_t* vt = vsm + half * VE;
+    f32x16 dv[ND], dk[ND];
+#pragma unroll
+    for (int i = 0; i < ND; ++i) {
+        dv[i] = f32x16{};
+        dk[i] = f32x16{};
+    }
+    const float sq = operand_scale(a.qkvmax), sk = operand_scale(a.qkvmax + 1);
+    const float isv = dz_scale(a.qkvmax + 2, D) / operand_scale(a.qkvmax + 2);   // t / sv
+    const float c2 = a.scale * kLog2e / (sq * sk);
+    const float sc = dout_scale(a.dmax);
+    const int32_t kg = ldc(a.k_blk_global, kb);
+
+    // walk: as bwd_dkdv_kernel (heads of the group in order, per head the
+    // union of the pair's two transposed lists)
+    int g = 0;
+    int64_t p0 = 0, e0 = 0, p1 = 0, e1 = 0;
+    auto open_head = [&]() {
+        const int64_t item = int64_t(b * a.Hq + hk * G + g) * a.nkb + kb0;
+        p0 = ldc(a.kblk_ptr, item);
+        e0 = ldc(a.kblk_ptr, item + 1);
+        p1 = e0;
+        e1 = has1 ? ldc(a.kblk_ptr, item + 2) : e0;
+    };
+    open_head();
+    auto next = [&](int& bh, int& qb, bool& in0, bool& in1, bool& diag) {
+        while (p0 >= e0 && p1 >= e1) {
+            if (++g >= G) return false;
+            open_head();
+        }
+        const int32_t q0 = p0 < e0 ? ldc(a.kblk_idx, p0) : INT32_MAX;
+        const int32_t q1 = p1 < e1 ? ldc(a.kblk_idx, p1) : INT32_MAX;
+        qb = min(q0, q1);
+        in0 = q0 == qb;
+        in1 = q1 == qb;
+        p0 += in0;
+        p1 += in1;
+        bh = b * a.Hq + hk * G + g;
+        diag = ldc(a.q_blk_global, qb) == kg;
+        return true;
+    };
+    uint16_t* t0s = tb;
+    uint16_t* t1s = tb + TE;
+    int bh = 0, qb = 0, bhn = 0, qbn = 0;
+    bool in0 = false, in1 = false, diag = false, in0n = false, in1n = false, diagn = false;
+    bool have = next(bh, qb, in0, in1, diag);
+    if (have) kv_load_query_tile<D, 8>(t0s, a, bh, qb, w, lane);
+    bool haven = have && next(bhn, qbn, in0n, in1n, diagn);
+    wait_vmem();
+    __syncthreads();
+    auto step = [&](const uint16_t* ct, uint16_t* nt) {
+        if (haven) kv_load_query_tile<D, 8>(nt, a, bhn, qbn, w, lane);
+        if (half == 0 ? in0 : in1) kv_tile_rows<D>(ct, kreg, vt, diag ? dlims : nullptr, key, rh, c2, isv, lane, dv, dk);
+        __builtin_amdgcn_sched_barrier(0);
+        int bh2 = 0, qb2 = 0;
+        bool in02 = false, in12 = false, diag2 = false;
+        const bool more2 = haven && next(bh2, qb2, in02, in12, diag2);
+        wait_vmem();
+        __syncthreads();
+        bh = bhn;
+        qb = qbn;
+        in0 = in0n;
+        in1 = in1n;
+        diag = diagn;
+        have = haven;
+        bhn = bh2;
+        qbn = qb2;
+        in0n = in02;
+        in1n = in12;
+        diagn = diag2;
+        haven = more2;
+    };
+    while (have) {
+        step(t0s, t1s);
+        if (!have) break;
+        step(t1s, t0s);
+    }
+    // rows 32-63's partial dK / dV are added to rows 0-31's (fixed order) through LDS
+    float* red = reinterpret_cast<float*>(tb);   // 4 slots of ND x 16 x 64 floats
+    float* slot = red + (2 * half + kh) * (ND * 16 * 64);
+    static_assert(2 * TE * 2 >= 4 * ND * 16 * 64 * 4, "reduction space");
+#pragma unroll
+    for (int pass = 0; pass < 2; ++pass) {
+        f32x16* acc = pass == 0 ? dv : dk;
+        if (rh == 1)
+#pragma unroll
+            for (int i = 0; i < ND; ++i)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) slot[(i * 16 + r) * 64 + lane] = acc[i][r];
+        __syncthreads();
+        if (rh == 0)
+#pragma unroll
+            for (int i = 0; i < ND; ++i)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[i][r] += slot[(i * 16 + r) * 64 + lane];
+        __syncthreads();
+    }
+    if (!live || rh != 0) return;
+    float* dkp = a.dk + krow * D;
+    float* dvp = a.dv + krow * D;
+    const float pt = dz_scale(a.qkvmax + 2, D);   // the tiles give s dV and t s dK
+    const float fk = a.scale / (sc * pt * sq), fv = 1.f / sc;
+#pragma unroll
+    for (int i = 0; i < ND; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            f32x4 x, y;
+            x.x = dk[i][4 * j + 0] * fk;
+            x.y = dk[i][4 * j + 1] * fk;
+            x.z = dk[i][4 * j + 2] * fk;
+            x.w = dk[i][4 * j + 3] * fk;
+            y.x = dv[i][4 * j + 0] * fv;
+            y.y = dv[i][4 * j + 1] * fv;
+            y.z = dv[i][4 * j + 2] * fv;
+            y.w = dv[i][4 * j + 3] * fv;
+            *reinterpret_cast<f32x4*>(dkp + 32 * i + 8 * j + 4 * h) = x;
+            *reinterpret_cast<f32x4*>(dvp + 32 * i + 8 * j + 4 * h) = y;
+        }
+}
+
 __device__ __forceinline__ bool dbit(const uint32_t* db, int32_t x) { return (db[x >> 5] >> (x & 31)) & 1u; }
 
 // ------------------------------------------------------------------ column pass
@@ -981,7 +1233,13 @@ hipError_t launch_bwd_d(const AttnArgs& a, hipStream_t s) {
     if (qgrid > 0) { TraceScope _t("bwd_dq", s); hipLaunchKernelGGL(bwd_dq_kernel<D>, dim3(unsigned(qgrid)), dim3(kDqThreads), 0, s, a); }
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const int64_t kpgrid = int64_t(a.B) * a.Hkv * ((a.nkb + 1) / 2);
-    if (kpgrid > 0) { TraceScope _t("bwd_dkdv", s); hipLaunchKernelGGL(bwd_dkdv_kernel<D>, dim3(unsigned(kpgrid)), dim3(kKvThreads), 0, s, a); }
+    if (kpgrid > 0) {
+        TraceScope _t("bwd_dkdv", s);
+        if (D == 128 && MS_DKDV_ROWSPLIT)
+            hipLaunchKernelGGL(bwd_dkdv_rows_kernel<D>, dim3(unsigned(kpgrid)), dim3(kKvRowsThreads), 0, s, a);
+        else
+            hipLaunchKernelGGL(bwd_dkdv_kernel<D>, dim3(unsigned(kpgrid)), dim3(kKvThreads), 0, s, a);
+    }
     if ((e = hipGetLastError()) != hipSuccess) return e;
     { TraceScope _t("bwd_colplan", s); hipLaunchKernelGGL(bwd_colplan_kernel, dim3(1), dim3(kPlanThreads), 0, s, a); }
     if ((e = hipGetLastError()) != hipSuccess) return e;
