@@ -44,6 +44,14 @@ def kernel_source_hash() -> str:
     return h.hexdigest()
 
 
+def kernel_symbol(label: str, d: int) -> str:
+    """The kernel's name in rocprofv3 output for a trace label (the key/value-
+    major backward runs its row-split kernel at head dim 128)."""
+    if label == "bwd_dkdv" and d == 128:
+        return f"bwd_dkdv_rows_kernel<{d}>"
+    return f"{label}_kernel<{d}>"
+
+
 def hbm_traffic(workload: str, kernel: str):
     """Bytes per launch of `kernel` from the committed PMC summary (FETCH_SIZE and
     WRITE_SIZE, copy-calibrated), or None when there is none for this workload
@@ -583,7 +591,7 @@ def main():
     dom = max(kern, key=lambda n: kern[n]["avg_ms"] * kern[n]["launches_per_step"])
     dk_ = kern[dom]
     achieved = dk_["tflops_counted"] if dk_["tflops_counted"] is not None else 0.0
-    traffic = hbm_traffic(wl.name, f"{dom}_kernel<{wl.head_dim}>")
+    traffic = hbm_traffic(wl.name, kernel_symbol(dom, wl.head_dim))
     for r in results.values():
         r["est_idx"] = estimation_and_index_report(r)
     # achievable dense fp16 MFMA rate on this GPU (probe kernel, no memory traffic): constant
