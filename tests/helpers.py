@@ -43,6 +43,60 @@ def oracle_indices(f64: dict, wl, heads=None):
     return OE.estimate(q, k, wl.last_q, wl.k_v, wl.k_s, 1 / math.sqrt(wl.head_dim))
 
 
+def oracle_sets_every_head(x: dict, wl) -> tuple[np.ndarray, np.ndarray]:
+    """Each head's own (v_idx, s_idx) from the oracle's fp64 estimator (Alg. 1:
+    the last last_q queries' column and diagonal sums, then the top k_v / k_s,
+    lower index first), computed head by head from CPU copies of the inputs
+    (which may live on the GPU)."""
+    B, Hq, Hkv, N = wl.batch, wl.heads_q, wl.heads_kv, wl.seq
+    G = Hq // Hkv
+    scale = 1 / math.sqrt(wl.head_dim)
+    vi = np.zeros((B, Hq, wl.k_v), np.int32)
+    si = np.zeros((B, Hq, wl.k_s), np.int32)
+    for b in range(B):
+        for g in range(Hkv):
+            k = to_f64(x["k"][b, g].cpu())
+            for h in range(g * G, (g + 1) * G):
+                vs, ss = OE.vs_scores(to_f64(x["q"][b, h, N - wl.last_q:].cpu()), k, scale)
+                vi[b, h] = OE.topk_lower(vs, wl.k_v)
+                si[b, h] = OE.topk_lower(ss, wl.k_s)
+            del k
+    return vi, si
+
+
+def weighted_identity_check(x: dict, out32, dq, dk, dv, rel_tol: float) -> None:
+    """Per KV group, the chain-rule identities of Eq. attention_backward on the
+    GPU's own outputs (fp64 sums on the device): sum_j dK_j . k_j equals the sum
+    of dQ_i . q_i over the group's heads and rows, and sum_j dV_j . v_j the sum
+    of dO_i . O_i.  Unlike sum dK = 0 and sum dV = sum dO, they weight each
+    key's gradient by that key's own row, so gradients accumulated into the
+    wrong keys (systematically) break them.  The bar is relative to the sum of
+    the terms' magnitudes."""
+    B, Hq = x["q"].shape[:2]
+    Hkv = x["k"].shape[1]
+    G = Hq // Hkv
+    for b in range(B):
+        for g in range(Hkv):
+            kk, vv = x["k"][b, g].double(), x["v"][b, g].double()
+            dkk, dvv = dk[b, g].double() * kk, dv[b, g].double() * vv
+            tk, tv = float(dkk.sum()), float(dvv.sum())
+            mk, mv = float(dkk.abs().sum()), float(dvv.abs().sum())
+            del kk, vv, dkk, dvv
+            tq = to = 0.0
+            for h in range(g * G, (g + 1) * G):
+                a = dq[b, h].double() * x["q"][b, h].double()
+                c = x["do"][b, h].double() * out32[b, h].double()
+                tq += float(a.sum())
+                to += float(c.sum())
+                mk += float(a.abs().sum())
+                mv += float(c.abs().sum())
+                del a, c
+            print(f"identities b{b} kv{g}: dK.k - dQ.q = {tk - tq:.3e} (rel {abs(tk - tq) / mk:.2e}), "
+                  f"dV.v - dO.O = {tv - to:.3e} (rel {abs(tv - to) / mv:.2e})", flush=True)
+            assert abs(tk - tq) <= rel_tol * mk, f"dK.k identity b{b} kv{g}"
+            assert abs(tv - to) <= rel_tol * mv, f"dV.v identity b{b} kv{g}"
+
+
 def gpu_csr(idx) -> dict:
     """Copy a GPU SparseIndex to host arrays trimmed to their used lengths."""
     t = {k: v.cpu().numpy() for k, v in idx.tensors.items()}

@@ -1,9 +1,9 @@
 """Full-size parity in the benchmark's launch configuration.
 
 The GPU runs index -> forward -> backward over every head of the workload's
-full shape.  The index comes from the oracle's estimator on two sampled heads
-(their sets are reused for the other heads, so no input comes from the GPU).
-The oracle then checks, on the sampled heads, sampled query rows spread over
+full shape.  Every head's vertical and slash sets come from the oracle's fp64
+estimator on that head (so no input comes from the GPU).  The oracle then
+checks, on four heads spread over two KV groups, sampled query rows spread over
 the sequence (out, lse and dQ need only the row itself), and the invariants
 that hold at any size: sum over keys of dK is 0 and sum over keys of dV equals
 the sum of dO over the group's query rows.  dK and dV of the last 128 keys of
@@ -18,10 +18,10 @@ import torch
 
 import paper_2510_18830_amd as ms
 from oracle import attn as OA
-from oracle import estimate as OE
 from oracle import index as OI
 from synth import WORKLOADS, make_inputs
-from tests.helpers import assert_close, assert_lse_close, to_f64
+from tests.helpers import (assert_close, assert_lse_close, oracle_sets_every_head, to_f64,
+                           weighted_identity_check)
 
 pytestmark = pytest.mark.gpu
 
@@ -34,15 +34,8 @@ def test_fullsize_sampled_rows_and_invariants(gpu, name):
     G = Hq // Hkv
     scale = 1 / math.sqrt(d)
     x = make_inputs(wl, gpu)
-    heads = [0, Hq - 1]
-    sets = {}
-    for h in heads:
-        q_last = to_f64(x["q"][0, h, N - wl.last_q:].cpu())
-        k = to_f64(x["k"][0, h // G].cpu())
-        vs, ss = OE.vs_scores(q_last, k, scale)
-        sets[h] = (OE.topk_lower(vs, wl.k_v), OE.topk_lower(ss, wl.k_s))
-    vi = np.stack([sets[heads[h % 2]][0] for h in range(Hq)])[None].astype(np.int32)
-    si = np.stack([sets[heads[h % 2]][1] for h in range(Hq)])[None].astype(np.int32)
+    heads = [0, G - 1, Hq - G, Hq - 1]
+    vi, si = oracle_sets_every_head(x, wl)
     print("oracle sets ready", flush=True)
 
     dims = ms.make_dims(B, N, Hq, Hkv, d)
@@ -86,6 +79,14 @@ def test_fullsize_sampled_rows_and_invariants(gpu, name):
             want += x["do"][0, h].double().sum(0)
         s_dv = dv64.sum(0)
         assert ((s_dv - want).abs() <= 1e-4 * dv64.abs().sum(0) + 1e-3).all(), f"sum dV kv{g}"
+    # the weighted identities over every key and row.  Both sides hold for
+    # whatever dS and P the kernels use (dQ and dK share dS, O and dV share P
+    # up to recomputation), so the residual is only the fp32 accumulation
+    # order: 1e-10 to 2e-7 of the magnitude at 32K-512K; bar 1e-5.  A gradient
+    # row moved to the wrong key shifts the sums by about its own weight, so
+    # this catches misrouted partials in bulk (a few tens of rows at 512K);
+    # single partials are compared element by element at 32K.
+    weighted_identity_check(x, out32, dq, dk, dv, 1e-5)
     # element-wise dK / dV of the last 128 keys of two KV heads: only the last
     # 128 query rows (causal) of the group's heads see them, so the oracle's
     # gradients over those rows alone are the full gradients of these keys
@@ -111,8 +112,9 @@ def test_fullsize_sampled_rows_and_invariants(gpu, name):
 
 @pytest.mark.parametrize("name", ["prefill_1m"])
 def test_prefill_forward_sampled_rows(gpu, name):
-    """Forward-only sparse prefill at 1M tokens: estimate sets from the oracle on
-    two heads, GPU index and forward over every head, sampled rows checked."""
+    """Forward-only sparse prefill at 1M tokens: every head's sets from the
+    oracle's estimator, GPU index and forward over every head, sampled rows of
+    two heads checked."""
     wl = WORKLOADS[name]
     print(f"prefill {name}", flush=True)
     B, Hq, Hkv, N, d = wl.batch, wl.heads_q, wl.heads_kv, wl.seq, wl.head_dim
@@ -120,13 +122,7 @@ def test_prefill_forward_sampled_rows(gpu, name):
     scale = 1 / math.sqrt(d)
     x = make_inputs(wl, gpu, with_do=False)
     heads = [3, Hq - 2]
-    sets = {}
-    for h in heads:
-        vs, ss = OE.vs_scores(to_f64(x["q"][0, h, N - wl.last_q:].cpu()), to_f64(x["k"][0, h // G].cpu()), scale)
-        sets[h] = (OE.topk_lower(vs, wl.k_v), OE.topk_lower(ss, wl.k_s))
-        del vs, ss
-    vi = np.stack([sets[heads[h % 2]][0] for h in range(Hq)])[None].astype(np.int32)
-    si = np.stack([sets[heads[h % 2]][1] for h in range(Hq)])[None].astype(np.int32)
+    vi, si = oracle_sets_every_head(x, wl)
     print("oracle sets ready", flush=True)
     dims = ms.make_dims(B, N, Hq, Hkv, d)
     idx = ms.make_index(dims, torch.from_numpy(vi).to(gpu), torch.from_numpy(si).to(gpu))
@@ -173,13 +169,7 @@ def test_ring_share_fullsize_sampled_rows(gpu, name, rank):
     scale = 1 / math.sqrt(d)
     x = make_inputs(wl, gpu)
     heads = [1, Hq - 1]
-    sets = {}
-    for h in heads:
-        vs, ss = OE.vs_scores(to_f64(x["q"][0, h, N - wl.last_q:].cpu()), to_f64(x["k"][0, h // G].cpu()), scale)
-        sets[h] = (OE.topk_lower(vs, wl.k_v), OE.topk_lower(ss, wl.k_s))
-        del vs, ss
-    vi = np.stack([sets[heads[h % 2]][0] for h in range(Hq)])[None].astype(np.int32)
-    si = np.stack([sets[heads[h % 2]][1] for h in range(Hq)])[None].astype(np.int32)
+    vi, si = oracle_sets_every_head(x, wl)
     print("oracle sets ready", flush=True)
 
     T = N // W

@@ -29,7 +29,8 @@ import torch
 
 import paper_2510_18830_amd as ms
 from synth import WORKLOADS, make_inputs
-from tests.helpers import (assert_close, assert_lse_close, gpu_csr, inputs_f64, oracle_heads, oracle_indices)
+from tests.helpers import (assert_close, assert_lse_close, gpu_csr, inputs_f64, oracle_heads, oracle_indices,
+                           weighted_identity_check)
 
 pytestmark = pytest.mark.gpu
 
@@ -49,6 +50,11 @@ def _run_gpu(gpu, wl, x, vi, si, bwd_workspace=None):
     got = dict(out=out.float().cpu().numpy(), out32=out32.cpu().numpy(), lse=lse.cpu().numpy(),
                dq=dq.cpu().numpy(), dk=dk.cpu().numpy(), dv=dv.cpu().numpy())
     return got, idx, ws
+
+
+def _identities(x, got):
+    t = {n: torch.from_numpy(got[n]) for n in ("out32", "dq", "dk", "dv")}
+    weighted_identity_check(x, t["out32"], t["dq"], t["dk"], t["dv"], 1e-5)
 
 
 def _compare_group(got, ref, group, G):
@@ -77,6 +83,7 @@ def test_layer_32k_full_kv_group(gpu):
     got, _, _ = _run_gpu(gpu, wl, x, vi, si)
     print("gpu done; oracle over the 8 heads of KV group 0", flush=True)
     G = wl.heads_q // wl.heads_kv
+    _identities(x, got)
     ref = oracle_heads(f, vi, si, list(range(G)), 1 / math.sqrt(wl.head_dim))
     _compare_group(got, ref, 0, G)
 

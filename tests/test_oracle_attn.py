@@ -117,6 +117,47 @@ def test_stochastic_rows_and_invariants():
     np.testing.assert_allclose(dv.sum(axis=2)[0, 0], do[0, 0:2].sum(axis=(0, 1)), atol=1e-11)
 
 
+def weighted_gradient_residuals(q, k, v, do, out, dq, dk, dv):
+    """Per KV group g, the two identities that follow from the chain rule of
+    Eq. attention_backward (S = scale Q K^T, O = P V):
+      sum_j dK_j . k_j = sum over the group's heads and rows of dQ_i . q_i
+        (both equal sum_ij dS_ij S_ij), and
+      sum_j dV_j . v_j = sum over the group's heads and rows of dO_i . O_i.
+    Returns [(residual_k, magnitude_k, residual_v, magnitude_v)] per (b, g)."""
+    B, Hq = q.shape[:2]
+    Hkv = k.shape[1]
+    G = Hq // Hkv
+    res = []
+    for b in range(B):
+        for g in range(Hkv):
+            hs = slice(g * G, (g + 1) * G)
+            tk, tq = (dk[b, g] * k[b, g]).sum(), (dq[b, hs] * q[b, hs]).sum()
+            tv, to = (dv[b, g] * v[b, g]).sum(), (do[b, hs] * out[b, hs]).sum()
+            mk = np.abs(dk[b, g] * k[b, g]).sum() + np.abs(dq[b, hs] * q[b, hs]).sum()
+            mv = np.abs(dv[b, g] * v[b, g]).sum() + np.abs(do[b, hs] * out[b, hs]).sum()
+            res.append((tk - tq, mk, tv - to, mv))
+    return res
+
+
+def test_weighted_gradient_identities():
+    """The oracle's gradients satisfy both identities to rounding, and a dK or
+    dV row added to the wrong key (a misrouted partial) breaks them."""
+    q, k, v, do, idx = _case(21)
+    scale = 0.3
+    out, _ = A.layer_fwd(q, k, v, idx, scale)
+    dq, dk, dv = A.layer_bwd(q, k, v, do, idx, scale)
+    for rk, mk, rv, mv in weighted_gradient_residuals(q, k, v, do, out, dq, dk, dv):
+        assert abs(rk) <= 1e-12 * mk and abs(rv) <= 1e-12 * mv
+    for name in ("dk", "dv"):
+        bad = {"dk": dk.copy(), "dv": dv.copy()}
+        t = bad[name]
+        t[0, 1, 200] += t[0, 1, 37]       # key 37's gradient moved to key 200
+        t[0, 1, 37] = 0.0
+        r = weighted_gradient_residuals(q, k, v, do, out, dq, bad["dk"], bad["dv"])[1]
+        rel = abs(r[0]) / r[1] if name == "dk" else abs(r[2]) / r[3]
+        assert rel > 1e-3, (name, rel)
+
+
 def test_empty_row():
     # no slash at the diagonal and no vertical in the first block: rows of block 0 see nothing
     N, d = 128, 4
