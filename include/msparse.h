@@ -18,7 +18,8 @@
  *   - Tensors are device pointers to contiguous row-major arrays, 16-byte
  *     aligned: Q, O, dO bf16 [B, Hq, Nq, d]; K, V bf16 [B, Hkv, Nk, d];
  *     lse fp32 [B, Hq, Nq] (natural log); dQ fp32 [B, Hq, Nq, d];
- *     dK, dV fp32 [B, Hkv, Nk, d].
+ *     dK, dV fp32 [B, Hkv, Nk, d].  A tensor off 16-byte alignment is
+ *     rejected with MSPARSE_ERR_INVALID.
  *   - GQA: query head h reads KV head h / (Hq / Hkv) (contiguous groups).
  *   - Causal attention with 64-token blocks only.  scale <= 0 selects
  *     1 / sqrt(head_dim).

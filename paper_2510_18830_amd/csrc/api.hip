@@ -6,6 +6,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <initializer_list>
 #include <mutex>
 #include <string>
 
@@ -26,6 +27,14 @@ msparse_status fail(msparse_status st, const char* fmt, ...) {
     va_end(ap);
     g_last_error = buf;
     return st;
+}
+
+// Every tensor named in the header's conventions is read or written with
+// 16-byte vector accesses; NULL (an optional tensor) passes.
+bool misaligned(std::initializer_list<const void*> ps) {
+    for (const void* p : ps)
+        if (reinterpret_cast<uintptr_t>(p) & 15u) return true;
+    return false;
 }
 
 bool sync_check_enabled() {
@@ -479,6 +488,7 @@ msparse_status msparse_attn_fwd(const msparse_dims* dims, const void* q, const v
     msparse_status st = check_dims(dims, false);
     if (st) return st;
     if (!q || !k || !v || (!out && !out_f32) || !lse) return fail(MSPARSE_ERR_INVALID, "tensor pointer is NULL");
+    if (misaligned({q, k, v, out, out_f32, lse})) return fail(MSPARSE_ERR_INVALID, "tensor not 16-byte aligned");
     if ((st = check_index_struct(dims, index, false))) return st;
     const size_t need = msparse_attn_fwd_workspace(dims);
     if (need && (!ws || ws_bytes < need))
@@ -503,6 +513,8 @@ msparse_status msparse_attn_fwd_merge(const msparse_dims* dims, const void* q, c
     msparse_status st = check_dims(dims, false);
     if (st) return st;
     if (!q || !k || !v || !o_acc || !lse_acc) return fail(MSPARSE_ERR_INVALID, "tensor pointer is NULL");
+    if (misaligned({q, k, v, o_acc, lse_acc, out_bf16}))
+        return fail(MSPARSE_ERR_INVALID, "tensor not 16-byte aligned");
     if ((st = check_index_struct(dims, index, false))) return st;
     const size_t need = msparse_attn_fwd_workspace(dims);
     if (need && (!ws || ws_bytes < need))
@@ -527,6 +539,8 @@ msparse_status msparse_merge_out_lse(const msparse_dims* dims, const float* o_pa
     msparse_status st = check_dims(dims, false);
     if (st) return st;
     if (!o_part || !lse_part || !o_acc || !lse_acc) return fail(MSPARSE_ERR_INVALID, "tensor pointer is NULL");
+    if (misaligned({o_part, lse_part, o_acc, lse_acc, out_bf16}))
+        return fail(MSPARSE_ERR_INVALID, "tensor not 16-byte aligned");
     if (dims->seq_q == 0) return MSPARSE_OK;
     MergeArgs m{};
     m.o_part = o_part;
@@ -601,6 +615,8 @@ msparse_status msparse_attn_bwd(const msparse_dims* dims, const void* q, const v
     if (st) return st;
     if (!q || !k || !v || !out || !dout || !lse || !dq || !dk || !dv)
         return fail(MSPARSE_ERR_INVALID, "tensor pointer is NULL");
+    if (misaligned({q, k, v, out, out_f32, dout, lse, dq, dk, dv}))
+        return fail(MSPARSE_ERR_INVALID, "tensor not 16-byte aligned");
     if ((st = check_index_struct(dims, index, true))) return st;
     if (flags & ~(MSPARSE_BWD_ACCUMULATE_DQ | MSPARSE_BWD_REUSE_QROWS))
         return fail(MSPARSE_ERR_INVALID, "backward flags 0x%x", unsigned(flags));
@@ -670,6 +686,7 @@ static msparse_status estimate_impl(const msparse_dims* dims, const void* q, con
     if (st) return st;
     const int32_t N = dims->seq_q;
     if (!q || !k || !v_idx || !s_idx) return fail(MSPARSE_ERR_INVALID, "tensor pointer is NULL");
+    if (misaligned({q, k})) return fail(MSPARSE_ERR_INVALID, "tensor not 16-byte aligned");
     if (N < 1) return fail(MSPARSE_ERR_INVALID, "empty sequence");
     if (last_q < 1 || last_q > N) return fail(MSPARSE_ERR_INVALID, "last_q %d outside [1, %d]", last_q, N);
     if (last_q > kBlock) return fail(MSPARSE_ERR_UNSUPPORTED, "last_q %d > 64", last_q);

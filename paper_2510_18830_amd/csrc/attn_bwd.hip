@@ -49,40 +49,77 @@ __global__ void bwd_init_kernel(AttnArgs a) {
 
 constexpr int kDeltaBlocks = 2048;
 
+// Delta = dO . O per row and max |dO|.  16 lanes per row, PER = d / 16
+// consecutive elements per lane read with one 16- or 8-byte load of dO and
+// one or two 16-byte loads of O; a workgroup takes 4 groups of 16 rows per
+// grid-stride step and issues all their loads before the arithmetic, so each
+// wave has 4 rows' loads in flight.  One max-atomic per workgroup.
+template <int PER, bool F32>
 __global__ void __launch_bounds__(256) bwd_delta_kernel(AttnArgs a) {
-    // 16 lanes per row, d / 16 consecutive elements per lane; grid-stride over
-    // groups of 16 rows, one max-atomic per workgroup
+    constexpr int U = 4;
     __shared__ float wmax[4];
     const int64_t rows = int64_t(a.B) * a.Hq * a.Nq;
     const int sub = threadIdx.x & 15;
-    const int per = a.d / 16;                 // 8 or 4
     float mx = 0.f;
-    for (int64_t row0 = int64_t(blockIdx.x) * 16; row0 < rows; row0 += int64_t(gridDim.x) * 16) {
-        const int64_t row = row0 + (threadIdx.x >> 4);
-        float acc = 0.f;
-        if (row < rows) {
-            const int64_t base = row * a.d + sub * per;
-            for (int j0 = 0; j0 < per; j0 += 4) {
-                const u32x2 g = *reinterpret_cast<const u32x2*>(a.dout + base + j0);
-                const float gv[4] = {bf16_lo(g.x), bf16_hi(g.x), bf16_lo(g.y), bf16_hi(g.y)};
-                float ov[4];
-                if (a.o_f32) {
-                    const f32x4 o = *reinterpret_cast<const f32x4*>(a.o_f32 + base + j0);
-                    ov[0] = o.x; ov[1] = o.y; ov[2] = o.z; ov[3] = o.w;
-                } else {
-                    const u32x2 o = *reinterpret_cast<const u32x2*>(a.o + base + j0);
-                    ov[0] = bf16_lo(o.x); ov[1] = bf16_hi(o.x); ov[2] = bf16_lo(o.y); ov[3] = bf16_hi(o.y);
-                }
+    for (int64_t row0 = int64_t(blockIdx.x) * 16 * U; row0 < rows; row0 += int64_t(gridDim.x) * 16 * U) {
+        float gv[U][PER], ov[U][PER];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t row = row0 + 16 * u + (threadIdx.x >> 4);
+            const int64_t base = (row < rows ? row : rows - 1) * (16 * PER) + sub * PER;
+            if constexpr (PER == 8) {
+                const u32x4 g = *reinterpret_cast<const u32x4*>(a.dout + base);
+                const uint32_t gw[4] = {g.x, g.y, g.z, g.w};
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
-                    acc += ov[j] * gv[j];
-                    mx = fmaxf(mx, fabsf(gv[j]));
+                    gv[u][2 * j] = bf16_lo(gw[j]);
+                    gv[u][2 * j + 1] = bf16_hi(gw[j]);
                 }
+            } else {
+                const u32x2 g = *reinterpret_cast<const u32x2*>(a.dout + base);
+                gv[u][0] = bf16_lo(g.x);
+                gv[u][1] = bf16_hi(g.x);
+                gv[u][2] = bf16_lo(g.y);
+                gv[u][3] = bf16_hi(g.y);
+            }
+            if constexpr (F32) {
+#pragma unroll
+                for (int j0 = 0; j0 < PER; j0 += 4) {
+                    const f32x4 o = *reinterpret_cast<const f32x4*>(a.o_f32 + base + j0);
+                    ov[u][j0] = o.x;
+                    ov[u][j0 + 1] = o.y;
+                    ov[u][j0 + 2] = o.z;
+                    ov[u][j0 + 3] = o.w;
+                }
+            } else if constexpr (PER == 8) {
+                const u32x4 o = *reinterpret_cast<const u32x4*>(a.o + base);
+                const uint32_t ow[4] = {o.x, o.y, o.z, o.w};
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    ov[u][2 * j] = bf16_lo(ow[j]);
+                    ov[u][2 * j + 1] = bf16_hi(ow[j]);
+                }
+            } else {
+                const u32x2 o = *reinterpret_cast<const u32x2*>(a.o + base);
+                ov[u][0] = bf16_lo(o.x);
+                ov[u][1] = bf16_hi(o.x);
+                ov[u][2] = bf16_lo(o.y);
+                ov[u][3] = bf16_hi(o.y);
             }
         }
 #pragma unroll
-        for (int off = 8; off >= 1; off >>= 1) acc += __shfl_xor(acc, off);
-        if (row < rows && sub == 0) a.draw[row] = acc;
+        for (int u = 0; u < U; ++u) {
+            const int64_t row = row0 + 16 * u + (threadIdx.x >> 4);
+            float acc = 0.f;
+#pragma unroll
+            for (int j = 0; j < PER; ++j) {
+                acc += ov[u][j] * gv[u][j];
+                if (row < rows) mx = fmaxf(mx, fabsf(gv[u][j]));
+            }
+#pragma unroll
+            for (int off = 8; off >= 1; off >>= 1) acc += __shfl_xor(acc, off);
+            if (row < rows && sub == 0) a.draw[row] = acc;
+        }
     }
     mx = wave_max(mx);
     if ((threadIdx.x & 63) == 0) wmax[threadIdx.x >> 6] = mx;
@@ -696,19 +733,19 @@ __global__ void __launch_bounds__(kKvThreads) __attribute__((amdgpu_waves_per_eu
 #endif
 constexpr int kKvRowsThreads = 512;
 
-// Rows 32 rh .. 32 rh + 31 of query tile t against this wave's 32 keys:
-// S = Q K^T (K in registers), dP = dO V^T (V rows of the key block from LDS),
-// then dV^T += (s dO)^T P and dK^T += Q^T dZ over those rows.
+// Rows 32 rh .. 32 rh + 31 of query tile t against this wave's 32 keys, in
+// three phases: rows_s_dp (MFMA) forms S = Q K^T (K in registers) and
+// dP = dO V^T (V rows of the key block from LDS); rows_terms (VALU) turns them
+// into P and t s dZ as fp16 B operands; rows_dv_dk (MFMA) adds
+// dV^T += (s dO)^T P and dK^T += Q^T dZ over those rows.
 template <int D>
-__device__ __forceinline__ void kv_tile_rows(const uint16_t* t, const u32x4* kreg, const uint16_t* vt,
-                                             const int32_t* lims, int key, int rh, float c2, float isv, int lane,
-                                             f32x16* dv, f32x16* dk) {
+__device__ __forceinline__ void rows_s_dp(const uint16_t* t, const u32x4* kreg, const uint16_t* vt, int key, int rh,
+                                          int lane, f32x16& sacc, f32x16& pacc) {
     using T = KvTile<D>;
-    constexpr int KD = D / 16, ND = D / 32;
+    constexpr int KD = D / 16;
     const int h = lane >> 5, l32 = lane & 31;
-    const float* lse2 = reinterpret_cast<const float*>(t + T::kRw);
-    const float* dlt = lse2 + 64;
-    f32x16 sacc = f32x16{}, pacc = f32x16{};
+    sacc = f32x16{};
+    pacc = f32x16{};
     u32x4 fq[2], fg[2], fv[2];
     auto rd = [&](int set, int s) {
         fq[set] = dma_read16<D, kDualPad>(t + T::kQ16, 32 * rh + l32, h + 2 * s);
@@ -725,8 +762,16 @@ __device__ __forceinline__ void kv_tile_rows(const uint16_t* t, const u32x4* kre
         pacc = mfma32h(fg[set], fv[set], pacc);
         __builtin_amdgcn_sched_barrier(0);
     }
-    // P and t s dZ of the wave's rows as the fp16 B operands of dV / dK
-    u32x4 pb[2], zb[2];
+}
+
+template <int D>
+__device__ __forceinline__ void rows_terms(const uint16_t* t, const int32_t* lims, int key, int rh, float c2,
+                                           float isv, int lane, const f32x16& sacc, const f32x16& pacc, u32x4* pb,
+                                           u32x4* zb) {
+    using T = KvTile<D>;
+    const int h = lane >> 5;
+    const float* lse2 = reinterpret_cast<const float*>(t + T::kRw);
+    const float* dlt = lse2 + 64;
 #pragma unroll
     for (int q4 = 0; q4 < 4; ++q4) {
         const int row0 = 32 * rh + 8 * q4 + 4 * h;
@@ -756,6 +801,13 @@ __device__ __forceinline__ void kv_tile_rows(const uint16_t* t, const u32x4* kre
                 zb[r >> 3][(r & 7) >> 1] &= keep;
             }
     }
+}
+
+template <int D>
+__device__ __forceinline__ void rows_dv_dk(const uint16_t* t, int rh, int lane, const u32x4* pb, const u32x4* zb,
+                                           f32x16* dv, f32x16* dk) {
+    using T = KvTile<D>;
+    constexpr int ND = D / 32;
     u32x4 av[2][2], ak[2][2];   // [set][j]: transposed dO^T / Q^T of one 32-wide d block
     auto rt = [&](int set, int i) {
 #pragma unroll
@@ -777,6 +829,17 @@ __device__ __forceinline__ void kv_tile_rows(const uint16_t* t, const u32x4* kre
         }
         __builtin_amdgcn_sched_barrier(0);
     }
+}
+
+template <int D>
+__device__ __forceinline__ void kv_tile_rows(const uint16_t* t, const u32x4* kreg, const uint16_t* vt,
+                                             const int32_t* lims, int key, int rh, float c2, float isv, int lane,
+                                             f32x16* dv, f32x16* dk) {
+    f32x16 sacc, pacc;
+    rows_s_dp<D>(t, kreg, vt, key, rh, lane, sacc, pacc);
+    u32x4 pb[2], zb[2];
+    rows_terms<D>(t, lims, key, rh, c2, isv, lane, sacc, pacc, pb, zb);
+    rows_dv_dk<D>(t, rh, lane, pb, zb, dv, dk);
 }
 
 template <int D>
@@ -1205,9 +1268,12 @@ hipError_t launch_bwd_d(const AttnArgs& a, hipStream_t s) {
     const bool qside = !a.reuse_qrows;
     if (qside && rows > 0) {
         TraceScope _t("bwd_delta", s);
-        const int64_t groups = (rows + 15) / 16;
-        hipLaunchKernelGGL(bwd_delta_kernel, dim3(unsigned(groups < kDeltaBlocks ? groups : int64_t(kDeltaBlocks))),
-                           dim3(256), 0, s, a);
+        const int64_t groups = (rows + 63) / 64;
+        const dim3 grid(unsigned(groups < kDeltaBlocks ? groups : int64_t(kDeltaBlocks)));
+        if (a.o_f32)
+            hipLaunchKernelGGL((bwd_delta_kernel<D / 16, true>), grid, dim3(256), 0, s, a);
+        else
+            hipLaunchKernelGGL((bwd_delta_kernel<D / 16, false>), grid, dim3(256), 0, s, a);
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

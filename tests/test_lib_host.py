@@ -75,6 +75,16 @@ def test_validation_before_launch():
     dd.head_dim = 96
     _bad(-2, L.msparse_attn_fwd_merge, ctypes.byref(dd), fake, fake, fake, None, fake, fake, None, 0, fake, 1 << 40,
          None)
+    # tensors off 16-byte alignment (checked before the index and workspace)
+    odd = ctypes.c_void_p(24)
+    _bad(-1, L.msparse_attn_fwd, ctypes.byref(d), fake, odd, fake, None, fake, fake, None, fake, 1 << 40, None)
+    _bad(-1, L.msparse_attn_fwd_merge, ctypes.byref(d), fake, fake, fake, None, odd, fake, None, 0, fake, 1 << 40,
+         None)
+    _bad(-1, L.msparse_attn_bwd, ctypes.byref(d), fake, fake, fake, fake, None, odd, fake, None, fake, fake, fake, 0,
+         fake, 1 << 40, None)
+    _bad(-1, L.msparse_estimate, ctypes.byref(d), odd, fake, 64, 10, 10, iv, iv, None, None, fake, 1 << 30, None)
+    _bad(-1, L.msparse_merge_out_lse, ctypes.byref(d), fake, fake, fake, fake, odd, 0, None)
+    assert "16-byte" in L.msparse_last_error().decode()
 
 
 def test_index_capacity_needs_overflow_flag_or_bound():
