@@ -299,29 +299,39 @@ __global__ void __launch_bounds__(128 * NH) est_scores_kernel(EstArgs a) {
                         for (int i = 0; i < 16; ++i)
                             if (32 * kh + l32 > 32 * rb + 8 * (i >> 2) + 4 * h + (i & 3)) acc[i] = 0.f;
                     }
+                    // element (r, c) of the 32 x 32 block goes to scratch row r,
+                    // column (c - r) mod 32: column m then holds diagonal r - c = -m
+                    // in rows r < 32 - m and diagonal 32 - m in the rows below
                     float cs = 0.f;
 #pragma unroll
                     for (int i = 0; i < 16; ++i) {
+                        const int r = 8 * (i >> 2) + 4 * h + (i & 3);
                         cs += acc[i];
-                        sc[(8 * (i >> 2) + 4 * h + (i & 3)) * SS + l32] = acc[i];
+                        sc[r * SS + ((l32 - r) & 31)] = acc[i];
                     }
                     cs += __shfl_xor(cs, 32);
                     if (h == 0) colp[hw][rb][32 * kh + l32] = cs;
                     wave_lds_sync();
-                    // diagonal r - c = e - 31 of the block (lanes 0..62)
-                    float d4[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll 1
-                    for (int r0 = 0; r0 < 32; r0 += 8) {
+                    // lane (h, m) sums rows 16 h .. 16 h + 15 of column m
+                    float upper = 0.f, lower = 0.f;
 #pragma unroll
-                        for (int k = 0; k < 8; ++k) {
-                            const int c = r0 + k - e + 31;
-                            const float v = sc[(r0 + k) * SS + (c & 31)];
-                            d4[k & 3] += (c >= 0 && c < 32) ? v : 0.f;
-                        }
+                    for (int k = 0; k < 16; ++k) {
+                        const int r = 16 * h + k;
+                        const float v = sc[r * SS + l32];
+                        const bool up = r < 32 - l32;
+                        upper += up ? v : 0.f;
+                        lower += up ? 0.f : v;
                     }
-                    const float dsum = e < 63 ? (d4[0] + d4[1]) + (d4[2] + d4[3]) : 0.f;
+                    upper += __shfl_xor(upper, 32);
+                    lower += __shfl_xor(lower, 32);
+                    // diagonal r - c = e - 31 of the block: e = 31 - m from the upper
+                    // rows, e = 63 - m from the rest (e = 63 does not exist: 0)
                     // block kind: rb < kh -> A (t = e), rb == kh -> B (t = e + 32), rb > kh -> C (t = e + 64)
-                    diagp[hw][rb < kh ? 0 : (rb > kh ? 3 : 1 + rb)][e] = dsum;
+                    float* dpk = diagp[hw][rb < kh ? 0 : (rb > kh ? 3 : 1 + rb)];
+                    if (h == 0) {
+                        dpk[31 - l32] = upper;
+                        dpk[63 - l32] = l32 == 0 ? 0.f : lower;
+                    }
                     wave_lds_sync();
                 }
             }
