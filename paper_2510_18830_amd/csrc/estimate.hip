@@ -536,10 +536,23 @@ __global__ void __launch_bounds__(256) sel_pick_kernel(EstArgs a, int shift) {
     const int b = threadIdx.x;
     uint32_t c = 0;
     uint64_t m = 0;
-    for (int sl = 0; sl < a.nslice; ++sl) {
-        const int64_t o = (int64_t(list) * a.nslice + sl) * 256 + b;
-        c += a.sel_cnt[o];
-        if (MASS) m += a.sel_mass[o];
+    // slices in groups of 8: the group's loads are all in flight at once
+    constexpr int U = 8;
+    for (int sl0 = 0; sl0 < a.nslice; sl0 += U) {
+        uint32_t cu[U];
+        uint64_t mu[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int sl = sl0 + u;
+            const int64_t o = (int64_t(list) * a.nslice + (sl < a.nslice ? sl : 0)) * 256 + b;
+            cu[u] = sl < a.nslice ? a.sel_cnt[o] : 0u;
+            mu[u] = MASS && sl < a.nslice ? a.sel_mass[o] : 0u;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            c += cu[u];
+            m += mu[u];
+        }
     }
     hc[b] = c;
     if (MASS) hm[b] = m;
