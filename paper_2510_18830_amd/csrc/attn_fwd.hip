@@ -98,7 +98,7 @@ __device__ __forceinline__ void fwd_tile(const uint16_t* kt, const uint16_t* vt,
     for (int c = 0; c < 2; ++c)
 #pragma unroll
         for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[c][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32)) * c2;
+    mx = half_swap_max(mx) * c2;
     // Lazy rescaling: keep the running maximum unless the tile exceeds it by
     // more than kSlack (P then stays below 2^kSlack, well inside fp16), so the
     // O accumulator is rescaled only on the rare tiles that raise the row

@@ -309,7 +309,7 @@ __global__ void __launch_bounds__(128 * NH) est_scores_kernel(EstArgs a) {
                         cs += acc[i];
                         sc[r * SS + ((l32 - r) & 31)] = acc[i];
                     }
-                    cs += __shfl_xor(cs, 32);
+                    cs = half_swap_sum(cs);
                     if (h == 0) colp[hw][rb][32 * kh + l32] = cs;
                     wave_lds_sync();
                     // lane (h, m) sums rows 16 h .. 16 h + 15 of column m
@@ -322,8 +322,8 @@ __global__ void __launch_bounds__(128 * NH) est_scores_kernel(EstArgs a) {
                         upper += up ? v : 0.f;
                         lower += up ? 0.f : v;
                     }
-                    upper += __shfl_xor(upper, 32);
-                    lower += __shfl_xor(lower, 32);
+                    upper = half_swap_sum(upper);
+                    lower = half_swap_sum(lower);
                     // diagonal r - c = e - 31 of the block: e = 31 - m from the upper
                     // rows, e = 63 - m from the rest (e = 63 does not exist: 0)
                     // block kind: rb < kh -> A (t = e), rb == kh -> B (t = e + 32), rb > kh -> C (t = e + 64)

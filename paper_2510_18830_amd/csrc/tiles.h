@@ -224,8 +224,7 @@ __device__ __forceinline__ float row_sum_f16(const u32x4* pb) {
         a = __builtin_amdgcn_fdot2(__builtin_bit_cast(h2, w2), one, a, false);
         b = __builtin_amdgcn_fdot2(__builtin_bit_cast(h2, w3), one, b, false);
     }
-    const float s = a + b;
-    return s + __shfl_xor(s, 32);
+    return half_swap_sum(a + b);
 }
 
 }  // namespace msparse
