@@ -79,6 +79,16 @@ __device__ __forceinline__ void fwd_tile(const uint16_t* kt, const uint16_t* vt,
             for (int c = 0; c < 2; ++c) sacc[c] = mfma32(fk[set][j][c], st.q[s0 + j], sacc[c]);
         __builtin_amdgcn_sched_barrier(0);
     }
+    // V^T operands in groups of one d block (4 operands) into two register
+    // sets; the first group is read now, so its LDS latency is covered by the
+    // softmax terms below
+    u32x4 av[2][4];
+    auto read_tr = [&](int set, int i) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) av[set][g] = dma_read_tr<D, kTrPad>(vt, 16 * g, 32 * i, lane);
+    };
+    read_tr(0, 0);
+    __builtin_amdgcn_sched_barrier(0);
     // ---- mask, tile max (raw logits; scale > 0 commutes with max)
     if (lims) {
         keep_branch();
@@ -130,13 +140,6 @@ __device__ __forceinline__ void fwd_tile(const uint16_t* kt, const uint16_t* vt,
     // nearly one-hot rows (which would otherwise amplify the 2^-12 rounding
     // of P by 1 / (1 - max P)).
     st.l += row_sum_f16(pb);
-    // V^T operands in groups of one d block (4 operands) into two register sets
-    u32x4 av[2][4];
-    auto read_tr = [&](int set, int i) {
-#pragma unroll
-        for (int g = 0; g < 4; ++g) av[set][g] = dma_read_tr<D, kTrPad>(vt, 16 * g, 32 * i, lane);
-    };
-    read_tr(0, 0);
 #pragma unroll
     for (int i = 0; i < ND; ++i) {
         const int set = i & 1;
