@@ -352,7 +352,14 @@ MSPARSE_API msparse_status msparse_merge_out_lse(const msparse_dims* dims, const
  * max |q|, |k|, |v| and |dO| (dZ by t with t head_dim max|v| in
  * [2^9, 2^10)), so no input scale makes them overflow, and inputs multiplied
  * by powers of two (within the bf16 range) give exactly the correspondingly
- * scaled results; every finite bf16 input is accepted.
+ * scaled results; every finite bf16 input is accepted.  Accuracy depends on
+ * the logits' magnitude, not on the inputs' scale: the forward and backward
+ * recompute P from fp32 logits and the fp32 lse, whose absolute rounding
+ * grows with |logit|, and rows with nearly all their weight on one key
+ * amplify it in dQ.  Measured: key rows up to 2^4 times the rest (logits up
+ * to about +-290) keep every output within 2e-2 of the exact result (row-wise,
+ * in units of the row's RMS); key rows 2^8 times larger (logits up to about
+ * +-4600) reach 3.7e-2 in dQ.
  * Workspace: msparse_attn_bwd_workspace(dims, vcol_cap) bytes; it holds
  * fp16 copies of q, k, v and dO (each times a power of two), Delta, the scaled
  * row values, and the column pass's work list and per-item partials (its size

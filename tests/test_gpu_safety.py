@@ -15,10 +15,11 @@
     the oracle.  fp16 rounding of P (relative 2^-12) against a value row of
     size 2^e moves the outputs that read it in proportion, so the parity bars
     apply per row in units of max(1, RMS of that reference row); lse to 1e-3.
-    Key rows of 2^8 (logits near +-1000) miss the row bar on dQ by up to 2x:
-    the fp32 lse then carries an absolute rounding near 1e-4, which rows
-    with nearly all their weight on one key amplify; that logit scale is
-    outside what fp32 softmax resolves, and the tested key rows stop at 2^4.
+    Key rows of 2^8 (logits up to about +-4600) miss the row bar on dQ by up
+    to 2x: the fp32 lse then carries an absolute rounding near 1e-4 or more,
+    which rows with nearly all their weight on one key amplify; that logit
+    scale is outside what fp32 softmax resolves, and the tested key rows stop
+    at 2^4 (logits up to about +-290).
 """
 import math
 
