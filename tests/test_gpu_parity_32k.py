@@ -16,7 +16,9 @@
     tiles, together with Delta taken from the forward's output, puts their dK
     error at 2.1e-2: a CPU emulation of exactly that rounding gives the same
     figure, so that case measures the precision of the fp16 second GEMM, not
-    the column plan.)
+    the column plan.  At head dim 64 the same layer gives span 55 and dK
+    2.14e-2, by the same mechanism: the larger logit scale 1/8 concentrates
+    more weight on the planted sink keys.)
 
 The oracle runs one head per worker process (about 25 s per head on one core
 pair), so each test takes about a minute of CPU time on the GPU host.
