@@ -29,7 +29,8 @@
  *   - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream) and
  *     returns before it finishes.  Only msparse_index_count waits for the GPU.
  *     Setting MSPARSE_SYNC_CHECK=1 in the environment makes every call wait
- *     for its kernels and report asynchronous faults as MSPARSE_ERR_HIP.
+ *     for its kernels and report asynchronous faults as MSPARSE_ERR_HIP
+ *     (except on a stream under graph capture, whose work runs at replay).
  *   - Arguments are validated on the host before anything is launched, so a
  *     call that returns an error has enqueued no work.
  */

@@ -48,7 +48,11 @@ bool sync_check_enabled() {
 msparse_status check_hip(hipError_t e, hipStream_t s, const char* what) {
     if (e != hipSuccess) return fail(MSPARSE_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
     if (sync_check_enabled()) {
-        e = hipStreamSynchronize(s);
+        // a stream under graph capture cannot be synchronised: its work runs
+        // at replay, so the check is skipped there
+        hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+        e = hipStreamIsCapturing(s, &cap);
+        if (e == hipSuccess && cap == hipStreamCaptureStatusNone) e = hipStreamSynchronize(s);
         if (e == hipSuccess) e = hipGetLastError();
         if (e != hipSuccess) return fail(MSPARSE_ERR_HIP, "%s (sync check): %s", what, hipGetErrorString(e));
     }
