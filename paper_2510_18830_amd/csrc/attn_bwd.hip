@@ -394,8 +394,9 @@ __device__ __forceinline__ void kv_load_query_tile(uint16_t* t, const AttnArgs& 
     }
 }
 
-// One 64-row query tile against this wave's 32 keys (`key` = this lane's key
-// inside the 64-key block; kreg, vreg its scaled fp16 K and V rows).  c2 =
+// One 64-row query tile against this wave's 32 keys, for the column pass
+// (one wave per SIMD; `key` = this lane's key inside the 64-key chunk; kreg,
+// vreg its scaled fp16 K and V rows).  c2 =
 // scale log2(e) / (sq sk); isv = t / sv turns the dP accumulator into t s dP.  lims (LDS, or NULL for a tile without masking):
 // the key is visible to in-block query row r iff r >= lims[key] (64: not
 // visible); a rare uniform branch whose limit comes from LDS, so nothing of
@@ -581,156 +582,18 @@ __device__ __forceinline__ void kv_tile(const uint16_t* t, const u32x4* kreg, co
     }
 }
 
-// Key-major pass: one workgroup of four waves per (b, KV head, pair of
-// consecutive 64-key blocks); waves 2j, 2j+1 hold 32 keys each of block j of
-// the pair in VGPRs.  For every query head of the KV group the pair walks the
-// union of its two transposed lists (query blocks that selected the key
-// block), the next query tile in flight (direct global->LDS loads, double
-// buffer) during the current one.
-constexpr int kKvThreads = 256;
-
-template <int D>
-__global__ void __launch_bounds__(kKvThreads) __attribute__((amdgpu_waves_per_eu(1, 1))) bwd_dkdv_kernel(AttnArgs a) {
-    constexpr int KD = D / 16, ND = D / 32;
-    __shared__ __attribute__((aligned(16))) uint16_t t0s[KvTile<D>::kElems], t1s[KvTile<D>::kElems];
-    __shared__ int32_t dlims[64];
-    if (index_overflowed(a.overflow)) return;   // incomplete lists: outputs are left untouched
-    const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, l32 = lane & 31;
-    const int w = __builtin_amdgcn_readfirstlane(tid >> 6), half = w >> 1;
-    if (tid < 64) dlims[tid] = tid;   // causal diagonal: key k visible to rows >= k
-    const int BK = a.B * a.Hkv;
-    const int npair = (a.nkb + 1) >> 1;
-    const int64_t u = xcd_chunk(blockIdx.x, int64_t(BK) * npair);
-    const int bk = int(u / npair);
-    const int kp = int(u % npair);          // heaviest (earliest) pairs first
-    const int b = bk / a.Hkv, hk = bk % a.Hkv;
-    const int G = a.Hq / a.Hkv;
-    const int kb0 = 2 * kp;
-    const bool has1 = kb0 + 1 < a.nkb;
-    const int kb = kb0 + (has1 ? half : 0);
-    const bool live = half == 0 || has1;
-    const int key = 32 * (w & 1) + l32;     // this lane's key inside the block
-    const int64_t krow = int64_t(bk) * a.Nk + int64_t(kb) * 64 + key;
-
-    u32x4 kreg[KD], vreg[KD];
-#pragma unroll
-    for (int s = 0; s < KD; ++s) {
-        kreg[s] = *reinterpret_cast<const u32x4*>(a.k16 + krow * D + 16 * s + 8 * h);
-        vreg[s] = *reinterpret_cast<const u32x4*>(a.v16 + krow * D + 16 * s + 8 * h);
-    }
-    f32x16 dv[ND], dk[ND];
-#pragma unroll
-    for (int i = 0; i < ND; ++i) {
-        dv[i] = f32x16{};
-        dk[i] = f32x16{};
-    }
-    const float sq = operand_scale(a.qkvmax), sk = operand_scale(a.qkvmax + 1);
-    const float isv = dz_scale(a.qkvmax + 2, D) / operand_scale(a.qkvmax + 2);   // t / sv
-    const float c2 = a.scale * kLog2e / (sq * sk);
-    const float sc = dout_scale(a.dmax);
-    const int32_t kg = ldc(a.k_blk_global, kb);
-
-    // walk: heads of the group in order, per head the union of the two lists
-    int g = 0;
-    int64_t p0 = 0, e0 = 0, p1 = 0, e1 = 0;
-    auto open_head = [&]() {
-        const int64_t item = int64_t(b * a.Hq + hk * G + g) * a.nkb + kb0;
-        p0 = ldc(a.kblk_ptr, item);
-        e0 = ldc(a.kblk_ptr, item + 1);
-        p1 = e0;
-        e1 = has1 ? ldc(a.kblk_ptr, item + 2) : e0;
-    };
-    open_head();
-    // the diagonal test is made here, one tile ahead, so that no scalar load
-    // is pending inside a tile (it would force the LDS waits to drain fully)
-    auto next = [&](int& bh, int& qb, bool& in0, bool& in1, bool& diag) {
-        while (p0 >= e0 && p1 >= e1) {
-            if (++g >= G) return false;
-            open_head();
-        }
-        const int32_t q0 = p0 < e0 ? ldc(a.kblk_idx, p0) : INT32_MAX;
-        const int32_t q1 = p1 < e1 ? ldc(a.kblk_idx, p1) : INT32_MAX;
-        qb = min(q0, q1);
-        in0 = q0 == qb;
-        in1 = q1 == qb;
-        p0 += in0;
-        p1 += in1;
-        bh = b * a.Hq + hk * G + g;
-        diag = ldc(a.q_blk_global, qb) == kg;
-        return true;
-    };
-    // the walk runs one tile ahead of the loads (as in the forward): no scalar
-    // load is outstanding inside a tile
-    int bh = 0, qb = 0, bhn = 0, qbn = 0;
-    bool in0 = false, in1 = false, diag = false, in0n = false, in1n = false, diagn = false;
-    bool have = next(bh, qb, in0, in1, diag);
-    if (have) kv_load_query_tile<D, 4>(t0s, a, bh, qb, w, lane);
-    bool haven = have && next(bhn, qbn, in0n, in1n, diagn);
-    wait_vmem();
-    __syncthreads();
-    auto step = [&](const uint16_t* ct, uint16_t* nt) {
-        if (haven) kv_load_query_tile<D, 4>(nt, a, bhn, qbn, w, lane);
-        if (half == 0 ? in0 : in1) kv_tile<D>(ct, kreg, vreg, diag ? dlims : nullptr, key, c2, isv, lane, dv, dk);
-        __builtin_amdgcn_sched_barrier(0);
-        int bh2 = 0, qb2 = 0;
-        bool in02 = false, in12 = false, diag2 = false;
-        const bool more2 = haven && next(bh2, qb2, in02, in12, diag2);
-        wait_vmem();
-        __syncthreads();
-        bh = bhn;
-        qb = qbn;
-        in0 = in0n;
-        in1 = in1n;
-        diag = diagn;
-        have = haven;
-        bhn = bh2;
-        qbn = qb2;
-        in0n = in02;
-        in1n = in12;
-        diagn = diag2;
-        haven = more2;
-    };
-    while (have) {
-        step(t0s, t1s);
-        if (!have) break;
-        step(t1s, t0s);
-    }
-    if (!live) return;
-    float* dkp = a.dk + krow * D;
-    float* dvp = a.dv + krow * D;
-    const float pt = dz_scale(a.qkvmax + 2, D);   // the tiles give s dV and t s dK
-    const float fk = a.scale / (sc * pt * sq), fv = 1.f / sc;
-#pragma unroll
-    for (int i = 0; i < ND; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            f32x4 x, y;
-            x.x = dk[i][4 * j + 0] * fk;
-            x.y = dk[i][4 * j + 1] * fk;
-            x.z = dk[i][4 * j + 2] * fk;
-            x.w = dk[i][4 * j + 3] * fk;
-            y.x = dv[i][4 * j + 0] * fv;
-            y.y = dv[i][4 * j + 1] * fv;
-            y.z = dv[i][4 * j + 2] * fv;
-            y.w = dv[i][4 * j + 3] * fv;
-            *reinterpret_cast<f32x4*>(dkp + 32 * i + 8 * j + 4 * h) = x;
-            *reinterpret_cast<f32x4*>(dvp + 32 * i + 8 * j + 4 * h) = y;
-        }
-}
-
 // ------------------------------------------------------------------ dK / dV, two waves per SIMD
-// Row-split variant of the key-major pass (head dim 128): eight waves per
-// workgroup, wave (blk, kh, rh) holds the 32 keys 32 kh .. 32 kh + 31 of key
-// block blk of the pair and takes rows 32 rh .. 32 rh + 31 of every query
-// tile.  Each wave reads only its own query rows (row-wise and transposed), so
-// the LDS bytes per MFMA stay those of the one-wave kernel apart from V,
-// which sits in LDS (staged once per workgroup) to leave room for two waves
-// per SIMD: one wave's MFMAs then cover the other's softmax terms and LDS
-// latency.  The two row halves' partial dK / dV are added once at the end
-// (through LDS, in a fixed order).
-#ifndef MS_DKDV_ROWSPLIT
-#define MS_DKDV_ROWSPLIT 1
-#endif
+// Key-major pass: one workgroup of eight waves per (b, KV head, pair of
+// consecutive 64-key blocks).  For every query head of the KV group the pair
+// walks the union of its two transposed lists (query blocks that selected the
+// key block), the next query tile in flight (direct global->LDS loads, double
+// buffer) during the current one.  Wave (blk, kh, rh) holds the 32 keys
+// 32 kh .. 32 kh + 31 of key block blk of the pair (K in registers) and takes
+// rows 32 rh .. 32 rh + 31 of every query tile, so each wave reads only its
+// own query rows (row-wise and transposed) and V sits in LDS (staged once per
+// workgroup): that leaves room for two waves per SIMD, one wave's MFMAs
+// covering the other's softmax terms and LDS latency.  The two row halves'
+// partial dK / dV are added once at the end (through LDS, in a fixed order).
 constexpr int kKvRowsThreads = 512;
 
 // Rows 32 rh .. 32 rh + 31 of query tile t against this wave's 32 keys, in
@@ -889,8 +752,8 @@ bwd_dkdv_rows_kernel(AttnArgs a) {
     const float sc = dout_scale(a.dmax);
     const int32_t kg = ldc(a.k_blk_global, kb);
 
-    // walk: as bwd_dkdv_kernel (heads of the group in order, per head the
-    // union of the pair's two transposed lists)
+    // walk: heads of the group in order, per head the union of the pair's two
+    // transposed lists
     int g = 0;
     int64_t p0 = 0, e0 = 0, p1 = 0, e1 = 0;
     auto open_head = [&]() {
@@ -1301,10 +1164,7 @@ hipError_t launch_bwd_d(const AttnArgs& a, hipStream_t s) {
     const int64_t kpgrid = int64_t(a.B) * a.Hkv * ((a.nkb + 1) / 2);
     if (kpgrid > 0) {
         TraceScope _t("bwd_dkdv", s);
-        if (D == 128 && MS_DKDV_ROWSPLIT)
-            hipLaunchKernelGGL(bwd_dkdv_rows_kernel<D>, dim3(unsigned(kpgrid)), dim3(kKvRowsThreads), 0, s, a);
-        else
-            hipLaunchKernelGGL(bwd_dkdv_kernel<D>, dim3(unsigned(kpgrid)), dim3(kKvThreads), 0, s, a);
+        hipLaunchKernelGGL(bwd_dkdv_rows_kernel<D>, dim3(unsigned(kpgrid)), dim3(kKvRowsThreads), 0, s, a);
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
     { TraceScope _t("bwd_colplan", s); hipLaunchKernelGGL(bwd_colplan_kernel, dim3(1), dim3(kPlanThreads), 0, s, a); }
