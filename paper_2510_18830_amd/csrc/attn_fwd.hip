@@ -157,14 +157,15 @@ __device__ __forceinline__ void fwd_tile(const uint16_t* kt, const uint16_t* vt,
 constexpr int kFwdBlocks = MS_FWD_NB;            // query blocks per workgroup
 constexpr int kFwdThreads = 128 * kFwdBlocks;    // two waves per block
 
-// Two waves per SIMD (at most 256 registers per lane): the staging and
-// barrier waits of one set of waves overlap the MFMA work of another.
+// Two waves per SIMD at head dim 128 (at most 256 registers per lane), three
+// at 64 (at most 168): the staging and barrier waits of one set of waves
+// overlap the MFMA work of another.
 // Workgroup = kFwdBlocks consecutive query blocks of one head; the blocks
 // walk the union of their ascending block lists (each key tile staged once,
 // computed by the blocks whose list selected it), then each block's column
 // tiles.
 template <int D>
-__global__ void __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+__global__ void __launch_bounds__(kFwdThreads) __attribute__((amdgpu_waves_per_eu(2, D == 64 ? 3 : 2)))
 attn_fwd_kernel(AttnArgs a) {
     constexpr int KD = FwdRows<D>::KD, ND = FwdRows<D>::ND;
     constexpr int NB = kFwdBlocks, NW = 2 * NB;
