@@ -869,8 +869,11 @@ __device__ __forceinline__ bool dbit(const uint32_t* db, int32_t x) { return (db
 // Work list: chunk = 64 consecutive entries of one head's vertical list.  The
 // query blocks that can see a chunk form a suffix of the local blocks (global
 // block numbers rise with the local block in both ring layouts), starting at
-// the first block at or after the chunk's smallest column; that suffix is cut
-// into items of `span` blocks.  One workgroup builds the list (plain scans, so
+// the first block whose global number reaches the block of the chunk's
+// smallest column plus the head's run of selected block-diagonals from 0
+// (nearer query blocks reach every column of the chunk through one of those
+// diagonals, i.e. through selected blocks); that suffix is cut into items of
+// `span` blocks.  One workgroup builds the list (plain scans, so
 // the list and hence the summation order are fixed by the index alone).
 constexpr int kPlanThreads = 1024;
 
@@ -935,10 +938,24 @@ __global__ void __launch_bounds__(kPlanThreads) bwd_colplan_kernel(AttnArgs a) {
         const int64_t e0 = a.vcol_ptr[lo] + int64_t(g - a.col_choff[lo]) * 64;
         const int32_t cb = min(max(a.vcol_idx[e0], 0), a.Nk - 1) >> 6;
         const int32_t cg = a.k_blk_global[cb];
-        int L = 0, R = a.nqb;  // first local query block with global block >= cg
+        // run of selected block-diagonals 0 .. run - 1 of the head: a column
+        // of block kc lies on one of them for every query block below kc + run,
+        // so no column of the chunk is seen before global block cg + run
+        int64_t run = 0;
+        const uint32_t* db = a.diag_bits + int64_t(lo) * a.dwords;
+        for (int w = 0; w < a.dwords; ++w) {
+            const uint32_t word = db[w];
+            if (word != 0xffffffffu) {
+                run += __builtin_ctz(~word);
+                break;
+            }
+            run += 32;
+        }
+        const int64_t first = int64_t(cg) + run;
+        int L = 0, R = a.nqb;  // first local query block with global block >= cg + run
         while (L < R) {
             const int m = (L + R) >> 1;
-            if (a.q_blk_global[m] < cg) L = m + 1; else R = m;
+            if (a.q_blk_global[m] < first) L = m + 1; else R = m;
         }
         a.col_head[g] = lo;
         a.col_e0[g] = e0;

@@ -6,7 +6,7 @@
     forward and backward (Eq. softmax_gradient, Eq. attention_backward) give
     out, lse and dQ of the eight heads of KV group 0 and that group's dK and dV
     over every key, compared element by element.
-(2) The same layer with a vertical budget of k_v 8192, which makes the
+(2) The same layer with a vertical budget of k_v 16384, which makes the
     column pass's work list split each chunk's query blocks into items of more
     than the minimum span: the span the kernel planned is read back from the
     workspace and checked against the plan recomputed here from the index,
@@ -107,17 +107,37 @@ def _bwd_offsets(dims, vcol_cap):
     return out, chunk_cap
 
 
+def _diag_run(words) -> int:
+    """Length of the run of set bits from bit 0 of a bitset (uint32 words)."""
+    run = 0
+    for w in words:
+        w = int(w)
+        if w == 0xFFFFFFFF:
+            run += 32
+            continue
+        while w & 1:
+            run += 1
+            w >>= 1
+        break
+    return run
+
+
 def _planned_span(csr, nqb, bh, chunk_cap):
     """The column pass's plan recomputed from the index: chunks of 64 entries of
-    each head's vertical list, each seen by the query blocks from the one that
-    holds its first column on; span = max(16, ceil(candidates / budget))."""
+    each head's vertical list, each seen by the query blocks from the first
+    whose global block reaches the chunk's first column block plus the head's
+    run of selected block-diagonals from 0 (every nearer query block covers
+    the chunk's columns with selected blocks); span = max(16, ceil(candidates
+    / budget))."""
     total = 0
     vp, vi = csr["vcol_ptr"], csr["vcol_idx"]
     qg = csr["q_blk_global"]
+    db = csr["diag_bits"].reshape(bh, -1)
     for h in range(bh):
+        run = _diag_run(db[h])
         for e0 in range(int(vp[h]), int(vp[h + 1]), 64):
             cg = int(csr["k_blk_global"][int(vi[e0]) >> 6])
-            lo = int(np.searchsorted(qg, cg, side="left"))
+            lo = int(np.searchsorted(qg, cg + run, side="left"))
             total += nqb - lo
     fine = chunk_cap * ((nqb + COL_MIN_SPAN - 1) // COL_MIN_SPAN)
     budget = min(COL_ITEMS, fine)
@@ -126,7 +146,7 @@ def _planned_span(csr, nqb, bh, chunk_cap):
 
 @pytest.mark.timeout(900)
 def test_column_pass_split_regime_full_tensors(gpu):
-    wl = WORKLOADS["layer_32k"].resized(k_v=8192)
+    wl = WORKLOADS["layer_32k"].resized(k_v=16384)
     print(f"column-pass regime {wl}", flush=True)
     x = make_inputs(wl, "cpu")
     f = inputs_f64(x)
