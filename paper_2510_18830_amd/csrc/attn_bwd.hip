@@ -991,8 +991,10 @@ __global__ void __launch_bounds__(kPlanThreads) bwd_colplan_kernel(AttnArgs a) {
 template <int D>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1))) bwd_dkdv_col_kernel(AttnArgs a) {
     constexpr int KD = D / 16, ND = D / 32;
-    __shared__ __attribute__((aligned(16))) uint16_t ts[KvTile<D>::kElems];
-    __shared__ int32_t clims[64];
+    // two query-tile buffers and their key limits: the next active tile's
+    // loads are in flight while the current one is computed
+    __shared__ __attribute__((aligned(16))) uint16_t ts[2][KvTile<D>::kElems];
+    __shared__ int32_t clims[2][64];
     if (index_overflowed(a.overflow)) return;   // no work list was planned
     const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5, l32 = lane & 31;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -1035,18 +1037,31 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1
     const float c2 = a.scale * kLog2e / (sq * sk);
     const float sc = dout_scale(a.dmax);
     const uint32_t* db = a.diag_bits + int64_t(bh) * a.dwords;
-    for (int qb = qb0; qb < qb1; ++qb) {
-        const int32_t qg = a.q_blk_global[qb];
-        const bool active = valid && qg >= cg && !dbit(db, qg - cg);
-        const int lim = qg == cg ? cin : 0;
-        // every column covered by a selected block-diagonal: nothing to do here
-        if (!__syncthreads_or(active)) continue;
-        clims[key] = active ? lim : 64;
-        kv_load_query_tile<D, 2>(ts, a, bh, qb, w, lane);
+    // the next query block from q on where some column of the chunk is not
+    // covered by a selected block-diagonal (qb1 if none); its key limits go
+    // to clims[buf] and its loads into ts[buf]
+    auto next_active = [&](int q, int buf) {
+        for (; q < qb1; ++q) {
+            const int32_t qg = a.q_blk_global[q];
+            const bool active = valid && qg >= cg && !dbit(db, qg - cg);
+            if (__syncthreads_or(active)) {
+                clims[buf][key] = active ? (qg == cg ? cin : 0) : 64;
+                kv_load_query_tile<D, 2>(ts[buf], a, bh, q, w, lane);
+                break;
+            }
+        }
+        return q;
+    };
+    int cur = next_active(qb0, 0), buf = 0;
+    wait_vmem();
+    __syncthreads();
+    while (cur < qb1) {
+        const int nxt = next_active(cur + 1, buf ^ 1);
+        kv_tile<D, true>(ts[buf], kreg, vreg, clims[buf], key, c2, isv, lane, dv, dk);
         wait_vmem();
         __syncthreads();
-        kv_tile<D, true>(ts, kreg, vreg, clims, key, c2, isv, lane, dv, dk);
-        __syncthreads();
+        cur = nxt;
+        buf ^= 1;
     }
     if (!valid) return;
     const int64_t slot = int64_t(item) * 64 + key;
