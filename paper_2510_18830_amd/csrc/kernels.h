@@ -138,7 +138,7 @@ hipError_t launch_attn_bwd(const AttnArgs& a, hipStream_t s);
 // vertical list; its candidate query blocks (a suffix of the local blocks) are
 // split into items of `span` blocks, one workgroup each.  span is the smallest
 // value >= kColMinSpan that keeps the item count within the budget.
-constexpr int kColItems = 4096;
+constexpr int kColItems = 2048;
 constexpr int kColMinSpan = 16;
 struct ColPlanSizes {
     int64_t chunk_cap;  // bound on the chunk count: sum over heads of ceil(n_h / 64)

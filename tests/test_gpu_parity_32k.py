@@ -36,7 +36,7 @@ from tests.helpers import (assert_close, assert_lse_close, gpu_csr, inputs_f64, 
 
 pytestmark = pytest.mark.gpu
 
-COL_ITEMS = 4096       # item budget of the column pass's plan
+COL_ITEMS = 2048       # item budget of the column pass's plan
 COL_MIN_SPAN = 16      # smallest span it uses
 
 
