@@ -51,12 +51,12 @@ constexpr int kDeltaBlocks = 2048;
 
 // Delta = dO . O per row and max |dO|.  16 lanes per row, PER = d / 16
 // consecutive elements per lane read with one 16- or 8-byte load of dO and
-// one or two 16-byte loads of O; a workgroup takes 4 groups of 16 rows per
+// one or two 16-byte loads of O; a workgroup takes 8 groups of 16 rows per
 // grid-stride step and issues all their loads before the arithmetic, so each
-// wave has 4 rows' loads in flight.  One max-atomic per workgroup.
+// wave has 8 rows' loads in flight.  One max-atomic per workgroup.
 template <int PER, bool F32>
 __global__ void __launch_bounds__(256) bwd_delta_kernel(AttnArgs a) {
-    constexpr int U = 4;
+    constexpr int U = 8;
     __shared__ float wmax[4];
     const int64_t rows = int64_t(a.B) * a.Hq * a.Nq;
     const int sub = threadIdx.x & 15;
@@ -1167,7 +1167,7 @@ hipError_t launch_bwd_d(const AttnArgs& a, hipStream_t s) {
     const bool qside = !a.reuse_qrows;
     if (qside && rows > 0) {
         TraceScope _t("bwd_delta", s);
-        const int64_t groups = (rows + 63) / 64;
+        const int64_t groups = (rows + 127) / 128;
         const dim3 grid(unsigned(groups < kDeltaBlocks ? groups : int64_t(kDeltaBlocks)));
         if (a.o_f32)
             hipLaunchKernelGGL((bwd_delta_kernel<D / 16, true>), grid, dim3(256), 0, s, a);
